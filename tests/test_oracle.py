@@ -1,0 +1,445 @@
+"""Pins for the CPU oracle: each check ties an oracle function to something
+other than itself -- brute force on tiny inputs, exact rational arithmetic,
+library routines (numpy float64 matmul, torch's bf16 conversion), closed
+forms, invariants and hand-worked examples under tests/golden/."""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle as O
+import oracle.nets as ON
+from paper_2008_06967_amd import synth
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def gold(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+def g(stream):
+    return synth.rng(99, stream)
+
+
+# ----------------------------------------------------------------------------
+# exact fp32 rounding of a rational, used to pin the distance op order
+# ----------------------------------------------------------------------------
+
+def round_f32(x: Fraction) -> np.float32:
+    """Nearest binary32 to the exact rational x, ties to even (checked against
+    both neighbours with exact arithmetic, so no double rounding)."""
+    f = np.float32(float(x))
+    best = f
+    for c in (np.nextafter(f, np.float32(-np.inf)), np.nextafter(f, np.float32(np.inf))):
+        dc, db = abs(Fraction(float(c)) - x), abs(Fraction(float(best)) - x)
+        if dc < db or (dc == db and (int(c.view(np.uint32)) & 1) == 0):
+            best = c
+    return np.float32(best)
+
+
+def dist2_exact_fma(a, b):
+    d = np.float32(0)
+    for ac, bc in zip(a, b):
+        t = np.float32(ac) - np.float32(bc)          # one fp32 subtraction
+        d = round_f32(Fraction(float(t)) * Fraction(float(t)) + Fraction(float(d)))  # fused multiply-add
+    return d
+
+
+def test_dist2_is_sequential_fma():
+    r = g(0)
+    for C in (1, 3, 7, 64):
+        for _ in range(20):
+            a = r.standard_normal(C).astype(np.float32)
+            b = r.standard_normal(C).astype(np.float32)
+            d = O.dist2(a, b)
+            assert d == dist2_exact_fma(a, b)
+            assert d == O.dist2(b, a)  # symmetric bit for bit
+
+
+def test_dist2_integer_points_exact():
+    assert O.dist2([0, 0, 0], [1, 2, 2]) == 9.0
+    assert O.dist2([3, 0, 0], [7, 0, 0]) == 16.0
+
+
+# ----------------------------------------------------------------------------
+# bf16 rounding pinned to torch's float32 -> bfloat16 conversion (RNE)
+# ----------------------------------------------------------------------------
+
+def test_bf16_round_matches_torch():
+    import torch
+    r = g(1)
+    x = np.concatenate([r.standard_normal(2000).astype(np.float32) * 10.0 ** r.integers(-6, 6, 2000),
+                        np.array([1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8, 1 + 2 ** -8 + 2 ** -20, -0.0, 0.0,
+                                  3.0e38, -1.5], np.float32)]).astype(np.float32)
+    ours = O.bf16_round(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(ours.view(np.uint32), ref.view(np.uint32))
+    # ties to even, worked by hand
+    assert O.bf16_round(np.float32([1 + 2 ** -8]))[0] == 1.0
+    assert O.bf16_round(np.float32([1 + 3 * 2 ** -8]))[0] == np.float32(1 + 2 ** -6)
+
+
+# ----------------------------------------------------------------------------
+# Pi1: farthest-point sampling
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["fps_collinear.json", "fps_square.json"])
+def test_fps_golden(name):
+    d = gold(name)
+    idx, cxyz = O.fps(np.array([d["xyz"]], np.float32), d["M"])
+    assert idx[0].tolist() == d["idx"]
+    assert np.array_equal(cxyz[0], np.array(d["xyz"], np.float32)[d["idx"]])
+
+
+def test_fps_matches_bruteforce_recompute():
+    r = g(2)
+    for trial in range(40):
+        N = int(r.integers(1, 14))
+        M = int(r.integers(1, N + 1))
+        if trial % 3 == 0:   # integer grid: many exact ties and duplicates
+            xyz = r.integers(0, 3, size=(2, N, 3)).astype(np.float32)
+        else:
+            xyz = r.standard_normal((2, N, 3)).astype(np.float32)
+        idx, cxyz = O.fps(xyz, M)
+        assert np.array_equal(idx, O.fps_bruteforce(xyz, M))
+        assert np.array_equal(cxyz, np.take_along_axis(xyz, idx[..., None].astype(np.int64), 1))
+
+
+def test_fps_invariants():
+    r = g(3)
+    xyz = r.standard_normal((3, 200, 3)).astype(np.float32)
+    idx, _ = O.fps(xyz, 200)
+    for b in range(3):
+        assert idx[b, 0] == 0
+        assert sorted(idx[b].tolist()) == list(range(200))   # M = N, distinct points: a permutation
+    # the selected min-distances never increase (float64 check on the chosen points)
+    idx, _ = O.fps(xyz, 64)
+    p = xyz[0].astype(np.float64)
+    sel = idx[0]
+    dsel = [np.min(((p[sel[:m]] - p[sel[m]]) ** 2).sum(1)) for m in range(1, 64)]
+    assert all(dsel[i + 1] <= dsel[i] * (1 + 1e-6) for i in range(len(dsel) - 1))
+
+
+# ----------------------------------------------------------------------------
+# Pi2: ball query
+# ----------------------------------------------------------------------------
+
+def test_ball_query_golden():
+    d = gold("ball_query_collinear.json")
+    nit, cnt, _ = O.ball_query(np.array([d["xyz"]], np.float32), np.array([d["queries"]], np.float32),
+                               d["radius"], d["K"])
+    assert nit[0].tolist() == d["nit"]
+    assert cnt[0].tolist() == d["cnt"]
+
+
+def _bq_brute(xyz, q, radius, K):
+    """All distances, filter, ascending, first K, pad (no early exit)."""
+    r2 = np.float32(radius) * np.float32(radius)
+    B, M = q.shape[0], q.shape[1]
+    nit = np.zeros((B, M, K), np.int32)
+    cnt = np.zeros((B, M), np.int32)
+    for b in range(B):
+        for m in range(M):
+            d = np.array([O.dist2(xyz[b, j], q[b, m]) for j in range(xyz.shape[1])], np.float32)
+            hits = np.nonzero(d < r2)[0][:K]
+            cnt[b, m] = len(hits)
+            row = list(hits) + [hits[0] if len(hits) else 0] * (K - len(hits))
+            nit[b, m] = row
+    return nit, cnt
+
+
+def test_ball_query_bruteforce():
+    r = g(4)
+    for trial in range(12):
+        N = int(r.integers(1, 40))
+        M = int(r.integers(1, 8))
+        K = int(r.integers(1, 10))
+        xyz = r.uniform(-1, 1, (2, N, 3)).astype(np.float32)
+        q = np.concatenate([xyz[:, :1], r.uniform(-1, 1, (2, M - 1, 3)).astype(np.float32)], 1)
+        rad = float(r.uniform(0.1, 1.2))
+        nit, cnt, scanned = O.ball_query(xyz, q, rad, K)
+        bn, bc = _bq_brute(xyz, q, rad, K)
+        assert np.array_equal(nit, bn) and np.array_equal(cnt, bc)
+        assert (cnt[:, 0] >= 1).all()   # a member query always finds itself
+
+
+def test_ball_query_radius_is_strict():
+    xyz = np.array([[[0, 0, 0], [1, 0, 0], [2, 0, 0]]], np.float32)
+    nit, cnt, _ = O.ball_query(xyz, xyz[:, :1], 1.0, 3)   # d2 = 1 == r2 is outside
+    assert nit[0, 0].tolist() == [0, 0, 0] and cnt[0, 0] == 1
+
+
+def test_ball_query_no_hit_pads_zero():
+    xyz = np.array([[[5, 5, 5], [6, 6, 6]]], np.float32)
+    nit, cnt, _ = O.ball_query(xyz, np.zeros((1, 1, 3), np.float32), 0.5, 4)
+    assert nit[0, 0].tolist() == [0, 0, 0, 0] and cnt[0, 0] == 0
+
+
+# ----------------------------------------------------------------------------
+# Pi3: kNN
+# ----------------------------------------------------------------------------
+
+def test_knn_golden():
+    d = gold("knn_collinear.json")
+    x = np.array([d["xyz"]], np.float32)
+    nit, _ = O.knn(x, x, d["K"])
+    assert nit[0].tolist() == d["nit"]
+    t = np.array([d["tie_xyz"]], np.float32)
+    nit, _ = O.knn(t, np.array([d["tie_query"]], np.float32), 2)
+    assert nit[0].tolist() == d["tie_nit"]
+
+
+def test_knn_bruteforce_sort():
+    r = g(5)
+    for trial in range(10):
+        N = int(r.integers(3, 40))
+        C = int(r.choice([1, 3, 5, 16]))
+        K = int(r.integers(1, N + 1))
+        if trial % 2:
+            ref = r.integers(0, 3, size=(1, N, C)).astype(np.float32)   # ties
+        else:
+            ref = r.standard_normal((1, N, C)).astype(np.float32)
+        nit, dist = O.knn(ref, ref, K)
+        for m in range(N):
+            d = np.array([O.dist2(ref[0, j], ref[0, m]) for j in range(N)], np.float32)
+            order = np.lexsort((np.arange(N), d))[:K]     # full stable sort by (d, j)
+            assert nit[0, m].tolist() == order.tolist()
+            assert np.array_equal(dist[0, m], d[order])
+            assert nit[0, m, 0] == m or d[nit[0, m, 0]] == 0   # self (distance 0) comes first
+
+
+def test_knn_distance_close_to_exact():
+    r = g(6)
+    ref = r.standard_normal((1, 50, 64)).astype(np.float32)
+    q = r.standard_normal((1, 5, 64)).astype(np.float32)
+    nit, dist = O.knn(ref, q, 6)
+    exact = ((ref[0][None].astype(np.float64) - q[0][:, None].astype(np.float64)) ** 2).sum(-1)
+    got = np.take_along_axis(exact, nit[0].astype(np.int64), 1)
+    assert np.allclose(dist[0], got, rtol=64 * 2 ** -23)
+    # the chosen set is the true K nearest up to rounding
+    kth = np.sort(exact, 1)[:, 5]
+    assert (got.max(1) <= kth * (1 + 1e-5)).all()
+
+
+# ----------------------------------------------------------------------------
+# Pi4: MLP
+# ----------------------------------------------------------------------------
+
+def _mlp_f64(x, Ws, bs, relu_mask):
+    a = x.astype(np.float64)
+    for l, (W, b) in enumerate(zip(Ws, bs)):
+        a = a @ W.astype(np.float64).T + b.astype(np.float64)
+        a = a.astype(np.float32).astype(np.float64)
+        if relu_mask >> l & 1:
+            a = np.maximum(a, 0.0)
+    return a.astype(np.float32)
+
+
+def test_mlp_matches_numpy_float64():
+    r = g(7)
+    dims = [7, 33, 5, 17]
+    Ws = [r.standard_normal((dims[i + 1], dims[i])).astype(np.float32) for i in range(3)]
+    bs = [r.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(3)]
+    x = r.standard_normal((50, 7)).astype(np.float32)
+    for mask in (0b111, 0b011, 0):
+        y = O.mlp(x, Ws, bs, relu_mask=mask)
+        ref = _mlp_f64(x, Ws, bs, mask)
+        assert np.allclose(y, ref, rtol=1e-6, atol=1e-6)
+
+
+def test_mlp_special_cases():
+    r = g(8)
+    x = np.abs(r.standard_normal((10, 6))).astype(np.float32)
+    y = O.mlp(x, [np.eye(6, dtype=np.float32)], [np.zeros(6, np.float32)])
+    assert np.array_equal(y, x)                       # identity passes non-negative input
+    b = r.uniform(-1, 1, 4).astype(np.float32)
+    y = O.mlp(x, [np.zeros((4, 6), np.float32)], [b])
+    assert np.array_equal(y, np.broadcast_to(np.maximum(b, 0), (10, 4)))  # W = 0 gives ReLU(b)
+
+
+def test_mlp_bf16_matches_torch_rounding():
+    import torch
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16).to(torch.float32).numpy()
+
+    r = g(9)
+    dims = [5, 24, 16]
+    Ws = [r.standard_normal((dims[i + 1], dims[i])).astype(np.float32) for i in range(2)]
+    bs = [r.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(2)]
+    x = r.standard_normal((40, 5)).astype(np.float32)
+    y = O.mlp(x, Ws, bs, bf16=True)
+    a = bf(x).astype(np.float64)
+    for W, b in zip(Ws, bs):
+        a = a @ bf(W).astype(np.float64).T + b.astype(np.float64)
+        a = bf(np.maximum(a.astype(np.float32), 0)).astype(np.float64)
+    # identical up to fp64 summation order
+    assert np.max(np.abs(y - a)) <= 1e-2 * np.max(np.abs(a))
+    assert np.mean(y == a.astype(np.float32)) > 0.99
+
+
+# ----------------------------------------------------------------------------
+# Pi5: aggregation
+# ----------------------------------------------------------------------------
+
+def test_aggregate_golden():
+    d = gold("aggregate_example.json")
+    out = O.aggregate_max(np.array([d["pft"]], np.float32), np.array([d["nit"]], np.int32),
+                          cidx=np.array([d["cidx"]], np.int32), sign=-1)
+    assert out[0].tolist() == d["out"]
+
+
+def test_max_subtract_identity_bitwise():
+    """max_k fl(f_k - f_c) == fl(max_k f_k - f_c): rounding is monotone."""
+    r = g(10)
+    B, N, M, K, C = 2, 60, 20, 9, 33
+    pft = (r.standard_normal((B, N, C)) * 10.0 ** r.integers(-3, 3, (B, N, C))).astype(np.float32)
+    nit = r.integers(0, N, (B, M, K)).astype(np.int32)
+    cidx = r.integers(0, N, (B, M)).astype(np.int32)
+    out = O.aggregate_max(pft, nit, cidx=cidx, sign=-1)
+    cen = np.take_along_axis(pft, cidx[..., None].astype(np.int64), 1)           # [B,M,C]
+    rows = pft[np.arange(B)[:, None, None], nit]                                  # [B,M,K,C]
+    ref = (rows - cen[:, :, None, :]).astype(np.float32).max(2)                   # subtract first, then max
+    assert np.array_equal(out.view(np.uint32), ref.view(np.uint32))
+    # duplicates (padding) never change the result
+    nit2 = nit.copy()
+    nit2[:, :, -1] = nit2[:, :, 0]
+    out2 = O.aggregate_max(pft, np.concatenate([nit2, nit], 2), cidx=cidx, sign=-1)
+    assert np.array_equal(out2, out)
+
+
+def test_aggregate_add_relu_and_table():
+    r = g(11)
+    B, N, M, K, C = 1, 30, 30, 5, 8
+    pft = r.standard_normal((B, N, C)).astype(np.float32)
+    tab = r.standard_normal((B, M, C)).astype(np.float32)
+    nit = r.integers(0, N, (B, M, K)).astype(np.int32)
+    out = O.aggregate_max(pft, nit, cfeat=tab, sign=+1, relu=True)
+    rows = pft[np.arange(B)[:, None, None], nit].max(2)
+    assert np.array_equal(out, np.maximum((rows + tab).astype(np.float32), 0))
+    out = O.aggregate_max(pft, nit)   # no centroid term
+    assert np.array_equal(out, rows)
+
+
+# ----------------------------------------------------------------------------
+# Pi6 - Pi9: module-level identities
+# ----------------------------------------------------------------------------
+
+def normwise(a, b):
+    return float(np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-30))
+
+
+def test_edgeconv_delayed_equals_conventional():
+    """ReLU is monotone and the edge function linear, so delayed is exact
+    in real arithmetic (one-layer modules, Sec. 6.3 Ltd discussion)."""
+    r = g(12)
+    X = r.standard_normal((2, 64, 6)).astype(np.float32)
+    W = (r.standard_normal((16, 12)) * 0.5).astype(np.float32)
+    b = r.uniform(-0.1, 0.1, 16).astype(np.float32)
+    a = ON.edgeconv_delayed(X, 5, W, b)
+    c = ON.edgeconv_conventional(X, 5, W, b)
+    assert np.array_equal(a["nit"], c["nit"])
+    assert normwise(a["out"], c["out"]) < 1e-5
+
+
+def test_linear_module_exact_without_phi():
+    """Eq. (3) without phi: one linear layer and zero bias make delayed ==
+    conventional; a bias b makes conventional - delayed == b."""
+    r = g(13)
+    xyz = r.uniform(-1, 1, (1, 80, 3)).astype(np.float32)
+    feat = r.standard_normal((1, 80, 4)).astype(np.float32)
+    W = r.standard_normal((10, 7)).astype(np.float32)
+    idx, cxyz = O.fps(xyz, 20)
+    nit, _, _ = O.ball_query(xyz, cxyz, 0.6, 8)
+    x = np.concatenate([xyz, feat], -1)
+    for b in (np.zeros(10, np.float32), r.uniform(-1, 1, 10).astype(np.float32)):
+        pft = O.mlp(x, [W], [b], relu_mask=0)
+        delayed = O.aggregate_max(pft, nit, cidx=idx, sign=-1)
+        nfm = O.group_offsets(xyz, feat, idx, nit)
+        h = O.mlp(nfm, [W], [b], relu_mask=0)
+        conv = O.rowgroup_max(h.reshape(1, 20 * 8, 10), 8)
+        assert np.allclose(conv - delayed, np.broadcast_to(b, conv.shape), atol=1e-5)
+
+
+def test_eq3_hand_example():
+    d = gold("eq3_approximation.json")
+    pts = np.array(d["points"], np.float32).reshape(1, 3, 1)
+    one = [np.ones((1, 1), np.float32)] * 2
+    zero = [np.zeros(1, np.float32)] * 2
+    pft = O.mlp(pts, one, zero)                                    # F on the raw points
+    delayed = O.aggregate_max(pft, np.array([[d["nit"]]], np.int32),
+                              cidx=np.array([[d["centroid"]]], np.int32), sign=-1)
+    offsets = (pts[0, d["nit"], 0] - pts[0, d["centroid"], 0]).reshape(1, 2, 1)
+    conv = O.rowgroup_max(O.mlp(offsets, one, zero), 2)
+    assert float(delayed[0, 0, 0]) == d["delayed"]
+    assert float(conv[0, 0, 0]) == d["conventional"]
+
+
+def test_group_all_same_in_both_orders():
+    spec = synth.workload("pointnet2_cls", B=1)
+    xyz, feat = synth.make_points(spec)
+    w = synth.make_weights(spec)
+    a = ON.forward(spec, xyz, feat, w, delayed=True)
+    c = ON.forward(spec, xyz, feat, w, delayed=False)
+    for ma, mc in zip(a["modules"], c["modules"]):
+        assert np.array_equal(ma["idx"], mc["idx"]) and np.array_equal(ma["nit"], mc["nit"])
+    # group-all on identical inputs is identical
+    m = a["modules"][-1]
+    g1 = ON.group_all(m["cxyz"], m["out"], *w["group_all"])
+    g2 = ON.group_all(m["cxyz"], m["out"], *w["group_all"])
+    assert np.array_equal(g1, g2)
+
+
+def test_walkthrough_shapes():
+    d = gold("walkthrough_shapes.json")
+    spec = synth.workload("sa_module")
+    assert (spec["N"], spec["sa"][0]["M"], spec["sa"][0]["K"], spec["sa"][0]["mlp"][-1]) == \
+        (d["N"], d["M"], d["K"], d["c_out"])
+    xyz, feat = synth.make_points(spec)
+    w = synth.make_weights(spec)
+    r = ON.forward(spec, xyz, feat, w, delayed=True)["modules"][0]
+    assert list(r["pft"].shape[1:]) == d["pft"] and list(r["nit"].shape[1:]) == d["nit"]
+    assert d["M"] * d["K"] == d["mlp_rows_conventional"]
+
+
+def test_group_pointnet_rows():
+    r = g(14)
+    xyz = r.standard_normal((1, 10, 3)).astype(np.float32)
+    feat = r.standard_normal((1, 10, 2)).astype(np.float32)
+    cxyz = xyz[:, [3, 7]]
+    nit = np.array([[[1, 2], [7, 9]]], np.int32)
+    nfm = O.group_pointnet(xyz, feat, cxyz, nit)
+    assert np.array_equal(nfm[0, 1, 1, :3], xyz[0, 9] - xyz[0, 7])
+    assert np.array_equal(nfm[0, 1, 1, 3:], feat[0, 9])
+    e = O.group_edge(feat, np.array([[[1]] * 10], np.int32))
+    assert np.array_equal(e[0, 4, 0], np.concatenate([feat[0, 4], feat[0, 1] - feat[0, 4]]))
+
+
+# ----------------------------------------------------------------------------
+# 3-NN interpolation
+# ----------------------------------------------------------------------------
+
+def test_interpolate3_properties():
+    r = g(15)
+    src = r.uniform(-1, 1, (1, 30, 3)).astype(np.float32)
+    dst = np.concatenate([src[:, :5], r.uniform(-1, 1, (1, 20, 3)).astype(np.float32)], 1)
+    f = r.standard_normal((1, 30, 7)).astype(np.float32)
+    out = O.interpolate3(dst, src, f)
+    # a destination that coincides with a source point takes its feature
+    assert np.allclose(out[0, :5], f[0, :5], atol=1e-6)
+    # constants are reproduced (weights sum to one)
+    c = np.full((1, 30, 2), 2.5, np.float32)
+    assert np.allclose(O.interpolate3(dst, src, c), 2.5, atol=1e-6)
+    # convex combination of the 3 nearest sources
+    nit, _ = O.knn(src, dst, 3)
+    for i in range(dst.shape[1]):
+        nb = f[0, nit[0, i]]
+        assert (out[0, i] >= nb.min(0) - 1e-6).all() and (out[0, i] <= nb.max(0) + 1e-6).all()
+    # equidistant sources give the plain average
+    s3 = np.array([[[1, 0, 0], [0, 1, 0], [0, 0, 1], [5, 5, 5]]], np.float32)
+    f3 = np.array([[[3.0], [6.0], [9.0], [100.0]]], np.float32)
+    assert np.allclose(O.interpolate3(np.zeros((1, 1, 3), np.float32), s3, f3), 6.0)
