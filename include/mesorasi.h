@@ -1,0 +1,243 @@
+/*
+ * mesorasi.h -- C ABI of the MI355X (gfx950) delayed-aggregation library
+ * libmesorasi.so.
+ *
+ * Method: Feng et al., "Mesorasi: Architecture Support for Point Cloud
+ * Analytics via Delayed-Aggregation" (arXiv 2008.06967).  A point-cloud
+ * module computes p_o = F(A(N(p_i), p_i)) (Sec. 2.1, Eq. (1)).  Delayed
+ * aggregation (Sec. 3.1, Eq. (2)-(3)) instead runs the shared MLP F once on
+ * the N input points (the point feature table, PFT), runs the neighbor
+ * search N concurrently into the neighbor index table (NIT), and finally
+ * aggregates PFT rows by the NIT: max over the K neighbors, then subtract
+ * the centroid's own PFT row (max(f_j - f_c) = max(f_j) - f_c, end of the
+ * Sec. 3.1 walk-through).
+ *
+ * General rules for every entry point
+ *  - Pointers are DEVICE pointers unless marked "host".  The caller owns
+ *    every buffer; the library never allocates, frees or synchronises, so
+ *    every call may be captured into a HIP graph.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Work is enqueued asynchronously on it; ordering across streams is the
+ *    caller's job (events).
+ *  - Arrays are row-major and contiguous unless a leading dimension `ld_*`
+ *    (in elements) is given.  Index arrays are int32 and local to their
+ *    cloud: 0 <= index < N.  Point coordinates are float32 [B, N, 3].
+ *  - Inputs are const; outputs must not alias inputs.  Every output element
+ *    is written, padding included.
+ *  - Return value: MESORASI_OK or a negative status.  All argument checks
+ *    run on the host BEFORE any HIP call, so a rejected call touches no
+ *    device state.  MESORASI_EHIP reports a failed launch; device faults
+ *    surface at the caller's next synchronisation.  Out-of-range indices
+ *    in a caller-supplied NIT/index array are undefined behaviour.
+ *  - mesorasi_last_error() returns a thread-local text describing the last
+ *    failure on the calling thread.
+ *  - Zero-sized batches (B == 0, M == 0 or rows == 0) are valid no-ops.
+ */
+#ifndef MESORASI_H
+#define MESORASI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MESORASI_VERSION 1
+
+enum {
+    MESORASI_OK = 0,
+    MESORASI_EINVAL = -1,        /* invalid argument (NULL, negative size, inconsistent shape) */
+    MESORASI_EUNSUPPORTED = -2,  /* valid but outside the implemented limits */
+    MESORASI_EHIP = -3,          /* the HIP runtime reported an error at launch */
+    MESORASI_EWORKSPACE = -4     /* workspace NULL or smaller than the matching *_workspace() size */
+};
+
+enum { MESORASI_F32 = 0, MESORASI_BF16 = 1 };
+
+/* Limits (MESORASI_EUNSUPPORTED beyond them). */
+#define MESORASI_MAX_N_FPS 65536     /* points per cloud for FPS */
+#define MESORASI_MAX_K_BALL 1024     /* neighbors per ball query */
+#define MESORASI_MAX_K_KNN 64        /* neighbors per kNN query */
+#define MESORASI_MAX_C_KNN 128       /* kNN feature width */
+#define MESORASI_MAX_LAYERS 8        /* MLP depth */
+#define MESORASI_MAX_WIDTH 4096      /* MLP layer width */
+
+int mesorasi_version(void);
+const char* mesorasi_strerror(int status);
+const char* mesorasi_last_error(void);
+
+/*
+ * Farthest-point sampling (the centroid sampling of the PointNet++ modules,
+ * Sec. 5 "Software Setup"; the paper names it without defining it).
+ * Greedy: start at point 0; keep for each point its squared distance to the
+ * nearest selected point; select the point where it is largest, the lowest
+ * index on ties.  Squared distance: t_c = x_c - y_c, d = fma(t_c, t_c, d)
+ * for c = x, y, z from d = 0, each step rounded to fp32 -- bit-exact and
+ * deterministic.
+ *   xyz   [B, N, 3] float32
+ *   idx   [B, M] int32 out: selected indices in selection order
+ *   cxyz  [B, M, 3] float32 out, nullable: copies of the selected points
+ * Errors: EINVAL for NULL xyz/idx, B/N/M < 0, M > N, N == 0 < M;
+ *         EUNSUPPORTED for N > MESORASI_MAX_N_FPS.
+ * One workgroup per cloud (the M iterations are sequential).
+ */
+int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, int32_t* idx, float* cxyz, void* stream);
+
+/*
+ * Ball query: neighbor search N (Sec. 2.1 "Neighbor Search") producing the
+ * NIT (Sec. 3.1 walk-through).  For each query q, the first K point indices
+ * in ascending order with squared distance (same rule as FPS) strictly
+ * below fl32(radius * radius); remaining slots repeat the first hit, or
+ * hold 0 when there is none.
+ *   xyz   [B, N, 3] float32 points;  qxyz [B, M, 3] float32 queries
+ *   nit   [B, M, K] int32 out
+ *   cnt   [B, M] int32 out, nullable: number of real hits (<= K)
+ * Errors: EINVAL for NULL xyz/qxyz/nit, B/N/M < 0, N == 0 < M, K < 1,
+ *         radius not finite or <= 0;  EUNSUPPORTED for K > MESORASI_MAX_K_BALL.
+ */
+int mesorasi_ball_query(const float* xyz, const float* qxyz, int64_t B, int64_t N, int64_t M, float radius,
+                        int32_t K, int32_t* nit, int32_t* cnt, void* stream);
+
+/*
+ * k nearest neighbours in C-dimensional feature space (the DGCNN search in
+ * the previous module's output space, Sec. 4.1 "Work Flow").  Squared
+ * distance t_c = r_c - q_c, d = fma(t_c, t_c, d) for c ascending from 0;
+ * the K smallest by (distance, index), sorted; self is included when the
+ * query is one of the reference points.
+ *   ref   [B, N, ld_ref] float32 (first C columns used)
+ *   query [B, M, ld_query] float32
+ *   nit   [B, M, K] int32 out;  dist [B, M, K] float32 out, nullable
+ * Errors: EINVAL for NULL ref/query/nit, sizes < 0, K < 1, K > N, C < 1,
+ *         ld < C;  EUNSUPPORTED for K > MESORASI_MAX_K_KNN or
+ *         C > MESORASI_MAX_C_KNN.
+ */
+int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query, int64_t ld_query, int64_t B, int64_t N,
+                 int64_t M, int32_t C, int32_t K, int32_t* nit, float* dist, void* stream);
+
+/*
+ * Shared per-point MLP: feature computation F (Sec. 2.1 "Feature
+ * Computation"; Eq. (3) with phi = ReLU), run on any set of rows -- in the
+ * delayed module on the N input points, producing the PFT.
+ *   layer l: h_{l+1} = phi_l(h_l W_l^T + b_l), phi_l = ReLU iff bit l of
+ *   relu_mask is set.
+ * Input rows are the column concatenation [x0 | x1]:
+ *   x0 [rows, ld0] float32 (first c0 columns), x1 [rows, ld1] float32 (first
+ *   c1 columns; NULL iff c1 == 0).  dims (host) has n_layers + 1 entries,
+ *   dims[0] == c0 + c1.
+ *   W    host array of n_layers device pointers; W[l] is [dims[l+1], dims[l]]
+ *        row-major (torch Linear layout), float32 when dtype == F32, bf16
+ *        bits (uint16, round-to-nearest-even) when dtype == BF16.
+ *   bias host array of n_layers float32 device pointers (entries nullable).
+ *   dtype F32: fp32 inputs/weights on fp32 MFMA, fp32 activations.
+ *         BF16: inputs rounded to bf16, bf16 weights, bf16 MFMA with fp32
+ *         accumulation; bias and ReLU in fp32; every stored activation
+ *         (intermediate and output) rounded to bf16.
+ *   out_dtype F32 or BF16: storage type of y (a BF16-path result stored as
+ *         F32 holds bf16-representable values).
+ *   pool_group 0: y is [rows, ld_y].  G > 0: rows % G == 0 and y is
+ *         [rows / G, ld_y] holding the column max over each group of G
+ *         consecutive rows (the reduction after F, Sec. 2.1; group-all
+ *         modules).  Pooling needs ReLU on the last layer and out_dtype F32.
+ *   ws   device workspace of at least mesorasi_pointwise_mlp_workspace()
+ *        bytes (NULL allowed when that size is 0).
+ * Errors: EINVAL for NULL x0/y/W/dims, c0 < 1, c1 < 0, ld < c, dims[0] !=
+ *         c0 + c1, a width < 1, ld_y < dims[n], rows % G != 0;
+ *         EUNSUPPORTED for n_layers outside [1, MESORASI_MAX_LAYERS], a width
+ *         above MESORASI_MAX_WIDTH, pooling without a final ReLU or with
+ *         out_dtype BF16;  EWORKSPACE when ws is too small.
+ */
+int mesorasi_pointwise_mlp(const float* x0, int32_t c0, int64_t ld0, const float* x1, int32_t c1, int64_t ld1,
+                           int64_t rows, int32_t n_layers, const int32_t* dims, const void* const* W,
+                           const float* const* bias, uint32_t relu_mask, int32_t dtype, int32_t out_dtype, void* y,
+                           int64_t ld_y, int64_t pool_group, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes for mesorasi_pointwise_mlp with these arguments (0 when
+ * none is needed).  Returns 0 for invalid arguments as well. */
+size_t mesorasi_pointwise_mlp_workspace(int64_t rows, int32_t n_layers, const int32_t* dims, int32_t dtype,
+                                        int64_t pool_group);
+
+/*
+ * Aggregation A on the PFT (Sec. 4.2 first paragraph; Sec. 3.1 max/subtract
+ * distributivity): for each NIT entry, gather the K PFT rows, take the
+ * column-wise max (exact), then combine with the centroid row in one fp32
+ * operation: out = max + sign * centroid, then ReLU when relu != 0.
+ *   pft   [B, N, ld_pft] of pft_dtype (F32 or BF16), first C columns used
+ *   nit   [B, M, K] int32
+ *   centroid row: cidx [B, M] int32 (a PFT row: pft[b, cidx]) or cfeat
+ *         [B, M, ld_c] of pft_dtype (explicit table); both NULL = no
+ *         centroid term.  At most one may be non-NULL.
+ *   sign  -1 (PointNet++: subtract the centroid feature) or +1 (DGCNN: add
+ *         the (W1 - W2) x_i term).
+ *   out   [B, M, ld_out] float32
+ * Errors: EINVAL for NULL pft/nit/out, sizes < 0, K < 1, C < 1, ld < C,
+ *         both cidx and cfeat set, sign not +-1, N == 0 < M;
+ *         EUNSUPPORTED for an unknown dtype or C > 65536.
+ */
+int mesorasi_aggregate_max(const void* pft, int64_t ld_pft, int32_t pft_dtype, const int32_t* nit, int64_t B,
+                           int64_t N, int64_t M, int32_t K, int32_t C, const int32_t* cidx, const void* cfeat,
+                           int64_t ld_c, int32_t sign, int32_t relu, float* out, int64_t ld_out, void* stream);
+
+/*
+ * Conventional module, kept as the comparison path (Eq. (1); Sec. 2.1
+ * "Aggregation" and "Feature Computation"): build the neighbor feature
+ * matrix (NFM) in the workspace, run the MLP on every (centroid, neighbor)
+ * row, and max-reduce over the K rows of each centroid.
+ *   grouping 0 (PointNet++): NFM row = [xyz_j - cxyz_c | feat_j], dims[0] =
+ *            3 + cf; needs xyz and cxyz [B, M, 3].
+ *   grouping 1 (DGCNN edge): NFM row = [f_i | f_j - f_i] with f = feat
+ *            [B, N, ld_f] (cf columns), centroid i = point i (M == N);
+ *            dims[0] = 2 cf; xyz/cxyz unused (nullable).
+ *   nit [B, M, K] int32; out [B, M, ld_out] float32.
+ *   MLP arguments as in mesorasi_pointwise_mlp (last layer must have ReLU).
+ *   ws  at least mesorasi_conventional_workspace() bytes.
+ * Errors: as mesorasi_pointwise_mlp plus EINVAL for an unknown grouping,
+ *         NULL nit, M != N for grouping 1, dims[0] inconsistent with cf.
+ */
+int mesorasi_conventional_module(const float* xyz, const float* feat, int32_t cf, int64_t ld_f, const float* cxyz,
+                                 const int32_t* nit, int64_t B, int64_t N, int64_t M, int32_t K, int32_t grouping,
+                                 int32_t n_layers, const int32_t* dims, const void* const* W,
+                                 const float* const* bias, uint32_t relu_mask, int32_t dtype, float* out,
+                                 int64_t ld_out, void* ws, size_t ws_bytes, void* stream);
+
+size_t mesorasi_conventional_workspace(int64_t B, int64_t M, int32_t K, int32_t n_layers, const int32_t* dims,
+                                       int32_t dtype);
+
+/*
+ * Feature propagation by 3-NN inverse-distance interpolation (the
+ * three_interpolate kernel of the PointNet++ segmentation baseline, Sec. 5
+ * "Software Setup").  For every destination point: its 3 nearest source
+ * points by the kNN rule above (C = 3), weights w = 1 / max(d2, 1e-10),
+ * f_dst = sum_k w_k f_k / sum_k w_k (fp32).
+ *   xyz_dst [B, Nd, 3], xyz_src [B, Ns, 3], f_src [B, Ns, ld_src] float32
+ *   f_dst   [B, Nd, ld_dst] float32 out (first C columns written)
+ * Errors: EINVAL for NULL pointers, sizes < 0, Ns < 3, C < 1, ld < C.
+ */
+int mesorasi_interpolate3(const float* xyz_dst, const float* xyz_src, const float* f_src, int64_t ld_src,
+                          int64_t B, int64_t Nd, int64_t Ns, int32_t C, float* f_dst, int64_t ld_dst, void* stream);
+
+/*
+ * float32 -> bf16 bits, round to nearest even (weights and inputs of the
+ * bf16 MLP variant).  x [n] float32, y [n] uint16 out.
+ * Errors: EINVAL for NULL pointers or n < 0.
+ */
+int mesorasi_cast_bf16(const float* x, int64_t n, uint16_t* y, void* stream);
+
+/*
+ * EdgeConv weight fold for the delayed DGCNN module.  The edge function
+ * W [x_i | x_j - x_i] + b equals (W1 - W2) x_i + W2 x_j + b, so the PFT of
+ * the delayed module is X [W1 - W2 ; W2]^T with bias [b ; 0].
+ *   W [C_out, 2 C] float32 (W1 = first C columns, W2 = last C)
+ *   b [C_out] float32 (nullable: treated as 0)
+ *   W_out [2 C_out, C] float32 out: rows 0..C_out-1 = fl32(W1 - W2),
+ *         rows C_out.. = W2;  b_out [2 C_out] float32 out = [b ; 0]
+ * Errors: EINVAL for NULL W/W_out/b_out, C < 1, C_out < 1.
+ */
+int mesorasi_edgeconv_fold(const float* W, const float* b, int32_t C, int32_t C_out, float* W_out, float* b_out,
+                           void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MESORASI_H */

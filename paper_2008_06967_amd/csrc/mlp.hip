@@ -1,0 +1,494 @@
+// Shared per-point MLP (feature computation F) on gfx950 MFMA, and the
+// conventional aggregate-then-MLP module built on it.
+//
+// F is a matrix-matrix product because all rows share the weights (Sec. 2.1
+// "Feature Computation"); with delayed aggregation it runs on the N input
+// points instead of the N_out x K neighbor rows (Sec. 3.1, Eq. (3)).
+//
+// One launch per layer: Y = phi(X W^T + b) with X = [x0 | x1] (two column
+// sources, so the first layer reads xyz and the previous module's features
+// without a concatenated copy).  Workgroup tile 64 x 64 over (rows, output
+// channels), 4 waves each owning a 32 x 32 block, K staged through LDS in
+// slices of 32:
+//  - fp32: v_mfma_f32_32x32x2_f32 (lane l feeds A[l%32][k + l/32] and
+//    B[k + l/32][l%32]); LDS tiles are k-major so the 32 lanes of a half
+//    wave read consecutive words.
+//  - bf16: v_mfma_f32_32x32x16_bf16 (lane l feeds 8 consecutive k of row
+//    l%32, k offset 8*(l/32)); LDS rows of 32 bf16 padded to 40 so the
+//    16-byte reads of a half wave hit distinct banks.
+// The accumulator of a 32 x 32 MFMA holds, in lane l and register r, row
+// 8*(r/4) + 4*(l/32) + r%4 and column l%32.
+// Epilogue: + bias, optional ReLU, optional bf16 rounding, then either a
+// store or a pooled column max (pool groups of G rows; values are >= 0
+// after ReLU, so the max is an unsigned atomicMax on the float bits, which
+// is exact and order independent).
+#include "common.h"
+
+namespace meso {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int BM = 64, BN = 64, BK = 32;
+constexpr int kPadF = 4;     // fp32 k-major rows: BM + 4 words
+constexpr int kRowH = 40;    // bf16 rows: 32 k + 8 pad (80 bytes)
+
+enum { EPI_F32 = 0, EPI_BF16 = 1, EPI_POOL = 2 };
+
+struct GemmArgs {
+    const void* x0;
+    int64_t ld0;
+    const float* x1;
+    int64_t ld1;
+    int c0, c1;
+    int a_bf16;          // x0 holds bf16 bits (intermediate activations of the bf16 path)
+    int64_t rows;
+    int K, N;
+    const void* W;       // [N, K]
+    const float* bias;   // [N] or null
+    int relu;
+    void* y;
+    int64_t ldy;
+    int64_t G;           // pool group (EPI_POOL)
+};
+
+// Element (r, k) of the virtual input [x0 | x1] as float (0 outside).
+__device__ __forceinline__ float a_elem(const GemmArgs& a, int64_t r, int k) {
+    if (r >= a.rows) return 0.0f;
+    if (k < a.c0) {
+        if (a.a_bf16) return bf16_to_f32(static_cast<const uint16_t*>(a.x0)[r * a.ld0 + k]);
+        return static_cast<const float*>(a.x0)[r * a.ld0 + k];
+    }
+    k -= a.c0;
+    if (k < a.c1) return a.x1[r * a.ld1 + k];
+    return 0.0f;
+}
+
+// Eight consecutive input elements (r, k0 .. k0+7) as float.
+template <bool FAST>
+__device__ __forceinline__ void load_a8(const GemmArgs& a, int64_t r, int k0, float (&v)[8]) {
+    if constexpr (FAST) {
+        // single fp32 source, 16-byte aligned rows, K multiple of 8
+        if (r < a.rows && k0 < a.K) {
+            const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(a.x0) + r * a.ld0 + k0);
+            const float4 u = p[0], w = p[1];
+            v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+            v[4] = w.x; v[5] = w.y; v[6] = w.z; v[7] = w.w;
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = 0.0f;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = a_elem(a, r, k0 + i);
+    }
+}
+
+template <bool FAST>
+__device__ __forceinline__ void load_w8_f32(const GemmArgs& a, int n, int k0, float (&v)[8]) {
+    const float* W = static_cast<const float*>(a.W);
+    if (FAST && n < a.N && k0 < a.K) {
+        const float4* p = reinterpret_cast<const float4*>(W + (int64_t)n * a.K + k0);
+        const float4 u = p[0], w = p[1];
+        v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+        v[4] = w.x; v[5] = w.y; v[6] = w.z; v[7] = w.w;
+        return;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (n < a.N && k0 + i < a.K) ? W[(int64_t)n * a.K + k0 + i] : 0.0f;
+}
+
+template <bool FAST>
+__device__ __forceinline__ uint4 load_w8_bf16(const GemmArgs& a, int n, int k0) {
+    const uint16_t* W = static_cast<const uint16_t*>(a.W);
+    if (FAST && n < a.N && k0 < a.K) return *reinterpret_cast<const uint4*>(W + (int64_t)n * a.K + k0);
+    uint16_t h[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = (n < a.N && k0 + i < a.K) ? W[(int64_t)n * a.K + k0 + i] : (uint16_t)0;
+    uint4 q;
+    q.x = h[0] | ((uint32_t)h[1] << 16);
+    q.y = h[2] | ((uint32_t)h[3] << 16);
+    q.z = h[4] | ((uint32_t)h[5] << 16);
+    q.w = h[6] | ((uint32_t)h[7] << 16);
+    return q;
+}
+
+// Load 8 input elements as bf16 bits (rounding fp32 sources to nearest even).
+template <bool FAST>
+__device__ __forceinline__ uint4 load_a8_bf16(const GemmArgs& a, int64_t r, int k0) {
+    if (a.a_bf16 && FAST) {
+        if (r < a.rows && k0 < a.K)
+            return *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.x0) + r * a.ld0 + k0);
+        return make_uint4(0, 0, 0, 0);
+    }
+    uint16_t h[8];
+    if (a.a_bf16) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            h[i] = (r < a.rows && k0 + i < a.c0) ? static_cast<const uint16_t*>(a.x0)[r * a.ld0 + k0 + i] : (uint16_t)0;
+    } else {
+        float v[8];
+        load_a8<FAST>(a, r, k0, v);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) h[i] = f32_to_bf16(v[i]);
+    }
+    uint4 q;
+    q.x = h[0] | ((uint32_t)h[1] << 16);
+    q.y = h[2] | ((uint32_t)h[3] << 16);
+    q.z = h[4] | ((uint32_t)h[5] << 16);
+    q.w = h[6] | ((uint32_t)h[7] << 16);
+    return q;
+}
+
+// Shared epilogue: acc holds the 32 x 32 block (row0, col0) of this wave.
+template <int EPI>
+__device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, int64_t row0, int col0, int lane,
+                                         bool round_bf16_out) {
+    const int col = col0 + (lane & 31);
+    const bool col_ok = col < a.N;
+    const float bias = (col_ok && a.bias) ? a.bias[col] : 0.0f;
+    float v[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        float t = acc[r] + bias;
+        if (a.relu) t = t > 0.0f ? t : 0.0f;
+        if (round_bf16_out) t = round_bf16(t);
+        v[r] = t;
+    }
+    const int64_t rbase = row0 + 4 * (lane >> 5);
+    if constexpr (EPI == EPI_POOL) {
+        float* y = static_cast<float*>(a.y);
+        unsigned* yu = reinterpret_cast<unsigned*>(y);
+        if (a.G % 32 == 0) {
+            // the whole 32-row block lies in one group (row0 is a multiple of 32)
+            if (row0 >= a.rows) return;
+            float m = v[0];
+#pragma unroll
+            for (int r = 1; r < 16; ++r) m = fmaxf(m, v[r]);
+            m = fmaxf(m, __shfl_xor(m, 32));
+            if (lane < 32 && col_ok) atomicMax(yu + (row0 / a.G) * a.ldy + col, __float_as_uint(m));
+            return;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t r0 = rbase + 8 * q;  // rows r0 .. r0 + 3 in registers 4q .. 4q+3
+            if (!col_ok || r0 >= a.rows) continue;
+            const int64_t g0 = r0 / a.G;
+            const int64_t rl = (r0 + 3 < a.rows) ? r0 + 3 : a.rows - 1;
+            if (rl / a.G == g0) {
+                float m = v[4 * q];
+                for (int i = 1; i < 4 && r0 + i < a.rows; ++i) m = fmaxf(m, v[4 * q + i]);
+                atomicMax(yu + g0 * a.ldy + col, __float_as_uint(m));
+            } else {
+                for (int i = 0; i < 4 && r0 + i < a.rows; ++i)
+                    atomicMax(yu + ((r0 + i) / a.G) * a.ldy + col, __float_as_uint(v[4 * q + i]));
+            }
+        }
+    } else {
+        if (!col_ok) return;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int64_t row = rbase + 8 * (r >> 2) + (r & 3);
+            if (row < a.rows) {
+                if constexpr (EPI == EPI_F32) static_cast<float*>(a.y)[row * a.ldy + col] = v[r];
+                else static_cast<uint16_t*>(a.y)[row * a.ldy + col] = f32_to_bf16(v[r]);
+            }
+        }
+    }
+}
+
+template <int EPI, bool FAST_A, bool FAST_W>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
+    __shared__ float As[BK][BM + kPadF];
+    __shared__ float Bs[BK][BN + kPadF];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t row_t = (int64_t)blockIdx.x * BM;
+    const int col_t = blockIdx.y * BN;
+    const int lr = tid >> 2, lk = (tid & 3) * 8;  // loader: row / k offset
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+
+    for (int k0 = 0; k0 < a.K; k0 += BK) {
+        float va[8], vw[8];
+        load_a8<FAST_A>(a, row_t + lr, k0 + lk, va);
+        load_w8_f32<FAST_W>(a, col_t + lr, k0 + lk, vw);
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            As[lk + i][lr] = va[i];
+            Bs[lk + i][lr] = vw[i];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 2) {
+            const float av = As[kk + (lane >> 5)][wm * 32 + (lane & 31)];
+            const float bv = Bs[kk + (lane >> 5)][wn * 32 + (lane & 31)];
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
+        }
+    }
+    epilogue<EPI>(a, acc, row_t + wm * 32, col_t + wn * 32, lane, false);
+}
+
+template <int EPI, bool FAST_A, bool FAST_W>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t As[BM * kRowH];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * kRowH];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t row_t = (int64_t)blockIdx.x * BM;
+    const int col_t = blockIdx.y * BN;
+    const int lr = tid >> 2, lk = (tid & 3) * 8;
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+
+    for (int k0 = 0; k0 < a.K; k0 += BK) {
+        const uint4 qa = load_a8_bf16<FAST_A>(a, row_t + lr, k0 + lk);
+        const uint4 qw = load_w8_bf16<FAST_W>(a, col_t + lr, k0 + lk);
+        __syncthreads();
+        *reinterpret_cast<uint4*>(As + lr * kRowH + lk) = qa;
+        *reinterpret_cast<uint4*>(Bs + lr * kRowH + lk) = qw;
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 16) {
+            const bf16x8 av = *reinterpret_cast<const bf16x8*>(As + (wm * 32 + (lane & 31)) * kRowH + kk + 8 * (lane >> 5));
+            const bf16x8 bv = *reinterpret_cast<const bf16x8*>(Bs + (wn * 32 + (lane & 31)) * kRowH + kk + 8 * (lane >> 5));
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc, 0, 0, 0);
+        }
+    }
+    epilogue<EPI>(a, acc, row_t + wm * 32, col_t + wn * 32, lane, true);
+}
+
+// Launch one layer.  epi: EPI_F32 / EPI_BF16 / EPI_POOL.
+static void launch_layer(const GemmArgs& a, bool bf16, int epi, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div(a.rows, BM), (unsigned)ceil_div(a.N, BN)), block(256);
+    const bool fast_w = (a.K % 8 == 0) && aligned(a.W, 16);
+    bool fast_a;
+    if (a.a_bf16) fast_a = a.c1 == 0 && a.c0 == a.K && a.K % 8 == 0 && a.ld0 % 8 == 0 && aligned(a.x0, 16);
+    else fast_a = a.c1 == 0 && a.c0 == a.K && a.K % 8 == 0 && a.ld0 % 4 == 0 && aligned(a.x0, 16);
+#define MESO_GEMM(KERN, E)                                                                           \
+    do {                                                                                             \
+        if (fast_a && fast_w) KERN<E, true, true><<<grid, block, 0, s>>>(a);                         \
+        else if (fast_w) KERN<E, false, true><<<grid, block, 0, s>>>(a);                             \
+        else KERN<E, false, false><<<grid, block, 0, s>>>(a);                                       \
+    } while (0)
+    if (bf16) {
+        if (epi == EPI_F32) MESO_GEMM(gemm_bf16_kernel, EPI_F32);
+        else if (epi == EPI_BF16) MESO_GEMM(gemm_bf16_kernel, EPI_BF16);
+        else MESO_GEMM(gemm_bf16_kernel, EPI_POOL);
+    } else {
+        if (epi == EPI_F32) MESO_GEMM(gemm_f32_kernel, EPI_F32);
+        else if (epi == EPI_BF16) MESO_GEMM(gemm_f32_kernel, EPI_BF16);
+        else MESO_GEMM(gemm_f32_kernel, EPI_POOL);
+    }
+#undef MESO_GEMM
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace: two ping-pong buffers for the intermediate activations.
+static size_t mlp_ws_bytes(int64_t rows, int n_layers, const int32_t* dims, int dtype) {
+    if (n_layers <= 1 || rows <= 0) return 0;
+    int64_t w = 0;
+    for (int l = 1; l < n_layers; ++l) w = std::max<int64_t>(w, dims[l]);
+    const size_t elem = dtype == MESORASI_BF16 ? 2 : 4;
+    const size_t one = align256((size_t)rows * (size_t)w * elem);
+    return n_layers == 2 ? one : 2 * one;
+}
+
+static int check_mlp_spec(const char* who, int64_t rows, int n_layers, const int32_t* dims, int dtype) {
+    MESO_REQUIRE(rows >= 0, MESORASI_EINVAL, "%s: rows < 0", who);
+    MESO_REQUIRE(dims != nullptr, MESORASI_EINVAL, "%s: NULL dims", who);
+    MESO_REQUIRE(n_layers >= 1 && n_layers <= MESORASI_MAX_LAYERS, MESORASI_EUNSUPPORTED, "%s: n_layers = %d", who,
+                 n_layers);
+    for (int l = 0; l <= n_layers; ++l) {
+        MESO_REQUIRE(dims[l] >= 1, MESORASI_EINVAL, "%s: dims[%d] = %d < 1", who, l, dims[l]);
+        MESO_REQUIRE(dims[l] <= MESORASI_MAX_WIDTH, MESORASI_EUNSUPPORTED, "%s: dims[%d] = %d > %d", who, l, dims[l],
+                     MESORASI_MAX_WIDTH);
+    }
+    MESO_REQUIRE(dtype == MESORASI_F32 || dtype == MESORASI_BF16, MESORASI_EUNSUPPORTED, "%s: dtype %d", who, dtype);
+    return MESORASI_OK;
+}
+
+// The MLP proper, after validation.
+static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
+                   int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
+                   uint32_t relu_mask, int dtype, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, void* ws,
+                   hipStream_t s) {
+    const bool bf16 = dtype == MESORASI_BF16;
+    const size_t elem = bf16 ? 2 : 4;
+    int64_t w = 0;
+    for (int l = 1; l < n_layers; ++l) w = std::max<int64_t>(w, dims[l]);
+    const size_t one = align256((size_t)rows * (size_t)w * elem);
+    char* buf[2] = {static_cast<char*>(ws), static_cast<char*>(ws) + one};
+    if (pool_group > 0) {
+        const int rc = zero_rows_f32(static_cast<float*>(y), rows / pool_group, dims[n_layers], ld_y, s);
+        if (rc != MESORASI_OK) return rc;
+    }
+    for (int l = 0; l < n_layers; ++l) {
+        GemmArgs a{};
+        if (l == 0) {
+            a.x0 = x0; a.ld0 = ld0; a.x1 = x1; a.ld1 = ld1; a.c0 = c0; a.c1 = c1; a.a_bf16 = 0;
+        } else {
+            a.x0 = buf[(l - 1) & 1]; a.ld0 = dims[l]; a.x1 = nullptr; a.ld1 = 0; a.c0 = dims[l]; a.c1 = 0;
+            a.a_bf16 = bf16 ? 1 : 0;
+        }
+        a.rows = rows;
+        a.K = dims[l];
+        a.N = dims[l + 1];
+        a.W = W[l];
+        a.bias = bias ? bias[l] : nullptr;
+        a.relu = (relu_mask >> l) & 1u;
+        int epi;
+        if (l + 1 < n_layers) {
+            a.y = buf[l & 1];
+            a.ldy = dims[l + 1];
+            epi = bf16 ? EPI_BF16 : EPI_F32;
+        } else {
+            a.y = y;
+            a.ldy = ld_y;
+            a.G = pool_group;
+            epi = pool_group > 0 ? EPI_POOL : (out_dtype == MESORASI_BF16 ? EPI_BF16 : EPI_F32);
+        }
+        launch_layer(a, bf16, epi, s);
+        const int rc = after_launch("mesorasi_pointwise_mlp");
+        if (rc != MESORASI_OK) return rc;
+    }
+    return MESORASI_OK;
+}
+
+// ---------------------------------------------------------------------------
+// conventional module: neighbor feature matrix, then the MLP with pooling
+// ---------------------------------------------------------------------------
+
+__global__ void group_pointnet_kernel(const float* __restrict__ xyz, const float* __restrict__ feat, int cf,
+                                      int64_t ldf, const float* __restrict__ cxyz, const int32_t* __restrict__ nit,
+                                      int N, int M, int K, int64_t total_rows, float* __restrict__ nfm) {
+    const int cin = 3 + cf;
+    const int64_t n = total_rows * cin;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = e / cin;
+        const int c = (int)(e - row * cin);
+        const int64_t cm = row / K;   // global centroid (b*M + m)
+        const int64_t b = cm / M;
+        const int64_t j = b * N + nit[row];
+        nfm[e] = c < 3 ? xyz[j * 3 + c] - cxyz[cm * 3 + c] : feat[j * ldf + (c - 3)];
+    }
+}
+
+__global__ void group_edge_kernel(const float* __restrict__ f, int C, int64_t ldf, const int32_t* __restrict__ nit,
+                                  int N, int K, int64_t total_rows, float* __restrict__ nfm) {
+    const int cin = 2 * C;
+    const int64_t n = total_rows * cin;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = e / cin;
+        const int c = (int)(e - row * cin);
+        const int64_t i = row / K;    // global point (b*N + i)
+        const int64_t b = i / N;
+        const float fi = f[i * ldf + (c < C ? c : c - C)];
+        if (c < C) {
+            nfm[e] = fi;
+        } else {
+            const int64_t j = b * N + nit[row];
+            nfm[e] = f[j * ldf + (c - C)] - fi;
+        }
+    }
+}
+
+}  // namespace meso
+
+using namespace meso;
+
+extern "C" size_t mesorasi_pointwise_mlp_workspace(int64_t rows, int32_t n_layers, const int32_t* dims, int32_t dtype,
+                                                   int64_t pool_group) {
+    (void)pool_group;
+    if (check_mlp_spec("mesorasi_pointwise_mlp_workspace", rows, n_layers, dims, dtype) != MESORASI_OK) return 0;
+    return mlp_ws_bytes(rows, n_layers, dims, dtype);
+}
+
+extern "C" int mesorasi_pointwise_mlp(const float* x0, int32_t c0, int64_t ld0, const float* x1, int32_t c1,
+                                      int64_t ld1, int64_t rows, int32_t n_layers, const int32_t* dims,
+                                      const void* const* W, const float* const* bias, uint32_t relu_mask,
+                                      int32_t dtype, int32_t out_dtype, void* y, int64_t ld_y, int64_t pool_group,
+                                      void* ws, size_t ws_bytes, void* stream) {
+    const char* who = "mesorasi_pointwise_mlp";
+    int rc = check_mlp_spec(who, rows, n_layers, dims, dtype);
+    if (rc != MESORASI_OK) return rc;
+    MESO_REQUIRE(c0 >= 1 && c1 >= 0, MESORASI_EINVAL, "%s: c0 = %d, c1 = %d", who, c0, c1);
+    MESO_REQUIRE(ld0 >= c0 && (c1 == 0 || ld1 >= c1), MESORASI_EINVAL, "%s: leading dimension < width", who);
+    MESO_REQUIRE(dims[0] == c0 + c1, MESORASI_EINVAL, "%s: dims[0] = %d != c0 + c1 = %d", who, dims[0], c0 + c1);
+    MESO_REQUIRE(ld_y >= dims[n_layers], MESORASI_EINVAL, "%s: ld_y < dims[n_layers]", who);
+    MESO_REQUIRE(out_dtype == MESORASI_F32 || out_dtype == MESORASI_BF16, MESORASI_EUNSUPPORTED, "%s: out_dtype %d",
+                 who, out_dtype);
+    MESO_REQUIRE(pool_group >= 0, MESORASI_EINVAL, "%s: pool_group < 0", who);
+    if (pool_group > 0) {
+        MESO_REQUIRE(rows % pool_group == 0, MESORASI_EINVAL, "%s: rows %% pool_group != 0", who);
+        MESO_REQUIRE((relu_mask >> (n_layers - 1)) & 1u, MESORASI_EUNSUPPORTED, "%s: pooling needs a final ReLU", who);
+        MESO_REQUIRE(out_dtype == MESORASI_F32, MESORASI_EUNSUPPORTED, "%s: pooling needs out_dtype F32", who);
+    }
+    if (rows == 0) return MESORASI_OK;
+    MESO_REQUIRE(x0 && y && W, MESORASI_EINVAL, "%s: NULL x0, y or W", who);
+    MESO_REQUIRE(c1 == 0 || x1, MESORASI_EINVAL, "%s: NULL x1 with c1 > 0", who);
+    for (int l = 0; l < n_layers; ++l) MESO_REQUIRE(W[l] != nullptr, MESORASI_EINVAL, "%s: W[%d] is NULL", who, l);
+    const size_t need = mlp_ws_bytes(rows, n_layers, dims, dtype);
+    MESO_REQUIRE(ws_bytes >= need && (need == 0 || ws), MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who,
+                 ws_bytes, need);
+    MESO_REQUIRE(rows / BM < 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: too many rows", who);
+    return run_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, dtype, out_dtype, y, ld_y,
+                   pool_group, ws, as_stream(stream));
+}
+
+extern "C" size_t mesorasi_conventional_workspace(int64_t B, int64_t M, int32_t K, int32_t n_layers,
+                                                  const int32_t* dims, int32_t dtype) {
+    if (B < 0 || M < 0 || K < 1) return 0;
+    const int64_t rows = B * M * K;
+    if (check_mlp_spec("mesorasi_conventional_workspace", rows, n_layers, dims, dtype) != MESORASI_OK) return 0;
+    return align256((size_t)rows * (size_t)dims[0] * 4) + mlp_ws_bytes(rows, n_layers, dims, dtype);
+}
+
+extern "C" int mesorasi_conventional_module(const float* xyz, const float* feat, int32_t cf, int64_t ld_f,
+                                            const float* cxyz, const int32_t* nit, int64_t B, int64_t N, int64_t M,
+                                            int32_t K, int32_t grouping, int32_t n_layers, const int32_t* dims,
+                                            const void* const* W, const float* const* bias, uint32_t relu_mask,
+                                            int32_t dtype, float* out, int64_t ld_out, void* ws, size_t ws_bytes,
+                                            void* stream) {
+    const char* who = "mesorasi_conventional_module";
+    MESO_REQUIRE(B >= 0 && N >= 0 && M >= 0, MESORASI_EINVAL, "%s: negative size", who);
+    MESO_REQUIRE(K >= 1, MESORASI_EINVAL, "%s: K = %d < 1", who, K);
+    MESO_REQUIRE(grouping == 0 || grouping == 1, MESORASI_EINVAL, "%s: grouping = %d", who, grouping);
+    MESO_REQUIRE(cf >= 0, MESORASI_EINVAL, "%s: cf < 0", who);
+    const int64_t rows = B * M * K;
+    int rc = check_mlp_spec(who, rows, n_layers, dims, dtype);
+    if (rc != MESORASI_OK) return rc;
+    const int cin = grouping == 0 ? 3 + cf : 2 * cf;
+    MESO_REQUIRE(dims[0] == cin, MESORASI_EINVAL, "%s: dims[0] = %d, expected %d", who, dims[0], cin);
+    MESO_REQUIRE(ld_out >= dims[n_layers], MESORASI_EINVAL, "%s: ld_out < dims[n_layers]", who);
+    MESO_REQUIRE(cf == 0 || ld_f >= cf, MESORASI_EINVAL, "%s: ld_f < cf", who);
+    MESO_REQUIRE(grouping == 0 || (cf >= 1 && M == N), MESORASI_EINVAL, "%s: edge grouping needs cf >= 1 and M == N",
+                 who);
+    MESO_REQUIRE((relu_mask >> (n_layers - 1)) & 1u, MESORASI_EUNSUPPORTED, "%s: the last layer needs ReLU", who);
+    if (B == 0 || M == 0) return MESORASI_OK;
+    MESO_REQUIRE(N >= 1, MESORASI_EINVAL, "%s: N = 0 with M > 0", who);
+    MESO_REQUIRE(nit && out && W, MESORASI_EINVAL, "%s: NULL nit, out or W", who);
+    if (grouping == 0) MESO_REQUIRE(xyz && cxyz && (cf == 0 || feat), MESORASI_EINVAL, "%s: NULL xyz/cxyz/feat", who);
+    else MESO_REQUIRE(feat != nullptr, MESORASI_EINVAL, "%s: NULL feat", who);
+    for (int l = 0; l < n_layers; ++l) MESO_REQUIRE(W[l] != nullptr, MESORASI_EINVAL, "%s: W[%d] is NULL", who, l);
+    const size_t nfm_bytes = align256((size_t)rows * (size_t)cin * 4);
+    const size_t need = nfm_bytes + mlp_ws_bytes(rows, n_layers, dims, dtype);
+    MESO_REQUIRE(ws && ws_bytes >= need, MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who, ws_bytes, need);
+    MESO_REQUIRE(N <= 0x7fffffff && M <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: size", who);
+    hipStream_t s = as_stream(stream);
+    float* nfm = static_cast<float*>(ws);
+    const int64_t blocks = std::min<int64_t>(ceil_div(rows * cin, 256), 16384);
+    if (grouping == 0)
+        group_pointnet_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(xyz, feat, cf, ld_f, cxyz, nit, (int)N,
+                                                                           (int)M, K, rows, nfm);
+    else
+        group_edge_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(feat, cf, ld_f, nit, (int)N, K, rows, nfm);
+    rc = after_launch(who);
+    if (rc != MESORASI_OK) return rc;
+    return run_mlp(nfm, cin, cin, nullptr, 0, 0, rows, n_layers, dims, W, bias, relu_mask, dtype, MESORASI_F32, out,
+                   ld_out, K, static_cast<char*>(ws) + nfm_bytes, s);
+}

@@ -1,0 +1,237 @@
+"""torch.Tensor wrappers over the C ABI (argument marshalling only).
+
+Every function allocates its outputs with ``torch.empty`` on the input's
+device (unless ``out=`` is given), passes raw device pointers, leading
+dimensions and the current HIP stream, and raises on a non-zero status.
+All arithmetic happens in libmesorasi.so.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+
+import torch
+
+from . import _lib
+from ._lib import F32, BF16, check
+
+_vp = ctypes.c_void_p
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _rows(t: torch.Tensor, width: int | None = None):
+    """(pointer, leading dimension) of a [..., rows, C] tensor whose last dim
+    is contiguous and whose leading dims collapse to one row index."""
+    assert t.stride(-1) == 1, "last dimension must be contiguous"
+    ld = t.stride(-2) if t.dim() >= 2 else t.shape[-1]
+    # all leading dims must be row-contiguous multiples of ld
+    expect = ld * t.shape[-2] if t.dim() >= 2 else None
+    for d in range(t.dim() - 3, -1, -1):
+        assert t.stride(d) == expect, "leading dimensions must collapse into rows"
+        expect *= t.shape[d]
+    if width is not None:
+        assert t.shape[-1] >= width
+    return t.data_ptr(), ld
+
+
+def _check_xyz(x: torch.Tensor, name: str):
+    assert x.dtype == torch.float32 and x.is_contiguous() and x.dim() == 3 and x.shape[-1] == 3, \
+        f"{name} must be a contiguous float32 [B, N, 3] tensor"
+
+
+def fps(xyz: torch.Tensor, M: int, want_xyz: bool = True):
+    _check_xyz(xyz, "xyz")
+    B, N, _ = xyz.shape
+    idx = torch.empty((B, M), dtype=torch.int32, device=xyz.device)
+    cxyz = torch.empty((B, M, 3), dtype=torch.float32, device=xyz.device) if want_xyz else None
+    check(_lib.lib().mesorasi_fps(xyz.data_ptr(), B, N, M, idx.data_ptr(), _ptr(cxyz), _stream()), "fps")
+    return idx, cxyz
+
+
+def ball_query(xyz: torch.Tensor, qxyz: torch.Tensor, radius: float, K: int, want_cnt: bool = False,
+               out: torch.Tensor | None = None):
+    _check_xyz(xyz, "xyz")
+    _check_xyz(qxyz, "qxyz")
+    B, N, _ = xyz.shape
+    M = qxyz.shape[1]
+    nit = out if out is not None else torch.empty((B, M, K), dtype=torch.int32, device=xyz.device)
+    cnt = torch.empty((B, M), dtype=torch.int32, device=xyz.device) if want_cnt else None
+    check(_lib.lib().mesorasi_ball_query(xyz.data_ptr(), qxyz.data_ptr(), B, N, M, float(radius), K, nit.data_ptr(),
+                                         _ptr(cnt), _stream()), "ball_query")
+    return nit, cnt
+
+
+def knn(ref: torch.Tensor, query: torch.Tensor, K: int, want_dist: bool = False):
+    """ref [B, N, >=C], query [B, M, >=C] (last dim contiguous, may be
+    column slices of wider tensors); C = ref.shape[-1]."""
+    assert ref.dtype == torch.float32 and query.dtype == torch.float32
+    B, N, C = ref.shape
+    M = query.shape[1]
+    pr, ldr = _rows(ref)
+    pq, ldq = _rows(query)
+    nit = torch.empty((B, M, K), dtype=torch.int32, device=ref.device)
+    dist = torch.empty((B, M, K), dtype=torch.float32, device=ref.device) if want_dist else None
+    check(_lib.lib().mesorasi_knn(pr, ldr, pq, ldq, B, N, M, C, K, nit.data_ptr(), _ptr(dist), _stream()), "knn")
+    return nit, dist
+
+
+class MLPParams:
+    """Weights of one shared MLP on the device, plus the host pointer arrays
+    the ABI takes.  W[l] is [C_out, C_in] (torch Linear layout)."""
+
+    def __init__(self, Ws, bs, dtype: int = F32, device="cuda"):
+        self.dtype = dtype
+        self.dims = [int(Ws[0].shape[1])] + [int(W.shape[0]) for W in Ws]
+        self.n = len(Ws)
+        self.W32 = [torch.as_tensor(W, dtype=torch.float32).to(device).contiguous() for W in Ws]
+        self.b = [None if b is None else torch.as_tensor(b, dtype=torch.float32).to(device).contiguous() for b in bs]
+        if dtype == BF16:
+            self.W = [cast_bf16(W) for W in self.W32]
+        else:
+            self.W = self.W32
+        self._dims_c = (ctypes.c_int32 * (self.n + 1))(*self.dims)
+        self._W_c = (_vp * self.n)(*[W.data_ptr() for W in self.W])
+        self._b_c = (_vp * self.n)(*[None if b is None else b.data_ptr() for b in self.b])
+
+    @property
+    def c_out(self):
+        return self.dims[-1]
+
+    def abi(self):
+        return (ctypes.cast(self._dims_c, _vp), ctypes.cast(self._W_c, _vp), ctypes.cast(self._b_c, _vp))
+
+
+def mlp_workspace_bytes(rows: int, p: MLPParams, pool_group: int = 0) -> int:
+    d, _, _ = p.abi()
+    return int(_lib.lib().mesorasi_pointwise_mlp_workspace(rows, p.n, d, p.dtype, pool_group))
+
+
+def pointwise_mlp(x0: torch.Tensor, p: MLPParams, x1: torch.Tensor | None = None, relu_mask: int | None = None,
+                  out_dtype: int = F32, pool_group: int = 0, out: torch.Tensor | None = None,
+                  ws: torch.Tensor | None = None):
+    """MLP on the rows of [x0 | x1].  x0 [..., R, c0], x1 [..., R, c1].
+    pool_group > 0 returns the column max over each group of rows."""
+    p0, ld0 = _rows(x0)
+    c0 = x0.shape[-1]
+    if x1 is not None:
+        p1, ld1 = _rows(x1)
+        c1 = x1.shape[-1]
+    else:
+        p1, ld1, c1 = None, 0, 0
+    rows = math.prod(x0.shape[:-1])
+    if relu_mask is None:
+        relu_mask = (1 << p.n) - 1
+    lead = tuple(x0.shape[:-1])
+    if out is None:
+        dt = torch.float32 if out_dtype == F32 else torch.bfloat16
+        if pool_group:
+            out = torch.empty((rows // pool_group, p.c_out), dtype=dt, device=x0.device)
+        else:
+            out = torch.empty(lead + (p.c_out,), dtype=dt, device=x0.device)
+    py, ldy = _rows(out)
+    need = mlp_workspace_bytes(rows, p, pool_group)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=x0.device)
+    d, W, b = p.abi()
+    check(_lib.lib().mesorasi_pointwise_mlp(p0, c0, ld0, p1, c1, ld1, rows, p.n, d, W, b, relu_mask, p.dtype,
+                                            out_dtype, py, ldy, pool_group, ws.data_ptr(), ws.numel(), _stream()),
+          "pointwise_mlp")
+    return out
+
+
+def aggregate_max(pft: torch.Tensor, nit: torch.Tensor, cidx: torch.Tensor | None = None,
+                  cfeat: torch.Tensor | None = None, sign: int = -1, relu: bool = False,
+                  out: torch.Tensor | None = None):
+    """pft [B, N, >=C] float32 or bfloat16; nit [B, M, K] int32;
+    cidx [B, M] int32 or cfeat [B, M, >=C] (same dtype as pft)."""
+    B, N, C = pft.shape
+    M, K = nit.shape[1], nit.shape[2]
+    dt = F32 if pft.dtype == torch.float32 else BF16
+    pp, ldp = _rows(pft)
+    if cfeat is not None:
+        assert cfeat.dtype == pft.dtype
+        pc, ldc = _rows(cfeat)
+    else:
+        pc, ldc = None, 0
+    if out is None:
+        out = torch.empty((B, M, C), dtype=torch.float32, device=pft.device)
+    po, ldo = _rows(out)
+    assert nit.is_contiguous() and nit.dtype == torch.int32
+    check(_lib.lib().mesorasi_aggregate_max(pp, ldp, dt, nit.data_ptr(), B, N, M, K, C, _ptr(cidx), pc, ldc, sign,
+                                            1 if relu else 0, po, ldo, _stream()), "aggregate_max")
+    return out
+
+
+def conventional_workspace_bytes(B: int, M: int, K: int, p: MLPParams) -> int:
+    d, _, _ = p.abi()
+    return int(_lib.lib().mesorasi_conventional_workspace(B, M, K, p.n, d, p.dtype))
+
+
+def conventional_module(nit: torch.Tensor, p: MLPParams, xyz: torch.Tensor | None = None,
+                        feat: torch.Tensor | None = None, cxyz: torch.Tensor | None = None, grouping: int = 0,
+                        relu_mask: int | None = None, out: torch.Tensor | None = None,
+                        ws: torch.Tensor | None = None):
+    """grouping 0: [xyz_j - cxyz_c | feat_j] (PointNet++); grouping 1:
+    [f_i | f_j - f_i] with f = feat (DGCNN edge features)."""
+    B, M, K = nit.shape
+    if grouping == 0:
+        N = xyz.shape[1]
+    else:
+        N = feat.shape[1]
+    cf = 0 if feat is None else feat.shape[-1]
+    pf, ldf = _rows(feat) if feat is not None else (None, max(cf, 1))
+    if relu_mask is None:
+        relu_mask = (1 << p.n) - 1
+    if out is None:
+        out = torch.empty((B, M, p.c_out), dtype=torch.float32, device=nit.device)
+    po, ldo = _rows(out)
+    need = conventional_workspace_bytes(B, M, K, p)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=nit.device)
+    d, W, b = p.abi()
+    check(_lib.lib().mesorasi_conventional_module(_ptr(xyz), pf, cf, ldf, _ptr(cxyz), nit.data_ptr(), B, N, M, K,
+                                                  grouping, p.n, d, W, b, relu_mask, p.dtype, po, ldo,
+                                                  ws.data_ptr(), ws.numel(), _stream()), "conventional_module")
+    return out
+
+
+def interpolate3(xyz_dst: torch.Tensor, xyz_src: torch.Tensor, f_src: torch.Tensor,
+                 out: torch.Tensor | None = None):
+    _check_xyz(xyz_dst, "xyz_dst")
+    _check_xyz(xyz_src, "xyz_src")
+    B, Nd, _ = xyz_dst.shape
+    Ns = xyz_src.shape[1]
+    C = f_src.shape[-1]
+    ps, lds = _rows(f_src)
+    if out is None:
+        out = torch.empty((B, Nd, C), dtype=torch.float32, device=f_src.device)
+    po, ldo = _rows(out)
+    check(_lib.lib().mesorasi_interpolate3(xyz_dst.data_ptr(), xyz_src.data_ptr(), ps, lds, B, Nd, Ns, C, po, ldo,
+                                           _stream()), "interpolate3")
+    return out
+
+
+def cast_bf16(x: torch.Tensor) -> torch.Tensor:
+    """float32 -> bfloat16 (round to nearest even) on the device."""
+    assert x.dtype == torch.float32 and x.is_contiguous()
+    y = torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
+    check(_lib.lib().mesorasi_cast_bf16(x.data_ptr(), x.numel(), y.data_ptr(), _stream()), "cast_bf16")
+    return y
+
+
+def edgeconv_fold(W: torch.Tensor, b: torch.Tensor | None):
+    """W [C_out, 2C] -> ([W1 - W2 ; W2] [2 C_out, C], [b ; 0])."""
+    Cout, C2 = W.shape
+    C = C2 // 2
+    Wo = torch.empty((2 * Cout, C), dtype=torch.float32, device=W.device)
+    bo = torch.empty((2 * Cout,), dtype=torch.float32, device=W.device)
+    check(_lib.lib().mesorasi_edgeconv_fold(W.data_ptr(), _ptr(b), C, Cout, Wo.data_ptr(), bo.data_ptr(), _stream()),
+          "edgeconv_fold")
+    return Wo, bo

@@ -1,0 +1,159 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, it
+exports every entry point include/mesorasi.h declares, and argument
+validation returns the documented status before any HIP call is made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2008_06967_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mesorasi.h")
+
+NULL = None
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation first
+
+
+def declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mesorasi_\w+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported_and_bound():
+    L = _lib.lib()
+    names = declared()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(_lib.SIGNATURES)
+
+
+def test_version_and_strings():
+    L = _lib.lib()
+    assert L.mesorasi_version() == 1
+    assert L.mesorasi_strerror(0) == b"ok"
+    assert L.mesorasi_strerror(-1) == b"invalid argument"
+    assert L.mesorasi_strerror(-4) == b"workspace too small"
+
+
+def st(fn, *args):
+    return getattr(_lib.lib(), fn)(*args)
+
+
+def test_fps_validation():
+    assert st("mesorasi_fps", FAKE, 1, 10, 11, FAKE, NULL, NULL) == _lib.EINVAL          # M > N
+    assert st("mesorasi_fps", FAKE, -1, 10, 5, FAKE, NULL, NULL) == _lib.EINVAL          # B < 0
+    assert st("mesorasi_fps", NULL, 1, 10, 5, FAKE, NULL, NULL) == _lib.EINVAL           # NULL xyz
+    assert st("mesorasi_fps", FAKE, 1, 70000, 5, FAKE, NULL, NULL) == _lib.EUNSUPPORTED  # N too large
+    assert st("mesorasi_fps", NULL, 0, 10, 5, NULL, NULL, NULL) == _lib.OK               # empty batch
+    st("mesorasi_fps", FAKE, 1, 10, 11, FAKE, NULL, NULL)
+    assert b"M = 11" in _lib.lib().mesorasi_last_error()
+
+
+def test_ball_query_validation():
+    f = "mesorasi_ball_query"
+    assert st(f, FAKE, FAKE, 1, 10, 5, 0.2, 0, FAKE, NULL, NULL) == _lib.EINVAL              # K < 1
+    assert st(f, FAKE, FAKE, 1, 10, 5, -0.2, 4, FAKE, NULL, NULL) == _lib.EINVAL             # radius <= 0
+    assert st(f, FAKE, FAKE, 1, 10, 5, float("nan"), 4, FAKE, NULL, NULL) == _lib.EINVAL
+    assert st(f, FAKE, FAKE, 1, 10, 5, float("inf"), 4, FAKE, NULL, NULL) == _lib.EINVAL
+    assert st(f, FAKE, FAKE, 1, 10, 5, 0.2, 2000, FAKE, NULL, NULL) == _lib.EUNSUPPORTED
+    assert st(f, FAKE, FAKE, 1, 0, 5, 0.2, 4, FAKE, NULL, NULL) == _lib.EINVAL               # N = 0 < M
+    assert st(f, NULL, FAKE, 1, 10, 5, 0.2, 4, FAKE, NULL, NULL) == _lib.EINVAL
+    assert st(f, NULL, NULL, 1, 10, 0, 0.2, 4, NULL, NULL, NULL) == _lib.OK                  # M = 0
+
+
+def test_knn_validation():
+    f = "mesorasi_knn"
+    assert st(f, FAKE, 3, FAKE, 3, 1, 10, 10, 3, 11, FAKE, NULL, NULL) == _lib.EINVAL        # K > N
+    assert st(f, FAKE, 2, FAKE, 3, 1, 10, 10, 3, 4, FAKE, NULL, NULL) == _lib.EINVAL         # ld < C
+    assert st(f, FAKE, 3, FAKE, 3, 1, 100, 10, 3, 65, FAKE, NULL, NULL) == _lib.EUNSUPPORTED # K > 64
+    assert st(f, FAKE, 300, FAKE, 300, 1, 100, 10, 300, 4, FAKE, NULL, NULL) == _lib.EUNSUPPORTED  # C > 128
+    assert st(f, FAKE, 3, FAKE, 3, 1, 10, 10, 0, 4, FAKE, NULL, NULL) == _lib.EINVAL         # C < 1
+
+
+def _mlp_args(dims):
+    d = (ctypes.c_int32 * len(dims))(*dims)
+    W = (ctypes.c_void_p * (len(dims) - 1))(*([0x1000] * (len(dims) - 1)))
+    b = (ctypes.c_void_p * (len(dims) - 1))()
+    return ctypes.cast(d, ctypes.c_void_p), ctypes.cast(W, ctypes.c_void_p), ctypes.cast(b, ctypes.c_void_p)
+
+
+def test_mlp_validation_and_workspace():
+    L = _lib.lib()
+    d, W, b = _mlp_args([3, 64, 64, 128])
+    f = "mesorasi_pointwise_mlp"
+    # dims[0] != c0 + c1
+    assert st(f, FAKE, 4, 4, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 128, 0, NULL, 0, NULL) == _lib.EINVAL
+    # pooling without final ReLU
+    assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, d, W, b, 3, 0, 0, FAKE, 128, 5, FAKE, 1 << 20, NULL) == \
+        _lib.EUNSUPPORTED
+    # rows % pool_group
+    assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 128, 3, FAKE, 1 << 20, NULL) == _lib.EINVAL
+    # workspace too small
+    need = L.mesorasi_pointwise_mlp_workspace(10, 3, d, 0, 0)
+    assert need > 0
+    assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 128, 0, FAKE, need - 1, NULL) == \
+        _lib.EWORKSPACE
+    # ld_y < width
+    assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 64, 0, FAKE, need, NULL) == _lib.EINVAL
+    # too many layers
+    d9, W9, b9 = _mlp_args([4] * 10)
+    assert st(f, FAKE, 4, 4, NULL, 0, 0, 10, 9, d9, W9, b9, 0, 0, 0, FAKE, 4, 0, NULL, 0, NULL) == \
+        _lib.EUNSUPPORTED
+    # one layer needs no workspace; two need one buffer, three need two
+    d1, _, _ = _mlp_args([3, 8])
+    assert L.mesorasi_pointwise_mlp_workspace(100, 1, d1, 0, 0) == 0
+    d2, _, _ = _mlp_args([3, 8, 8])
+    d3, _, _ = _mlp_args([3, 8, 8, 8])
+    one = L.mesorasi_pointwise_mlp_workspace(100, 2, d2, 0, 0)
+    assert one >= 100 * 8 * 4 and L.mesorasi_pointwise_mlp_workspace(100, 3, d3, 0, 0) == 2 * one
+    assert L.mesorasi_pointwise_mlp_workspace(100, 2, d2, 1, 0) < one   # bf16 activations are half the size
+    assert st(f, NULL, 3, 3, NULL, 0, 0, 0, 3, d, W, b, 7, 0, 0, NULL, 128, 0, NULL, 0, NULL) == _lib.OK  # rows = 0
+
+
+def test_aggregate_validation():
+    f = "mesorasi_aggregate_max"
+    assert st(f, FAKE, 64, 0, FAKE, 1, 10, 5, 4, 64, FAKE, FAKE, 64, -1, 0, FAKE, 64, NULL) == _lib.EINVAL  # both
+    assert st(f, FAKE, 64, 0, FAKE, 1, 10, 5, 4, 64, NULL, NULL, 0, 2, 0, FAKE, 64, NULL) == _lib.EINVAL    # sign
+    assert st(f, FAKE, 32, 0, FAKE, 1, 10, 5, 4, 64, NULL, NULL, 0, -1, 0, FAKE, 64, NULL) == _lib.EINVAL   # ld
+    assert st(f, FAKE, 64, 7, FAKE, 1, 10, 5, 4, 64, NULL, NULL, 0, -1, 0, FAKE, 64, NULL) == \
+        _lib.EUNSUPPORTED                                                                                  # dtype
+    assert st(f, NULL, 64, 0, FAKE, 1, 10, 5, 4, 64, NULL, NULL, 0, -1, 0, FAKE, 64, NULL) == _lib.EINVAL
+
+
+def test_conventional_validation_and_workspace():
+    L = _lib.lib()
+    d, W, b = _mlp_args([3, 64, 64, 128])
+    f = "mesorasi_conventional_module"
+    # grouping 1 needs M == N
+    assert st(f, NULL, FAKE, 3, 3, NULL, FAKE, 1, 10, 5, 4, 1, 3, d, W, b, 7, 0, FAKE, 128, FAKE, 1 << 30,
+              NULL) == _lib.EINVAL
+    # dims[0] inconsistent with grouping 0 and cf = 2
+    assert st(f, FAKE, FAKE, 2, 2, FAKE, FAKE, 1, 10, 5, 4, 0, 3, d, W, b, 7, 0, FAKE, 128, FAKE, 1 << 30,
+              NULL) == _lib.EINVAL
+    need = L.mesorasi_conventional_workspace(1, 5, 4, 3, d, 0)
+    assert need >= 5 * 4 * 3 * 4
+    assert st(f, FAKE, NULL, 0, 1, FAKE, FAKE, 1, 10, 5, 4, 0, 3, d, W, b, 7, 0, FAKE, 128, FAKE, need - 1,
+              NULL) == _lib.EWORKSPACE
+    assert st(f, FAKE, NULL, 0, 1, FAKE, FAKE, 1, 10, 5, 4, 0, 3, d, W, b, 3, 0, FAKE, 128, FAKE, need,
+              NULL) == _lib.EUNSUPPORTED   # last layer without ReLU
+
+
+def test_misc_validation():
+    assert st("mesorasi_interpolate3", FAKE, FAKE, FAKE, 8, 1, 10, 2, 8, FAKE, 8, NULL) == _lib.EINVAL  # Ns < 3
+    assert st("mesorasi_cast_bf16", FAKE, -1, FAKE, NULL) == _lib.EINVAL
+    assert st("mesorasi_cast_bf16", NULL, 0, NULL, NULL) == _lib.OK
+    assert st("mesorasi_edgeconv_fold", FAKE, NULL, 0, 4, FAKE, FAKE, NULL) == _lib.EINVAL
+
+
+def test_product_path_does_not_touch_the_oracle():
+    """The HIP path's sources never import, load or name the oracle."""
+    pkg = os.path.join(ROOT, "paper_2008_06967_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".h", ".cpp")):
+                src = open(os.path.join(dirpath, fn)).read()
+                assert "import oracle" not in src and "from oracle" not in src and "liboracle" not in src, fn

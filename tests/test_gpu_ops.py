@@ -1,0 +1,344 @@
+"""GPU parity of every C-ABI entry point against the CPU oracle, on seeded
+inputs from the shared generators.
+
+Bars: FPS indices, ball-query and kNN neighbor tables, and aggregation of an
+identical PFT are bit-exact (values compared as numbers, so +0 == -0);
+MLP features are within a normwise relative error of 1e-4 (fp32) or 2e-2
+(bf16): max|gpu - oracle| / max|oracle| per output tensor.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2008_06967_amd import ops, synth
+from paper_2008_06967_amd._lib import F32, BF16
+
+pytestmark = pytest.mark.gpu
+
+TOL = {F32: 1e-4, BF16: 2e-2}
+
+
+def normwise(g, r):
+    g, r = np.asarray(g, np.float64), np.asarray(r, np.float64)
+    return float(np.max(np.abs(g - r)) / max(np.max(np.abs(r)), 1e-30))
+
+
+def dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return t if dtype is None else t.to(dtype)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def g(stream):
+    return synth.rng(77, stream)
+
+
+# ----------------------------------------------------------------------------
+# FPS
+# ----------------------------------------------------------------------------
+
+FPS_CASES = [
+    ("tiny", 2, 5, 5, "normal"),
+    ("one", 3, 1, 1, "normal"),
+    ("ragged", 3, 100, 37, "normal"),
+    ("grid_ties", 2, 300, 300, "grid"),
+    ("dups", 2, 700, 500, "dups"),
+    ("sa_module", 1, 1024, 512, "cube"),
+    ("cls_sa2", 4, 512, 128, "mesh"),
+    ("seg_sa1", 2, 4096, 1024, "normal"),
+    ("n2000", 2, 2000, 700, "normal"),
+    ("n9000", 1, 9000, 300, "normal"),
+    ("lidar_sa1", 1, 16384, 4096, "lidar"),
+    ("n20000", 1, 20000, 64, "normal"),
+]
+
+
+def _points(kind, B, N, r):
+    if kind == "grid":
+        return r.integers(0, 4, size=(B, N, 3)).astype(np.float32)
+    if kind == "dups":
+        base = r.standard_normal((B, N // 4, 3)).astype(np.float32)
+        return base[:, r.integers(0, N // 4, N)]
+    if kind == "cube":
+        return synth.uniform_cube(r, B, N)
+    if kind == "mesh":
+        return synth.mesh_surfaces(r, B, N)
+    if kind == "lidar":
+        return synth.lidar_scene(r, B, N)
+    return r.standard_normal((B, N, 3)).astype(np.float32)
+
+
+@pytest.mark.parametrize("name,B,N,M,kind", FPS_CASES, ids=[c[0] for c in FPS_CASES])
+def test_fps_bit_exact(gpu, name, B, N, M, kind):
+    x = _points(kind, B, N, g(1))
+    ri, rc = O.fps(x, M)
+    idx, cxyz = ops.fps(dev(x), M)
+    assert np.array_equal(host(idx), ri)
+    assert np.array_equal(host(cxyz), rc)
+
+
+# ----------------------------------------------------------------------------
+# ball query
+# ----------------------------------------------------------------------------
+
+BQ_CASES = [
+    ("sa_module", 1, 1024, 512, 0.2, 32, "cube"),
+    ("cls_sa1", 4, 1024, 512, 0.2, 32, "mesh"),
+    ("cls_sa2", 4, 512, 128, 0.4, 64, "mesh"),
+    ("ragged", 3, 77, 13, 0.7, 5, "normal"),
+    ("k1", 2, 200, 50, 0.5, 1, "normal"),
+    ("k100", 2, 300, 40, 1.5, 100, "normal"),
+    ("nohit", 1, 50, 10, 1e-3, 8, "normal"),
+    ("grid_boundary", 1, 64, 64, 1.0, 16, "grid"),
+    ("lidar_sa1", 1, 16384, 4096, 0.1, 64, "lidar"),
+]
+
+
+@pytest.mark.parametrize("name,B,N,M,r,K,kind", BQ_CASES, ids=[c[0] for c in BQ_CASES])
+def test_ball_query_bit_exact(gpu, name, B, N, M, r, K, kind):
+    rr = g(2)
+    x = _points(kind, B, N, rr)
+    if kind in ("grid", "normal") and name != "nohit":
+        q = x[:, rr.choice(N, M, replace=False)]
+    elif name == "nohit":
+        q = rr.standard_normal((B, M, 3)).astype(np.float32) + 50.0
+    else:
+        _, q = O.fps(x, M)
+    rn, rc, _ = O.ball_query(x, q, r, K)
+    nit, cnt = ops.ball_query(dev(x), dev(q), r, K, want_cnt=True)
+    assert np.array_equal(host(nit), rn)
+    assert np.array_equal(host(cnt), rc)
+
+
+# ----------------------------------------------------------------------------
+# kNN
+# ----------------------------------------------------------------------------
+
+KNN_CASES = [
+    ("dgcnn_l1", 2, 1024, 1024, 3, 20, "self"),
+    ("dgcnn_l2", 2, 1024, 1024, 64, 20, "self"),
+    ("dgcnn_l4", 1, 1024, 1024, 128, 20, "self"),
+    ("ragged", 3, 100, 37, 5, 7, "other"),
+    ("k1", 2, 70, 70, 3, 1, "self"),
+    ("k64", 1, 200, 50, 16, 64, "other"),
+    ("ties", 2, 150, 150, 3, 10, "grid"),
+    ("interp_like", 2, 256, 1024, 3, 3, "other"),
+]
+
+
+@pytest.mark.parametrize("name,B,N,M,C,K,kind", KNN_CASES, ids=[c[0] for c in KNN_CASES])
+def test_knn_bit_exact(gpu, name, B, N, M, C, K, kind):
+    rr = g(3)
+    if kind == "grid":
+        ref = rr.integers(0, 3, size=(B, N, C)).astype(np.float32)
+    else:
+        ref = rr.standard_normal((B, N, C)).astype(np.float32)
+    query = ref if kind in ("self", "grid") else rr.standard_normal((B, M, C)).astype(np.float32)
+    rn, rd = O.knn(ref, query, K)
+    nit, dist = ops.knn(dev(ref), dev(query), K, want_dist=True)
+    assert np.array_equal(host(nit), rn)
+    assert np.array_equal(host(dist), rd)
+
+
+def test_knn_strided_columns(gpu):
+    """Reference/query as a column slice of a wider buffer (leading dim > C)."""
+    rr = g(4)
+    wide = rr.standard_normal((2, 300, 40)).astype(np.float32)
+    rn, _ = O.knn(wide[:, :, 8:24], wide[:, :, 8:24], 20)
+    t = dev(wide)
+    nit, _ = ops.knn(t[:, :, 8:24], t[:, :, 8:24], 20)
+    assert np.array_equal(host(nit), rn)
+
+
+# ----------------------------------------------------------------------------
+# aggregation (identical PFT on both sides: bit-exact)
+# ----------------------------------------------------------------------------
+
+AGG_CASES = [
+    ("sa_module", 1, 1024, 512, 32, 128, "f32", "cidx"),
+    ("cls_sa2", 2, 512, 128, 64, 256, "f32", "cidx"),
+    ("lidar_bf16", 1, 4096, 1024, 64, 128, "bf16", "cidx"),
+    ("dgcnn_add_relu", 2, 1024, 1024, 20, 64, "f32", "cfeat"),
+    ("dgcnn_bf16", 1, 300, 300, 20, 64, "bf16", "cfeat"),
+    ("odd_channels", 2, 100, 33, 7, 13, "f32", "cidx"),
+    ("odd_bf16", 2, 100, 33, 7, 13, "bf16", "cidx"),
+    ("wide", 1, 64, 16, 32, 1024, "f32", "cidx"),
+    ("none", 2, 80, 20, 5, 24, "f32", "none"),
+    ("k1", 2, 50, 50, 1, 8, "f32", "cidx"),
+]
+
+
+@pytest.mark.parametrize("name,B,N,M,K,C,dt,cen", AGG_CASES, ids=[c[0] for c in AGG_CASES])
+def test_aggregate_bit_exact(gpu, name, B, N, M, K, C, dt, cen):
+    rr = g(5)
+    pft = (rr.standard_normal((B, N, C)) * 3).astype(np.float32)
+    if dt == "bf16":
+        pft = O.bf16_round(pft)
+    nit = rr.integers(0, N, (B, M, K)).astype(np.int32)
+    cidx = rr.integers(0, N, (B, M)).astype(np.int32) if cen == "cidx" else None
+    cfeat = O.bf16_round(rr.standard_normal((B, M, C)).astype(np.float32)) if cen == "cfeat" else None
+    sign = +1 if cen == "cfeat" else -1
+    relu = cen == "cfeat"
+    ref = O.aggregate_max(pft, nit, cidx=cidx, cfeat=cfeat, sign=sign, relu=relu)
+    tdt = torch.float32 if dt == "f32" else torch.bfloat16
+    out = ops.aggregate_max(dev(pft).to(tdt), dev(nit), cidx=None if cidx is None else dev(cidx),
+                            cfeat=None if cfeat is None else dev(cfeat).to(tdt), sign=sign, relu=relu)
+    assert np.array_equal(host(out), ref)
+
+
+def test_aggregate_strided_pft_and_out(gpu):
+    """DGCNN layout: PFT = [A | Bm] in one [N, 2C] table, output into a
+    column slice of a wider concat buffer."""
+    rr = g(6)
+    B, N, K, C = 2, 200, 20, 64
+    P = rr.standard_normal((B, N, 2 * C)).astype(np.float32)
+    nit = rr.integers(0, N, (B, N, K)).astype(np.int32)
+    ref = O.aggregate_max(np.ascontiguousarray(P[..., C:]), nit, cfeat=np.ascontiguousarray(P[..., :C]), sign=+1,
+                          relu=True)
+    t = dev(P)
+    cat = torch.full((B, N, 5 * C), 7.0, device="cuda")
+    ops.aggregate_max(t[..., C:], dev(nit), cfeat=t[..., :C], sign=+1, relu=True, out=cat[..., 2 * C:3 * C])
+    c = host(cat)
+    assert np.array_equal(c[..., 2 * C:3 * C], ref)
+    assert (c[..., :2 * C] == 7.0).all() and (c[..., 3 * C:] == 7.0).all()
+
+
+# ----------------------------------------------------------------------------
+# MLP
+# ----------------------------------------------------------------------------
+
+MLP_CASES = [
+    ("sa1_f32", 1000, [3], [64, 64, 128], F32),
+    ("sa2_two_src", 517, [3, 128], [128, 128, 256], F32),
+    ("sa3_groupall", 256, [3, 256], [256, 512, 1024], F32),
+    ("fc_head", 32, [1024], [512, 256, 40], F32),
+    ("seg_head", 300, [128], [128, 13], F32),
+    ("odd_widths", 77, [5, 2], [33, 17, 9], F32),
+    ("sa1_bf16", 1000, [3], [32, 32, 64], BF16),
+    ("sa2_bf16_two_src", 333, [3, 64], [64, 64, 128], BF16),
+    ("fp_bf16", 200, [256, 128], [256, 256], BF16),
+    ("odd_bf16", 45, [6, 1], [20, 12], BF16),
+]
+
+
+def _weights(rr, dims):
+    Ws = [(rr.standard_normal((dims[i + 1], dims[i])) * np.sqrt(2.0 / dims[i])).astype(np.float32)
+          for i in range(len(dims) - 1)]
+    bs = [rr.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(len(dims) - 1)]
+    return Ws, bs
+
+
+@pytest.mark.parametrize("name,rows,srcs,widths,dt", MLP_CASES, ids=[c[0] for c in MLP_CASES])
+def test_mlp_parity(gpu, name, rows, srcs, widths, dt):
+    rr = g(7)
+    xs = [rr.standard_normal((rows, c)).astype(np.float32) for c in srcs]
+    dims = [sum(srcs)] + widths
+    Ws, bs = _weights(rr, dims)
+    relu_mask = (1 << (len(widths) - 1)) - 1 if name in ("fc_head", "seg_head") else (1 << len(widths)) - 1
+    ref = O.mlp(np.concatenate(xs, -1), Ws, bs, relu_mask=relu_mask, bf16=dt == BF16)
+    p = ops.MLPParams(Ws, bs, dtype=dt)
+    y = ops.pointwise_mlp(dev(xs[0]), p, x1=dev(xs[1]) if len(xs) > 1 else None, relu_mask=relu_mask)
+    assert normwise(host(y), ref) <= TOL[dt]
+    if dt == BF16:   # stored activations are bf16 values
+        yb = ops.pointwise_mlp(dev(xs[0]), p, x1=dev(xs[1]) if len(xs) > 1 else None, relu_mask=relu_mask,
+                               out_dtype=BF16)
+        assert yb.dtype == torch.bfloat16
+        assert np.array_equal(host(yb.float()), host(y))
+
+
+@pytest.mark.parametrize("dt", [F32, BF16])
+@pytest.mark.parametrize("G", [128, 20, 64, 1])
+def test_mlp_pooled(gpu, dt, G):
+    rr = g(8)
+    groups = 7
+    rows = G * groups
+    x = rr.standard_normal((rows, 10)).astype(np.float32)
+    Ws, bs = _weights(rr, [10, 48, 80])
+    ref = O.rowgroup_max(O.mlp(x, Ws, bs, bf16=dt == BF16).reshape(groups, G, 80), G)
+    p = ops.MLPParams(Ws, bs, dtype=dt)
+    y = ops.pointwise_mlp(dev(x), p, pool_group=G)
+    assert normwise(host(y).reshape(groups, 80), ref.reshape(groups, 80)) <= TOL[dt]
+
+
+def test_mlp_strided_input(gpu):
+    rr = g(9)
+    wide = rr.standard_normal((100, 50)).astype(np.float32)
+    Ws, bs = _weights(rr, [20, 16])
+    ref = O.mlp(wide[:, 10:30], Ws, bs)
+    t = dev(wide)
+    y = ops.pointwise_mlp(t[:, 10:30], ops.MLPParams(Ws, bs))
+    assert normwise(host(y), ref) <= 1e-4
+
+
+# ----------------------------------------------------------------------------
+# conventional module, interpolation, small entry points
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dt", [F32, BF16])
+def test_conventional_pointnet(gpu, dt):
+    rr = g(10)
+    B, N, M, K, cf = 2, 512, 128, 32, 13
+    xyz = synth.mesh_surfaces(rr, B, N)
+    feat = rr.standard_normal((B, N, cf)).astype(np.float32)
+    idx, cxyz = O.fps(xyz, M)
+    nit, _, _ = O.ball_query(xyz, cxyz, 0.4, K)
+    Ws, bs = _weights(rr, [3 + cf, 32, 48])
+    h = O.mlp(O.group_pointnet(xyz, feat, cxyz, nit), Ws, bs, bf16=dt == BF16)
+    ref = O.rowgroup_max(h.reshape(B, M * K, 48), K)
+    out = ops.conventional_module(dev(nit), ops.MLPParams(Ws, bs, dtype=dt), xyz=dev(xyz), feat=dev(feat),
+                                  cxyz=dev(cxyz), grouping=0)
+    assert normwise(host(out), ref) <= TOL[dt]
+
+
+def test_conventional_edge(gpu):
+    rr = g(11)
+    B, N, K, C = 2, 256, 20, 24
+    X = rr.standard_normal((B, N, C)).astype(np.float32)
+    nit, _ = O.knn(X, X, K)
+    Ws, bs = _weights(rr, [2 * C, 40])
+    h = O.mlp(O.group_edge(X, nit), Ws, bs)
+    ref = O.rowgroup_max(h.reshape(B, N * K, 40), K)
+    out = ops.conventional_module(dev(nit), ops.MLPParams(Ws, bs), feat=dev(X), grouping=1)
+    assert normwise(host(out), ref) <= 1e-4
+
+
+@pytest.mark.parametrize("B,Nd,Ns,C", [(2, 4096, 1024, 128), (3, 100, 17, 5), (1, 64, 16, 512), (2, 10, 3, 8)])
+def test_interpolate3(gpu, B, Nd, Ns, C):
+    rr = g(12)
+    dst = rr.uniform(-1, 1, (B, Nd, 3)).astype(np.float32)
+    src = np.concatenate([dst[:, :min(Ns, Nd) // 2], rr.uniform(-1, 1, (B, Ns - min(Ns, Nd) // 2, 3))], 1)
+    src = src.astype(np.float32)
+    f = rr.standard_normal((B, Ns, C)).astype(np.float32)
+    ref = O.interpolate3(dst, src, f)
+    out = ops.interpolate3(dev(dst), dev(src), dev(f))
+    assert normwise(host(out), ref) <= 1e-5
+
+
+def test_cast_bf16_matches_oracle_rounding(gpu):
+    rr = g(13)
+    x = (rr.standard_normal(5000) * 10.0 ** rr.integers(-5, 5, 5000)).astype(np.float32)
+    y = ops.cast_bf16(dev(x))
+    assert np.array_equal(host(y.float()), O.bf16_round(x))
+
+
+def test_edgeconv_fold(gpu):
+    rr = g(14)
+    W = rr.standard_normal((16, 10)).astype(np.float32)
+    b = rr.standard_normal(16).astype(np.float32)
+    from oracle.nets import edgeconv_fold as ofold
+    rW, rb = ofold(W, b)
+    Wo, bo = ops.edgeconv_fold(dev(W), dev(b))
+    assert np.array_equal(host(Wo), rW) and np.array_equal(host(bo), rb)
+
+
+def test_empty_batches_are_noops(gpu):
+    x = torch.zeros((0, 10, 3), device="cuda")
+    idx, cxyz = ops.fps(x, 5)
+    assert idx.shape == (0, 5)
+    nit, _ = ops.ball_query(torch.zeros((2, 10, 3), device="cuda"), torch.zeros((2, 0, 3), device="cuda"), 0.1, 4)
+    assert nit.shape == (2, 0, 4)
