@@ -1,0 +1,229 @@
+"""The point-cloud networks of the synthetic workloads, composed from C-ABI
+calls only (every arithmetic step runs in libmesorasi.so; torch provides
+device memory, streams and events).
+
+Delayed aggregation (Sec. 3.1): the neighbor search N does not depend on
+the MLP F, so all searches run on a side stream while F runs on the main
+stream; an event joins them right before each aggregation A.  For
+PointNet++ the whole xyz chain (FPS -> ball query -> FPS of the next
+level ...) depends on coordinates only and runs ahead (Sec. 4.1 "Work
+Flow"); for DGCNN each layer's kNN overlaps that layer's MLP.  The
+conventional path (Eq. (1)) serialises N -> A -> F per module.
+
+All intermediate buffers are allocated once per input shape and kept, so a
+forward pass only enqueues kernels and can be captured into a HIP graph
+(:meth:`Net.capture`).
+"""
+from __future__ import annotations
+
+import torch
+
+from . import ops
+from ._lib import F32, BF16
+
+
+class Net:
+    def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda"):
+        self.spec = spec
+        self.delayed = delayed
+        self.device = torch.device(device)
+        self.dt = BF16 if spec.get("dtype") == "bf16" else F32
+        self.side = torch.cuda.Stream(device=self.device)
+        self._bufs: dict[str, torch.Tensor] = {}
+        self._params(weights)
+
+    # -- buffers ------------------------------------------------------------
+    def _buf(self, name, shape, dtype=torch.float32):
+        t = self._bufs.get(name)
+        if t is None or tuple(t.shape) != tuple(shape) or t.dtype != dtype:
+            t = torch.empty(shape, dtype=dtype, device=self.device)
+            self._bufs[name] = t
+        return t
+
+    def _ws(self, name, nbytes):
+        t = self._bufs.get(name)
+        if t is None or t.numel() < nbytes:
+            t = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=self.device)
+            self._bufs[name] = t
+        return t
+
+    def _params(self, weights):
+        raise NotImplementedError
+
+    def forward(self, xyz, feat=None) -> dict:
+        raise NotImplementedError
+
+    __call__ = forward
+
+    def capture(self, xyz, feat=None):
+        """Warm up, then capture one forward into a CUDA/HIP graph.  Returns
+        (graph, outputs); graph.replay() recomputes outputs in place from the
+        same input tensors."""
+        self.forward(xyz, feat)
+        torch.cuda.synchronize(self.device)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            outs = self.forward(xyz, feat)
+        return graph, outs
+
+
+class PointNet2(Net):
+    """Set-abstraction stack, optionally followed by a group-all module and
+    an FC head (classifier), or by feature propagation and a per-point head
+    (segmentation)."""
+
+    def _params(self, w):
+        P = lambda Wb: ops.MLPParams(Wb[0], Wb[1], dtype=self.dt, device=self.device)
+        self.sa = [P(Wb) for Wb in w["sa"]]
+        self.ga = P(w["group_all"]) if "group_all" in w else None
+        self.fc = P(w["fc"]) if "fc" in w else None
+        self.fp = [P(Wb) for Wb in w.get("fp", [])]
+        self.head = P(w["head"]) if "head" in w else None
+
+    def _search_chain(self, xyz, B):
+        """FPS and ball query of every level on the side stream."""
+        main, side = torch.cuda.current_stream(self.device), self.side
+        side.wait_stream(main)
+        ev_fps, ev_bq = [], []
+        with torch.cuda.stream(side):
+            p = xyz
+            for i, m in enumerate(self.spec["sa"]):
+                idx = self._buf(f"idx{i}", (B, m["M"]), torch.int32)
+                cx = self._buf(f"cxyz{i}", (B, m["M"], 3))
+                ops.fps(p, m["M"], out_idx=idx, out_xyz=cx)
+                e = torch.cuda.Event()
+                e.record(side)
+                ev_fps.append(e)
+                nit = self._buf(f"nit{i}", (B, m["M"], m["K"]), torch.int32)
+                ops.ball_query(p, cx, m["radius"], m["K"], out=nit)
+                e = torch.cuda.Event()
+                e.record(side)
+                ev_bq.append(e)
+                p = cx
+        return ev_fps, ev_bq
+
+    def _sa_levels(self, xyz, feat):
+        B = xyz.shape[0]
+        main = torch.cuda.current_stream(self.device)
+        ev_fps, ev_bq = self._search_chain(xyz, B)
+        levels = [(xyz, feat)]
+        p, f = xyz, feat
+        for i, m in enumerate(self.spec["sa"]):
+            prm = self.sa[i]
+            N = p.shape[1]
+            if i > 0:
+                main.wait_event(ev_fps[i - 1])          # p = centroids of the previous level
+            idx, cx, nit = self._bufs[f"idx{i}"], self._bufs[f"cxyz{i}"], self._bufs[f"nit{i}"]
+            out = self._buf(f"f{i}", (B, m["M"], prm.c_out))
+            if self.delayed:
+                # F on all N input points -> PFT, overlapping the search chain
+                pft_dt = torch.bfloat16 if self.dt == BF16 else torch.float32
+                pft = self._buf(f"pft{i}", (B, N, prm.c_out), pft_dt)
+                ws = self._ws(f"ws_sa{i}", ops.mlp_workspace_bytes(B * N, prm))
+                ops.pointwise_mlp(p, prm, x1=f, out_dtype=self.dt, out=pft, ws=ws)
+                main.wait_event(ev_bq[i])
+                ops.aggregate_max(pft, nit, cidx=idx, sign=-1, out=out)
+            else:
+                main.wait_event(ev_bq[i])
+                ws = self._ws(f"ws_sa{i}", ops.conventional_workspace_bytes(B, m["M"], m["K"], prm))
+                ops.conventional_module(nit, prm, xyz=p, feat=f, cxyz=cx, grouping=0, out=out, ws=ws)
+            p, f = cx, out
+            levels.append((p, f))
+        return levels
+
+    def forward(self, xyz, feat=None) -> dict:
+        B = xyz.shape[0]
+        levels = self._sa_levels(xyz, feat)
+        res = {}
+        for i in range(len(self.spec["sa"])):
+            for k in ("idx", "nit", "cxyz", "f"):
+                res[f"{k}{i}"] = self._bufs[f"{k}{i}"]
+        p, f = levels[-1]
+        res["out"] = f
+        if self.ga is not None:
+            g = self._buf("global", (B, self.ga.c_out))
+            ws = self._ws("ws_ga", ops.mlp_workspace_bytes(B * p.shape[1], self.ga, p.shape[1]))
+            ops.pointwise_mlp(p, self.ga, x1=f, pool_group=p.shape[1], out=g, ws=ws)
+            res["global"] = res["out"] = g
+            if self.fc is not None:
+                logits = self._buf("logits", (B, self.fc.c_out))
+                ws = self._ws("ws_fc", ops.mlp_workspace_bytes(B, self.fc))
+                ops.pointwise_mlp(g, self.fc, relu_mask=(1 << (self.fc.n - 1)) - 1, out=logits, ws=ws)
+                res["out"] = logits
+        if self.fp:
+            coarse_xyz, coarse_f = levels[-1]
+            for i, prm in enumerate(self.fp):
+                fine_xyz, fine_f = levels[len(levels) - 2 - i]
+                Nf = fine_xyz.shape[1]
+                interp = self._buf(f"interp{i}", (B, Nf, coarse_f.shape[-1]))
+                ops.interpolate3(fine_xyz, coarse_xyz, coarse_f, out=interp)
+                y = self._buf(f"fp{i}", (B, Nf, prm.c_out))
+                ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, prm))
+                ops.pointwise_mlp(interp, prm, x1=fine_f, out=y, ws=ws)
+                res[f"fp{i}"] = y
+                coarse_xyz, coarse_f = fine_xyz, y
+            logits = self._buf("logits", (B, coarse_f.shape[1], self.head.c_out))
+            ws = self._ws("ws_head", ops.mlp_workspace_bytes(B * coarse_f.shape[1], self.head))
+            ops.pointwise_mlp(coarse_f, self.head, relu_mask=(1 << (self.head.n - 1)) - 1, out=logits, ws=ws)
+            res["out"] = logits
+        return res
+
+
+class DGCNN(Net):
+    """EdgeConv stack (kNN in the current feature space), concatenation,
+    1x1 convolution to 1024 channels and a global max."""
+
+    def _params(self, w):
+        self.k = self.spec["k"]
+        self.widths = list(self.spec["edge"])
+        self.edge = []
+        self.folded = []
+        for W, b in w["edge"]:
+            Wd = torch.as_tensor(W, dtype=torch.float32).to(self.device).contiguous()
+            bd = torch.as_tensor(b, dtype=torch.float32).to(self.device).contiguous()
+            self.edge.append(ops.MLPParams([W], [b], dtype=self.dt, device=self.device))
+            Wf, bf = ops.edgeconv_fold(Wd, bd)           # [W1 - W2 ; W2], [b ; 0]
+            self.folded.append(ops.MLPParams([Wf], [bf], dtype=self.dt, device=self.device))
+        self.conv = ops.MLPParams([w["conv"][0]], [w["conv"][1]], dtype=self.dt, device=self.device)
+
+    def forward(self, xyz, feat=None) -> dict:
+        B, N, _ = xyz.shape
+        main, side = torch.cuda.current_stream(self.device), self.side
+        cat = self._buf("cat", (B, N, sum(self.widths)))
+        res = {}
+        X = xyz
+        off = 0
+        for l, cout in enumerate(self.widths):
+            nit = self._buf(f"nit{l}", (B, N, self.k), torch.int32)
+            side.wait_stream(main)                       # X of this layer is ready
+            with torch.cuda.stream(side):
+                ops.knn(X, X, self.k, out=nit)
+                ev = torch.cuda.Event()
+                ev.record(side)
+            dst = cat[..., off:off + cout]
+            if self.delayed:
+                P = self._buf(f"P{l}", (B, N, 2 * cout))
+                ops.pointwise_mlp(X, self.folded[l], relu_mask=0, out=P)   # [A | Bm] for every point
+                main.wait_event(ev)
+                ops.aggregate_max(P[..., cout:], nit, cfeat=P[..., :cout], sign=+1, relu=True, out=dst)
+            else:
+                main.wait_event(ev)
+                ws = self._ws(f"ws_e{l}", ops.conventional_workspace_bytes(B, N, self.k, self.edge[l]))
+                ops.conventional_module(nit, self.edge[l], feat=X, grouping=1, out=dst, ws=ws)
+            res[f"nit{l}"] = nit
+            res[f"x{l}"] = dst
+            X = dst
+            off += cout
+        g = self._buf("global", (B, self.conv.c_out))
+        ops.pointwise_mlp(cat, self.conv, pool_group=N, out=g)
+        res["cat"] = cat
+        res["out"] = g
+        return res
+
+
+def build(spec: dict, weights: dict, delayed: bool = True, device="cuda") -> Net:
+    if spec["kind"] in ("pointnet2_cls", "pointnet2_seg"):
+        return PointNet2(spec, weights, delayed, device)
+    if spec["kind"] == "dgcnn":
+        return DGCNN(spec, weights, delayed, device)
+    raise ValueError(spec["kind"])

@@ -46,11 +46,13 @@ def _check_xyz(x: torch.Tensor, name: str):
         f"{name} must be a contiguous float32 [B, N, 3] tensor"
 
 
-def fps(xyz: torch.Tensor, M: int, want_xyz: bool = True):
+def fps(xyz: torch.Tensor, M: int, want_xyz: bool = True, out_idx: torch.Tensor | None = None,
+        out_xyz: torch.Tensor | None = None):
     _check_xyz(xyz, "xyz")
     B, N, _ = xyz.shape
-    idx = torch.empty((B, M), dtype=torch.int32, device=xyz.device)
-    cxyz = torch.empty((B, M, 3), dtype=torch.float32, device=xyz.device) if want_xyz else None
+    idx = out_idx if out_idx is not None else torch.empty((B, M), dtype=torch.int32, device=xyz.device)
+    cxyz = out_xyz if out_xyz is not None else (
+        torch.empty((B, M, 3), dtype=torch.float32, device=xyz.device) if want_xyz else None)
     check(_lib.lib().mesorasi_fps(xyz.data_ptr(), B, N, M, idx.data_ptr(), _ptr(cxyz), _stream()), "fps")
     return idx, cxyz
 
@@ -68,7 +70,7 @@ def ball_query(xyz: torch.Tensor, qxyz: torch.Tensor, radius: float, K: int, wan
     return nit, cnt
 
 
-def knn(ref: torch.Tensor, query: torch.Tensor, K: int, want_dist: bool = False):
+def knn(ref: torch.Tensor, query: torch.Tensor, K: int, want_dist: bool = False, out: torch.Tensor | None = None):
     """ref [B, N, >=C], query [B, M, >=C] (last dim contiguous, may be
     column slices of wider tensors); C = ref.shape[-1]."""
     assert ref.dtype == torch.float32 and query.dtype == torch.float32
@@ -76,7 +78,7 @@ def knn(ref: torch.Tensor, query: torch.Tensor, K: int, want_dist: bool = False)
     M = query.shape[1]
     pr, ldr = _rows(ref)
     pq, ldq = _rows(query)
-    nit = torch.empty((B, M, K), dtype=torch.int32, device=ref.device)
+    nit = out if out is not None else torch.empty((B, M, K), dtype=torch.int32, device=ref.device)
     dist = torch.empty((B, M, K), dtype=torch.float32, device=ref.device) if want_dist else None
     check(_lib.lib().mesorasi_knn(pr, ldr, pq, ldq, B, N, M, C, K, nit.data_ptr(), _ptr(dist), _stream()), "knn")
     return nit, dist
@@ -137,11 +139,12 @@ def pointwise_mlp(x0: torch.Tensor, p: MLPParams, x1: torch.Tensor | None = None
             out = torch.empty(lead + (p.c_out,), dtype=dt, device=x0.device)
     py, ldy = _rows(out)
     need = mlp_workspace_bytes(rows, p, pool_group)
-    if ws is None or ws.numel() < need:
-        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=x0.device)
+    if need and (ws is None or ws.numel() < need):
+        ws = torch.empty(need, dtype=torch.uint8, device=x0.device)
+    wp, wn = (ws.data_ptr(), ws.numel()) if need else (None, 0)
     d, W, b = p.abi()
     check(_lib.lib().mesorasi_pointwise_mlp(p0, c0, ld0, p1, c1, ld1, rows, p.n, d, W, b, relu_mask, p.dtype,
-                                            out_dtype, py, ldy, pool_group, ws.data_ptr(), ws.numel(), _stream()),
+                                            out_dtype, py, ldy, pool_group, wp, wn, _stream()),
           "pointwise_mlp")
     return out
 
