@@ -1,0 +1,319 @@
+"""Benchmark: PointNet++ SSG classifier forward, batch 32 x 1024 points,
+delayed aggregation, on one MI355X.
+
+One step = one full forward of the batch (FPS, ball query, per-point MLP,
+aggregation for both set-abstraction levels, group-all MLP, FC head).
+Inputs and weights are resident in HBM before timing; the timed steps
+replay a HIP graph of the two-stream forward.  The JSON line also carries:
+  - conventional: the same network in the original order (Eq. (1)) on the
+    GPU and the delayed/conventional speedup;
+  - stages: per-kernel-call durations from HIP events on the stream each
+    kernel runs on (an eager pass over the same steps);
+  - roofline: the dominant kernel's achieved rate against MI355X peak;
+  - cpu_baseline: the CPU oracle timed on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "clouds/sec end-to-end + centroids/sec per module; % HBM and MFMA peak"
+WORKLOAD = "pointnet2_cls"
+HBM_PEAK_GBS = 8000.0
+MFMA_F32_PEAK_TFLOPS = 157.3
+MFMA_BF16_PEAK_TFLOPS = 2516.6
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--eager", action="store_true", help="time eager launches instead of graph replay")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 256 MiB device copy (reference for HBM counters)")
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------------------
+# per-call event timing (eager pass)
+# ----------------------------------------------------------------------------
+
+class StageTimer:
+    """Wraps the ops entry points so every call records a start/end event on
+    the stream it is launched on."""
+
+    NAMES = ("fps", "ball_query", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3")
+
+    def __init__(self, ops):
+        import torch
+        self.torch = torch
+        self.ops = ops
+        self.orig = {n: getattr(ops, n) for n in self.NAMES}
+        self.records = []     # (name#k, start, end, args-summary)
+        self.counts = {}
+        self.active = False
+
+    def install(self):
+        torch = self.torch
+        for n, fn in self.orig.items():
+            def wrap(*a, __n=n, __fn=fn, **kw):
+                if not self.active:
+                    return __fn(*a, **kw)
+                k = self.counts.get(__n, 0)
+                self.counts[__n] = k + 1
+                s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                s.record()
+                r = __fn(*a, **kw)
+                e.record()
+                self.records.append((f"{__n}#{k}", s, e))
+                return r
+            setattr(self.ops, n, wrap)
+
+    def uninstall(self):
+        for n, fn in self.orig.items():
+            setattr(self.ops, n, fn)
+
+    def begin_step(self):
+        self.counts = {}
+
+    def summary(self):
+        self.torch.cuda.synchronize()
+        acc = {}
+        for name, s, e in self.records:
+            acc.setdefault(name, []).append(s.elapsed_time(e))
+        return {k: float(np.mean(v)) for k, v in acc.items()}
+
+
+# ----------------------------------------------------------------------------
+# algorithmic work per call of the classifier (documented in the design doc)
+# ----------------------------------------------------------------------------
+
+def work_per_call(spec):
+    """name#k -> (bound, amount, unit) for the kernel calls of one forward.
+
+    fps:          (M-1) * N point updates per cloud, 8 flops each (3 sub,
+                  1 mul, 2 fma) -> alu
+    ball_query:   B * M * N candidate tests (upper bound; early exit scans
+                  fewer), 8 flops each -> alu
+    pointwise_mlp: 2 * rows * sum(C_l * C_l+1) -> mfma
+    aggregate_max: compulsory HBM bytes -- every PFT row read once, the NIT,
+                  the centroid indices and the output -> hbm
+    """
+    B = spec["B"]
+    out = {}
+    N = spec["N"]
+    cin = 3 + spec["n_feat"]
+    s = 2 if spec.get("dtype") == "bf16" else 4
+    for i, m in enumerate(spec["sa"]):
+        M, K, dims = m["M"], m["K"], [cin] + m["mlp"]
+        C = dims[-1]
+        out[f"fps#{i}"] = ("alu", 8.0 * B * (M - 1) * N / 1e12, "TFLOP")
+        out[f"ball_query#{i}"] = ("alu", 8.0 * B * M * N / 1e12, "TFLOP")
+        flops = 2.0 * B * N * sum(a * b for a, b in zip(dims[:-1], dims[1:]))
+        out[f"pointwise_mlp#{i}"] = ("mfma", flops / 1e12, "TFLOP")
+        compulsory = B * N * C * s + 4 * B * M * K + 4 * B * M + 4 * B * M * C
+        out[f"aggregate_max#{i}"] = ("hbm", compulsory / 1e9, "GB")
+        N, cin = M, 3 + C
+    if spec.get("group_all"):
+        dims = [cin] + spec["group_all"]
+        flops = 2.0 * B * N * sum(a * b for a, b in zip(dims[:-1], dims[1:]))
+        out[f"pointwise_mlp#{len(spec['sa'])}"] = ("mfma", flops / 1e12, "TFLOP")
+    return out
+
+
+def logical_gather_bytes(spec):
+    """Bytes the aggregation reads as gathered rows (each neighbor row once
+    per centroid that lists it), per call -- reuse served by L2/MALL."""
+    B, out, N, cin = spec["B"], {}, spec["N"], 3 + spec["n_feat"]
+    s = 2 if spec.get("dtype") == "bf16" else 4
+    for i, m in enumerate(spec["sa"]):
+        C = m["mlp"][-1]
+        out[f"aggregate_max#{i}"] = B * m["M"] * m["K"] * C * s
+        N, cin = m["M"], 3 + C
+    return out
+
+
+PEAKS = {"alu": (157.3, "TFLOP/s"), "mfma": (MFMA_F32_PEAK_TFLOPS, "TFLOP/s"), "hbm": (HBM_PEAK_GBS, "GB/s")}
+
+
+def load_traffic(kernel_key):
+    """HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE,
+    recorded in profiles/pmc_traffic.txt together with a hash of the kernel's
+    source file; None if absent or if the source has changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "pmc_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        f = line.split()
+        if len(f) >= 5 and not line.startswith("#") and f[0] == kernel_key:
+            src = os.path.join(ROOT, "paper_2008_06967_amd", "csrc", f[4])
+            if not os.path.exists(src):
+                return None
+            h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+            if h != f[3]:
+                return None
+            return {"fetch_bytes": float(f[1]), "write_bytes": float(f[2]), "bytes": float(f[1]) + float(f[2])}
+    return None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2008_06967_amd import nets, ops, synth
+
+    spec = synth.workload(args.workload)
+    xyz_np, feat_np = synth.make_points(spec)
+    w = synth.make_weights(spec)
+    dev = torch.device("cuda:0")
+    xyz = torch.from_numpy(xyz_np).to(dev)
+    feat = None if feat_np is None else torch.from_numpy(feat_np).to(dev)
+    B = spec["B"]
+    print(f"[bench] workload={args.workload} B={B} N={spec['N']} steps={args.steps} warmup={args.warmup}",
+          file=sys.stderr, flush=True)
+
+    def time_net(delayed, steps, warmup, graph):
+        net = nets.build(spec, w, delayed=delayed, device=dev)
+        if graph:
+            g, _ = net.capture(xyz, feat)
+            run = g.replay
+        else:
+            run = lambda: net.forward(xyz, feat)
+        for _ in range(warmup):
+            run()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            run()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / steps
+
+    if args.calibrate_copy:
+        src = torch.empty(64 << 20, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copy calibration: {src.numel() * 4} bytes read, {dst.numel() * 4} bytes written per copy",
+              file=sys.stderr, flush=True)
+        del src, dst
+
+    # timed region: delayed forward, graph replay (or eager with --eager)
+    t_step = time_net(True, args.steps, args.warmup, not args.eager)
+    print(f"[bench] delayed {t_step * 1e3:.3f} ms/step", file=sys.stderr, flush=True)
+    t_conv = time_net(False, max(5, args.steps // 2), 2, not args.eager)
+    print(f"[bench] conventional {t_conv * 1e3:.3f} ms/step", file=sys.stderr, flush=True)
+    t_step_eager = time_net(True, max(5, args.steps // 2), 2, False)
+
+    # per-call durations (eager pass with events on each call's stream)
+    timer = StageTimer(ops)
+    timer.install()
+    net = nets.build(spec, w, delayed=True, device=dev)
+    net.forward(xyz, feat)
+    torch.cuda.synchronize()
+    timer.active = True
+    for _ in range(max(5, args.steps // 2)):
+        timer.begin_step()
+        net.forward(xyz, feat)
+    stages = timer.summary()
+    timer.active = False
+    timer.uninstall()
+
+    # dominant kernel = the longest call of the step; roofline for each call
+    work = work_per_call(spec)
+    gathered = logical_gather_bytes(spec)
+    roofs = {}
+    for k, ms in stages.items():
+        if k not in work:
+            continue
+        kd, am, un = work[k]
+        rate = am / (ms * 1e-3)
+        pk, pu = PEAKS[kd]
+        roofs[k] = {"bound": kd, "achieved": round(rate, 4), "peak": pk, "unit": pu, "frac": round(rate / pk, 5)}
+        if k in gathered:
+            roofs[k]["logical_gather_GBps"] = round(gathered[k] / (ms * 1e-3) / 1e9, 1)
+    dom = max((k for k in stages if k in work), key=lambda k: stages[k])
+    roof = dict(roofs[dom])
+    roof["kernel"] = dom
+    roof["avg_ms"] = stages[dom]
+    tr = load_traffic(dom.split("#")[0] + "#" + dom.split("#")[1] + "@" + args.workload)
+    roof["traffic"] = None if tr is None else tr["bytes"]
+
+    per_module = {}
+    for i, m in enumerate(spec["sa"]):
+        per_module[f"sa{i + 1}_centroids_per_s"] = B * m["M"] / t_step
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(spec, xyz_np, feat_np, w, args.cpu_seconds)
+
+    res = {
+        "metric": METRIC,
+        "value": B / t_step,
+        "unit": "clouds/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": t_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if spec.get("dtype") != "bf16" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload} (PointNet++ SSG classifier, delayed aggregation)",
+                   "global_batch": B, "points": spec["N"], "path": "delayed",
+                   "timing": "eager launches" if args.eager else "HIP graph replay, search chain on a side stream",
+                   "parallelism": "single GPU"},
+        "centroids_per_s": per_module,
+        "conventional": {"ms_per_step": t_conv * 1e3, "clouds_per_s": B / t_conv, "speedup_delayed": t_conv / t_step},
+        "eager_ms_per_step": t_step_eager * 1e3,
+        "stages_ms": {k: round(v, 5) for k, v in stages.items()},
+        "stage_roofline": roofs,
+        "critical_path_note": "fps/ball_query run on a side stream concurrently with the MLP chain",
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "paper_context": {"software_speedup_mobile_gpu": 1.6, "hardware_speedup_up_to": 3.6},
+    }
+    print(json.dumps(res))
+
+
+def cpu_baseline(spec, xyz, feat, w, seconds):
+    """The CPU oracle (single thread) on the same workload, repeated over the
+    batch until about `seconds` of work has been done."""
+    import oracle.nets as ON
+    B = spec["B"]
+    clouds = 0
+    t0 = time.perf_counter()
+    chunk = 4
+    while True:
+        for s in range(0, B, chunk):
+            sub = dict(spec, B=min(chunk, B - s))
+            ON.forward(sub, xyz[s:s + chunk], None if feat is None else feat[s:s + chunk], w, delayed=True)
+            clouds += sub["B"]
+            if time.perf_counter() - t0 >= seconds:
+                break
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": clouds / dt, "unit": "clouds/s", "cores": 1, "kind": "oracle",
+            "sample": f"{clouds} clouds of the same batch (delayed forward), {dt:.1f} s, single thread"}
+
+
+if __name__ == "__main__":
+    main()

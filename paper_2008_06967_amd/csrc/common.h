@@ -71,33 +71,45 @@ __device__ __forceinline__ int mask_rank(uint64_t m) {
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
 
+// v = max(v, dpp(v)) as one v_max_i32_dpp (bound_ctrl lets the compiler fuse
+// the move into the max).
 template <int CTRL>
-__device__ __forceinline__ int dpp_i32(int v) {
-    return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xf, 0xf, false);
+__device__ __forceinline__ int dpp_max_i32(int v) {
+    return max(v, __builtin_amdgcn_mov_dpp(v, CTRL, 0xf, 0xf, true));
 }
 
-// Max of a signed int over the wave, returned to every lane.  Row-level
-// butterfly with DPP row rotations (every lane of a 16-lane row ends with
-// the row max), then the four row maxima are combined through readlane.
-__device__ __forceinline__ int wave_max_i32(int v) {
-    v = max(v, dpp_i32<0x121>(v));  // row_ror:1
-    v = max(v, dpp_i32<0x122>(v));  // row_ror:2
-    v = max(v, dpp_i32<0x124>(v));  // row_ror:4
-    v = max(v, dpp_i32<0x128>(v));  // row_ror:8
-    const int a = __builtin_amdgcn_readlane(v, 0);
-    const int b = __builtin_amdgcn_readlane(v, 16);
-    const int c = __builtin_amdgcn_readlane(v, 32);
-    const int d = __builtin_amdgcn_readlane(v, 48);
-    return max(max(a, b), max(c, d));
-}
-
-// Max over the lanes of one 16-lane row (row-local result in every lane).
+// Max over the lanes of each 16-lane row, returned in every lane of the row
+// (butterfly of row rotations).
 __device__ __forceinline__ int row_max_i32(int v) {
-    v = max(v, dpp_i32<0x121>(v));
-    v = max(v, dpp_i32<0x122>(v));
-    v = max(v, dpp_i32<0x124>(v));
-    v = max(v, dpp_i32<0x128>(v));
+    v = dpp_max_i32<0x121>(v);  // row_ror:1
+    v = dpp_max_i32<0x122>(v);  // row_ror:2
+    v = dpp_max_i32<0x124>(v);  // row_ror:4
+    v = dpp_max_i32<0x128>(v);  // row_ror:8
     return v;
+}
+
+// Max over each group of 4 lanes, in every lane of the group.
+__device__ __forceinline__ int quad_max_i32(int v) {
+    v = dpp_max_i32<0xB1>(v);   // quad_perm [1,0,3,2]
+    v = dpp_max_i32<0x4E>(v);   // quad_perm [2,3,0,1]
+    return v;
+}
+
+// Max over each group of 8 lanes; lane 8g+7 holds the max of lanes 8g..8g+7.
+__device__ __forceinline__ int oct_max_i32(int v) {
+    v = dpp_max_i32<0x121>(v);  // row_ror:1
+    v = dpp_max_i32<0x122>(v);  // row_ror:2
+    v = dpp_max_i32<0x124>(v);  // row_ror:4
+    return v;
+}
+
+// Max of a signed int over the wave, returned to every lane (uniform): row
+// butterfly, then the GFX9 row broadcasts fold rows 0..3 into lane 63.
+__device__ __forceinline__ int wave_max_i32(int v) {
+    v = row_max_i32(v);
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x142, 0xa, 0xf, false));  // row_bcast:15 into rows 1, 3
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x143, 0xc, 0xf, false));  // row_bcast:31 into rows 2, 3
+    return __builtin_amdgcn_readlane(v, 63);
 }
 
 }  // namespace meso

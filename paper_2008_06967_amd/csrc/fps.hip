@@ -12,9 +12,14 @@
 // distance bits (non-negative floats order like signed ints) followed by a
 // "first lane holding the max" ballot.
 //
-// One barrier per iteration: the per-wave winners go to a double-buffered
-// LDS slot array indexed by iteration parity, so a wave that runs ahead
-// writes the other buffer while slower waves still read this one.
+// An iteration: each thread updates its P running minima and keeps only
+// their max; a fused-DPP butterfly gives the wave max; the lowest lane
+// holding it then picks its lowest matching slot (so the argmax and the
+// winner's coordinates are selected once, after the reduction).  One
+// barrier per iteration: the per-wave winners go to a double-buffered LDS
+// slot array indexed by iteration parity, so a wave that runs ahead writes
+// the other buffer while slower waves still read this one.  A single-wave
+// workgroup needs no barrier at all.
 #include "common.h"
 
 namespace meso {
@@ -23,10 +28,8 @@ template <int T, int P, bool REG_XYZ>
 __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, int N, int M, int32_t* __restrict__ idx,
                                                 float* __restrict__ cxyz) {
     constexpr int W = T / 64;
-    __shared__ int s_d[2][W];
-    __shared__ int s_i[2][W];
-    __shared__ float s_x[2][W];
-    __shared__ float s_y[2][W];
+    // per-wave winner of iteration m, double-buffered by m & 1: {dist bits, index, x, y} and z
+    __shared__ int4 s_slot[2][W];
     __shared__ float s_z[2][W];
 
     const int b = blockIdx.x;
@@ -63,9 +66,8 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
     }
 
     for (int m = 1; m < M; ++m) {
-        int bestd = __float_as_int(-1.0f);
-        int bestq = 0;
-        float bx = 0.0f, by = 0.0f, bz = 0.0f;
+        // 1. distance to the newest centroid, running min, this thread's max
+        int tmax = INT32_MIN;
 #pragma unroll
         for (int q = 0; q < P; ++q) {
             float x, y, z;
@@ -80,47 +82,61 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
                 z = p[3 * j + 2];
             }
             const float d = dist3(x, y, z, cx, cy, cz);
-            const float nm = fminf(dm[q], d);
+            const float nm = d < dm[q] ? d : dm[q];
             dm[q] = nm;
-            const int nb = __float_as_int(nm);
-            if (nb > bestd) {
-                bestd = nb;
-                bestq = q;
-                bx = x;
-                by = y;
-                bz = z;
+            tmax = max(tmax, __float_as_int(nm));
+        }
+        // 2. wave max; the lowest lane holding it; that lane's lowest slot
+        const int wmax = wave_max_i32(tmax);
+        const int wl = __builtin_ctzll(ballot(tmax == wmax));
+        int sq = P - 1;
+        float sx = 0.0f, sy = 0.0f, sz = 0.0f;
+#pragma unroll
+        for (int q = P - 1; q >= 0; --q) {
+            const bool eq = __float_as_int(dm[q]) == wmax;
+            sq = eq ? q : sq;
+            if constexpr (REG_XYZ) {
+                sx = eq ? px[q] : sx;
+                sy = eq ? py[q] : sy;
+                sz = eq ? pz[q] : sz;
             }
         }
-        // wave winner: max distance, lowest lane among equals
-        const int wmax = wave_max_i32(bestd);
-        const uint64_t hit = ballot(bestd == wmax);
-        const int wl = __builtin_ctzll(hit);
-        const int buf = m & 1;
-        if (lane == wl) {
-            s_d[buf][wave] = wmax;
-            s_i[buf][wave] = base + bestq;
-            s_x[buf][wave] = bx;
-            s_y[buf][wave] = by;
-            s_z[buf][wave] = bz;
+        if constexpr (!REG_XYZ) {
+            const int j = min(base + sq, N - 1);
+            sx = p[3 * j + 0];
+            sy = p[3 * j + 1];
+            sz = p[3 * j + 2];
         }
-        __syncthreads();
-        // block winner: lane w < W inspects wave w's slot
-        int vd = INT32_MIN;  // below every slot value (slots hold >= bits(-1.0f))
-        int vi = 0;
-        float vx = 0.0f, vy = 0.0f, vz = 0.0f;
-        if (lane < W) {
-            vd = s_d[buf][lane];
-            vi = s_i[buf][lane];
-            vx = s_x[buf][lane];
-            vy = s_y[buf][lane];
-            vz = s_z[buf][lane];
+        int sel;
+        if constexpr (W == 1) {
+            sel = __builtin_amdgcn_readlane(base + sq, wl);
+            cx = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sx), wl));
+            cy = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sy), wl));
+            cz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sz), wl));
+        } else {
+            const int buf = m & 1;
+            if (lane == wl) {
+                s_slot[buf][wave] = make_int4(wmax, base + sq, __float_as_int(sx), __float_as_int(sy));
+                s_z[buf][wave] = sz;
+            }
+            __syncthreads();
+            // 3. block winner: lane w < W inspects wave w's slot
+            int4 sl = make_int4(INT32_MIN, 0, 0, 0);
+            float slz = 0.0f;
+            if (lane < W) {
+                sl = s_slot[buf][lane];
+                slz = s_z[buf][lane];
+            }
+            int gm;
+            if constexpr (W <= 4) gm = __builtin_amdgcn_readlane(quad_max_i32(sl.x), 0);
+            else if constexpr (W <= 8) gm = __builtin_amdgcn_readlane(oct_max_i32(sl.x), 7);
+            else gm = __builtin_amdgcn_readlane(row_max_i32(sl.x), 0);
+            const int ww = __builtin_ctzll(ballot(sl.x == gm));
+            sel = __builtin_amdgcn_readlane(sl.y, ww);
+            cx = __int_as_float(__builtin_amdgcn_readlane(sl.z, ww));
+            cy = __int_as_float(__builtin_amdgcn_readlane(sl.w, ww));
+            cz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(slz), ww));
         }
-        const int gmax = (W <= 16) ? __builtin_amdgcn_readlane(row_max_i32(vd), 0) : wave_max_i32(vd);
-        const int ww = __builtin_ctzll(ballot(vd == gmax));
-        const int sel = __builtin_amdgcn_readlane(vi, ww);
-        cx = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(vx), ww));
-        cy = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(vy), ww));
-        cz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(vz), ww));
         if (tid == 0) {
             out_idx[m] = sel;
             if (out_c) {
@@ -153,13 +169,14 @@ extern "C" int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, i
     MESO_REQUIRE(B <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_fps: B too large");
     hipStream_t s = as_stream(stream);
     const int n = (int)N, m = (int)M;
-    if (n <= 64) launch_fps<64, 1, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 128) launch_fps<64, 2, true>(xyz, B, n, m, idx, cxyz, s);
+    // workgroup shape per cloud size, from a sweep on MI355X: the iteration
+    // time is a fixed reduction/barrier chain plus P points of VALU work
+    if (n <= 128) launch_fps<64, 2, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 256) launch_fps<128, 2, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 512) launch_fps<256, 2, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 1024) launch_fps<256, 4, true>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 1024) launch_fps<512, 2, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 2048) launch_fps<512, 4, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 4096) launch_fps<1024, 4, true>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 4096) launch_fps<512, 8, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 8192) launch_fps<1024, 8, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 16384) launch_fps<1024, 16, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 32768) launch_fps<1024, 32, false>(xyz, B, n, m, idx, cxyz, s);

@@ -7,9 +7,10 @@
 //
 // One launch per layer: Y = phi(X W^T + b) with X = [x0 | x1] (two column
 // sources, so the first layer reads xyz and the previous module's features
-// without a concatenated copy).  Workgroup tile 64 x 64 over (rows, output
-// channels), 4 waves each owning a 32 x 32 block, K staged through LDS in
-// slices of 32:
+// without a concatenated copy).  Workgroup tiles of 64 or 128 rows by 64 or
+// 128 output channels (chosen per layer to fill the 256 CUs), 4 waves each
+// owning up to 2 x 2 blocks of 32 x 32; layers with too few tiles (the FC
+// head's 32 rows) split K and sum the partials in a fixed order:
 //  - fp32: v_mfma_f32_32x32x2_f32 (lane l feeds A[l%32][k + l/32] and
 //    B[k + l/32][l%32]); LDS tiles are k-major so the 32 lanes of a half
 //    wave read consecutive words.
@@ -29,11 +30,13 @@ namespace meso {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int BM = 64, BN = 64, BK = 32;
-constexpr int kPadF = 4;     // fp32 k-major rows: BM + 4 words
-constexpr int kRowH = 40;    // bf16 rows: 32 k + 8 pad (80 bytes)
+constexpr int BKF = 16;      // fp32 k-slice
+constexpr int BKH = 32;      // bf16 k-slice
+constexpr int kPadF = 4;     // fp32 k-major LDS rows: tile width + 4 words
+constexpr int kRowH = 40;    // bf16 LDS rows: 32 k + 8 pad (80 bytes)
+constexpr int kTargetTiles = 256;   // one tile per CU
 
-enum { EPI_F32 = 0, EPI_BF16 = 1, EPI_POOL = 2 };
+enum { EPI_F32 = 0, EPI_BF16 = 1, EPI_POOL = 2, EPI_PARTIAL = 3 };
 
 struct GemmArgs {
     const void* x0;
@@ -44,12 +47,15 @@ struct GemmArgs {
     int a_bf16;          // x0 holds bf16 bits (intermediate activations of the bf16 path)
     int64_t rows;
     int K, N;
+    int kc;              // K range per split (multiple of the k-slice)
     const void* W;       // [N, K]
     const float* bias;   // [N] or null
     int relu;
+    int round_bf16;      // round activations to bf16 (bf16 path)
     void* y;
     int64_t ldy;
     int64_t G;           // pool group (EPI_POOL)
+    float* part;         // split-K partial sums [splits, rows, N]
 };
 
 // Element (r, k) of the virtual input [x0 | x1] as float (0 outside).
@@ -64,44 +70,56 @@ __device__ __forceinline__ float a_elem(const GemmArgs& a, int64_t r, int k) {
     return 0.0f;
 }
 
-// Eight consecutive input elements (r, k0 .. k0+7) as float.
-template <bool FAST>
-__device__ __forceinline__ void load_a8(const GemmArgs& a, int64_t r, int k0, float (&v)[8]) {
+// L consecutive input elements (r, k0 .. k0+L-1) as float, L in {4, 8}.
+template <int L, bool FAST>
+__device__ __forceinline__ void load_a(const GemmArgs& a, int64_t r, int k0, float (&v)[L]) {
     if constexpr (FAST) {
-        // single fp32 source, 16-byte aligned rows, K multiple of 8
+        // single fp32 source, 16-byte aligned rows, K a multiple of 8
         if (r < a.rows && k0 < a.K) {
             const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(a.x0) + r * a.ld0 + k0);
-            const float4 u = p[0], w = p[1];
-            v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
-            v[4] = w.x; v[5] = w.y; v[6] = w.z; v[7] = w.w;
+#pragma unroll
+            for (int h = 0; h < L / 4; ++h) {
+                const float4 u = p[h];
+                v[4 * h + 0] = u.x; v[4 * h + 1] = u.y; v[4 * h + 2] = u.z; v[4 * h + 3] = u.w;
+            }
         } else {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) v[i] = 0.0f;
+            for (int i = 0; i < L; ++i) v[i] = 0.0f;
         }
     } else {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = a_elem(a, r, k0 + i);
+        for (int i = 0; i < L; ++i) v[i] = a_elem(a, r, k0 + i);
     }
 }
 
-template <bool FAST>
-__device__ __forceinline__ void load_w8_f32(const GemmArgs& a, int n, int k0, float (&v)[8]) {
+template <int L, bool FAST>
+__device__ __forceinline__ void load_w_f32(const GemmArgs& a, int n, int k0, float (&v)[L]) {
     const float* W = static_cast<const float*>(a.W);
-    if (FAST && n < a.N && k0 < a.K) {
-        const float4* p = reinterpret_cast<const float4*>(W + (int64_t)n * a.K + k0);
-        const float4 u = p[0], w = p[1];
-        v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
-        v[4] = w.x; v[5] = w.y; v[6] = w.z; v[7] = w.w;
+    if constexpr (FAST) {
+        if (n < a.N && k0 < a.K) {
+            const float4* p = reinterpret_cast<const float4*>(W + (int64_t)n * a.K + k0);
+#pragma unroll
+            for (int h = 0; h < L / 4; ++h) {
+                const float4 u = p[h];
+                v[4 * h + 0] = u.x; v[4 * h + 1] = u.y; v[4 * h + 2] = u.z; v[4 * h + 3] = u.w;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < L; ++i) v[i] = 0.0f;
+        }
         return;
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = (n < a.N && k0 + i < a.K) ? W[(int64_t)n * a.K + k0 + i] : 0.0f;
+    for (int i = 0; i < L; ++i) v[i] = (n < a.N && k0 + i < a.K) ? W[(int64_t)n * a.K + k0 + i] : 0.0f;
 }
 
 template <bool FAST>
 __device__ __forceinline__ uint4 load_w8_bf16(const GemmArgs& a, int n, int k0) {
     const uint16_t* W = static_cast<const uint16_t*>(a.W);
-    if (FAST && n < a.N && k0 < a.K) return *reinterpret_cast<const uint4*>(W + (int64_t)n * a.K + k0);
+    if (FAST) {
+        if (n < a.N && k0 < a.K) return *reinterpret_cast<const uint4*>(W + (int64_t)n * a.K + k0);
+        return make_uint4(0, 0, 0, 0);
+    }
     uint16_t h[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) h[i] = (n < a.N && k0 + i < a.K) ? W[(int64_t)n * a.K + k0 + i] : (uint16_t)0;
@@ -128,7 +146,7 @@ __device__ __forceinline__ uint4 load_a8_bf16(const GemmArgs& a, int64_t r, int 
             h[i] = (r < a.rows && k0 + i < a.c0) ? static_cast<const uint16_t*>(a.x0)[r * a.ld0 + k0 + i] : (uint16_t)0;
     } else {
         float v[8];
-        load_a8<FAST>(a, r, k0, v);
+        load_a<8, FAST>(a, r, k0, v);
 #pragma unroll
         for (int i = 0; i < 8; ++i) h[i] = f32_to_bf16(v[i]);
     }
@@ -140,25 +158,36 @@ __device__ __forceinline__ uint4 load_a8_bf16(const GemmArgs& a, int64_t r, int 
     return q;
 }
 
-// Shared epilogue: acc holds the 32 x 32 block (row0, col0) of this wave.
+// bias, ReLU and bf16 rounding of one pre-activation value
+__device__ __forceinline__ float activate(const GemmArgs& a, float t, float bias) {
+    t += bias;
+    if (a.relu) t = t > 0.0f ? t : 0.0f;
+    if (a.round_bf16) t = round_bf16(t);
+    return t;
+}
+
+// Epilogue of one 32 x 32 accumulator block at (row0, col0).
 template <int EPI>
-__device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, int64_t row0, int col0, int lane,
-                                         bool round_bf16_out) {
+__device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, int64_t row0, int col0, int lane) {
     const int col = col0 + (lane & 31);
     const bool col_ok = col < a.N;
+    const int64_t rbase = row0 + 4 * (lane >> 5);
+    if constexpr (EPI == EPI_PARTIAL) {
+        if (!col_ok) return;
+        float* part = a.part + (int64_t)blockIdx.z * a.rows * a.N;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int64_t row = rbase + 8 * (r >> 2) + (r & 3);
+            if (row < a.rows) part[row * a.N + col] = acc[r];
+        }
+        return;
+    }
     const float bias = (col_ok && a.bias) ? a.bias[col] : 0.0f;
     float v[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        float t = acc[r] + bias;
-        if (a.relu) t = t > 0.0f ? t : 0.0f;
-        if (round_bf16_out) t = round_bf16(t);
-        v[r] = t;
-    }
-    const int64_t rbase = row0 + 4 * (lane >> 5);
+    for (int r = 0; r < 16; ++r) v[r] = activate(a, acc[r], bias);
     if constexpr (EPI == EPI_POOL) {
-        float* y = static_cast<float*>(a.y);
-        unsigned* yu = reinterpret_cast<unsigned*>(y);
+        unsigned* yu = static_cast<unsigned*>(a.y);
         if (a.G % 32 == 0) {
             // the whole 32-row block lies in one group (row0 is a multiple of 32)
             if (row0 >= a.rows) return;
@@ -197,105 +226,284 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, i
     }
 }
 
-template <int EPI, bool FAST_A, bool FAST_W>
+// fp32 MFMA GEMM.  Workgroup tile BM x BN, 2 x 2 waves, each wave TM x TN
+// blocks of 32 x 32.  K advances in slices of 16 through double-buffered
+// k-major LDS; the next slice is fetched into registers while the current
+// one feeds the MFMAs, so one barrier per slice suffices.
+template <int BM, int BN, int EPI, bool FAST_A, bool FAST_W>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
-    __shared__ float As[BK][BM + kPadF];
-    __shared__ float Bs[BK][BN + kPadF];
+    constexpr int BK = BKF;
+    constexpr int TM = BM / 64, TN = BN / 64;
+    constexpr int AL = BM * BK / 256, BL = BN * BK / 256;   // elements per thread per slice
+    __shared__ float As[2][BK][BM + kPadF];
+    __shared__ float Bs[2][BK][BN + kPadF];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t row_t = (int64_t)blockIdx.x * BM;
     const int col_t = blockIdx.y * BN;
-    const int lr = tid >> 2, lk = (tid & 3) * 8;  // loader: row / k offset
-    f32x16 acc;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+    const int ar = tid / (BK / AL), ak = (tid % (BK / AL)) * AL;
+    const int br = tid / (BK / BL), bk = (tid % (BK / BL)) * BL;
+    const int k_lo = blockIdx.z * a.kc;
+    const int k_hi = min(a.K, k_lo + a.kc);
 
-    for (int k0 = 0; k0 < a.K; k0 += BK) {
-        float va[8], vw[8];
-        load_a8<FAST_A>(a, row_t + lr, k0 + lk, va);
-        load_w8_f32<FAST_W>(a, col_t + lr, k0 + lk, vw);
-        __syncthreads();
+    f32x16 acc[TM][TN];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            As[lk + i][lr] = va[i];
-            Bs[lk + i][lr] = vw[i];
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    float ra[AL], rb[BL];
+    load_a<AL, FAST_A>(a, row_t + ar, k_lo + ak, ra);
+    load_w_f32<BL, FAST_W>(a, col_t + br, k_lo + bk, rb);
+#pragma unroll
+    for (int i = 0; i < AL; ++i) As[0][ak + i][ar] = ra[i];
+#pragma unroll
+    for (int i = 0; i < BL; ++i) Bs[0][bk + i][br] = rb[i];
+    __syncthreads();
+
+    int cur = 0;
+    for (int k0 = k_lo; k0 < k_hi; k0 += BK) {
+        const bool more = k0 + BK < k_hi;
+        if (more) {
+            load_a<AL, FAST_A>(a, row_t + ar, k0 + BK + ak, ra);
+            load_w_f32<BL, FAST_W>(a, col_t + br, k0 + BK + bk, rb);
         }
-        __syncthreads();
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 2) {
-            const float av = As[kk + (lane >> 5)][wm * 32 + (lane & 31)];
-            const float bv = Bs[kk + (lane >> 5)][wn * 32 + (lane & 31)];
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
+            float av[TM], bv[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) av[i] = As[cur][kk + (lane >> 5)][wm * (BM / 2) + i * 32 + (lane & 31)];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bv[j] = Bs[cur][kk + (lane >> 5)][wn * (BN / 2) + j * 32 + (lane & 31)];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
         }
+        if (more) {
+#pragma unroll
+            for (int i = 0; i < AL; ++i) As[cur ^ 1][ak + i][ar] = ra[i];
+#pragma unroll
+            for (int i = 0; i < BL; ++i) Bs[cur ^ 1][bk + i][br] = rb[i];
+        }
+        __syncthreads();
+        cur ^= 1;
     }
-    epilogue<EPI>(a, acc, row_t + wm * 32, col_t + wn * 32, lane, false);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            epilogue<EPI>(a, acc[i][j], row_t + wm * (BM / 2) + i * 32, col_t + wn * (BN / 2) + j * 32, lane);
 }
 
-template <int EPI, bool FAST_A, bool FAST_W>
+// bf16 MFMA GEMM, same structure with k-slices of 32 and row-major LDS
+// tiles (8 consecutive k per lane per MFMA operand).
+template <int BM, int BN, int EPI, bool FAST_A, bool FAST_W>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
-    __shared__ __attribute__((aligned(16))) uint16_t As[BM * kRowH];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * kRowH];
+    constexpr int BK = BKH;
+    constexpr int TM = BM / 64, TN = BN / 64;
+    constexpr int PA = BM / 64, PB = BN / 64;   // 8-element runs per thread per slice
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * kRowH];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * kRowH];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t row_t = (int64_t)blockIdx.x * BM;
     const int col_t = blockIdx.y * BN;
     const int lr = tid >> 2, lk = (tid & 3) * 8;
-    f32x16 acc;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+    const int k_lo = blockIdx.z * a.kc;
+    const int k_hi = min(a.K, k_lo + a.kc);
 
-    for (int k0 = 0; k0 < a.K; k0 += BK) {
-        const uint4 qa = load_a8_bf16<FAST_A>(a, row_t + lr, k0 + lk);
-        const uint4 qw = load_w8_bf16<FAST_W>(a, col_t + lr, k0 + lk);
-        __syncthreads();
-        *reinterpret_cast<uint4*>(As + lr * kRowH + lk) = qa;
-        *reinterpret_cast<uint4*>(Bs + lr * kRowH + lk) = qw;
-        __syncthreads();
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    uint4 qa[PA], qb[PB];
+#pragma unroll
+    for (int p = 0; p < PA; ++p) qa[p] = load_a8_bf16<FAST_A>(a, row_t + lr + 64 * p, k_lo + lk);
+#pragma unroll
+    for (int p = 0; p < PB; ++p) qb[p] = load_w8_bf16<FAST_W>(a, col_t + lr + 64 * p, k_lo + lk);
+#pragma unroll
+    for (int p = 0; p < PA; ++p) *reinterpret_cast<uint4*>(&As[0][(lr + 64 * p) * kRowH + lk]) = qa[p];
+#pragma unroll
+    for (int p = 0; p < PB; ++p) *reinterpret_cast<uint4*>(&Bs[0][(lr + 64 * p) * kRowH + lk]) = qb[p];
+    __syncthreads();
+
+    int cur = 0;
+    for (int k0 = k_lo; k0 < k_hi; k0 += BK) {
+        const bool more = k0 + BK < k_hi;
+        if (more) {
+#pragma unroll
+            for (int p = 0; p < PA; ++p) qa[p] = load_a8_bf16<FAST_A>(a, row_t + lr + 64 * p, k0 + BK + lk);
+#pragma unroll
+            for (int p = 0; p < PB; ++p) qb[p] = load_w8_bf16<FAST_W>(a, col_t + lr + 64 * p, k0 + BK + lk);
+        }
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 16) {
-            const bf16x8 av = *reinterpret_cast<const bf16x8*>(As + (wm * 32 + (lane & 31)) * kRowH + kk + 8 * (lane >> 5));
-            const bf16x8 bv = *reinterpret_cast<const bf16x8*>(Bs + (wn * 32 + (lane & 31)) * kRowH + kk + 8 * (lane >> 5));
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc, 0, 0, 0);
+            bf16x8 av[TM], bv[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                av[i] = *reinterpret_cast<const bf16x8*>(
+                    &As[cur][(wm * (BM / 2) + i * 32 + (lane & 31)) * kRowH + kk + 8 * (lane >> 5)]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                bv[j] = *reinterpret_cast<const bf16x8*>(
+                    &Bs[cur][(wn * (BN / 2) + j * 32 + (lane & 31)) * kRowH + kk + 8 * (lane >> 5)]);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
         }
+        if (more) {
+#pragma unroll
+            for (int p = 0; p < PA; ++p) *reinterpret_cast<uint4*>(&As[cur ^ 1][(lr + 64 * p) * kRowH + lk]) = qa[p];
+#pragma unroll
+            for (int p = 0; p < PB; ++p) *reinterpret_cast<uint4*>(&Bs[cur ^ 1][(lr + 64 * p) * kRowH + lk]) = qb[p];
+        }
+        __syncthreads();
+        cur ^= 1;
     }
-    epilogue<EPI>(a, acc, row_t + wm * 32, col_t + wn * 32, lane, true);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            epilogue<EPI>(a, acc[i][j], row_t + wm * (BM / 2) + i * 32, col_t + wn * (BN / 2) + j * 32, lane);
 }
 
-// Launch one layer.  epi: EPI_F32 / EPI_BF16 / EPI_POOL.
-static void launch_layer(const GemmArgs& a, bool bf16, int epi, hipStream_t s) {
-    const dim3 grid((unsigned)ceil_div(a.rows, BM), (unsigned)ceil_div(a.N, BN)), block(256);
-    const bool fast_w = (a.K % 8 == 0) && aligned(a.W, 16);
-    bool fast_a;
-    if (a.a_bf16) fast_a = a.c1 == 0 && a.c0 == a.K && a.K % 8 == 0 && a.ld0 % 8 == 0 && aligned(a.x0, 16);
-    else fast_a = a.c1 == 0 && a.c0 == a.K && a.K % 8 == 0 && a.ld0 % 4 == 0 && aligned(a.x0, 16);
-#define MESO_GEMM(KERN, E)                                                                           \
-    do {                                                                                             \
-        if (fast_a && fast_w) KERN<E, true, true><<<grid, block, 0, s>>>(a);                         \
-        else if (fast_w) KERN<E, false, true><<<grid, block, 0, s>>>(a);                             \
-        else KERN<E, false, false><<<grid, block, 0, s>>>(a);                                       \
-    } while (0)
-    if (bf16) {
-        if (epi == EPI_F32) MESO_GEMM(gemm_bf16_kernel, EPI_F32);
-        else if (epi == EPI_BF16) MESO_GEMM(gemm_bf16_kernel, EPI_BF16);
-        else MESO_GEMM(gemm_bf16_kernel, EPI_POOL);
-    } else {
-        if (epi == EPI_F32) MESO_GEMM(gemm_f32_kernel, EPI_F32);
-        else if (epi == EPI_BF16) MESO_GEMM(gemm_f32_kernel, EPI_BF16);
-        else MESO_GEMM(gemm_f32_kernel, EPI_POOL);
+// Split-K finish: sum the partial products in split order (deterministic),
+// then bias / ReLU / rounding and the store or pooled max.
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_finish_kernel(GemmArgs a, int splits) {
+    const int64_t n = a.rows * a.N;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = e / a.N;
+        const int col = (int)(e - row * a.N);
+        float t = 0.0f;
+        for (int z = 0; z < splits; ++z) t += a.part[(int64_t)z * n + e];
+        const float v = activate(a, t, a.bias ? a.bias[col] : 0.0f);
+        if constexpr (EPI == EPI_POOL)
+            atomicMax(static_cast<unsigned*>(a.y) + (row / a.G) * a.ldy + col, __float_as_uint(v));
+        else if constexpr (EPI == EPI_F32)
+            static_cast<float*>(a.y)[row * a.ldy + col] = v;
+        else
+            static_cast<uint16_t*>(a.y)[row * a.ldy + col] = f32_to_bf16(v);
     }
-#undef MESO_GEMM
+}
+
+struct LayerPlan {
+    int bm, bn, splits, kc;
+};
+
+// Tile shape and K split of one layer: a pure function of the shape, shared
+// by the workspace query and the launch.  Picks the tile with the smallest
+// estimated makespan (tile rounds x tile area) and, when even 64 x 64 tiles
+// leave most CUs idle, splits K.
+static LayerPlan plan_layer(int64_t rows, int N, int K, bool bf16) {
+    static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+    const int bk = bf16 ? BKH : BKF;
+    LayerPlan best{64, 64, 1, K};
+    double best_cost = 1e300;
+    for (const auto& c : cand) {
+        const int64_t tiles = ceil_div(rows, c[0]) * ceil_div(N, c[1]);
+        const double cost = (double)ceil_div(tiles, kTargetTiles) * c[0] * c[1];
+        if (cost < best_cost * (1.0 - 1e-9)) {
+            best_cost = cost;
+            best = {c[0], c[1], 1, K};
+        }
+    }
+    const int64_t tiles = ceil_div(rows, best.bm) * ceil_div(N, best.bn);
+    if (tiles < kTargetTiles / 2) {
+        int splits = 1;
+        while (tiles * splits * 2 <= kTargetTiles && K / (splits * 2) >= 4 * bk) splits *= 2;
+        if (splits > 1) {
+            const int kc = (int)ceil_div(ceil_div(K, splits), bk) * bk;
+            best.splits = (int)ceil_div(K, kc);
+            best.kc = kc;
+        }
+    }
+    return best;
 }
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Workspace: two ping-pong buffers for the intermediate activations.
-static size_t mlp_ws_bytes(int64_t rows, int n_layers, const int32_t* dims, int dtype) {
-    if (n_layers <= 1 || rows <= 0) return 0;
-    int64_t w = 0;
-    for (int l = 1; l < n_layers; ++l) w = std::max<int64_t>(w, dims[l]);
+// Workspace: two ping-pong buffers for the intermediate activations, then
+// the split-K partial sums of the largest split layer.
+struct MlpWs {
+    size_t act, part;
+};
+static MlpWs mlp_ws_layout(int64_t rows, int n_layers, const int32_t* dims, int dtype) {
+    MlpWs w{0, 0};
+    if (rows <= 0) return w;
+    int64_t width = 0;
+    for (int l = 1; l < n_layers; ++l) width = std::max<int64_t>(width, dims[l]);
     const size_t elem = dtype == MESORASI_BF16 ? 2 : 4;
-    const size_t one = align256((size_t)rows * (size_t)w * elem);
-    return n_layers == 2 ? one : 2 * one;
+    const size_t one = align256((size_t)rows * (size_t)width * elem);
+    w.act = n_layers <= 1 ? 0 : (n_layers == 2 ? one : 2 * one);
+    for (int l = 0; l < n_layers; ++l) {
+        const LayerPlan pl = plan_layer(rows, dims[l + 1], dims[l], dtype == MESORASI_BF16);
+        if (pl.splits > 1) w.part = std::max(w.part, align256((size_t)pl.splits * rows * dims[l + 1] * 4));
+    }
+    return w;
+}
+static size_t mlp_ws_bytes(int64_t rows, int n_layers, const int32_t* dims, int dtype) {
+    const MlpWs w = mlp_ws_layout(rows, n_layers, dims, dtype);
+    return w.act + w.part;
+}
+
+template <int BM, int BN, int EPI>
+static void launch_tile(const GemmArgs& a, bool bf16, bool fast_a, bool fast_w, dim3 grid, hipStream_t s) {
+    const dim3 block(256);
+    if (bf16) {
+        if (fast_a && fast_w) gemm_bf16_kernel<BM, BN, EPI, true, true><<<grid, block, 0, s>>>(a);
+        else if (fast_w) gemm_bf16_kernel<BM, BN, EPI, false, true><<<grid, block, 0, s>>>(a);
+        else gemm_bf16_kernel<BM, BN, EPI, false, false><<<grid, block, 0, s>>>(a);
+    } else {
+        if (fast_a && fast_w) gemm_f32_kernel<BM, BN, EPI, true, true><<<grid, block, 0, s>>>(a);
+        else if (fast_w) gemm_f32_kernel<BM, BN, EPI, false, true><<<grid, block, 0, s>>>(a);
+        else gemm_f32_kernel<BM, BN, EPI, false, false><<<grid, block, 0, s>>>(a);
+    }
+}
+
+template <int EPI>
+static void launch_epi(const GemmArgs& a, const LayerPlan& pl, bool bf16, bool fast_a, bool fast_w, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div(a.rows, pl.bm), (unsigned)ceil_div(a.N, pl.bn), (unsigned)pl.splits);
+    if (pl.bm == 128 && pl.bn == 128) launch_tile<128, 128, EPI>(a, bf16, fast_a, fast_w, grid, s);
+    else if (pl.bm == 128) launch_tile<128, 64, EPI>(a, bf16, fast_a, fast_w, grid, s);
+    else if (pl.bn == 128) launch_tile<64, 128, EPI>(a, bf16, fast_a, fast_w, grid, s);
+    else launch_tile<64, 64, EPI>(a, bf16, fast_a, fast_w, grid, s);
+}
+
+// Launch one layer.  epi: EPI_F32 / EPI_BF16 / EPI_POOL.
+static int launch_layer(GemmArgs a, bool bf16, int epi, float* part, hipStream_t s) {
+    const LayerPlan pl = plan_layer(a.rows, a.N, a.K, bf16);
+    a.kc = pl.kc;
+    const bool fast_w = (a.K % 8 == 0) && aligned(a.W, 16);
+    bool fast_a;
+    if (a.a_bf16) fast_a = a.c1 == 0 && a.c0 == a.K && a.K % 8 == 0 && a.ld0 % 8 == 0 && aligned(a.x0, 16);
+    else fast_a = a.c1 == 0 && a.c0 == a.K && a.K % 8 == 0 && a.ld0 % 4 == 0 && aligned(a.x0, 16);
+    if (pl.splits > 1) {
+        a.part = part;
+        launch_epi<EPI_PARTIAL>(a, pl, bf16, fast_a, fast_w, s);
+        int rc = after_launch("mesorasi_pointwise_mlp");
+        if (rc != MESORASI_OK) return rc;
+        const int64_t n = a.rows * a.N;
+        const dim3 grid((unsigned)std::min<int64_t>(ceil_div(n, 256), 4096)), block(256);
+        if (epi == EPI_POOL) splitk_finish_kernel<EPI_POOL><<<grid, block, 0, s>>>(a, pl.splits);
+        else if (epi == EPI_F32) splitk_finish_kernel<EPI_F32><<<grid, block, 0, s>>>(a, pl.splits);
+        else splitk_finish_kernel<EPI_BF16><<<grid, block, 0, s>>>(a, pl.splits);
+        return after_launch("mesorasi_pointwise_mlp");
+    }
+    if (epi == EPI_POOL) launch_epi<EPI_POOL>(a, pl, bf16, fast_a, fast_w, s);
+    else if (epi == EPI_F32) launch_epi<EPI_F32>(a, pl, bf16, fast_a, fast_w, s);
+    else launch_epi<EPI_BF16>(a, pl, bf16, fast_a, fast_w, s);
+    return after_launch("mesorasi_pointwise_mlp");
 }
 
 static int check_mlp_spec(const char* who, int64_t rows, int n_layers, const int32_t* dims, int dtype) {
@@ -322,7 +530,9 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
     int64_t w = 0;
     for (int l = 1; l < n_layers; ++l) w = std::max<int64_t>(w, dims[l]);
     const size_t one = align256((size_t)rows * (size_t)w * elem);
+    const MlpWs lay = mlp_ws_layout(rows, n_layers, dims, dtype);
     char* buf[2] = {static_cast<char*>(ws), static_cast<char*>(ws) + one};
+    float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + lay.act);
     if (pool_group > 0) {
         const int rc = zero_rows_f32(static_cast<float*>(y), rows / pool_group, dims[n_layers], ld_y, s);
         if (rc != MESORASI_OK) return rc;
@@ -341,6 +551,7 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
         a.W = W[l];
         a.bias = bias ? bias[l] : nullptr;
         a.relu = (relu_mask >> l) & 1u;
+        a.round_bf16 = bf16 ? 1 : 0;
         int epi;
         if (l + 1 < n_layers) {
             a.y = buf[l & 1];
@@ -352,8 +563,7 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
             a.G = pool_group;
             epi = pool_group > 0 ? EPI_POOL : (out_dtype == MESORASI_BF16 ? EPI_BF16 : EPI_F32);
         }
-        launch_layer(a, bf16, epi, s);
-        const int rc = after_launch("mesorasi_pointwise_mlp");
+        const int rc = launch_layer(a, bf16, epi, part, s);
         if (rc != MESORASI_OK) return rc;
     }
     return MESORASI_OK;
@@ -435,7 +645,7 @@ extern "C" int mesorasi_pointwise_mlp(const float* x0, int32_t c0, int64_t ld0, 
     const size_t need = mlp_ws_bytes(rows, n_layers, dims, dtype);
     MESO_REQUIRE(ws_bytes >= need && (need == 0 || ws), MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who,
                  ws_bytes, need);
-    MESO_REQUIRE(rows / BM < 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: too many rows", who);
+    MESO_REQUIRE(rows / 64 < 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: too many rows", who);
     return run_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, dtype, out_dtype, y, ld_y,
                    pool_group, ws, as_stream(stream));
 }
