@@ -8,9 +8,12 @@
 // of a row (4 fp32 or 8 bf16 channels); LPR lanes cover a row slice of
 // LPR*VEC channels, so one wave-wide load fetches RPW = 64/LPR neighbor rows
 // at once (a C = 128 fp32 PFT: 32 lanes per row, 2 rows per load).  The
-// running max lives in registers; the RPW partial maxima are folded with
-// cross-lane max at the end and one fp32 add/subtract applies the centroid
-// row.  Nothing N x K x C sized is ever written.  Wider PFTs are split into
+// centroid's NIT row is read once (one index per lane) and distributed by
+// cross-lane reads, so eight row gathers per lane are in flight at a time.
+// The running max lives in registers; the RPW partial maxima are folded
+// with cross-lane max at the end and one fp32 add/subtract applies the
+// centroid row.  Workgroups are renumbered so that each XCD's L2 serves a
+// contiguous range of clouds.  Nothing N x K x C sized is ever written.  Wider PFTs are split into
 // channel slices processed by different waves -- the column partitioning
 // of the paper's PFT buffer (Sec. 4.2, "PFT Partitioning").
 #include "common.h"
@@ -53,13 +56,18 @@ __device__ __forceinline__ void load_vec(const T* __restrict__ p, float (&v)[VEC
 template <typename T, int VEC, int LPR>
 __global__ __launch_bounds__(256) void aggregate_kernel(const T* __restrict__ pft, int64_t ldp,
                                                         const int32_t* __restrict__ nit, int N, int M, int K, int C,
-                                                        int chunks, int64_t total_waves,
+                                                        int chunks, int64_t total_waves, int per_xcd,
                                                         const int32_t* __restrict__ cidx,
                                                         const T* __restrict__ cfeat, int64_t ldc, int sign, int relu,
                                                         float* __restrict__ out, int64_t ldo) {
     constexpr int RPW = 64 / LPR;
     constexpr int CPW = LPR * VEC;
-    const int64_t gw = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    constexpr int U = 8;   // row loads in flight per lane
+    // Workgroups are dealt to the 8 XCDs round-robin by id; renumber them so
+    // each XCD runs one contiguous range of centroids (hence whole clouds),
+    // keeping a cloud's PFT rows in that XCD's L2.
+    const int64_t lb = (int64_t)(blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    const int64_t gw = lb * 4 + (threadIdx.x >> 6);
     if (gw >= total_waves) return;
     const int lane = threadIdx.x & 63;
     const int64_t c = gw / chunks;              // global centroid index in [0, B*M)
@@ -69,32 +77,46 @@ __global__ __launch_bounds__(256) void aggregate_kernel(const T* __restrict__ pf
     const int ch0 = chunk * CPW + (lane % LPR) * VEC;
     const bool active = ch0 < C;
     const int32_t* __restrict__ nrow = nit + c * K;
-    const T* __restrict__ cloud = pft + b * (int64_t)N * ldp;
+    const T* __restrict__ cloud = pft + b * (int64_t)N * ldp + ch0;
 
     float mx[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) mx[v] = -__builtin_huge_valf();
 
-    int k = sub;
-    for (; k + 3 * RPW < K; k += 4 * RPW) {
-        const int j0 = nrow[k], j1 = nrow[k + RPW], j2 = nrow[k + 2 * RPW], j3 = nrow[k + 3 * RPW];
-        if (active) {
-            float a0[VEC], a1[VEC], a2[VEC], a3[VEC];
-            load_vec<T, VEC>(cloud + (int64_t)j0 * ldp + ch0, a0);
-            load_vec<T, VEC>(cloud + (int64_t)j1 * ldp + ch0, a1);
-            load_vec<T, VEC>(cloud + (int64_t)j2 * ldp + ch0, a2);
-            load_vec<T, VEC>(cloud + (int64_t)j3 * ldp + ch0, a3);
+    for (int kb = 0; kb < K; kb += 64) {
+        // lane l holds neighbor kb + l of this centroid; rows are then
+        // addressed through cross-lane reads, so all gathers issue together
+        const int kn = min(64, K - kb);
+        const int jreg = lane < kn ? nrow[kb + lane] : 0;
+        const int nt = (kn + RPW - 1) / RPW;
+        int t = 0;
+        for (; t + U <= nt; t += U) {
+            float a[U][VEC];
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) mx[v] = fmaxf(fmaxf(mx[v], fmaxf(a0[v], a1[v])), fmaxf(a2[v], a3[v]));
+            for (int u = 0; u < U; ++u) {
+                const int k = sub + RPW * (t + u);
+                const int j = __shfl(jreg, k < kn ? k : 0);
+                if (active && k < kn) {
+                    load_vec<T, VEC>(cloud + (int64_t)j * ldp, a[u]);
+                } else {
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) a[u][v] = -__builtin_huge_valf();
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) mx[v] = fmaxf(mx[v], a[u][v]);
         }
-    }
-    for (; k < K; k += RPW) {
-        const int j = nrow[k];
-        if (active) {
-            float a[VEC];
-            load_vec<T, VEC>(cloud + (int64_t)j * ldp + ch0, a);
+        for (; t < nt; ++t) {
+            const int k = sub + RPW * t;
+            const int j = __shfl(jreg, k < kn ? k : 0);
+            if (active && k < kn) {
+                float a[VEC];
+                load_vec<T, VEC>(cloud + (int64_t)j * ldp, a);
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) mx[v] = fmaxf(mx[v], a[v]);
+                for (int v = 0; v < VEC; ++v) mx[v] = fmaxf(mx[v], a[v]);
+            }
         }
     }
     // fold the RPW row slots (lanes l, l + LPR, l + 2 LPR, ...)
@@ -109,7 +131,7 @@ __global__ __launch_bounds__(256) void aggregate_kernel(const T* __restrict__ pf
     for (int v = 0; v < VEC; ++v) r[v] = mx[v];
     if (cidx || cfeat) {
         float cen[VEC];
-        if (cidx) load_vec<T, VEC>(cloud + (int64_t)cidx[c] * ldp + ch0, cen);
+        if (cidx) load_vec<T, VEC>(cloud + (int64_t)cidx[c] * ldp, cen);
         else load_vec<T, VEC>(cfeat + c * ldc + ch0, cen);
 #pragma unroll
         for (int v = 0; v < VEC; ++v) r[v] = sign < 0 ? mx[v] - cen[v] : mx[v] + cen[v];
@@ -138,11 +160,13 @@ static void launch_aggregate(const T* pft, int64_t ldp, const int32_t* nit, int6
     while (lpr < lanes_needed && lpr < 64) lpr <<= 1;
     const int chunks = (C + lpr * VEC - 1) / (lpr * VEC);
     const int64_t total = B * (int64_t)M * chunks;
-    const dim3 grid((unsigned)ceil_div(total, 4)), block(256);
-#define MESO_AGG_CASE(L)                                                                                         \
-    case L:                                                                                                      \
-        aggregate_kernel<T, VEC, L><<<grid, block, 0, s>>>(pft, ldp, nit, N, M, K, C, chunks, total, cidx, cfeat, \
-                                                           ldc, sign, relu, out, ldo);                           \
+    const int64_t logical_blocks = ceil_div(total, 4);
+    const int per_xcd = (int)ceil_div(logical_blocks, 8);
+    const dim3 grid((unsigned)(8 * (int64_t)per_xcd)), block(256);
+#define MESO_AGG_CASE(L)                                                                                          \
+    case L:                                                                                                       \
+        aggregate_kernel<T, VEC, L><<<grid, block, 0, s>>>(pft, ldp, nit, N, M, K, C, chunks, total, per_xcd, cidx, \
+                                                           cfeat, ldc, sign, relu, out, ldo);                     \
         break;
     switch (lpr) {
         MESO_AGG_CASE(1)

@@ -24,6 +24,7 @@
 // after ReLU, so the max is an unsigned atomicMax on the float bits, which
 // is exact and order independent).
 #include "common.h"
+#include "mlp_internal.h"
 
 namespace meso {
 
@@ -71,55 +72,66 @@ __device__ __forceinline__ float a_elem(const GemmArgs& a, int64_t r, int k) {
 }
 
 // L consecutive input elements (r, k0 .. k0+L-1) as float, L in {4, 8}.
+// The fast form always loads from a clamped, in-bounds address and zeroes
+// out-of-range values by selection: no divergent branch, so a prefetch can
+// stay in flight across the MFMAs that follow it.
 template <int L, bool FAST>
-__device__ __forceinline__ void load_a(const GemmArgs& a, int64_t r, int k0, float (&v)[L]) {
+__device__ __forceinline__ void load_a(const GemmArgs& a, int64_t r, int k0, float (&v)[L], bool& ok) {
     if constexpr (FAST) {
-        // single fp32 source, 16-byte aligned rows, K a multiple of 8
-        if (r < a.rows && k0 < a.K) {
-            const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(a.x0) + r * a.ld0 + k0);
+        // single fp32 source, 16-byte aligned rows, K a multiple of 8; the
+        // caller zeroes the values when !ok (at its LDS store)
+        ok = r < a.rows && k0 < a.K;
+        const int64_t rc = ok ? r : 0;
+        const int kc = ok ? k0 : 0;
+        const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(a.x0) + rc * a.ld0 + kc);
 #pragma unroll
-            for (int h = 0; h < L / 4; ++h) {
-                const float4 u = p[h];
-                v[4 * h + 0] = u.x; v[4 * h + 1] = u.y; v[4 * h + 2] = u.z; v[4 * h + 3] = u.w;
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < L; ++i) v[i] = 0.0f;
+        for (int h = 0; h < L / 4; ++h) {
+            const float4 u = p[h];
+            v[4 * h + 0] = u.x;
+            v[4 * h + 1] = u.y;
+            v[4 * h + 2] = u.z;
+            v[4 * h + 3] = u.w;
         }
     } else {
+        ok = true;
 #pragma unroll
         for (int i = 0; i < L; ++i) v[i] = a_elem(a, r, k0 + i);
     }
 }
 
 template <int L, bool FAST>
-__device__ __forceinline__ void load_w_f32(const GemmArgs& a, int n, int k0, float (&v)[L]) {
+__device__ __forceinline__ void load_w_f32(const GemmArgs& a, int n, int k0, float (&v)[L], bool& ok) {
     const float* W = static_cast<const float*>(a.W);
     if constexpr (FAST) {
-        if (n < a.N && k0 < a.K) {
-            const float4* p = reinterpret_cast<const float4*>(W + (int64_t)n * a.K + k0);
+        ok = n < a.N && k0 < a.K;
+        const float4* p = reinterpret_cast<const float4*>(W + (int64_t)(ok ? n : 0) * a.K + (ok ? k0 : 0));
 #pragma unroll
-            for (int h = 0; h < L / 4; ++h) {
-                const float4 u = p[h];
-                v[4 * h + 0] = u.x; v[4 * h + 1] = u.y; v[4 * h + 2] = u.z; v[4 * h + 3] = u.w;
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < L; ++i) v[i] = 0.0f;
+        for (int h = 0; h < L / 4; ++h) {
+            const float4 u = p[h];
+            v[4 * h + 0] = u.x;
+            v[4 * h + 1] = u.y;
+            v[4 * h + 2] = u.z;
+            v[4 * h + 3] = u.w;
         }
         return;
     }
+    ok = true;
 #pragma unroll
     for (int i = 0; i < L; ++i) v[i] = (n < a.N && k0 + i < a.K) ? W[(int64_t)n * a.K + k0 + i] : 0.0f;
 }
 
+__device__ __forceinline__ uint4 select_u4(bool ok, uint4 q) {
+    return make_uint4(ok ? q.x : 0u, ok ? q.y : 0u, ok ? q.z : 0u, ok ? q.w : 0u);
+}
+
 template <bool FAST>
-__device__ __forceinline__ uint4 load_w8_bf16(const GemmArgs& a, int n, int k0) {
+__device__ __forceinline__ uint4 load_w8_bf16(const GemmArgs& a, int n, int k0, bool& ok) {
     const uint16_t* W = static_cast<const uint16_t*>(a.W);
     if (FAST) {
-        if (n < a.N && k0 < a.K) return *reinterpret_cast<const uint4*>(W + (int64_t)n * a.K + k0);
-        return make_uint4(0, 0, 0, 0);
+        ok = n < a.N && k0 < a.K;
+        return *reinterpret_cast<const uint4*>(W + (int64_t)(ok ? n : 0) * a.K + (ok ? k0 : 0));
     }
+    ok = true;
     uint16_t h[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) h[i] = (n < a.N && k0 + i < a.K) ? W[(int64_t)n * a.K + k0 + i] : (uint16_t)0;
@@ -133,12 +145,13 @@ __device__ __forceinline__ uint4 load_w8_bf16(const GemmArgs& a, int n, int k0) 
 
 // Load 8 input elements as bf16 bits (rounding fp32 sources to nearest even).
 template <bool FAST>
-__device__ __forceinline__ uint4 load_a8_bf16(const GemmArgs& a, int64_t r, int k0) {
+__device__ __forceinline__ uint4 load_a8_bf16(const GemmArgs& a, int64_t r, int k0, bool& ok) {
     if (a.a_bf16 && FAST) {
-        if (r < a.rows && k0 < a.K)
-            return *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.x0) + r * a.ld0 + k0);
-        return make_uint4(0, 0, 0, 0);
+        ok = r < a.rows && k0 < a.K;
+        return *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.x0) + (ok ? r : 0) * a.ld0 +
+                                               (ok ? k0 : 0));
     }
+    ok = true;
     uint16_t h[8];
     if (a.a_bf16) {
 #pragma unroll
@@ -146,9 +159,10 @@ __device__ __forceinline__ uint4 load_a8_bf16(const GemmArgs& a, int64_t r, int 
             h[i] = (r < a.rows && k0 + i < a.c0) ? static_cast<const uint16_t*>(a.x0)[r * a.ld0 + k0 + i] : (uint16_t)0;
     } else {
         float v[8];
-        load_a<8, FAST>(a, r, k0, v);
+        bool okv;
+        load_a<8, FAST>(a, r, k0, v, okv);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) h[i] = f32_to_bf16(v[i]);
+        for (int i = 0; i < 8; ++i) h[i] = f32_to_bf16(okv ? v[i] : 0.0f);
     }
     uint4 q;
     q.x = h[0] | ((uint32_t)h[1] << 16);
@@ -255,40 +269,43 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     float ra[AL], rb[BL];
-    load_a<AL, FAST_A>(a, row_t + ar, k_lo + ak, ra);
-    load_w_f32<BL, FAST_W>(a, col_t + br, k_lo + bk, rb);
+    bool oka, okb;
+    load_a<AL, FAST_A>(a, row_t + ar, k_lo + ak, ra, oka);
+    load_w_f32<BL, FAST_W>(a, col_t + br, k_lo + bk, rb, okb);
 #pragma unroll
-    for (int i = 0; i < AL; ++i) As[0][ak + i][ar] = ra[i];
+    for (int i = 0; i < AL; ++i) As[0][ak + i][ar] = oka ? ra[i] : 0.0f;
 #pragma unroll
-    for (int i = 0; i < BL; ++i) Bs[0][bk + i][br] = rb[i];
+    for (int i = 0; i < BL; ++i) Bs[0][bk + i][br] = okb ? rb[i] : 0.0f;
     __syncthreads();
 
     int cur = 0;
     for (int k0 = k_lo; k0 < k_hi; k0 += BK) {
-        const bool more = k0 + BK < k_hi;
-        if (more) {
-            load_a<AL, FAST_A>(a, row_t + ar, k0 + BK + ak, ra);
-            load_w_f32<BL, FAST_W>(a, col_t + br, k0 + BK + bk, rb);
+        // prefetch the next slice (the loaders zero-fill past K, so the last
+        // iteration's prefetch is harmless and the loads stay unconditional)
+        load_a<AL, FAST_A>(a, row_t + ar, k0 + BK + ak, ra, oka);
+        load_w_f32<BL, FAST_W>(a, col_t + br, k0 + BK + bk, rb, okb);
+        // all operands of this slice into registers first, then the MFMAs
+        float av[BK / 2][TM], bv[BK / 2][TN];
+#pragma unroll
+        for (int kk = 0; kk < BK / 2; ++kk) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) av[kk][i] = As[cur][2 * kk + (lane >> 5)][wm * (BM / 2) + i * 32 + (lane & 31)];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bv[kk][j] = Bs[cur][2 * kk + (lane >> 5)][wn * (BN / 2) + j * 32 + (lane & 31)];
         }
+        __builtin_amdgcn_sched_barrier(0);   // keep the operand reads ahead of the MFMAs
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 2) {
-            float av[TM], bv[TN];
-#pragma unroll
-            for (int i = 0; i < TM; ++i) av[i] = As[cur][kk + (lane >> 5)][wm * (BM / 2) + i * 32 + (lane & 31)];
-#pragma unroll
-            for (int j = 0; j < TN; ++j) bv[j] = Bs[cur][kk + (lane >> 5)][wn * (BN / 2) + j * 32 + (lane & 31)];
+        for (int kk = 0; kk < BK / 2; ++kk)
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
-        }
-        if (more) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[kk][i], bv[kk][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);   // next slice's LDS stores after all MFMAs
 #pragma unroll
-            for (int i = 0; i < AL; ++i) As[cur ^ 1][ak + i][ar] = ra[i];
+        for (int i = 0; i < AL; ++i) As[cur ^ 1][ak + i][ar] = oka ? ra[i] : 0.0f;
 #pragma unroll
-            for (int i = 0; i < BL; ++i) Bs[cur ^ 1][bk + i][br] = rb[i];
-        }
+        for (int i = 0; i < BL; ++i) Bs[cur ^ 1][bk + i][br] = okb ? rb[i] : 0.0f;
         __syncthreads();
         cur ^= 1;
     }
@@ -312,7 +329,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t row_t = (int64_t)blockIdx.x * BM;
     const int col_t = blockIdx.y * BN;
-    const int lr = tid >> 2, lk = (tid & 3) * 8;
+    const int lr = tid >> 2, lk = (tid & 3) * 8;   // 64 rows x 32 k per pass
     const int k_lo = blockIdx.z * a.kc;
     const int k_hi = min(a.K, k_lo + a.kc);
 
@@ -325,48 +342,51 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     uint4 qa[PA], qb[PB];
+    bool oka[PA], okb[PB];
 #pragma unroll
-    for (int p = 0; p < PA; ++p) qa[p] = load_a8_bf16<FAST_A>(a, row_t + lr + 64 * p, k_lo + lk);
+    for (int p = 0; p < PA; ++p) qa[p] = load_a8_bf16<FAST_A>(a, row_t + lr + 64 * p, k_lo + lk, oka[p]);
 #pragma unroll
-    for (int p = 0; p < PB; ++p) qb[p] = load_w8_bf16<FAST_W>(a, col_t + lr + 64 * p, k_lo + lk);
+    for (int p = 0; p < PB; ++p) qb[p] = load_w8_bf16<FAST_W>(a, col_t + lr + 64 * p, k_lo + lk, okb[p]);
 #pragma unroll
-    for (int p = 0; p < PA; ++p) *reinterpret_cast<uint4*>(&As[0][(lr + 64 * p) * kRowH + lk]) = qa[p];
+    for (int p = 0; p < PA; ++p) *reinterpret_cast<uint4*>(&As[0][(lr + 64 * p) * kRowH + lk]) = select_u4(oka[p], qa[p]);
 #pragma unroll
-    for (int p = 0; p < PB; ++p) *reinterpret_cast<uint4*>(&Bs[0][(lr + 64 * p) * kRowH + lk]) = qb[p];
+    for (int p = 0; p < PB; ++p) *reinterpret_cast<uint4*>(&Bs[0][(lr + 64 * p) * kRowH + lk]) = select_u4(okb[p], qb[p]);
     __syncthreads();
 
     int cur = 0;
     for (int k0 = k_lo; k0 < k_hi; k0 += BK) {
-        const bool more = k0 + BK < k_hi;
-        if (more) {
+        // unconditional prefetch of the next slice (zero-filled past K)
 #pragma unroll
-            for (int p = 0; p < PA; ++p) qa[p] = load_a8_bf16<FAST_A>(a, row_t + lr + 64 * p, k0 + BK + lk);
+        for (int p = 0; p < PA; ++p) qa[p] = load_a8_bf16<FAST_A>(a, row_t + lr + 64 * p, k0 + BK + lk, oka[p]);
 #pragma unroll
-            for (int p = 0; p < PB; ++p) qb[p] = load_w8_bf16<FAST_W>(a, col_t + lr + 64 * p, k0 + BK + lk);
-        }
+        for (int p = 0; p < PB; ++p) qb[p] = load_w8_bf16<FAST_W>(a, col_t + lr + 64 * p, k0 + BK + lk, okb[p]);
+        bf16x8 av[BK / 16][TM], bv[BK / 16][TN];
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 16) {
-            bf16x8 av[TM], bv[TN];
+        for (int kk = 0; kk < BK / 16; ++kk) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
-                av[i] = *reinterpret_cast<const bf16x8*>(
-                    &As[cur][(wm * (BM / 2) + i * 32 + (lane & 31)) * kRowH + kk + 8 * (lane >> 5)]);
+                av[kk][i] = *reinterpret_cast<const bf16x8*>(
+                    &As[cur][(wm * (BM / 2) + i * 32 + (lane & 31)) * kRowH + 16 * kk + 8 * (lane >> 5)]);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                bv[j] = *reinterpret_cast<const bf16x8*>(
-                    &Bs[cur][(wn * (BN / 2) + j * 32 + (lane & 31)) * kRowH + kk + 8 * (lane >> 5)]);
+                bv[kk][j] = *reinterpret_cast<const bf16x8*>(
+                    &Bs[cur][(wn * (BN / 2) + j * 32 + (lane & 31)) * kRowH + 16 * kk + 8 * (lane >> 5)]);
+        }
+        __builtin_amdgcn_sched_barrier(0);   // keep the operand reads ahead of the MFMAs
+#pragma unroll
+        for (int kk = 0; kk < BK / 16; ++kk)
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
-        }
-        if (more) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[kk][i], bv[kk][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);   // next slice's LDS stores after all MFMAs
 #pragma unroll
-            for (int p = 0; p < PA; ++p) *reinterpret_cast<uint4*>(&As[cur ^ 1][(lr + 64 * p) * kRowH + lk]) = qa[p];
+        for (int p = 0; p < PA; ++p)
+            *reinterpret_cast<uint4*>(&As[cur ^ 1][(lr + 64 * p) * kRowH + lk]) = select_u4(oka[p], qa[p]);
 #pragma unroll
-            for (int p = 0; p < PB; ++p) *reinterpret_cast<uint4*>(&Bs[cur ^ 1][(lr + 64 * p) * kRowH + lk]) = qb[p];
-        }
+        for (int p = 0; p < PB; ++p)
+            *reinterpret_cast<uint4*>(&Bs[cur ^ 1][(lr + 64 * p) * kRowH + lk]) = select_u4(okb[p], qb[p]);
         __syncthreads();
         cur ^= 1;
     }
@@ -453,6 +473,7 @@ static MlpWs mlp_ws_layout(int64_t rows, int n_layers, const int32_t* dims, int 
     return w;
 }
 static size_t mlp_ws_bytes(int64_t rows, int n_layers, const int32_t* dims, int dtype) {
+    if (fused_mlp_supported(n_layers, dims, dtype)) return 0;
     const MlpWs w = mlp_ws_layout(rows, n_layers, dims, dtype);
     return w.act + w.part;
 }
@@ -525,6 +546,9 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
                    int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
                    uint32_t relu_mask, int dtype, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, void* ws,
                    hipStream_t s) {
+    if (fused_mlp_supported(n_layers, dims, dtype))
+        return run_fused_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, out_dtype, y, ld_y,
+                             pool_group, s);
     const bool bf16 = dtype == MESORASI_BF16;
     const size_t elem = bf16 ? 2 : 4;
     int64_t w = 0;

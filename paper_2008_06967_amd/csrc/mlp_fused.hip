@@ -1,0 +1,271 @@
+// Fused multi-layer shared MLP for narrow layers, gfx950.
+//
+// With delayed aggregation the MLP runs on the N input points, so its layer
+// outputs are small enough to stay on chip (Sec. 3.2: layer outputs shrink
+// from 8-32 MB to 512 KB-1 MB).  A workgroup keeps one 64-row tile's
+// activations in LDS through all layers (k-major, odd stride); only the last
+// layer goes to HBM (or is pooled).
+//
+// Weights never pass through LDS.  Within each 16-wide k-slice the MFMA
+// steps use a permuted k order -- lane l at step i takes k = 8*(l/32) + i --
+// which MFMA allows as long as both operands agree.  Then the 8 B-operands a
+// lane needs for one slice and one 32-column block are 8 consecutive floats
+// of one row of W ([C_out, C_in] row-major): two 16-byte loads, fetched a
+// slice ahead into registers.  A-operands come from the resident LDS tile.
+// Each wave owns whole 32-column blocks (both 32-row halves), so every
+// weight is fetched once per workgroup and a layer needs no barrier.
+// MFMA: v_mfma_f32_32x32x2_f32 (fp32 in, fp32 accumulate).
+// Used for fp32 MLPs whose layer inputs are at most 160 wide and whose
+// outputs are at most 128 wide; other MLPs run layer by layer (mlp.hip).
+#include "common.h"
+#include "mlp_internal.h"
+
+namespace meso {
+
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int FBM = 64;        // rows per workgroup (two 32-row halves)
+constexpr int FST = FBM + 1;   // k-major activation stride (odd: conflict-free)
+constexpr int kMaxIn = 160;    // widest layer input kept in LDS (padded to 16)
+constexpr int kMaxOut = 128;   // widest layer output: 4 column blocks, one per wave
+
+struct FusedArgs {
+    const float* x0;
+    int64_t ld0;
+    const float* x1;
+    int64_t ld1;
+    int c0, c1;
+    int64_t rows;
+    int n_layers;
+    int dims[MESORASI_MAX_LAYERS + 1];
+    const float* W[MESORASI_MAX_LAYERS];
+    const float* bias[MESORASI_MAX_LAYERS];
+    uint32_t relu_mask;
+    void* y;
+    int64_t ldy;
+    int out_bf16;
+    int64_t G;      // pool group (0: store)
+    int hsize;      // floats per activation buffer
+};
+
+__host__ __device__ __forceinline__ int pad16(int x) { return (x + 15) & ~15; }
+
+// 8 consecutive weights W[n][k .. k+7] of a row, zero where k >= K or n >= N.
+// 16-byte loads when the row is aligned and fully inside; element loads
+// (from clamped, in-bounds addresses) otherwise.
+__device__ __forceinline__ void load_w8(const float* __restrict__ W, int n, int N, int k, int K, bool vec,
+                                        float (&v)[8]) {
+    const bool nok = n < N;
+    const float* row = W + (int64_t)(nok ? n : 0) * K;
+    if (vec && k + 8 <= K) {
+        const float4 a = *reinterpret_cast<const float4*>(row + k);
+        const float4 b = *reinterpret_cast<const float4*>(row + k + 4);
+        v[0] = nok ? a.x : 0.0f; v[1] = nok ? a.y : 0.0f; v[2] = nok ? a.z : 0.0f; v[3] = nok ? a.w : 0.0f;
+        v[4] = nok ? b.x : 0.0f; v[5] = nok ? b.y : 0.0f; v[6] = nok ? b.z : 0.0f; v[7] = nok ? b.w : 0.0f;
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const bool ok = nok && k + i < K;
+            const float w = row[ok ? k + i : 0];
+            v[i] = ok ? w : 0.0f;
+        }
+    }
+}
+
+// One layer: hin [K][FST] (LDS) x W^T -> CB column blocks of 32 per wave.
+template <int CB>
+__device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const float* __restrict__ hin,
+                                            float* __restrict__ hout, int64_t row_t, int tid, int lane, int wave) {
+    const int K = a.dims[l], N = a.dims[l + 1];
+    const float* __restrict__ W = a.W[l];
+    const int ncb = (N + 31) / 32;
+    const bool last = l + 1 == a.n_layers;
+    const bool vec = (K % 4) == 0 && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
+    const int kh = 8 * (lane >> 5);              // this lane's half of each 16-slice
+    const int cl = lane & 31;
+
+    // column blocks of this wave: cb = wave + 4 j; blocks past ncb repeat a
+    // valid block (discarded) so the MFMA chain stays unconditional
+    int cbs[CB];
+#pragma unroll
+    for (int j = 0; j < CB; ++j) cbs[j] = (wave + 4 * j < ncb) ? wave + 4 * j : min(wave, ncb - 1);
+
+    f32x16 acc[CB][2];
+#pragma unroll
+    for (int j = 0; j < CB; ++j)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[j][h][r] = 0.0f;
+
+    float wb[2][CB][8];
+#pragma unroll
+    for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + cl, N, kh, K, vec, wb[0][j]);
+    const float* hrow = hin + kh * FST + cl;
+
+    for (int k0 = 0; k0 < K; k0 += 32) {
+        // two slices per trip so the double-buffered weights keep static indices
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int ks = k0 + 16 * half;
+            if (ks >= K) break;
+#pragma unroll
+            for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + cl, N, ks + 16 + kh, K, vec, wb[half ^ 1][j]);
+            float av[8][2];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                av[i][0] = hrow[(ks + i) * FST];
+                av[i][1] = hrow[(ks + i) * FST + 32];
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int j = 0; j < CB; ++j)
+#pragma unroll
+                    for (int h = 0; h < 2; ++h)
+                        acc[j][h] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][h], wb[half][j][i], acc[j][h], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
+    // epilogue: bias + ReLU, then LDS (next layer's input) or HBM
+    const bool relu = (a.relu_mask >> l) & 1u;
+    const float* __restrict__ bias = a.bias[l];
+#pragma unroll
+    for (int j = 0; j < CB; ++j) {
+        if (wave + 4 * j >= ncb) continue;
+        const int col = cbs[j] * 32 + cl;
+        const bool col_ok = col < N;
+        const float bv = (col_ok && bias) ? bias[col] : 0.0f;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int rbase = h * 32 + 4 * (lane >> 5);
+            if (!last) {
+                if (col_ok) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        float t = acc[j][h][r] + bv;
+                        if (relu) t = t > 0.0f ? t : 0.0f;
+                        hout[col * FST + rbase + 8 * (r >> 2) + (r & 3)] = t;
+                    }
+                }
+            } else if (a.G > 0) {
+                unsigned* yu = static_cast<unsigned*>(a.y);
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = row_t + rbase + 8 * (r >> 2) + (r & 3);
+                    float t = acc[j][h][r] + bv;
+                    t = t > 0.0f ? t : 0.0f;   // pooling requires a final ReLU
+                    if (col_ok && row < a.rows) atomicMax(yu + (row / a.G) * a.ldy + col, __float_as_uint(t));
+                }
+            } else {
+                const int64_t row0 = row_t + rbase;
+                if (a.out_bf16) {
+                    uint16_t* yb = static_cast<uint16_t*>(a.y) + row0 * a.ldy + col;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int dr = 8 * (r >> 2) + (r & 3);
+                        float t = acc[j][h][r] + bv;
+                        if (relu) t = t > 0.0f ? t : 0.0f;
+                        if (col_ok && row0 + dr < a.rows) yb[dr * a.ldy] = f32_to_bf16(t);
+                    }
+                } else {
+                    float* yf = static_cast<float*>(a.y) + row0 * a.ldy + col;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int dr = 8 * (r >> 2) + (r & 3);
+                        float t = acc[j][h][r] + bv;
+                        if (relu) t = t > 0.0f ? t : 0.0f;
+                        if (col_ok && row0 + dr < a.rows) yf[dr * a.ldy] = t;
+                    }
+                }
+            }
+        }
+    }
+    if (!last) {
+        // zero the k-padding rows of the next input so 0 * garbage never appears
+        const int Np = pad16(N);
+        for (int e = tid; e < (Np - N) * FBM; e += 256) hout[(N + e / FBM) * FST + (e % FBM)] = 0.0f;
+    }
+    __syncthreads();
+}
+
+// One 32-column block per wave (outputs up to 128 wide); the register budget
+// leaves room for three workgroups per CU, which hide each other's memory
+// latency.  (Wider outputs measured slower than the per-layer GEMMs.)
+template <int CB>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+void mlp_fused_f32_kernel(FusedArgs a) {
+    extern __shared__ float smem[];
+    float* H0 = smem;
+    float* H1 = smem + a.hsize;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t row_t = (int64_t)blockIdx.x * FBM;
+
+    // layer-0 input tile -> H0 (k-major), zero beyond c0 + c1 up to the slice edge
+    {
+        const int K0 = a.c0 + a.c1, K0p = pad16(K0);
+        for (int e = tid; e < FBM * K0p; e += 256) {
+            const int r = e / K0p, k = e - r * K0p;
+            const int64_t row = row_t + r;
+            float v = 0.0f;
+            if (row < a.rows) {
+                if (k < a.c0) v = a.x0[row * a.ld0 + k];
+                else if (k < K0) v = a.x1[row * a.ld1 + (k - a.c0)];
+            }
+            H0[k * FST + r] = v;
+        }
+    }
+    __syncthreads();
+
+    for (int l = 0; l < a.n_layers; ++l) {
+        const float* hin = (l & 1) ? H1 : H0;
+        float* hout = (l & 1) ? H0 : H1;
+        fused_layer<CB>(a, l, hin, hout, row_t, tid, lane, wave);
+    }
+}
+
+}  // namespace
+
+bool fused_mlp_supported(int n_layers, const int32_t* dims, int dtype) {
+    if (dtype != MESORASI_F32 || n_layers < 2) return false;
+    for (int l = 0; l < n_layers; ++l)
+        if (pad16(dims[l]) > kMaxIn) return false;
+    for (int l = 1; l <= n_layers; ++l)
+        if (dims[l] > kMaxOut) return false;
+    return true;
+}
+
+int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
+                  int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
+                  uint32_t relu_mask, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, hipStream_t s) {
+    FusedArgs a{};
+    a.x0 = x0; a.ld0 = ld0; a.x1 = x1; a.ld1 = ld1; a.c0 = c0; a.c1 = c1;
+    a.rows = rows;
+    a.n_layers = n_layers;
+    int hmax = 16;
+    for (int l = 0; l <= n_layers; ++l) a.dims[l] = dims[l];
+    for (int l = 0; l < n_layers; ++l) {
+        a.W[l] = static_cast<const float*>(W[l]);
+        a.bias[l] = bias ? bias[l] : nullptr;
+        hmax = std::max(hmax, pad16(dims[l]));   // every layer input (the last output goes to HBM)
+    }
+    a.relu_mask = relu_mask;
+    a.y = y;
+    a.ldy = ld_y;
+    a.out_bf16 = out_dtype == MESORASI_BF16;
+    a.G = pool_group;
+    a.hsize = hmax * FST;
+    const size_t lds = sizeof(float) * 2 * (size_t)a.hsize;
+    if (pool_group > 0) {
+        const int rc = zero_rows_f32(static_cast<float*>(y), rows / pool_group, dims[n_layers], ld_y, s);
+        if (rc != MESORASI_OK) return rc;
+    }
+    mlp_fused_f32_kernel<1><<<dim3((unsigned)ceil_div(rows, FBM)), dim3(256), lds, s>>>(a);
+    return after_launch("mesorasi_pointwise_mlp (fused)");
+}
+
+}  // namespace meso

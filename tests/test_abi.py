@@ -92,10 +92,12 @@ def test_mlp_validation_and_workspace():
         _lib.EUNSUPPORTED
     # rows % pool_group
     assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 128, 3, FAKE, 1 << 20, NULL) == _lib.EINVAL
-    # workspace too small
-    need = L.mesorasi_pointwise_mlp_workspace(10, 3, d, 0, 0)
+    # narrow fp32 MLPs run fused and need no workspace; wide ones run layer by layer
+    assert L.mesorasi_pointwise_mlp_workspace(10, 3, d, 0, 0) == 0
+    dw, Ww, bw = _mlp_args([3, 200, 200, 256])
+    need = L.mesorasi_pointwise_mlp_workspace(10, 3, dw, 0, 0)
     assert need > 0
-    assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 128, 0, FAKE, need - 1, NULL) == \
+    assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, dw, Ww, bw, 7, 0, 0, FAKE, 256, 0, FAKE, need - 1, NULL) == \
         _lib.EWORKSPACE
     # ld_y < width
     assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 64, 0, FAKE, need, NULL) == _lib.EINVAL
@@ -106,11 +108,12 @@ def test_mlp_validation_and_workspace():
     # one layer needs no workspace; two need one buffer, three need two
     d1, _, _ = _mlp_args([3, 8])
     assert L.mesorasi_pointwise_mlp_workspace(100, 1, d1, 0, 0) == 0
-    d2, _, _ = _mlp_args([3, 8, 8])
-    d3, _, _ = _mlp_args([3, 8, 8, 8])
-    one = L.mesorasi_pointwise_mlp_workspace(100, 2, d2, 0, 0)
-    assert one >= 100 * 8 * 4 and L.mesorasi_pointwise_mlp_workspace(100, 3, d3, 0, 0) == 2 * one
-    assert L.mesorasi_pointwise_mlp_workspace(100, 2, d2, 1, 0) < one   # bf16 activations are half the size
+    d2, _, _ = _mlp_args([3, 200, 200])
+    d3, _, _ = _mlp_args([3, 200, 200, 200])
+    one = L.mesorasi_pointwise_mlp_workspace(1000, 2, d2, 0, 0)
+    # (includes split-K partial sums when the tile grid is small)
+    assert one >= 1000 * 200 * 4 and L.mesorasi_pointwise_mlp_workspace(1000, 3, d3, 0, 0) >= one + 1000 * 200 * 4
+    assert L.mesorasi_pointwise_mlp_workspace(1000, 2, d2, 1, 0) < one   # bf16 activations are half the size
     assert st(f, NULL, 3, 3, NULL, 0, 0, 0, 3, d, W, b, 7, 0, 0, NULL, 128, 0, NULL, 0, NULL) == _lib.OK  # rows = 0
 
 
