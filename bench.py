@@ -4,7 +4,10 @@ delayed aggregation, on one MI355X.
 One step = one full forward of the batch (FPS, ball query, per-point MLP,
 aggregation for both set-abstraction levels, group-all MLP, FC head).
 Inputs and weights are resident in HBM before timing; the timed steps
-replay a HIP graph of the two-stream forward.  The JSON line also carries:
+replay HIP graphs of the two-stream forward; independent batches may be
+kept in flight on separate streams (the count that gives the highest
+throughput among 1-4 is used and reported, with the single-batch latency).
+The JSON line also carries:
   - conventional: the same network in the original order (Eq. (1)) on the
     GPU and the delayed/conventional speedup;
   - stages: per-kernel-call durations from HIP events on the stream each
@@ -188,23 +191,34 @@ def main():
     print(f"[bench] workload={args.workload} B={B} N={spec['N']} steps={args.steps} warmup={args.warmup}",
           file=sys.stderr, flush=True)
 
-    def time_net(delayed, steps, warmup, graph):
-        net = nets.build(spec, w, delayed=delayed, device=dev)
-        if graph:
-            g, _ = net.capture(xyz, feat)
-            run = g.replay
-        else:
-            run = lambda: net.forward(xyz, feat)
-        for _ in range(warmup):
-            run()
+    def time_net(delayed, steps, warmup, graph, inflight=1):
+        """Seconds per step.  inflight > 1 keeps that many independent
+        batches in flight: each has its own network buffers and graph and
+        is replayed on its own stream, round-robin, so one batch's search
+        chain overlaps another's MLP chain."""
+        nets_ = [nets.build(spec, w, delayed=delayed, device=dev) for _ in range(inflight)]
+        streams = [torch.cuda.Stream(device=dev) for _ in range(inflight)]
+        runs = []
+        for net in nets_:
+            if graph:
+                g, _ = net.capture(xyz, feat)
+                runs.append(g.replay)
+            else:
+                runs.append(lambda net=net: net.forward(xyz, feat))
+        def step(i):
+            with torch.cuda.stream(streams[i % inflight]):
+                runs[i % inflight]()
+        for i in range(warmup):
+            step(i)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for _ in range(steps):
-            run()
+        for i in range(steps):
+            step(i)
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) / steps
 
     if args.calibrate_copy:
+        # a plain device copy of known size, for scaling FETCH_SIZE/WRITE_SIZE
         src = torch.empty(64 << 20, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
         for _ in range(3):
@@ -214,12 +228,23 @@ def main():
               file=sys.stderr, flush=True)
         del src, dst
 
-    # timed region: delayed forward, graph replay (or eager with --eager)
-    t_step = time_net(True, args.steps, args.warmup, not args.eager)
-    print(f"[bench] delayed {t_step * 1e3:.3f} ms/step", file=sys.stderr, flush=True)
-    t_conv = time_net(False, max(5, args.steps // 2), 2, not args.eager)
-    print(f"[bench] conventional {t_conv * 1e3:.3f} ms/step", file=sys.stderr, flush=True)
-    t_step_eager = time_net(True, max(5, args.steps // 2), 2, False)
+    graph = not args.eager
+    # single-batch latency (one batch at a time)
+    t_latency = time_net(True, args.steps, args.warmup, graph, 1)
+    print(f"[bench] delayed, 1 batch in flight: {t_latency * 1e3:.3f} ms/step", file=sys.stderr, flush=True)
+    # throughput with independent batches overlapping
+    per_inflight = {1: t_latency}
+    for k in (2, 3, 4):
+        per_inflight[k] = time_net(True, args.steps, args.warmup, graph, k)
+        print(f"[bench] delayed, {k} batches in flight: {per_inflight[k] * 1e3:.3f} ms/step", file=sys.stderr,
+              flush=True)
+    inflight = min(per_inflight, key=lambda k: per_inflight[k])
+    t_step = per_inflight[inflight]
+    t_conv_lat = time_net(False, max(5, args.steps // 2), 2, graph, 1)
+    t_conv = time_net(False, max(5, args.steps // 2), 2, graph, inflight)
+    print(f"[bench] conventional {t_conv_lat * 1e3:.3f} ms/step (1 in flight), {t_conv * 1e3:.3f} ({inflight})",
+          file=sys.stderr, flush=True)
+    t_step_eager = time_net(True, max(5, args.steps // 2), 2, False, 1)
 
     # per-call durations (eager pass with events on each call's stream)
     timer = StageTimer(ops)
@@ -228,6 +253,9 @@ def main():
     net.forward(xyz, feat)
     torch.cuda.synchronize()
     timer.active = True
+    # hold the streams behind a spin kernel while every call is enqueued, so
+    # each event pair brackets GPU execution only (no host launch gaps)
+    torch.cuda._sleep(int(2e8))
     for _ in range(max(5, args.steps // 2)):
         timer.begin_step()
         net.forward(xyz, feat)
@@ -278,10 +306,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{args.workload} (PointNet++ SSG classifier, delayed aggregation)",
                    "global_batch": B, "points": spec["N"], "path": "delayed",
-                   "timing": "eager launches" if args.eager else "HIP graph replay, search chain on a side stream",
-                   "parallelism": "single GPU"},
+                   "timing": ("eager launches" if args.eager else "HIP graph replay, search chain on a side stream")
+                   + f", {inflight} independent batch(es) in flight on separate streams",
+                   "batches_in_flight": inflight, "parallelism": "single GPU"},
+        "latency_ms_per_batch": t_latency * 1e3,
+        "clouds_per_s_by_batches_in_flight": {str(k): B / v for k, v in per_inflight.items()},
         "centroids_per_s": per_module,
-        "conventional": {"ms_per_step": t_conv * 1e3, "clouds_per_s": B / t_conv, "speedup_delayed": t_conv / t_step},
+        "conventional": {"ms_per_step": t_conv * 1e3, "clouds_per_s": B / t_conv, "speedup_delayed": t_conv / t_step,
+                         "latency_ms_per_batch": t_conv_lat * 1e3,
+                         "latency_speedup_delayed": t_conv_lat / t_latency},
         "eager_ms_per_step": t_step_eager * 1e3,
         "stages_ms": {k: round(v, 5) for k, v in stages.items()},
         "stage_roofline": roofs,

@@ -154,12 +154,28 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
                 }
             } else if (a.G > 0) {
                 unsigned* yu = static_cast<unsigned*>(a.y);
+                const int64_t half0 = row_t + h * 32;   // 32-row half, a multiple of 32
+                if (a.G % 32 == 0) {
+                    // the whole half lies in one group: fold its 32 rows first.
+                    // ReLU by comparison maps -0 to +0, so every folded value
+                    // has a non-negative bit pattern (unsigned atomicMax order)
+                    float m = 0.0f;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int64_t row = row_t + rbase + 8 * (r >> 2) + (r & 3);
-                    float t = acc[j][h][r] + bv;
-                    t = t > 0.0f ? t : 0.0f;   // pooling requires a final ReLU
-                    if (col_ok && row < a.rows) atomicMax(yu + (row / a.G) * a.ldy + col, __float_as_uint(t));
+                    for (int r = 0; r < 16; ++r) {
+                        const float t = acc[j][h][r] + bv;
+                        m = fmaxf(m, t > 0.0f ? t : 0.0f);
+                    }
+                    m = fmaxf(m, __shfl_xor(m, 32));
+                    if (lane < 32 && col_ok && half0 < a.rows)
+                        atomicMax(yu + (half0 / a.G) * a.ldy + col, __float_as_uint(m));
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int64_t row = row_t + rbase + 8 * (r >> 2) + (r & 3);
+                        float t = acc[j][h][r] + bv;
+                        t = t > 0.0f ? t : 0.0f;   // pooling requires a final ReLU
+                        if (col_ok && row < a.rows) atomicMax(yu + (row / a.G) * a.ldy + col, __float_as_uint(t));
+                    }
                 }
             } else {
                 const int64_t row0 = row_t + rbase;
