@@ -31,7 +31,6 @@ namespace meso {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int BKF = 16;      // fp32 k-slice
 constexpr int BKH = 32;      // bf16 k-slice
 constexpr int kPadF = 4;     // fp32 k-major LDS rows: tile width + 4 words
 constexpr int kRowH = 40;    // bf16 LDS rows: 32 k + 8 pad (80 bytes)
@@ -99,6 +98,40 @@ __device__ __forceinline__ void load_a(const GemmArgs& a, int64_t r, int k0, flo
     }
 }
 
+// L consecutive elements (r, k0 ..) of [x0 | x1] for fp32 sources of any
+// widths and alignment: per element the address is selected (clamped to the
+// row's first element when past K) and the value zeroed, without branches,
+// so the loads stay in flight like the vector ones.
+template <int L>
+__device__ __forceinline__ void load_a_mixed(const GemmArgs& a, int64_t r, int k0, float (&v)[L], bool& ok) {
+    ok = r < a.rows;
+    const int64_t rr = ok ? r : 0;
+    const float* r0 = static_cast<const float*>(a.x0) + rr * a.ld0;
+    const float* r1 = a.x1 ? a.x1 + rr * a.ld1 : r0;
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+        const int k = k0 + i;
+        const bool in0 = k < a.c0;
+        const bool in1 = !in0 && k < a.K;
+        const float* p = in0 ? r0 + k : (in1 ? r1 + (k - a.c0) : r0);
+        const float t = *p;
+        v[i] = (in0 || in1) ? t : 0.0f;
+    }
+}
+
+// L consecutive weights (n, k0 ..) for rows of any length, branch-free.
+template <int L>
+__device__ __forceinline__ void load_w_mixed(const GemmArgs& a, int n, int k0, float (&v)[L], bool& ok) {
+    ok = n < a.N;
+    const float* wr = static_cast<const float*>(a.W) + (int64_t)(ok ? n : 0) * a.K;
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+        const bool in = k0 + i < a.K;
+        const float t = *(in ? wr + k0 + i : wr);
+        v[i] = in ? t : 0.0f;
+    }
+}
+
 template <int L, bool FAST>
 __device__ __forceinline__ void load_w_f32(const GemmArgs& a, int n, int k0, float (&v)[L], bool& ok) {
     const float* W = static_cast<const float*>(a.W);
@@ -131,10 +164,15 @@ __device__ __forceinline__ uint4 load_w8_bf16(const GemmArgs& a, int n, int k0, 
         ok = n < a.N && k0 < a.K;
         return *reinterpret_cast<const uint4*>(W + (int64_t)(ok ? n : 0) * a.K + (ok ? k0 : 0));
     }
-    ok = true;
+    ok = n < a.N;
+    const uint16_t* wr = W + (int64_t)(ok ? n : 0) * a.K;
     uint16_t h[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) h[i] = (n < a.N && k0 + i < a.K) ? W[(int64_t)n * a.K + k0 + i] : (uint16_t)0;
+    for (int i = 0; i < 8; ++i) {
+        const bool in = k0 + i < a.K;
+        const uint16_t t = *(in ? wr + k0 + i : wr);
+        h[i] = in ? t : (uint16_t)0;
+    }
     uint4 q;
     q.x = h[0] | ((uint32_t)h[1] << 16);
     q.y = h[2] | ((uint32_t)h[3] << 16);
@@ -160,7 +198,8 @@ __device__ __forceinline__ uint4 load_a8_bf16(const GemmArgs& a, int64_t r, int 
     } else {
         float v[8];
         bool okv;
-        load_a<8, FAST>(a, r, k0, v, okv);
+        if constexpr (FAST) load_a<8, true>(a, r, k0, v, okv);
+        else load_a_mixed<8>(a, r, k0, v, okv);
 #pragma unroll
         for (int i = 0; i < 8; ++i) h[i] = f32_to_bf16(okv ? v[i] : 0.0f);
     }
@@ -172,16 +211,18 @@ __device__ __forceinline__ uint4 load_a8_bf16(const GemmArgs& a, int64_t r, int 
     return q;
 }
 
-// bias, ReLU and bf16 rounding of one pre-activation value
+// bias, ReLU and (bf16 path) rounding of one pre-activation value
+template <bool ROUND>
 __device__ __forceinline__ float activate(const GemmArgs& a, float t, float bias) {
     t += bias;
     if (a.relu) t = t > 0.0f ? t : 0.0f;
-    if (a.round_bf16) t = round_bf16(t);
+    if constexpr (ROUND) t = round_bf16(t);
     return t;
 }
 
-// Epilogue of one 32 x 32 accumulator block at (row0, col0).
-template <int EPI>
+// Epilogue of one 32 x 32 accumulator block at (row0, col0).  ROUND: the
+// bf16 path rounds every stored activation to bf16.
+template <int EPI, bool ROUND>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, int64_t row0, int col0, int lane) {
     const int col = col0 + (lane & 31);
     const bool col_ok = col < a.N;
@@ -199,7 +240,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, i
     const float bias = (col_ok && a.bias) ? a.bias[col] : 0.0f;
     float v[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) v[r] = activate(a, acc[r], bias);
+    for (int r = 0; r < 16; ++r) v[r] = activate<ROUND>(a, acc[r], bias);
     if constexpr (EPI == EPI_POOL) {
         unsigned* yu = static_cast<unsigned*>(a.y);
         if (a.G % 32 == 0) {
@@ -229,6 +270,16 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, i
         }
     } else {
         if (!col_ok) return;
+        if (row0 + 32 <= a.rows) {
+            // whole block in range: unguarded stores
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = rbase + 8 * (r >> 2) + (r & 3);
+                if constexpr (EPI == EPI_F32) static_cast<float*>(a.y)[row * a.ldy + col] = v[r];
+                else static_cast<uint16_t*>(a.y)[row * a.ldy + col] = f32_to_bf16(v[r]);
+            }
+            return;
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int64_t row = rbase + 8 * (r >> 2) + (r & 3);
@@ -241,24 +292,34 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, i
 }
 
 // fp32 MFMA GEMM.  Workgroup tile BM x BN, 2 x 2 waves, each wave TM x TN
-// blocks of 32 x 32.  K advances in slices of 16 through double-buffered
-// k-major LDS; the next slice is fetched into registers while the current
-// one feeds the MFMAs, so one barrier per slice suffices.
-template <int BM, int BN, int EPI, bool FAST_A, bool FAST_W>
+// blocks of 32 x 32.  K advances in slices of BK through double-buffered
+// row-major LDS tiles (rows of BK words + 4 pad); the next slice is fetched
+// into registers while the current one feeds the MFMAs, so one barrier per
+// slice suffices.  Inside a slice the k order is permuted to the MFMA lane
+// layout: at step kk lane l contributes k = (BK/2)*(l/32) + kk for both
+// operands, so each lane's operands of a slice are BK/2 consecutive words
+// of one LDS row, read with 16-byte loads (conflict-free: row stride
+// BK + 4 words puts 8 consecutive lanes on distinct bank quads).  The
+// product is the same sum over k, accumulated in a different order.
+template <int BM, int BN, int BK, int EPI, bool FAST_A, bool FAST_W>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
-    constexpr int BK = BKF;
     constexpr int TM = BM / 64, TN = BN / 64;
-    constexpr int AL = BM * BK / 256, BL = BN * BK / 256;   // elements per thread per slice
-    __shared__ float As[2][BK][BM + kPadF];
-    __shared__ float Bs[2][BK][BN + kPadF];
+    constexpr int LW = BK + kPadF;           // LDS row stride in words
+    constexpr int CPR = BK / 4;              // 16-byte chunks per tile row
+    constexpr int QA = BM * CPR / 256, QB = BN * CPR / 256;   // chunks per thread per slice
+    constexpr int HK = BK / 2;               // k per lane per slice
+    static_assert(QA >= 1 && QB >= 1 && HK % 4 == 0, "tile shape");
+    __shared__ __attribute__((aligned(16))) float As[2][BM * LW];
+    __shared__ __attribute__((aligned(16))) float Bs[2][BN * LW];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t row_t = (int64_t)blockIdx.x * BM;
     const int col_t = blockIdx.y * BN;
-    const int ar = tid / (BK / AL), ak = (tid % (BK / AL)) * AL;
-    const int br = tid / (BK / BL), bk = (tid % (BK / BL)) * BL;
     const int k_lo = blockIdx.z * a.kc;
     const int k_hi = min(a.K, k_lo + a.kc);
+    // chunk c = tid + 256 p covers tile row c / CPR, words 4 (c % CPR) .. +3
+    const int crow = tid / CPR, ck = 4 * (tid % CPR);
+    constexpr int RSTEP = 256 / CPR;         // tile rows between a thread's chunks
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -268,52 +329,123 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    float ra[AL], rb[BL];
-    bool oka, okb;
-    load_a<AL, FAST_A>(a, row_t + ar, k_lo + ak, ra, oka);
-    load_w_f32<BL, FAST_W>(a, col_t + br, k_lo + bk, rb, okb);
+    // Two register stages alternate, so the global loads of a slice are
+    // issued two slices before its LDS store: their latency is covered by
+    // two slices of MFMAs.  Fast sources keep one clamped row pointer per
+    // chunk; a chunk past K loads column 0 of its row and is zeroed at the
+    // store, so every address stays inside the operand.
+    float ra0[QA][4], rb0[QB][4], ra1[QA][4], rb1[QB][4];
+    bool oka0[QA], okb0[QB], oka1[QA], okb1[QB];
+    const float* pa[QA];
+    const float* pb[QB];
+    bool rowa[QA], rowb[QB];
 #pragma unroll
-    for (int i = 0; i < AL; ++i) As[0][ak + i][ar] = oka ? ra[i] : 0.0f;
+    for (int p = 0; p < QA; ++p) {
+        const int64_t r = row_t + crow + RSTEP * p;
+        rowa[p] = r < a.rows;
+        pa[p] = static_cast<const float*>(a.x0) + (rowa[p] ? r : 0) * a.ld0;
+    }
 #pragma unroll
-    for (int i = 0; i < BL; ++i) Bs[0][bk + i][br] = okb ? rb[i] : 0.0f;
-    __syncthreads();
-
-    int cur = 0;
-    for (int k0 = k_lo; k0 < k_hi; k0 += BK) {
-        // prefetch the next slice (the loaders zero-fill past K, so the last
-        // iteration's prefetch is harmless and the loads stay unconditional)
-        load_a<AL, FAST_A>(a, row_t + ar, k0 + BK + ak, ra, oka);
-        load_w_f32<BL, FAST_W>(a, col_t + br, k0 + BK + bk, rb, okb);
-        // all operands of this slice into registers first, then the MFMAs
-        float av[BK / 2][TM], bv[BK / 2][TN];
+    for (int p = 0; p < QB; ++p) {
+        const int n = col_t + crow + RSTEP * p;
+        rowb[p] = n < a.N;
+        pb[p] = static_cast<const float*>(a.W) + (int64_t)(rowb[p] ? n : 0) * a.K;
+    }
+    auto fetch = [&](float (&ra)[QA][4], bool (&oka)[QA], float (&rb)[QB][4], bool (&okb)[QB], int k0) {
+        const bool kin = k0 + ck < a.K;
+        const int ko = kin ? k0 + ck : 0;    // columns past K read column 0 of the row
 #pragma unroll
-        for (int kk = 0; kk < BK / 2; ++kk) {
+        for (int p = 0; p < QA; ++p) {
+            if constexpr (FAST_A) {
+                const float4 u = *reinterpret_cast<const float4*>(pa[p] + ko);
+                ra[p][0] = u.x; ra[p][1] = u.y; ra[p][2] = u.z; ra[p][3] = u.w;
+                oka[p] = rowa[p] && kin;
+            } else {
+                load_a_mixed<4>(a, row_t + crow + RSTEP * p, k0 + ck, ra[p], oka[p]);
+            }
+        }
 #pragma unroll
-            for (int i = 0; i < TM; ++i) av[kk][i] = As[cur][2 * kk + (lane >> 5)][wm * (BM / 2) + i * 32 + (lane & 31)];
+        for (int p = 0; p < QB; ++p) {
+            if constexpr (FAST_W) {
+                const float4 u = *reinterpret_cast<const float4*>(pb[p] + ko);
+                rb[p][0] = u.x; rb[p][1] = u.y; rb[p][2] = u.z; rb[p][3] = u.w;
+                okb[p] = rowb[p] && kin;
+            } else {
+                load_w_mixed<4>(a, col_t + crow + RSTEP * p, k0 + ck, rb[p], okb[p]);
+            }
+        }
+    };
+    auto stage = [&](const float (&ra)[QA][4], const bool (&oka)[QA], const float (&rb)[QB][4],
+                     const bool (&okb)[QB], int buf) {
 #pragma unroll
-            for (int j = 0; j < TN; ++j) bv[kk][j] = Bs[cur][2 * kk + (lane >> 5)][wn * (BN / 2) + j * 32 + (lane & 31)];
+        for (int p = 0; p < QA; ++p)
+            *reinterpret_cast<float4*>(&As[buf][(crow + RSTEP * p) * LW + ck]) =
+                oka[p] ? make_float4(ra[p][0], ra[p][1], ra[p][2], ra[p][3]) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int p = 0; p < QB; ++p)
+            *reinterpret_cast<float4*>(&Bs[buf][(crow + RSTEP * p) * LW + ck]) =
+                okb[p] ? make_float4(rb[p][0], rb[p][1], rb[p][2], rb[p][3]) : make_float4(0.f, 0.f, 0.f, 0.f);
+    };
+    const int hk = HK * (lane >> 5);
+    // operands of one slice into registers, then its MFMAs
+    auto compute = [&](int buf) {
+        float av[TM][HK], bv[TN][HK];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const float* src = &As[buf][(wm * (BM / 2) + i * 32 + (lane & 31)) * LW + hk];
+#pragma unroll
+            for (int q = 0; q < HK / 4; ++q) {
+                const float4 u = reinterpret_cast<const float4*>(src)[q];
+                av[i][4 * q] = u.x; av[i][4 * q + 1] = u.y; av[i][4 * q + 2] = u.z; av[i][4 * q + 3] = u.w;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const float* src = &Bs[buf][(wn * (BN / 2) + j * 32 + (lane & 31)) * LW + hk];
+#pragma unroll
+            for (int q = 0; q < HK / 4; ++q) {
+                const float4 u = reinterpret_cast<const float4*>(src)[q];
+                bv[j][4 * q] = u.x; bv[j][4 * q + 1] = u.y; bv[j][4 * q + 2] = u.z; bv[j][4 * q + 3] = u.w;
+            }
         }
         __builtin_amdgcn_sched_barrier(0);   // keep the operand reads ahead of the MFMAs
 #pragma unroll
-        for (int kk = 0; kk < BK / 2; ++kk)
+        for (int kk = 0; kk < HK; ++kk)
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[kk][i], bv[kk][j], acc[i][j], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);   // next slice's LDS stores after all MFMAs
-#pragma unroll
-        for (int i = 0; i < AL; ++i) As[cur ^ 1][ak + i][ar] = oka ? ra[i] : 0.0f;
-#pragma unroll
-        for (int i = 0; i < BL; ++i) Bs[cur ^ 1][bk + i][br] = okb ? rb[i] : 0.0f;
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][kk], bv[j][kk], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);   // the LDS stores that follow stay after the MFMAs
+    };
+
+    // Slices come in pairs (compute from LDS buffer 0 then 1), so buffers
+    // and register stages are fixed per half and nothing rotates across
+    // the loop edge; an odd last slice is computed after the loop.  Slices
+    // past this range are fetched (zero-filled or clamped) and never
+    // computed, so every load is unconditional.
+    const int n_slices = (k_hi - k_lo + BK - 1) / BK;
+    fetch(ra0, oka0, rb0, okb0, k_lo);
+    stage(ra0, oka0, rb0, okb0, 0);
+    fetch(ra1, oka1, rb1, okb1, k_lo + BK);
+    __syncthreads();
+    int k0 = k_lo;
+    for (int t = 0; t + 1 < n_slices; t += 2, k0 += 2 * BK) {
+        fetch(ra0, oka0, rb0, okb0, k0 + 2 * BK);
+        compute(0);
+        stage(ra1, oka1, rb1, okb1, 1);
         __syncthreads();
-        cur ^= 1;
+        fetch(ra1, oka1, rb1, okb1, k0 + 3 * BK);
+        compute(1);
+        stage(ra0, oka0, rb0, okb0, 0);
+        __syncthreads();
     }
+    if (n_slices & 1) compute(0);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-            epilogue<EPI>(a, acc[i][j], row_t + wm * (BM / 2) + i * 32, col_t + wn * (BN / 2) + j * 32, lane);
+            epilogue<EPI, false>(a, acc[i][j], row_t + wm * (BM / 2) + i * 32, col_t + wn * (BN / 2) + j * 32, lane);
 }
 
 // bf16 MFMA GEMM, same structure with k-slices of 32 and row-major LDS
@@ -394,7 +526,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-            epilogue<EPI>(a, acc[i][j], row_t + wm * (BM / 2) + i * 32, col_t + wn * (BN / 2) + j * 32, lane);
+            epilogue<EPI, true>(a, acc[i][j], row_t + wm * (BM / 2) + i * 32, col_t + wn * (BN / 2) + j * 32, lane);
 }
 
 // Split-K finish: sum the partial products in split order (deterministic),
@@ -407,7 +539,8 @@ __global__ __launch_bounds__(256) void splitk_finish_kernel(GemmArgs a, int spli
         const int col = (int)(e - row * a.N);
         float t = 0.0f;
         for (int z = 0; z < splits; ++z) t += a.part[(int64_t)z * n + e];
-        const float v = activate(a, t, a.bias ? a.bias[col] : 0.0f);
+        const float v = a.round_bf16 ? activate<true>(a, t, a.bias ? a.bias[col] : 0.0f)
+                                     : activate<false>(a, t, a.bias ? a.bias[col] : 0.0f);
         if constexpr (EPI == EPI_POOL)
             atomicMax(static_cast<unsigned*>(a.y) + (row / a.G) * a.ldy + col, __float_as_uint(v));
         else if constexpr (EPI == EPI_F32)
@@ -418,8 +551,13 @@ __global__ __launch_bounds__(256) void splitk_finish_kernel(GemmArgs a, int spli
 }
 
 struct LayerPlan {
-    int bm, bn, splits, kc;
+    int bm, bn, bk, splits, kc;
 };
+
+// fp32 k-slice depth for a tile: about 2K MFMA cycles per slice and wave
+// (TM x TN blocks x BK/2 MFMAs of 64 cycles), enough to cover the latency of
+// the next slice's global loads.
+static int f32_slice(int bm, int bn) { return (bm / 64) * (bn / 64) >= 2 ? 32 : 64; }
 
 // Tile shape and K split of one layer: a pure function of the shape, shared
 // by the workspace query and the launch.  Picks the tile with the smallest
@@ -427,17 +565,18 @@ struct LayerPlan {
 // leave most CUs idle, splits K.
 static LayerPlan plan_layer(int64_t rows, int N, int K, bool bf16) {
     static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
-    const int bk = bf16 ? BKH : BKF;
-    LayerPlan best{64, 64, 1, K};
+    LayerPlan best{64, 64, 0, 1, K};
     double best_cost = 1e300;
     for (const auto& c : cand) {
         const int64_t tiles = ceil_div(rows, c[0]) * ceil_div(N, c[1]);
         const double cost = (double)ceil_div(tiles, kTargetTiles) * c[0] * c[1];
         if (cost < best_cost * (1.0 - 1e-9)) {
             best_cost = cost;
-            best = {c[0], c[1], 1, K};
+            best = {c[0], c[1], 0, 1, K};
         }
     }
+    best.bk = bf16 ? BKH : f32_slice(best.bm, best.bn);
+    const int bk = best.bk;
     const int64_t tiles = ceil_div(rows, best.bm) * ceil_div(N, best.bn);
     if (tiles < kTargetTiles / 2) {
         int splits = 1;
@@ -481,14 +620,15 @@ static size_t mlp_ws_bytes(int64_t rows, int n_layers, const int32_t* dims, int 
 template <int BM, int BN, int EPI>
 static void launch_tile(const GemmArgs& a, bool bf16, bool fast_a, bool fast_w, dim3 grid, hipStream_t s) {
     const dim3 block(256);
+    constexpr int BK = (BM / 64) * (BN / 64) >= 2 ? 32 : 64;   // f32_slice(BM, BN)
     if (bf16) {
         if (fast_a && fast_w) gemm_bf16_kernel<BM, BN, EPI, true, true><<<grid, block, 0, s>>>(a);
         else if (fast_w) gemm_bf16_kernel<BM, BN, EPI, false, true><<<grid, block, 0, s>>>(a);
         else gemm_bf16_kernel<BM, BN, EPI, false, false><<<grid, block, 0, s>>>(a);
     } else {
-        if (fast_a && fast_w) gemm_f32_kernel<BM, BN, EPI, true, true><<<grid, block, 0, s>>>(a);
-        else if (fast_w) gemm_f32_kernel<BM, BN, EPI, false, true><<<grid, block, 0, s>>>(a);
-        else gemm_f32_kernel<BM, BN, EPI, false, false><<<grid, block, 0, s>>>(a);
+        if (fast_a && fast_w) gemm_f32_kernel<BM, BN, BK, EPI, true, true><<<grid, block, 0, s>>>(a);
+        else if (fast_w) gemm_f32_kernel<BM, BN, BK, EPI, false, true><<<grid, block, 0, s>>>(a);
+        else gemm_f32_kernel<BM, BN, BK, EPI, false, false><<<grid, block, 0, s>>>(a);
     }
 }
 
@@ -505,10 +645,13 @@ static void launch_epi(const GemmArgs& a, const LayerPlan& pl, bool bf16, bool f
 static int launch_layer(GemmArgs a, bool bf16, int epi, float* part, hipStream_t s) {
     const LayerPlan pl = plan_layer(a.rows, a.N, a.K, bf16);
     a.kc = pl.kc;
-    const bool fast_w = (a.K % 8 == 0) && aligned(a.W, 16);
+    // vector loads: 16-byte aligned rows and whole 16-byte chunks (4 fp32
+    // per chunk in the fp32 kernel, 8 bf16 in the bf16 kernel)
+    const int kq = bf16 ? 8 : 4;
+    const bool fast_w = (a.K % kq == 0) && aligned(a.W, 16);
     bool fast_a;
     if (a.a_bf16) fast_a = a.c1 == 0 && a.c0 == a.K && a.K % 8 == 0 && a.ld0 % 8 == 0 && aligned(a.x0, 16);
-    else fast_a = a.c1 == 0 && a.c0 == a.K && a.K % 8 == 0 && a.ld0 % 4 == 0 && aligned(a.x0, 16);
+    else fast_a = a.c1 == 0 && a.c0 == a.K && a.K % kq == 0 && a.ld0 % 4 == 0 && aligned(a.x0, 16);
     if (pl.splits > 1) {
         a.part = part;
         launch_epi<EPI_PARTIAL>(a, pl, bf16, fast_a, fast_w, s);
