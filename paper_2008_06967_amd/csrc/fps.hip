@@ -56,14 +56,22 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
     }
 
     float cx = p[0], cy = p[1], cz = p[2];
-    if (tid == 0) {
-        out_idx[0] = 0;
-        if (out_c) {
-            out_c[0] = cx;
-            out_c[1] = cy;
-            out_c[2] = cz;
+    // Results are kept in wave 0, iteration m in lane m % 64, and written
+    // 64 iterations at a time (one coalesced store instead of one
+    // single-lane store per iteration).
+    int keep_i = 0;
+    float keep_x = cx, keep_y = cy, keep_z = cz;
+    auto flush = [&](int m_last) {   // iterations (m_last & ~63) .. m_last
+        const int m0 = m_last & ~63;
+        if (m0 + lane <= m_last) {
+            out_idx[m0 + lane] = keep_i;
+            if (out_c) {
+                out_c[3 * (m0 + lane) + 0] = keep_x;
+                out_c[3 * (m0 + lane) + 1] = keep_y;
+                out_c[3 * (m0 + lane) + 2] = keep_z;
+            }
         }
-    }
+    };
 
     for (int m = 1; m < M; ++m) {
         // 1. distance to the newest centroid, running min, this thread's max
@@ -81,8 +89,9 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
                 y = p[3 * j + 1];
                 z = p[3 * j + 2];
             }
-            const float d = dist3(x, y, z, cx, cy, cz);
-            const float nm = d < dm[q] ? d : dm[q];
+            // both operands are >= 0 or the -1 sentinel, never NaN: fminf is
+            // the strict-less running minimum
+            const float nm = fminf(dist3(x, y, z, cx, cy, cz), dm[q]);
             dm[q] = nm;
             tmax = max(tmax, __float_as_int(nm));
         }
@@ -137,15 +146,16 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
             cy = __int_as_float(__builtin_amdgcn_readlane(sl.w, ww));
             cz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(slz), ww));
         }
-        if (tid == 0) {
-            out_idx[m] = sel;
-            if (out_c) {
-                out_c[3 * m + 0] = cx;
-                out_c[3 * m + 1] = cy;
-                out_c[3 * m + 2] = cz;
-            }
+        if (wave == 0) {
+            const bool mine = lane == (m & 63);
+            keep_i = mine ? sel : keep_i;
+            keep_x = mine ? cx : keep_x;
+            keep_y = mine ? cy : keep_y;
+            keep_z = mine ? cz : keep_z;
+            if ((m & 63) == 63) flush(m);
         }
     }
+    if (wave == 0 && ((M - 1) & 63) != 63) flush(M - 1);
 }
 
 template <int T, int P, bool REG>
