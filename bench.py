@@ -228,9 +228,33 @@ def main():
               file=sys.stderr, flush=True)
         del src, dst
 
+    def step_latencies(delayed, steps, warmup, graph):
+        """Per-step GPU times of one batch at a time: an event after every
+        replay on a backlogged stream; consecutive differences are the
+        step times (ms)."""
+        net = nets.build(spec, w, delayed=delayed, device=dev)
+        stream = torch.cuda.Stream(device=dev)
+        run = net.capture(xyz, feat)[0].replay if graph else (lambda: net.forward(xyz, feat))
+        with torch.cuda.stream(stream):
+            for _ in range(warmup):
+                run()
+        torch.cuda.synchronize()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        with torch.cuda.stream(stream):
+            torch.cuda._sleep(int(5e7))
+            evs[0].record(stream)
+            for i in range(steps):
+                run()
+                evs[i + 1].record(stream)
+        torch.cuda.synchronize()
+        t = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(steps)])
+        return {"median": float(np.median(t)), "p10": float(np.percentile(t, 10)), "p90": float(np.percentile(t, 90)),
+                "mean": float(t.mean()), "std": float(t.std()), "n": int(steps)}
+
     graph = not args.eager
     # single-batch latency (one batch at a time)
     t_latency = time_net(True, args.steps, args.warmup, graph, 1)
+    lat_stats = step_latencies(True, max(args.steps, 50), args.warmup, graph)
     print(f"[bench] delayed, 1 batch in flight: {t_latency * 1e3:.3f} ms/step", file=sys.stderr, flush=True)
     # throughput with independent batches overlapping
     per_inflight = {1: t_latency}
@@ -284,8 +308,13 @@ def main():
     roof["traffic"] = None if tr is None else tr["bytes"]
 
     per_module = {}
+    module_ms = {}
     for i, m in enumerate(spec["sa"]):
         per_module[f"sa{i + 1}_centroids_per_s"] = B * m["M"] / t_step
+        # serial sum of this module's calls (search + MLP + aggregation)
+        ms = sum(stages.get(f"{n}#{i}", 0.0) for n in ("fps", "ball_query", "pointwise_mlp", "aggregate_max"))
+        module_ms[f"sa{i + 1}"] = round(ms, 5)
+        per_module[f"sa{i + 1}_centroids_per_s_serial_stage_sum"] = B * m["M"] / (ms * 1e-3)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -310,6 +339,8 @@ def main():
                    + f", {inflight} independent batch(es) in flight on separate streams",
                    "batches_in_flight": inflight, "parallelism": "single GPU"},
         "latency_ms_per_batch": t_latency * 1e3,
+        "latency_ms_per_batch_stats": {k: (round(v, 5) if isinstance(v, float) else v) for k, v in lat_stats.items()},
+        "module_serial_ms": module_ms,
         "clouds_per_s_by_batches_in_flight": {str(k): B / v for k, v in per_inflight.items()},
         "centroids_per_s": per_module,
         "conventional": {"ms_per_step": t_conv * 1e3, "clouds_per_s": B / t_conv, "speedup_delayed": t_conv / t_step,
@@ -326,26 +357,59 @@ def main():
     print(json.dumps(res))
 
 
-def cpu_baseline(spec, xyz, feat, w, seconds):
-    """The CPU oracle (single thread) on the same workload, repeated over the
-    batch until about `seconds` of work has been done."""
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_rate(spec, xyz, feat, w, seconds, delayed, threads):
+    """Clouds/s of the CPU oracle forward over clouds of the batch, one cloud
+    per call, on `threads` threads (the oracle's C routines run without the
+    interpreter lock), for about `seconds`."""
+    import threading
     import oracle.nets as ON
     B = spec["B"]
-    clouds = 0
+    lock = threading.Lock()
+    state = {"next": 0, "done": 0}
     t0 = time.perf_counter()
-    chunk = 4
-    while True:
-        for s in range(0, B, chunk):
-            sub = dict(spec, B=min(chunk, B - s))
-            ON.forward(sub, xyz[s:s + chunk], None if feat is None else feat[s:s + chunk], w, delayed=True)
-            clouds += sub["B"]
-            if time.perf_counter() - t0 >= seconds:
-                break
-        if time.perf_counter() - t0 >= seconds:
-            break
+
+    def worker():
+        while time.perf_counter() - t0 < seconds:
+            with lock:
+                c = state["next"] % B
+                state["next"] += 1
+            sub = dict(spec, B=1)
+            ON.forward(sub, xyz[c:c + 1], None if feat is None else feat[c:c + 1], w, delayed=delayed)
+            with lock:
+                state["done"] += 1
+
+    ts = [threading.Thread(target=worker) for _ in range(threads)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
     dt = time.perf_counter() - t0
-    return {"value": clouds / dt, "unit": "clouds/s", "cores": 1, "kind": "oracle",
-            "sample": f"{clouds} clouds of the same batch (delayed forward), {dt:.1f} s, single thread"}
+    return state["done"] / dt, state["done"], dt
+
+
+def cpu_baseline(spec, xyz, feat, w, seconds):
+    """The CPU oracle on the same workload: the delayed forward on one
+    thread (the reported value), on one thread per available core (up to
+    16), and the conventional forward on one thread."""
+    cores = min(16, len(os.sched_getaffinity(0)))
+    v1, n1, d1 = _oracle_rate(spec, xyz, feat, w, 0.5 * seconds, True, 1)
+    vm, nm, dm = _oracle_rate(spec, xyz, feat, w, 0.25 * seconds, True, cores)
+    vc, nc, dc = _oracle_rate(spec, xyz, feat, w, 0.25 * seconds, False, 1)
+    return {"value": v1, "unit": "clouds/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n1} clouds of the batch (delayed forward, fp64 accumulation), {d1:.1f} s, single thread",
+            "multithread": {"value": vm, "cores": cores, "sample": f"{nm} clouds in {dm:.1f} s"},
+            "conventional_single_thread": {"value": vc, "sample": f"{nc} clouds in {dc:.1f} s"},
+            "cpu_model": _cpu_model()}
 
 
 if __name__ == "__main__":

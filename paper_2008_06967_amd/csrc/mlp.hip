@@ -550,6 +550,131 @@ __global__ __launch_bounds__(256) void splitk_finish_kernel(GemmArgs a, int spli
     }
 }
 
+// Skinny layers: at most 64 rows (the classifier head runs on one row per
+// cloud).  A row-block GEMM would leave almost every CU idle and split K
+// through partial sums; here a workgroup owns 16 output columns for all
+// rows, its four waves split K, each accumulating 16 x 16 blocks with
+// v_mfma_f32_16x16x4_f32 from operands loaded straight from L2 (lane l:
+// row or column l % 16, k offset 4 (l / 16) inside a 16-wide chunk, one
+// 16-byte load per operand and chunk, the MFMA steps consuming its four
+// words), loads issued one group of chunks ahead.  The partial blocks are
+// summed in wave order through LDS (deterministic), then bias and ReLU.
+// The accumulator of a 16 x 16 MFMA holds, in lane l and register r, row
+// 4 (l / 16) + r and column l % 16.
+constexpr int kSkinnyRows = 64;
+constexpr int kSkinnyWaves = 4;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int TM>
+__global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_f32_kernel(const float* __restrict__ x, int64_t ldx, int rows, int K,
+                                                         const float* __restrict__ W, const float* __restrict__ bias,
+                                                         int N, int relu, float* __restrict__ y, int64_t ldy) {
+    constexpr int G = 4;   // 16-wide k chunks per load group
+    constexpr int NW = kSkinnyWaves;
+    __shared__ float red[NW][TM * 4][64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int i = lane & 15, q = lane >> 4;
+    const int col0 = blockIdx.x * 16;
+    const bool col_ok = col0 + i < N;
+    const float* wr = W + (int64_t)(col_ok ? col0 + i : 0) * K;
+    const float* xr[TM];
+    bool rok[TM];
+#pragma unroll
+    for (int t = 0; t < TM; ++t) {
+        const int r = 16 * t + i;
+        rok[t] = r < rows;
+        xr[t] = x + (int64_t)(rok[t] ? r : 0) * ldx;
+    }
+    const int nch = (K + 15) / 16;
+    const int per = (nch + NW - 1) / NW;
+    const int c_lo = min(nch, wave * per), c_hi = min(nch, c_lo + per);
+    const int ngroups = (c_hi - c_lo + G - 1) / G;
+
+    f32x4 acc[TM];
+#pragma unroll
+    for (int t = 0; t < TM; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 la0[G][TM], lb0[G], la1[G][TM], lb1[G];
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    // chunks past this wave's range or past K load column 0 and are zeroed
+    auto load = [&](f32x4 (&la)[G][TM], f32x4 (&lb)[G], int c0) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int k = 16 * (c0 + g) + 4 * q;
+            const bool in = c0 + g < c_hi && k < K;
+            const int ko = in ? k : 0;
+            const f32x4 u = *reinterpret_cast<const f32x4*>(wr + ko);
+            lb[g] = (in && col_ok) ? u : zero;
+#pragma unroll
+            for (int t = 0; t < TM; ++t) {
+                const f32x4 v = *reinterpret_cast<const f32x4*>(xr[t] + ko);
+                la[g][t] = (in && rok[t]) ? v : zero;
+            }
+        }
+    };
+    auto compute = [&](const f32x4 (&la)[G][TM], const f32x4 (&lb)[G]) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+                for (int t = 0; t < TM; ++t)
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(la[g][t][kk], lb[g][kk], acc[t], 0, 0, 0);
+    };
+    int c = c_lo;
+    load(la0, lb0, c);
+    load(la1, lb1, c + G);
+    for (int t = 0; t + 1 < ngroups; t += 2, c += 2 * G) {
+        compute(la0, lb0);
+        load(la0, lb0, c + 2 * G);
+        compute(la1, lb1);
+        load(la1, lb1, c + 3 * G);
+    }
+    if (ngroups & 1) compute(la0, lb0);
+
+#pragma unroll
+    for (int t = 0; t < TM; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[wave][4 * t + r][lane] = acc[t][r];
+    __syncthreads();
+    for (int o = tid; o < TM * 4 * 64; o += 64 * NW) {
+        const int tr = o >> 6, l = o & 63;
+        float sum = 0.0f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) sum += red[w][tr][l];
+        const int row = 16 * (tr >> 2) + 4 * (l >> 4) + (tr & 3);
+        const int cc = col0 + (l & 15);
+        if (row < rows && cc < N) {
+            float v = sum + (bias ? bias[cc] : 0.0f);
+            if (relu) v = v > 0.0f ? v : 0.0f;
+            y[(int64_t)row * ldy + cc] = v;
+        }
+    }
+}
+
+static int launch_skinny(const float* x, int64_t ldx, int rows, int K, const float* W, const float* bias, int N,
+                         int relu, float* y, int64_t ldy, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div(N, 16)), block(64 * kSkinnyWaves);
+    const int tm = (int)ceil_div(rows, 16);
+    if (tm == 1) skinny_f32_kernel<1><<<grid, block, 0, s>>>(x, ldx, rows, K, W, bias, N, relu, y, ldy);
+    else if (tm == 2) skinny_f32_kernel<2><<<grid, block, 0, s>>>(x, ldx, rows, K, W, bias, N, relu, y, ldy);
+    else if (tm == 3) skinny_f32_kernel<3><<<grid, block, 0, s>>>(x, ldx, rows, K, W, bias, N, relu, y, ldy);
+    else skinny_f32_kernel<4><<<grid, block, 0, s>>>(x, ldx, rows, K, W, bias, N, relu, y, ldy);
+    return after_launch("mesorasi_pointwise_mlp");
+}
+
+// The skinny path takes fp32 MLPs on at most 64 rows with one 16-byte
+// aligned input source, layer widths that are multiples of 4, 16-byte
+// aligned weights, fp32 output and no pooling.
+static bool skinny_ok(const float* x0, int64_t ld0, const float* x1, int c1, int64_t rows, int n_layers,
+                      const int32_t* dims, const void* const* W, int dtype, int out_dtype, int64_t pool_group) {
+    if (dtype != MESORASI_F32 || out_dtype != MESORASI_F32 || pool_group > 0) return false;
+    if (rows < 1 || rows > kSkinnyRows || c1 != 0 || x1 != nullptr) return false;
+    if (ld0 % 4 != 0 || !aligned(x0, 16)) return false;
+    for (int l = 0; l < n_layers; ++l)
+        if (dims[l] % 4 != 0 || !aligned(W[l], 16)) return false;
+    return true;
+}
+
 struct LayerPlan {
     int bm, bn, bk, splits, kc;
 };
@@ -699,6 +824,20 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
     const size_t one = align256((size_t)rows * (size_t)w * elem);
     const MlpWs lay = mlp_ws_layout(rows, n_layers, dims, dtype);
     char* buf[2] = {static_cast<char*>(ws), static_cast<char*>(ws) + one};
+    if (skinny_ok(x0, ld0, x1, c1, rows, n_layers, dims, W, dtype, out_dtype, pool_group)) {
+        // uses only the activation part of the workspace
+        for (int l = 0; l < n_layers; ++l) {
+            const float* xin = l == 0 ? x0 : reinterpret_cast<const float*>(buf[(l - 1) & 1]);
+            const int64_t ldx = l == 0 ? ld0 : dims[l];
+            const bool last = l + 1 == n_layers;
+            float* yout = last ? static_cast<float*>(y) : reinterpret_cast<float*>(buf[l & 1]);
+            const int64_t ldo = last ? ld_y : dims[l + 1];
+            const int rc = launch_skinny(xin, ldx, (int)rows, dims[l], static_cast<const float*>(W[l]),
+                                         bias ? bias[l] : nullptr, dims[l + 1], (relu_mask >> l) & 1u, yout, ldo, s);
+            if (rc != MESORASI_OK) return rc;
+        }
+        return MESORASI_OK;
+    }
     float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + lay.act);
     if (pool_group > 0) {
         const int rc = zero_rows_f32(static_cast<float*>(y), rows / pool_group, dims[n_layers], ld_y, s);

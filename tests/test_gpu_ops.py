@@ -217,6 +217,12 @@ MLP_CASES = [
     ("sa2_two_src", 517, [3, 128], [128, 128, 256], F32),
     ("sa3_groupall", 256, [3, 256], [256, 512, 1024], F32),
     ("fc_head", 32, [1024], [512, 256, 40], F32),
+    # at most 64 rows: the skinny path (16-column MFMA blocks, K split over waves)
+    ("fc_skinny_1row", 1, [1024], [512, 256, 40], F32),
+    ("fc_skinny_17rows", 17, [256], [100, 40], F32),
+    ("fc_skinny_64rows", 64, [64], [48, 12], F32),
+    ("fc_skinny_long_k", 33, [4096], [36], F32),
+    ("fc_skinny_unaligned_widths", 20, [30], [22, 6], F32),   # widths not multiples of 4: GEMM path
     ("seg_head", 300, [128], [128, 13], F32),
     ("odd_widths", 77, [5, 2], [33, 17, 9], F32),
     ("sa1_bf16", 1000, [3], [32, 32, 64], BF16),
@@ -239,7 +245,7 @@ def test_mlp_parity(gpu, name, rows, srcs, widths, dt):
     xs = [rr.standard_normal((rows, c)).astype(np.float32) for c in srcs]
     dims = [sum(srcs)] + widths
     Ws, bs = _weights(rr, dims)
-    relu_mask = (1 << (len(widths) - 1)) - 1 if name in ("fc_head", "seg_head") else (1 << len(widths)) - 1
+    relu_mask = (1 << (len(widths) - 1)) - 1 if name.startswith("fc") or name == "seg_head" else (1 << len(widths)) - 1
     ref = O.mlp(np.concatenate(xs, -1), Ws, bs, relu_mask=relu_mask, bf16=dt == BF16)
     p = ops.MLPParams(Ws, bs, dtype=dt)
     y = ops.pointwise_mlp(dev(xs[0]), p, x1=dev(xs[1]) if len(xs) > 1 else None, relu_mask=relu_mask)
