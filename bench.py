@@ -30,6 +30,13 @@ sys.path.insert(0, ROOT)
 
 METRIC = "clouds/sec end-to-end + centroids/sec per module; % HBM and MFMA peak"
 WORKLOAD = "pointnet2_cls"
+DESCRIBE = {
+    "sa_module": "one set-abstraction module, 1024 -> 512 centroids, K 32, 3 -> 64 -> 64 -> 128",
+    "pointnet2_cls": "PointNet++ SSG classifier",
+    "dgcnn": "DGCNN, 4 EdgeConv layers with k = 20 in feature space, 1x1 conv to 1024, global max",
+    "pointnet2_seg": "PointNet++ SSG segmentation of indoor rooms, 4 SA levels, 4 FP levels",
+    "lidar": "3-level PointNet++ backbone on 16384-point LiDAR sweeps, bf16 MLPs",
+}
 HBM_PEAK_GBS = 8000.0
 MFMA_F32_PEAK_TFLOPS = 157.3
 MFMA_BF16_PEAK_TFLOPS = 2516.6
@@ -64,7 +71,8 @@ class StageTimer:
         self.torch = torch
         self.ops = ops
         self.orig = {n: getattr(ops, n) for n in self.NAMES}
-        self.records = []     # (name#k, start, end, args-summary)
+        self.records = []     # (name#k, start, end)
+        self.work = {}        # name#k -> (bound, amount, extra)
         self.counts = {}
         self.active = False
 
@@ -81,6 +89,7 @@ class StageTimer:
                 r = __fn(*a, **kw)
                 e.record()
                 self.records.append((f"{__n}#{k}", s, e))
+                self.work[f"{__n}#{k}"] = call_work(__n, a, kw)
                 return r
             setattr(self.ops, n, wrap)
 
@@ -100,52 +109,66 @@ class StageTimer:
 
 
 # ----------------------------------------------------------------------------
-# algorithmic work per call of the classifier (documented in the design doc)
+# algorithmic work of one call, from its arguments (documented in the design doc)
 # ----------------------------------------------------------------------------
 
-def work_per_call(spec):
-    """name#k -> (bound, amount, unit) for the kernel calls of one forward.
+def call_work(name, a, kw):
+    """(bound, amount, extra) for one entry-point call; amount in TFLOP
+    (alu / mfma) or GB (hbm).
 
-    fps:          (M-1) * N point updates per cloud, 8 flops each (3 sub,
-                  1 mul, 2 fma) -> alu
-    ball_query:   B * M * N candidate tests (upper bound; early exit scans
-                  fewer), 8 flops each -> alu
-    pointwise_mlp: 2 * rows * sum(C_l * C_l+1) -> mfma
-    aggregate_max: compulsory HBM bytes -- every PFT row read once, the NIT,
-                  the centroid indices and the output -> hbm
+    fps:            (M-1) * N point updates per cloud, 8 flops each (3 sub,
+                    1 mul, 2 fma) -> alu
+    ball_query:     B * M * N candidate tests (upper bound; early exit scans
+                    fewer), 8 flops each -> alu
+    knn:            B * M * N pairs, 3 * C flops each (sub, mul, add) -> alu
+    pointwise_mlp:  2 * rows * sum(C_l * C_l+1) -> mfma
+    aggregate_max:  compulsory HBM bytes -- every PFT row read once, the NIT,
+                    the centroid indices or rows, the output -> hbm (the
+                    bytes of the gathered rows are reported beside it)
+    conventional:   2 * B*M*K * sum(C_l * C_l+1) -> mfma
+    interpolate3:   B * Nd * Ns pairs, 8 flops each -> alu
     """
-    B = spec["B"]
-    out = {}
-    N = spec["N"]
-    cin = 3 + spec["n_feat"]
-    s = 2 if spec.get("dtype") == "bf16" else 4
-    for i, m in enumerate(spec["sa"]):
-        M, K, dims = m["M"], m["K"], [cin] + m["mlp"]
-        C = dims[-1]
-        out[f"fps#{i}"] = ("alu", 8.0 * B * (M - 1) * N / 1e12, "TFLOP")
-        out[f"ball_query#{i}"] = ("alu", 8.0 * B * M * N / 1e12, "TFLOP")
-        flops = 2.0 * B * N * sum(a * b for a, b in zip(dims[:-1], dims[1:]))
-        out[f"pointwise_mlp#{i}"] = ("mfma", flops / 1e12, "TFLOP")
-        compulsory = B * N * C * s + 4 * B * M * K + 4 * B * M + 4 * B * M * C
-        out[f"aggregate_max#{i}"] = ("hbm", compulsory / 1e9, "GB")
-        N, cin = M, 3 + C
-    if spec.get("group_all"):
-        dims = [cin] + spec["group_all"]
-        flops = 2.0 * B * N * sum(a * b for a, b in zip(dims[:-1], dims[1:]))
-        out[f"pointwise_mlp#{len(spec['sa'])}"] = ("mfma", flops / 1e12, "TFLOP")
-    return out
+    def arg(i, key, default=None):
+        return a[i] if len(a) > i else kw.get(key, default)
 
-
-def logical_gather_bytes(spec):
-    """Bytes the aggregation reads as gathered rows (each neighbor row once
-    per centroid that lists it), per call -- reuse served by L2/MALL."""
-    B, out, N, cin = spec["B"], {}, spec["N"], 3 + spec["n_feat"]
-    s = 2 if spec.get("dtype") == "bf16" else 4
-    for i, m in enumerate(spec["sa"]):
-        C = m["mlp"][-1]
-        out[f"aggregate_max#{i}"] = B * m["M"] * m["K"] * C * s
-        N, cin = m["M"], 3 + C
-    return out
+    if name == "fps":
+        xyz, M = arg(0, "xyz"), arg(1, "M")
+        B, N = xyz.shape[0], xyz.shape[1]
+        return ("alu", 8.0 * B * (M - 1) * N / 1e12, None)
+    if name == "ball_query":
+        xyz, q = arg(0, "xyz"), arg(1, "qxyz")
+        return ("alu", 8.0 * xyz.shape[0] * q.shape[1] * xyz.shape[1] / 1e12, None)
+    if name == "knn":
+        ref, q = arg(0, "ref"), arg(1, "query")
+        B, N, C = ref.shape
+        return ("alu", 3.0 * C * B * q.shape[1] * N / 1e12, None)
+    if name == "pointwise_mlp":
+        x0, prm = arg(0, "x0"), arg(1, "p")
+        rows = int(np.prod(x0.shape[:-1]))
+        d = prm.dims
+        return ("mfma", 2.0 * rows * sum(x * y for x, y in zip(d[:-1], d[1:])) / 1e12, None)
+    if name == "aggregate_max":
+        pft, nit = arg(0, "pft"), arg(1, "nit")
+        cidx, cfeat, out = arg(2, "cidx"), arg(3, "cfeat"), kw.get("out")
+        B, N = pft.shape[0], pft.shape[1]
+        M, K = nit.shape[1], nit.shape[2]
+        C = out.shape[-1] if out is not None else pft.shape[-1]
+        s = pft.element_size()
+        comp = B * N * C * s + 4 * B * M * K + 4 * B * M * C
+        if cidx is not None:
+            comp += 4 * B * M
+        if cfeat is not None:
+            comp += B * M * C * s
+        return ("hbm", comp / 1e9, {"logical_gather_bytes": B * M * K * C * s})
+    if name == "conventional_module":
+        nit, prm = arg(0, "nit"), arg(1, "p")
+        rows = int(np.prod(nit.shape))
+        d = prm.dims
+        return ("mfma", 2.0 * rows * sum(x * y for x, y in zip(d[:-1], d[1:])) / 1e12, None)
+    if name == "interpolate3":
+        dst, src = arg(0, "xyz_dst"), arg(1, "xyz_src")
+        return ("alu", 8.0 * dst.shape[0] * dst.shape[1] * src.shape[1] / 1e12, None)
+    return None
 
 
 PEAKS = {"alu": (157.3, "TFLOP/s"), "mfma": (MFMA_F32_PEAK_TFLOPS, "TFLOP/s"), "hbm": (HBM_PEAK_GBS, "GB/s")}
@@ -288,18 +311,20 @@ def main():
     timer.uninstall()
 
     # dominant kernel = the longest call of the step; roofline for each call
-    work = work_per_call(spec)
-    gathered = logical_gather_bytes(spec)
+    work = {k: v for k, v in timer.work.items() if v is not None}
+    mfma_peak = MFMA_BF16_PEAK_TFLOPS if spec.get("dtype") == "bf16" else MFMA_F32_PEAK_TFLOPS
     roofs = {}
     for k, ms in stages.items():
         if k not in work:
             continue
-        kd, am, un = work[k]
+        kd, am, extra = work[k]
         rate = am / (ms * 1e-3)
         pk, pu = PEAKS[kd]
+        if kd == "mfma":
+            pk = mfma_peak
         roofs[k] = {"bound": kd, "achieved": round(rate, 4), "peak": pk, "unit": pu, "frac": round(rate / pk, 5)}
-        if k in gathered:
-            roofs[k]["logical_gather_GBps"] = round(gathered[k] / (ms * 1e-3) / 1e9, 1)
+        if extra and "logical_gather_bytes" in extra:
+            roofs[k]["logical_gather_GBps"] = round(extra["logical_gather_bytes"] / (ms * 1e-3) / 1e9, 1)
     dom = max((k for k in stages if k in work), key=lambda k: stages[k])
     roof = dict(roofs[dom])
     roof["kernel"] = dom
@@ -309,7 +334,7 @@ def main():
 
     per_module = {}
     module_ms = {}
-    for i, m in enumerate(spec["sa"]):
+    for i, m in enumerate(spec.get("sa", [])):
         per_module[f"sa{i + 1}_centroids_per_s"] = B * m["M"] / t_step
         # serial sum of this module's calls (search + MLP + aggregation)
         ms = sum(stages.get(f"{n}#{i}", 0.0) for n in ("fps", "ball_query", "pointwise_mlp", "aggregate_max"))
@@ -333,7 +358,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if spec.get("dtype") != "bf16" else "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload} (PointNet++ SSG classifier, delayed aggregation)",
+        "config": {"workload": f"{args.workload} ({DESCRIBE.get(args.workload, args.workload)}, delayed aggregation)",
                    "global_batch": B, "points": spec["N"], "path": "delayed",
                    "timing": ("eager launches" if args.eager else "HIP graph replay, search chain on a side stream")
                    + f", {inflight} independent batch(es) in flight on separate streams",

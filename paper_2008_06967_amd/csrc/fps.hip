@@ -12,14 +12,19 @@
 // distance bits (non-negative floats order like signed ints) followed by a
 // "first lane holding the max" ballot.
 //
-// An iteration: each thread updates its P running minima and keeps only
-// their max; a fused-DPP butterfly gives the wave max; the lowest lane
-// holding it then picks its lowest matching slot (so the argmax and the
-// winner's coordinates are selected once, after the reduction).  One
-// barrier per iteration: the per-wave winners go to a double-buffered LDS
-// slot array indexed by iteration parity, so a wave that runs ahead writes
-// the other buffer while slower waves still read this one.  A single-wave
-// workgroup needs no barrier at all.
+// An iteration: each thread updates its P running minima (as float bits:
+// every value is >= 0 or the -1 padding sentinel, so a signed-int min is
+// the strict-less minimum in one instruction) and keeps their max; a
+// fused-DPP butterfly gives the wave max; one ballot per slot then finds
+// the lowest lane holding it and that lane's lowest slot as wave-uniform
+// scalars, and the winner's coordinates are read once with a uniform
+// register index -- per-lane work after the reduction does not grow with
+// P.  One barrier per iteration: the per-wave winners go to a
+// double-buffered LDS slot array indexed by iteration parity, so a wave
+// that runs ahead writes the other buffer while slower waves still read
+// this one.  A single-wave workgroup needs no barrier at all.  The
+// iteration is bound by VALU issue for large P (four waves per SIMD at
+// 16 points per thread) and by the reduction chain for small P.
 #include "common.h"
 
 namespace meso {
@@ -89,28 +94,32 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
                 y = p[3 * j + 1];
                 z = p[3 * j + 2];
             }
-            // both operands are >= 0 or the -1 sentinel, never NaN: fminf is
-            // the strict-less running minimum
-            const float nm = fminf(dist3(x, y, z, cx, cy, cz), dm[q]);
-            dm[q] = nm;
-            tmax = max(tmax, __float_as_int(nm));
+            // both operands are >= 0 or the -1 sentinel, never NaN, so a
+            // signed-int min on the bits is the strict-less running minimum
+            // (one instruction; fminf would also canonicalize)
+            const int nm = min(__float_as_int(dist3(x, y, z, cx, cy, cz)), __float_as_int(dm[q]));
+            dm[q] = __int_as_float(nm);
+            tmax = max(tmax, nm);
         }
-        // 2. wave max; the lowest lane holding it; that lane's lowest slot
+        // 2. wave max; the lowest lane holding it; that lane's lowest slot.
+        //    One ballot per slot, then a scalar search: the slot and the
+        //    lane are wave-uniform, so only the winning lane's point is read
+        //    (no per-lane select chain over the P slots).
         const int wmax = wave_max_i32(tmax);
         const int wl = __builtin_ctzll(ballot(tmax == wmax));
         int sq = P - 1;
-        float sx = 0.0f, sy = 0.0f, sz = 0.0f;
 #pragma unroll
         for (int q = P - 1; q >= 0; --q) {
-            const bool eq = __float_as_int(dm[q]) == wmax;
-            sq = eq ? q : sq;
-            if constexpr (REG_XYZ) {
-                sx = eq ? px[q] : sx;
-                sy = eq ? py[q] : sy;
-                sz = eq ? pz[q] : sz;
-            }
+            const uint64_t hold = ballot(__float_as_int(dm[q]) == wmax);
+            sq = ((hold >> wl) & 1ull) ? q : sq;
         }
-        if constexpr (!REG_XYZ) {
+        sq = __builtin_amdgcn_readfirstlane(sq);
+        float sx, sy, sz;
+        if constexpr (REG_XYZ) {
+            sx = px[sq];   // wave-uniform index into the register arrays
+            sy = py[sq];
+            sz = pz[sq];
+        } else {
             const int j = min(base + sq, N - 1);
             sx = p[3 * j + 0];
             sy = p[3 * j + 1];
