@@ -127,6 +127,8 @@ KNN_CASES = [
     ("k1", 2, 70, 70, 3, 1, "self"),
     ("k64", 1, 200, 50, 16, 64, "other"),
     ("ties", 2, 150, 150, 3, 10, "grid"),
+    ("ties_4ch_groups", 2, 150, 150, 8, 10, "grid"),      # 16-byte channel path with exact ties
+    ("c28_scalar_path", 1, 90, 90, 28, 5, "self"),         # 4-channel groups, bank-conflicting stride: scalar path
     ("interp_like", 2, 256, 1024, 3, 3, "other"),
 ]
 
@@ -313,13 +315,29 @@ def test_conventional_edge(gpu):
     assert normwise(host(out), ref) <= 1e-4
 
 
-@pytest.mark.parametrize("B,Nd,Ns,C", [(2, 4096, 1024, 128), (3, 100, 17, 5), (1, 64, 16, 512), (2, 10, 3, 8)])
+@pytest.mark.parametrize("B,Nd,Ns,C", [(2, 4096, 1024, 128), (3, 100, 17, 5), (1, 64, 16, 512), (2, 10, 3, 8),
+                                       (1, 300, 2500, 7), (2, 129, 3, 4)])
 def test_interpolate3(gpu, B, Nd, Ns, C):
     rr = g(12)
     dst = rr.uniform(-1, 1, (B, Nd, 3)).astype(np.float32)
     src = np.concatenate([dst[:, :min(Ns, Nd) // 2], rr.uniform(-1, 1, (B, Ns - min(Ns, Nd) // 2, 3))], 1)
     src = src.astype(np.float32)
     f = rr.standard_normal((B, Ns, C)).astype(np.float32)
+    ref = O.interpolate3(dst, src, f)
+    out = ops.interpolate3(dev(dst), dev(src), dev(f))
+    assert normwise(host(out), ref) <= 1e-5
+
+
+@pytest.mark.parametrize("Ns_half", [40, 700])
+def test_interpolate3_ties_take_lowest_index(gpu, Ns_half):
+    """Every source point appears twice (indices i and i + Ns_half) with
+    different features: equal distances must resolve to the lower index,
+    across source chunks and across the waves that split them."""
+    rr = g(13)
+    base = rr.uniform(-1, 1, (2, Ns_half, 3)).astype(np.float32)
+    src = np.concatenate([base, base], 1)
+    dst = rr.uniform(-1, 1, (2, 257, 3)).astype(np.float32)
+    f = rr.standard_normal((2, 2 * Ns_half, 6)).astype(np.float32)
     ref = O.interpolate3(dst, src, f)
     out = ops.interpolate3(dev(dst), dev(src), dev(f))
     assert normwise(host(out), ref) <= 1e-5
