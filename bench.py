@@ -1,19 +1,23 @@
 """Benchmark: PointNet++ SSG classifier forward, batch 32 x 1024 points,
-delayed aggregation, on one MI355X.
+delayed aggregation, on one MI355X (--workload picks any of the five
+synthetic workloads instead).
 
 One step = one full forward of the batch (FPS, ball query, per-point MLP,
 aggregation for both set-abstraction levels, group-all MLP, FC head).
 Inputs and weights are resident in HBM before timing; the timed steps
 replay HIP graphs of the two-stream forward; independent batches may be
 kept in flight on separate streams (the count that gives the highest
-throughput among 1-4 is used and reported, with the single-batch latency).
+throughput among 1-4 is used and reported, with the single-batch latency
+and its per-step distribution).
 The JSON line also carries:
   - conventional: the same network in the original order (Eq. (1)) on the
     GPU and the delayed/conventional speedup;
   - stages: per-kernel-call durations from HIP events on the stream each
-    kernel runs on (an eager pass over the same steps);
+    kernel runs on (an eager pass over the same steps), with each call's
+    algorithmic work derived from its arguments;
   - roofline: the dominant kernel's achieved rate against MI355X peak;
-  - cpu_baseline: the CPU oracle timed on this host.
+  - cpu_baseline: the CPU oracle timed on this host (single thread, all
+    cores, and the conventional forward).
 """
 from __future__ import annotations
 
