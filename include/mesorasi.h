@@ -4,13 +4,13 @@
  *
  * Method: Feng et al., "Mesorasi: Architecture Support for Point Cloud
  * Analytics via Delayed-Aggregation" (arXiv 2008.06967).  A point-cloud
- * module computes p_o = F(A(N(p_i), p_i)) (Sec. 2.1, Eq. (1)).  Delayed
- * aggregation (Sec. 3.1, Eq. (2)-(3)) instead runs the shared MLP F once on
+ * module computes p_o = F(A(N(p_i), p_i)) (Sec. 3.1, Eq. (1)).  Delayed
+ * aggregation (Sec. 4.1, Eq. (2)-(3)) instead runs the shared MLP F once on
  * the N input points (the point feature table, PFT), runs the neighbor
  * search N concurrently into the neighbor index table (NIT), and finally
  * aggregates PFT rows by the NIT: max over the K neighbors, then subtract
  * the centroid's own PFT row (max(f_j - f_c) = max(f_j) - f_c, end of the
- * Sec. 3.1 walk-through).
+ * Sec. 4.1 walk-through).
  *
  * General rules for every entry point
  *  - Pointers are DEVICE pointers unless marked "host".  The caller owns
@@ -69,7 +69,7 @@ const char* mesorasi_last_error(void);
 
 /*
  * Farthest-point sampling (the centroid sampling of the PointNet++ modules,
- * Sec. 5 "Software Setup"; the paper names it without defining it).
+ * Sec. 6 "Software Setup"; the paper names it without defining it).
  * Greedy: start at point 0; keep for each point its squared distance to the
  * nearest selected point; select the point where it is largest, the lowest
  * index on ties.  Squared distance: t_c = x_c - y_c, d = fma(t_c, t_c, d)
@@ -85,8 +85,8 @@ const char* mesorasi_last_error(void);
 int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, int32_t* idx, float* cxyz, void* stream);
 
 /*
- * Ball query: neighbor search N (Sec. 2.1 "Neighbor Search") producing the
- * NIT (Sec. 3.1 walk-through).  For each query q, the first K point indices
+ * Ball query: neighbor search N (Sec. 3.1 "Neighbor Search") producing the
+ * NIT (Sec. 4.1 walk-through).  For each query q, the first K point indices
  * in ascending order with squared distance (same rule as FPS) strictly
  * below fl32(radius * radius); remaining slots repeat the first hit, or
  * hold 0 when there is none.
@@ -101,7 +101,7 @@ int mesorasi_ball_query(const float* xyz, const float* qxyz, int64_t B, int64_t 
 
 /*
  * k nearest neighbours in C-dimensional feature space (the DGCNN search in
- * the previous module's output space, Sec. 4.1 "Work Flow").  Squared
+ * the previous module's output space, Sec. 5.1 "Work Flow").  Squared
  * distance t_c = r_c - q_c, d = fma(t_c, t_c, d) for c ascending from 0;
  * the K smallest by (distance, index), sorted; self is included when the
  * query is one of the reference points.
@@ -116,7 +116,7 @@ int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query, int64_t l
                  int64_t M, int32_t C, int32_t K, int32_t* nit, float* dist, void* stream);
 
 /*
- * Shared per-point MLP: feature computation F (Sec. 2.1 "Feature
+ * Shared per-point MLP: feature computation F (Sec. 3.1 "Feature
  * Computation"; Eq. (3) with phi = ReLU), run on any set of rows -- in the
  * delayed module on the N input points, producing the PFT.
  *   layer l: h_{l+1} = phi_l(h_l W_l^T + b_l), phi_l = ReLU iff bit l of
@@ -137,7 +137,7 @@ int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query, int64_t l
  *         F32 holds bf16-representable values).
  *   pool_group 0: y is [rows, ld_y].  G > 0: rows % G == 0 and y is
  *         [rows / G, ld_y] holding the column max over each group of G
- *         consecutive rows (the reduction after F, Sec. 2.1; group-all
+ *         consecutive rows (the reduction after F, Sec. 3.1; group-all
  *         modules).  Pooling needs ReLU on the last layer and out_dtype F32.
  *   ws   device workspace of at least mesorasi_pointwise_mlp_workspace()
  *        bytes (NULL allowed when that size is 0).
@@ -158,7 +158,7 @@ size_t mesorasi_pointwise_mlp_workspace(int64_t rows, int32_t n_layers, const in
                                         int64_t pool_group);
 
 /*
- * Aggregation A on the PFT (Sec. 4.2 first paragraph; Sec. 3.1 max/subtract
+ * Aggregation A on the PFT (Sec. 5.2 first paragraph; Sec. 4.1 max/subtract
  * distributivity): for each NIT entry, gather the K PFT rows, take the
  * column-wise max (exact), then combine with the centroid row in one fp32
  * operation: out = max + sign * centroid, then ReLU when relu != 0.
@@ -179,7 +179,7 @@ int mesorasi_aggregate_max(const void* pft, int64_t ld_pft, int32_t pft_dtype, c
                            int64_t ld_c, int32_t sign, int32_t relu, float* out, int64_t ld_out, void* stream);
 
 /*
- * Conventional module, kept as the comparison path (Eq. (1); Sec. 2.1
+ * Conventional module, kept as the comparison path (Eq. (1); Sec. 3.1
  * "Aggregation" and "Feature Computation"): build the neighbor feature
  * matrix (NFM) in the workspace, run the MLP on every (centroid, neighbor)
  * row, and max-reduce over the K rows of each centroid.
@@ -205,7 +205,7 @@ size_t mesorasi_conventional_workspace(int64_t B, int64_t M, int32_t K, int32_t 
 
 /*
  * Feature propagation by 3-NN inverse-distance interpolation (the
- * three_interpolate kernel of the PointNet++ segmentation baseline, Sec. 5
+ * three_interpolate kernel of the PointNet++ segmentation baseline, Sec. 6
  * "Software Setup").  For every destination point: its 3 nearest source
  * points by the kNN rule above (C = 3), weights w = 1 / max(d2, 1e-10),
  * f_dst = sum_k w_k f_k / sum_k w_k (fp32).

@@ -7,11 +7,11 @@ numpy arrays; every arithmetic step is one of the C primitives in
 one-off EdgeConv weight fold ``fl32(W1 - W2)``, which is a float32 numpy
 subtraction, i.e. one IEEE binary32 subtraction per element).
 
-Delayed modules follow Sec. 3.1 (Eq. (2)-(3), walk-through): F runs once on
+Delayed modules follow Sec. 4.1 (Eq. (2)-(3), walk-through): F runs once on
 the N input points into the point feature table (PFT), N produces the
 neighbor index table (NIT), and A gathers PFT rows by the NIT, reduces them
 with max and then combines the centroid's own PFT row.  Conventional
-modules follow Sec. 2.1 (Eq. (1)): N, then A builds the neighbor feature
+modules follow Sec. 3.1 (Eq. (1)): N, then A builds the neighbor feature
 matrix, then F on every (centroid, neighbor) row, then the max reduction.
 """
 from __future__ import annotations

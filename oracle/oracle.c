@@ -6,12 +6,12 @@
  * order written.
  *
  * Paper sections followed (Feng et al., arXiv 2008.06967):
- *  - module N -> A -> F -> reduce: Sec. 2.1 "Module Internals", Eq. (1)
- *  - delayed-aggregation, PFT and NIT: Sec. 3.1, Eq. (2)-(3), walk-through
- *  - max/subtract distributivity: Sec. 3.1, last paragraph of walk-through
- *  - aggregation loop over NIT entries: Sec. 4.2, first paragraph
+ *  - module N -> A -> F -> reduce: Sec. 3.1 "Module Internals", Eq. (1)
+ *  - delayed-aggregation, PFT and NIT: Sec. 4.1, Eq. (2)-(3), walk-through
+ *  - max/subtract distributivity: Sec. 4.1, last paragraph of walk-through
+ *  - aggregation loop over NIT entries: Sec. 5.2, first paragraph
  *  - sampling / grouping / three_interpolate kernels of the PointNet++
- *    baselines: Sec. 5, "Software Setup"
+ *    baselines: Sec. 6, "Software Setup"
  */
 #include "oracle.h"
 
@@ -43,7 +43,7 @@ float orc_bf16_round(float f) {
 
 /* ------------------------------------------------------------------------
  * Farthest-point sampling.  The paper names the sampling step of its
- * PointNet++ baselines (Sec. 5, Software Setup) without defining it; this is
+ * PointNet++ baselines (Sec. 6, Software Setup) without defining it; this is
  * the standard greedy definition: keep, for every point, its distance to the
  * nearest already-selected point, and select the point where that distance
  * is largest.  Start at index 0, lowest index wins a tie.
@@ -105,7 +105,7 @@ void orc_fps_bruteforce(const float* xyz, int64_t B, int64_t N, int64_t M, int32
 }
 
 /* ------------------------------------------------------------------------
- * Ball query (neighbor search N of Eq. (1); Sec. 2.1 "Neighbor Search").
+ * Ball query (neighbor search N of Eq. (1); Sec. 3.1 "Neighbor Search").
  * First K points in index order strictly inside the radius; remaining slots
  * repeat the first hit.  cnt = number of real hits (<= K); scanned = number
  * of candidates examined before the K-th hit (N when fewer than K hits).
@@ -133,7 +133,7 @@ void orc_ball_query(const float* xyz, const float* qxyz, int64_t B, int64_t N, i
 
 /* ------------------------------------------------------------------------
  * k nearest neighbours in C-dimensional space (DGCNN search in the previous
- * module's output space, Sec. 4.1 "Work Flow"; PointNet++ 3-NN
+ * module's output space, Sec. 5.1 "Work Flow"; PointNet++ 3-NN
  * interpolation).  Output sorted by (dist2, index); self included.
  * Insertion into a sorted list of K; candidates arrive in ascending index
  * order, so a strict '<' keeps equal distances in index order.
@@ -170,7 +170,7 @@ void orc_knn(const float* ref, int64_t ld_ref, const float* query, int64_t ld_qu
 }
 
 /* ------------------------------------------------------------------------
- * Shared per-point MLP (feature computation F, Sec. 2.1 "Feature
+ * Shared per-point MLP (feature computation F, Sec. 3.1 "Feature
  * Computation"; Eq. (3) with phi = ReLU).  y is [rows, dims[n_layers]].
  * ---------------------------------------------------------------------- */
 void orc_mlp(const float* x, int64_t rows, int32_t n_layers, const int32_t* dims, const float* const* W,
@@ -214,8 +214,8 @@ void orc_mlp(const float* x, int64_t rows, int32_t n_layers, const int32_t* dims
 }
 
 /* ------------------------------------------------------------------------
- * Aggregation A on the point feature table (Sec. 4.2 first paragraph;
- * Sec. 3.1 max/subtract distributivity): for each NIT entry gather the K
+ * Aggregation A on the point feature table (Sec. 5.2 first paragraph;
+ * Sec. 4.1 max/subtract distributivity): for each NIT entry gather the K
  * PFT rows, reduce them column-wise with max, then combine with the
  * centroid's row: out = max + sign * centroid (sign -1 for PointNet++
  * offsets, +1 for the DGCNN x_i term).  Centroid row from cidx (a PFT row),
@@ -246,7 +246,7 @@ void orc_aggregate_max(const float* pft, int64_t ld_pft, const int32_t* nit, int
 }
 
 /* ------------------------------------------------------------------------
- * Conventional aggregation before F (Eq. (1); Sec. 2.1 "Aggregation"):
+ * Conventional aggregation before F (Eq. (1); Sec. 3.1 "Aggregation"):
  * build the neighbor feature matrix, one row per (centroid, neighbor).
  *  - pointnet: [x_j - c, f_j]            (dims[0] = 3 + cf)
  *  - offsets : [x_j - x_c, f_j - f_c]    (whole-vector offsets p_k - p_i,
@@ -298,7 +298,7 @@ void orc_group_edge(const float* f, int64_t ld_f, int32_t C, const int32_t* nit,
             }
 }
 
-/* Reduction after F in the conventional module (Sec. 2.1, last paragraph of
+/* Reduction after F in the conventional module (Sec. 3.1, last paragraph of
  * "Feature Computation"): column-wise max over each group of G rows. */
 void orc_rowgroup_max(const float* y, int64_t groups, int32_t G, int32_t C, float* out, int64_t ld_out) {
     for (int64_t g = 0; g < groups; ++g)
@@ -314,7 +314,7 @@ void orc_rowgroup_max(const float* y, int64_t groups, int32_t G, int32_t C, floa
 
 /* ------------------------------------------------------------------------
  * Feature propagation by 3-NN inverse-distance interpolation
- * (three_interpolate of the PointNet++ segmentation baseline, Sec. 5,
+ * (three_interpolate of the PointNet++ segmentation baseline, Sec. 6,
  * Software Setup).  Weights 1 / max(d2, 1e-10) over the 3 nearest source
  * points (by orc_knn's rule), normalised; arithmetic in fp64, one final
  * rounding to fp32.

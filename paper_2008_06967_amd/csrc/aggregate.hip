@@ -1,8 +1,8 @@
 // Aggregation on the point feature table, gfx950.
 //
-// Sec. 4.2 (first paragraph): for every NIT entry gather the K PFT rows,
+// Sec. 5.2 (first paragraph): for every NIT entry gather the K PFT rows,
 // reduce them column-wise with max, then combine with the centroid's row
-// (max(f_j - f_c) = max(f_j) - f_c, end of the Sec. 3.1 walk-through).
+// (max(f_j - f_c) = max(f_j) - f_c, end of the Sec. 4.1 walk-through).
 //
 // Mapping: one wave per (centroid, channel slice).  A lane loads 16 bytes
 // of a row (4 fp32 or 8 bf16 channels); LPR lanes cover a row slice of
@@ -15,7 +15,7 @@
 // centroid row.  Workgroups are renumbered so that each XCD's L2 serves a
 // contiguous range of clouds.  Nothing N x K x C sized is ever written.  Wider PFTs are split into
 // channel slices processed by different waves -- the column partitioning
-// of the paper's PFT buffer (Sec. 4.2, "PFT Partitioning").
+// of the paper's PFT buffer (Sec. 5.2, "PFT Partitioning").
 #include "common.h"
 
 namespace meso {

@@ -1,5 +1,5 @@
-// Ball query on gfx950 -- the neighbor search N (Sec. 2.1 "Neighbor Search")
-// that fills the neighbor index table (NIT, Sec. 3.1 walk-through).
+// Ball query on gfx950 -- the neighbor search N (Sec. 3.1 "Neighbor Search")
+// that fills the neighbor index table (NIT, Sec. 4.1 walk-through).
 //
 // One wave per query.  The wave walks the cloud in 64-point chunks in index
 // order; each lane tests one point, a ballot collects the chunk's hits and

@@ -1,6 +1,6 @@
 // Farthest-point sampling on gfx950: one workgroup per cloud.
 //
-// The sampling step of the PointNet++ modules (Sec. 5, "Software Setup")
+// The sampling step of the PointNet++ modules (Sec. 6, "Software Setup")
 // read as greedy max-min sampling from point 0, lowest index on ties.
 //
 // Layout: thread t of a T-thread workgroup owns the P consecutive points
@@ -191,7 +191,7 @@ extern "C" int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, i
     // workgroup shape per cloud size, from a sweep on MI355X: the iteration
     // time is a fixed reduction/barrier chain plus P points of VALU work
     if (n <= 128) launch_fps<64, 2, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 256) launch_fps<128, 2, true>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 256) launch_fps<64, 4, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 512) launch_fps<256, 2, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 1024) launch_fps<512, 2, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 2048) launch_fps<512, 4, true>(xyz, B, n, m, idx, cxyz, s);

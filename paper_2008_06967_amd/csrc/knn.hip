@@ -1,7 +1,7 @@
 // k-nearest-neighbour search and 3-NN interpolation on gfx950.
 //
 // kNN: the DGCNN neighbor search in the previous module's output space
-// (Sec. 4.1 "Work Flow").  A workgroup of 8 waves serves 32 queries of one
+// (Sec. 5.1 "Work Flow").  A workgroup of 8 waves serves 32 queries of one
 // cloud (4 per wave).  Reference points stream through LDS in tiles of 64;
 // lane l of every wave computes the distance from reference l of the tile
 // to each of its wave's 4 queries (query rows are read from LDS by
@@ -15,7 +15,7 @@
 //
 // interpolate3: feature propagation by inverse squared-distance weights
 // over the 3 nearest coarse points (the three_interpolate kernel of the
-// PointNet++ segmentation baseline, Sec. 5 "Software Setup"); layout at the
+// PointNet++ segmentation baseline, Sec. 6 "Software Setup"); layout at the
 // kernel.
 #include "common.h"
 

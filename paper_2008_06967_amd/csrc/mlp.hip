@@ -1,9 +1,9 @@
 // Shared per-point MLP (feature computation F) on gfx950 MFMA, and the
 // conventional aggregate-then-MLP module built on it.
 //
-// F is a matrix-matrix product because all rows share the weights (Sec. 2.1
+// F is a matrix-matrix product because all rows share the weights (Sec. 3.1
 // "Feature Computation"); with delayed aggregation it runs on the N input
-// points instead of the N_out x K neighbor rows (Sec. 3.1, Eq. (3)).
+// points instead of the N_out x K neighbor rows (Sec. 4.1, Eq. (3)).
 //
 // One launch per layer: Y = phi(X W^T + b) with X = [x0 | x1] (two column
 // sources, so the first layer reads xyz and the previous module's features

@@ -1,7 +1,7 @@
 // Fused multi-layer shared MLP for narrow layers, gfx950.
 //
 // With delayed aggregation the MLP runs on the N input points, so its layer
-// outputs are small enough to stay on chip (Sec. 3.2: layer outputs shrink
+// outputs are small enough to stay on chip (Sec. 4.2: layer outputs shrink
 // from 8-32 MB to 512 KB-1 MB).  A workgroup keeps one 64-row tile's
 // activations in LDS through all layers (k-major, odd stride); only the last
 // layer goes to HBM (or is pooled).

@@ -2,11 +2,11 @@
 calls only (every arithmetic step runs in libmesorasi.so; torch provides
 device memory, streams and events).
 
-Delayed aggregation (Sec. 3.1): the neighbor search N does not depend on
+Delayed aggregation (Sec. 4.1): the neighbor search N does not depend on
 the MLP F, so all searches run on a side stream while F runs on the main
 stream; an event joins them right before each aggregation A.  For
 PointNet++ the whole xyz chain (FPS -> ball query -> FPS of the next
-level ...) depends on coordinates only and runs ahead (Sec. 4.1 "Work
+level ...) depends on coordinates only and runs ahead (Sec. 5.1 "Work
 Flow"); for DGCNN each layer's kNN overlaps that layer's MLP.  The
 conventional path (Eq. (1)) serialises N -> A -> F per module.
 

@@ -261,7 +261,7 @@ def _sa(M, radius, K, mlp):
 
 WORKLOADS = {
     # one set-abstraction module, the paper's walk-through shape
-    # (1024 -> 512 centroids, K = 32, 3 -> 128; Sec. 3.1)
+    # (1024 -> 512 centroids, K = 32, 3 -> 128; Sec. 4.1)
     "sa_module": dict(id=0, kind="pointnet2_cls", B=1, N=1024, gen="uniform_cube", n_feat=0,
                       sa=[_sa(512, 0.2, 32, [64, 64, 128])], group_all=None, fc=None, dtype="f32"),
     # PointNet++ SSG classifier (ModelNet40-like objects)

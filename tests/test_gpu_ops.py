@@ -47,6 +47,8 @@ FPS_CASES = [
     ("one", 3, 1, 1, "normal"),
     ("ragged", 3, 100, 37, "normal"),
     ("grid_ties", 2, 300, 300, "grid"),
+    ("n200_one_wave", 3, 200, 180, "normal"),        # 129..256 points: one wave, 4 points per lane
+    ("grid_ties_256", 2, 256, 256, "grid"),
     ("dups", 2, 700, 500, "dups"),
     ("sa_module", 1, 1024, 512, "cube"),
     ("cls_sa2", 4, 512, 128, "mesh"),

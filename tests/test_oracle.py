@@ -335,7 +335,7 @@ def normwise(a, b):
 
 def test_edgeconv_delayed_equals_conventional():
     """ReLU is monotone and the edge function linear, so delayed is exact
-    in real arithmetic (one-layer modules, Sec. 6.3 Ltd discussion)."""
+    in real arithmetic (one-layer modules, Sec. 7.3 Ltd discussion)."""
     r = g(12)
     X = r.standard_normal((2, 64, 6)).astype(np.float32)
     W = (r.standard_normal((16, 12)) * 0.5).astype(np.float32)
