@@ -48,8 +48,9 @@ def lib():
         L.orc_group_edge.argtypes = [_p, _i64, _i32, _p, _i64, _i64, _i32, _p]
         L.orc_rowgroup_max.argtypes = [_p, _i64, _i32, _i32, _p, _i64]
         L.orc_interpolate3.argtypes = [_p, _p, _p, _i64, _i64, _i64, _i64, _i32, _p, _i64]
+        L.orc_ltd_group.argtypes = [_p, _p, _p, _p, _i64, _i64, _i64, _i32, _i32, _p]
         for fn in ("orc_fps", "orc_fps_bruteforce", "orc_ball_query", "orc_knn", "orc_mlp", "orc_aggregate_max",
-                   "orc_group_pointnet", "orc_group_offsets", "orc_group_edge", "orc_rowgroup_max",
+                   "orc_group_pointnet", "orc_group_offsets", "orc_group_edge", "orc_rowgroup_max", "orc_ltd_group",
                    "orc_interpolate3"):
             getattr(L, fn).restype = None
         _lib = L
@@ -146,6 +147,19 @@ def mlp(x, Ws, bs, relu_mask=None, bf16=False):
     lib().orc_mlp(_ptr(x), rows, n, _ptr(dims_a), ctypes.cast(Wp, ctypes.c_void_p),
                   ctypes.cast(bp, ctypes.c_void_p), relu_mask, 1 if bf16 else 0, _ptr(y))
     return y.reshape(lead + (dims[-1],))
+
+
+def ltd_group(p1, q, b1, nit):
+    """p1 [B,N,C]; q [B,M,C]; b1 [C] or None; nit [B,M,K] -> h1 [B,M,K,C] =
+    ReLU(p1[nit] - q + b1) (the first layer of a limited-delayed module)."""
+    p1, q, nit = _f32(p1), _f32(q), _i32a(nit)
+    B, N, C = p1.shape
+    M, K = nit.shape[1], nit.shape[2]
+    assert q.shape == (B, M, C)
+    bb = None if b1 is None else _f32(b1)
+    h1 = np.empty((B, M, K, C), np.float32)
+    lib().orc_ltd_group(_ptr(p1), _ptr(q), _ptr(bb), _ptr(nit), B, N, M, K, C, _ptr(h1))
+    return h1
 
 
 def aggregate_max(pft, nit, cidx=None, cfeat=None, sign=-1, relu=False):

@@ -19,7 +19,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import (fps, ball_query, knn, mlp, aggregate_max, group_pointnet, group_edge, rowgroup_max,
-               interpolate3)
+               interpolate3, ltd_group)
 
 
 def _cat(xyz, feat):
@@ -44,6 +44,27 @@ def sa_conventional(xyz, feat, M, radius, K, Ws, bs, bf16=False):
     B, C = xyz.shape[0], h.shape[-1]
     out = rowgroup_max(h.reshape(B, M * K, C), K)             # [B, M, C]
     return dict(idx=idx, cxyz=cxyz, nit=nit, cnt=cnt, out=out)
+
+
+def sa_ltd(xyz, feat, M, radius, K, Ws, bs):
+    """Set-abstraction module with limited delayed aggregation (Sec. 7.3):
+    the first layer's matrix product runs once on the N input points (P1)
+    and once on the centroids' coordinates with the xyz columns of W1 (Q);
+    each (centroid, neighbor) row then starts from ReLU(P1[j] - Q[c] + b1)
+    and the remaining layers run on the K neighbor rows before the max.
+    Exact in real arithmetic: W1 [x_j - x_c | f_j] = W1 [x_j | f_j] -
+    W1[:, :3] x_c."""
+    idx, cxyz = fps(xyz, M)
+    nit, cnt, _ = ball_query(xyz, cxyz, radius, K)
+    W1 = np.asarray(Ws[0], np.float32)
+    p1 = mlp(_cat(xyz, feat), [W1], [None], relu_mask=0)          # [B, N, C1]
+    q = mlp(cxyz, [np.ascontiguousarray(W1[:, :3])], [None], relu_mask=0)   # [B, M, C1]
+    h = ltd_group(p1, q, bs[0], nit)                              # [B, M, K, C1]
+    if len(Ws) > 1:
+        h = mlp(h, Ws[1:], bs[1:])
+    B, C = xyz.shape[0], h.shape[-1]
+    out = rowgroup_max(h.reshape(B, M * K, C), K)
+    return dict(idx=idx, cxyz=cxyz, nit=nit, cnt=cnt, p1=p1, q=q, out=out)
 
 
 def group_all(xyz, feat, Ws, bs, bf16=False):
@@ -94,11 +115,21 @@ def edgeconv_conventional(X, k, W, b):
 # networks
 # ----------------------------------------------------------------------------
 
+def _sa_order(delayed, bf16):
+    """delayed: True (Sec. 4.1), False (conventional, Sec. 3.1) or "ltd"
+    (limited delayed aggregation, Sec. 7.3; fp32 networks)."""
+    if delayed == "ltd":
+        if bf16:
+            raise ValueError("the limited delayed order is composed for fp32 networks")
+        return lambda p, f, M, r, K, Ws, bs, bf16=False: sa_ltd(p, f, M, r, K, Ws, bs)
+    return sa_delayed if delayed else sa_conventional
+
+
 def pointnet2_cls(spec, xyz, feat, weights, delayed=True):
     """Set-abstraction stack [+ group-all + FC head].  Returns a dict with
     per-module outputs and the final tensor under 'out'."""
     bf16 = spec["dtype"] == "bf16"
-    sa = sa_delayed if delayed else sa_conventional
+    sa = _sa_order(delayed, bf16)
     res = dict(modules=[])
     p, f = xyz, feat
     for m, (Ws, bs) in zip(spec["sa"], weights["sa"]):
@@ -116,6 +147,9 @@ def pointnet2_cls(spec, xyz, feat, weights, delayed=True):
 
 
 def dgcnn(spec, xyz, weights, delayed=True):
+    """delayed=True or "ltd": the delayed EdgeConv.  Its module has one
+    layer, so hoisting that layer's product (the limited order, Sec. 7.3)
+    is the whole delayed order."""
     ec = edgeconv_delayed if delayed else edgeconv_conventional
     X = xyz
     res = dict(layers=[])
@@ -134,7 +168,7 @@ def dgcnn(spec, xyz, weights, delayed=True):
 
 def pointnet2_seg(spec, xyz, feat, weights, delayed=True):
     bf16 = spec["dtype"] == "bf16"
-    sa = sa_delayed if delayed else sa_conventional
+    sa = _sa_order(delayed, bf16)
     levels = [(xyz, feat)]
     res = dict(modules=[], fp=[])
     p, f = xyz, feat

@@ -298,6 +298,36 @@ void orc_group_edge(const float* f, int64_t ld_f, int32_t C, const int32_t* nit,
             }
 }
 
+/*
+ * Limited delayed aggregation (Sec. 7.3, "Ltd"): only the first layer's
+ * matrix product is hoisted before aggregation, which keeps the module
+ * exact because that product is linear.  With the PointNet++ grouping row
+ * [x_j - x_c | f_j], the first layer's pre-activation is
+ *   W1 [x_j | f_j] - W1[:, :3] x_c + b1 = P1[j] - Q[c] + b1,
+ * where P1 = [x | f] W1^T is computed once per input point and Q[c] is the
+ * centroid's term.  This routine forms the first layer's output for every
+ * (centroid, neighbor) row:
+ *   h1[b, c, k, :] = ReLU(P1[b, nit[b, c, k], :] - Q[b, c, :] + b1)
+ * in fp64 on the stored fp32 tables, one rounding to fp32.  Layout:
+ * p1 [B, N, C], q [B, M, C], b1 [C] (may be NULL), nit [B, M, K],
+ * h1 [B, M, K, C].
+ */
+void orc_ltd_group(const float* p1, const float* q, const float* b1, const int32_t* nit, int64_t B, int64_t N,
+                   int64_t M, int32_t K, int32_t C, float* h1) {
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t c = 0; c < M; ++c)
+            for (int32_t k = 0; k < K; ++k) {
+                const int64_t j = nit[(b * M + c) * K + k];
+                const float* pr = p1 + (b * N + j) * C;
+                const float* qr = q + (b * M + c) * C;
+                float* out = h1 + ((b * M + c) * K + k) * C;
+                for (int32_t ch = 0; ch < C; ++ch) {
+                    double v = (double)pr[ch] - (double)qr[ch] + (b1 ? (double)b1[ch] : 0.0);
+                    out[ch] = (float)(v > 0.0 ? v : 0.0);
+                }
+            }
+}
+
 /* Reduction after F in the conventional module (Sec. 3.1, last paragraph of
  * "Feature Computation"): column-wise max over each group of G rows. */
 void orc_rowgroup_max(const float* y, int64_t groups, int32_t G, int32_t C, float* out, int64_t ld_out) {

@@ -60,6 +60,9 @@ void orc_group_edge(const float* f, int64_t ld_f, int32_t C, const int32_t* nit,
 
 void orc_rowgroup_max(const float* y, int64_t groups, int32_t G, int32_t C, float* out, int64_t ld_out);
 
+void orc_ltd_group(const float* p1, const float* q, const float* b1, const int32_t* nit, int64_t B, int64_t N,
+                   int64_t M, int32_t K, int32_t C, float* h1);
+
 void orc_interpolate3(const float* xyz_dst, const float* xyz_src, const float* f_src, int64_t ld_src,
                       int64_t B, int64_t Nd, int64_t Ns, int32_t C, float* f_dst, int64_t ld_dst);
 

@@ -346,6 +346,58 @@ def test_edgeconv_delayed_equals_conventional():
     assert normwise(a["out"], c["out"]) < 1e-5
 
 
+@pytest.mark.parametrize("with_feat", [True, False])
+def test_ltd_module_equals_conventional(with_feat):
+    """Limited delayed aggregation (Sec. 7.3) hoists only the first layer's
+    matrix product, which is linear, so the module is exact: the oracle's
+    Ltd composition matches the conventional one up to fp32 rounding of its
+    intermediate tables."""
+    r = g(21)
+    xyz = r.uniform(-1, 1, (2, 96, 3)).astype(np.float32)
+    feat = r.standard_normal((2, 96, 5)).astype(np.float32) if with_feat else None
+    cin = 3 + (5 if with_feat else 0)
+    dims = [cin, 16, 12, 20]
+    Ws = [(r.standard_normal((dims[i + 1], dims[i])) * np.sqrt(2.0 / dims[i])).astype(np.float32) for i in range(3)]
+    bs = [r.uniform(-0.1, 0.1, dims[i + 1]).astype(np.float32) for i in range(3)]
+    a = ON.sa_ltd(xyz, feat, 24, 0.5, 8, Ws, bs)
+    c = ON.sa_conventional(xyz, feat, 24, 0.5, 8, Ws, bs)
+    assert np.array_equal(a["nit"], c["nit"])
+    assert normwise(a["out"], c["out"]) < 1e-5
+    d = ON.sa_delayed(xyz, feat, 24, 0.5, 8, Ws, bs)
+    assert normwise(d["out"], c["out"]) > 1e-3          # the full delayed order is approximate
+
+
+def test_ltd_network_matches_conventional():
+    """The classifier in the limited order equals the conventional order to
+    fp32 rounding (every SA module exact, group-all and FC shared)."""
+    spec = synth.workload("pointnet2_cls", B=1)
+    xyz, feat = synth.make_points(spec)
+    w = synth.make_weights(spec)
+    a = ON.forward(spec, xyz, feat, w, delayed="ltd")
+    c = ON.forward(spec, xyz, feat, w, delayed=False)
+    for ma, mc in zip(a["modules"], c["modules"]):
+        assert np.array_equal(ma["nit"], mc["nit"])
+        assert normwise(ma["out"], mc["out"]) < 1e-5
+    assert normwise(a["out"], c["out"]) < 1e-5
+
+
+def test_ltd_group_needs_the_centroid_term():
+    """Dropping the centroid term Q (or its sign) breaks the identity: the
+    first-layer rows then differ from the conventional first layer."""
+    r = g(22)
+    xyz = r.uniform(-1, 1, (1, 64, 3)).astype(np.float32)
+    W1 = r.standard_normal((8, 3)).astype(np.float32)
+    b1 = r.uniform(-0.1, 0.1, 8).astype(np.float32)
+    idx, cxyz = O.fps(xyz, 16)
+    nit, _, _ = O.ball_query(xyz, cxyz, 0.7, 6)
+    p1 = O.mlp(xyz, [W1], [None], relu_mask=0)
+    q = O.mlp(cxyz, [W1], [None], relu_mask=0)
+    conv1 = O.mlp(O.group_pointnet(xyz, None, cxyz, nit), [W1], [b1])     # first layer on NFM rows
+    assert normwise(O.ltd_group(p1, q, b1, nit), conv1) < 1e-6
+    assert normwise(O.ltd_group(p1, np.zeros_like(q), b1, nit), conv1) > 1e-2
+    assert normwise(O.ltd_group(p1, -q, b1, nit), conv1) > 1e-2
+
+
 def test_linear_module_exact_without_phi():
     """Eq. (3) without phi: one linear layer and zero bias make delayed ==
     conventional; a bias b makes conventional - delayed == b."""
