@@ -204,6 +204,34 @@ size_t mesorasi_conventional_workspace(int64_t B, int64_t M, int32_t K, int32_t 
                                        int32_t dtype);
 
 /*
+ * Limited delayed aggregation (Sec. 7.3, "Ltd"): only the first MLP
+ * layer's matrix product is hoisted before aggregation, which keeps the
+ * module exact because that product is linear.  The caller computes
+ *   p1 = [xyz | feat] W1^T on the N input points  (mesorasi_pointwise_mlp,
+ *        one layer, no bias, no ReLU)            -> [B, N, ld_p], C1 columns
+ *   q  = cxyz W1[:, :3]^T on the M centroids      -> [B, M, ld_q], C1 columns
+ * and this call forms, for every (centroid c, neighbor k) row,
+ *   h1 = ReLU(p1[b, nit[b, c, k], :] - q[b, c, :] + b1)
+ * (fp32: the subtraction, then the bias) in the workspace, runs the
+ * remaining layers (n_layers >= 1, dims[0] == C1) on those B*M*K rows and
+ * max-reduces over the K rows of each centroid into out [B, M, ld_out].
+ *   b1  [C1] float32 or NULL (no first-layer bias).
+ *   nit [B, M, K] int32, per-cloud indices in [0, N).
+ *   MLP arguments as in mesorasi_pointwise_mlp (last layer must have ReLU).
+ *   ws  at least mesorasi_ltd_workspace() bytes.
+ * Errors: as mesorasi_pointwise_mlp plus EINVAL for NULL p1, q or nit,
+ *         ld_p or ld_q < C1, dims[0] != C1; EUNSUPPORTED for n_layers < 1
+ *         (a one-layer module's limited order is its delayed order:
+ *         mesorasi_aggregate_max).
+ */
+int mesorasi_ltd_module(const float* p1, int64_t ld_p, const float* q, int64_t ld_q, const float* b1,
+                        const int32_t* nit, int64_t B, int64_t N, int64_t M, int32_t K, int32_t C1, int32_t n_layers,
+                        const int32_t* dims, const void* const* W, const float* const* bias, uint32_t relu_mask,
+                        int32_t dtype, float* out, int64_t ld_out, void* ws, size_t ws_bytes, void* stream);
+
+size_t mesorasi_ltd_workspace(int64_t B, int64_t M, int32_t K, int32_t n_layers, const int32_t* dims, int32_t dtype);
+
+/*
  * Feature propagation by 3-NN inverse-distance interpolation (the
  * three_interpolate kernel of the PointNet++ segmentation baseline, Sec. 6
  * "Software Setup").  For every destination point: its 3 nearest source

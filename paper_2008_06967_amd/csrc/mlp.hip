@@ -913,6 +913,43 @@ __global__ void group_edge_kernel(const float* __restrict__ f, int C, int64_t ld
     }
 }
 
+// First layer of a limited-delayed module (Sec. 7.3): every (centroid,
+// neighbor) row h1 = ReLU(p1[neighbor] - q[centroid] + b1), four channels
+// per thread when the rows allow 16-byte access.
+template <bool VEC>
+__global__ void ltd_group_kernel(const float* __restrict__ p1, int64_t ldp, const float* __restrict__ q, int64_t ldq,
+                                 const float* __restrict__ b1, const int32_t* __restrict__ nit, int N, int M, int K,
+                                 int C, int64_t total_rows, float* __restrict__ h1) {
+    const int L = VEC ? 4 : 1;
+    const int CL = C / L;
+    const int64_t n = total_rows * CL;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = e / CL;
+        const int c = (int)(e - row * CL) * L;
+        const int64_t cm = row / K;            // global centroid (b * M + m)
+        const int64_t b = cm / M;
+        const int64_t j = b * N + nit[row];
+        if constexpr (VEC) {
+            const float4 pv = *reinterpret_cast<const float4*>(p1 + j * ldp + c);
+            const float4 qv = *reinterpret_cast<const float4*>(q + cm * ldq + c);
+            const float4 bv = b1 ? *reinterpret_cast<const float4*>(b1 + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+            float4 v;
+            v.x = (pv.x - qv.x) + bv.x;
+            v.y = (pv.y - qv.y) + bv.y;
+            v.z = (pv.z - qv.z) + bv.z;
+            v.w = (pv.w - qv.w) + bv.w;
+            v.x = v.x > 0.0f ? v.x : 0.0f;
+            v.y = v.y > 0.0f ? v.y : 0.0f;
+            v.z = v.z > 0.0f ? v.z : 0.0f;
+            v.w = v.w > 0.0f ? v.w : 0.0f;
+            *reinterpret_cast<float4*>(h1 + row * C + c) = v;
+        } else {
+            const float v = (p1[j * ldp + c] - q[cm * ldq + c]) + (b1 ? b1[c] : 0.0f);
+            h1[row * C + c] = v > 0.0f ? v : 0.0f;
+        }
+    }
+}
+
 }  // namespace meso
 
 using namespace meso;
@@ -1007,4 +1044,55 @@ extern "C" int mesorasi_conventional_module(const float* xyz, const float* feat,
     if (rc != MESORASI_OK) return rc;
     return run_mlp(nfm, cin, cin, nullptr, 0, 0, rows, n_layers, dims, W, bias, relu_mask, dtype, MESORASI_F32, out,
                    ld_out, K, static_cast<char*>(ws) + nfm_bytes, s);
+}
+
+extern "C" size_t mesorasi_ltd_workspace(int64_t B, int64_t M, int32_t K, int32_t n_layers, const int32_t* dims,
+                                         int32_t dtype) {
+    if (B < 0 || M < 0 || K < 1 || n_layers < 1) return 0;
+    const int64_t rows = B * M * K;
+    if (check_mlp_spec("mesorasi_ltd_workspace", rows, n_layers, dims, dtype) != MESORASI_OK) return 0;
+    return align256((size_t)rows * (size_t)dims[0] * 4) + mlp_ws_bytes(rows, n_layers, dims, dtype);
+}
+
+extern "C" int mesorasi_ltd_module(const float* p1, int64_t ld_p, const float* q, int64_t ld_q, const float* b1,
+                                   const int32_t* nit, int64_t B, int64_t N, int64_t M, int32_t K, int32_t C1,
+                                   int32_t n_layers, const int32_t* dims, const void* const* W,
+                                   const float* const* bias, uint32_t relu_mask, int32_t dtype, float* out,
+                                   int64_t ld_out, void* ws, size_t ws_bytes, void* stream) {
+    const char* who = "mesorasi_ltd_module";
+    MESO_REQUIRE(B >= 0 && N >= 0 && M >= 0, MESORASI_EINVAL, "%s: negative size", who);
+    MESO_REQUIRE(K >= 1 && C1 >= 1, MESORASI_EINVAL, "%s: K = %d, C1 = %d", who, K, C1);
+    MESO_REQUIRE(n_layers >= 1, MESORASI_EUNSUPPORTED,
+                 "%s: n_layers = %d; a one-layer module's limited order is its delayed order", who, n_layers);
+    const int64_t rows = B * M * K;
+    int rc = check_mlp_spec(who, rows, n_layers, dims, dtype);
+    if (rc != MESORASI_OK) return rc;
+    MESO_REQUIRE(dims[0] == C1, MESORASI_EINVAL, "%s: dims[0] = %d != C1 = %d", who, dims[0], C1);
+    MESO_REQUIRE(ld_p >= C1 && ld_q >= C1, MESORASI_EINVAL, "%s: ld_p / ld_q < C1", who);
+    MESO_REQUIRE(ld_out >= dims[n_layers], MESORASI_EINVAL, "%s: ld_out < dims[n_layers]", who);
+    MESO_REQUIRE((relu_mask >> (n_layers - 1)) & 1u, MESORASI_EUNSUPPORTED, "%s: the last layer needs ReLU", who);
+    if (B == 0 || M == 0) return MESORASI_OK;
+    MESO_REQUIRE(N >= 1, MESORASI_EINVAL, "%s: N = 0 with M > 0", who);
+    MESO_REQUIRE(p1 && q && nit && out && W, MESORASI_EINVAL, "%s: NULL p1, q, nit, out or W", who);
+    for (int l = 0; l < n_layers; ++l) MESO_REQUIRE(W[l] != nullptr, MESORASI_EINVAL, "%s: W[%d] is NULL", who, l);
+    const size_t h1_bytes = align256((size_t)rows * (size_t)C1 * 4);
+    const size_t need = h1_bytes + mlp_ws_bytes(rows, n_layers, dims, dtype);
+    MESO_REQUIRE(ws && ws_bytes >= need, MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who, ws_bytes, need);
+    MESO_REQUIRE(N <= 0x7fffffff && M <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: size", who);
+    hipStream_t s = as_stream(stream);
+    float* h1 = static_cast<float*>(ws);
+    const bool vec = C1 % 4 == 0 && ld_p % 4 == 0 && ld_q % 4 == 0 && aligned(p1, 16) && aligned(q, 16) &&
+                     (b1 == nullptr || aligned(b1, 16));
+    const int64_t work = rows * (vec ? C1 / 4 : C1);
+    const int64_t blocks = std::min<int64_t>(ceil_div(work, 256), 16384);
+    if (vec)
+        ltd_group_kernel<true><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(p1, ld_p, q, ld_q, b1, nit, (int)N, (int)M,
+                                                                           K, C1, rows, h1);
+    else
+        ltd_group_kernel<false><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(p1, ld_p, q, ld_q, b1, nit, (int)N,
+                                                                            (int)M, K, C1, rows, h1);
+    rc = after_launch(who);
+    if (rc != MESORASI_OK) return rc;
+    return run_mlp(h1, C1, C1, nullptr, 0, 0, rows, n_layers, dims, W, bias, relu_mask, dtype, MESORASI_F32, out,
+                   ld_out, K, static_cast<char*>(ws) + h1_bytes, s);
 }

@@ -8,7 +8,12 @@ stream; an event joins them right before each aggregation A.  For
 PointNet++ the whole xyz chain (FPS -> ball query -> FPS of the next
 level ...) depends on coordinates only and runs ahead (Sec. 5.1 "Work
 Flow"); for DGCNN each layer's kNN overlaps that layer's MLP.  The
-conventional path (Eq. (1)) serialises N -> A -> F per module.
+conventional path (Eq. (1)) serialises N -> A -> F per module.  The
+limited order (delayed="ltd", Sec. 7.3) hoists only each PointNet++
+module's first-layer product onto the input points (overlapping the
+search), subtracts the centroid term before bias and ReLU, and runs the
+remaining layers on the neighbor rows; for DGCNN's one-layer EdgeConv it
+is the delayed order.
 
 All intermediate buffers are allocated once per input shape and kept, so a
 forward pass only enqueues kernels and can be captured into a HIP graph
@@ -16,6 +21,7 @@ forward pass only enqueues kernels and can be captured into a HIP graph
 """
 from __future__ import annotations
 
+import numpy as np
 import torch
 
 from . import ops
@@ -79,6 +85,21 @@ class PointNet2(Net):
         self.fc = P(w["fc"]) if "fc" in w else None
         self.fp = [P(Wb) for Wb in w.get("fp", [])]
         self.head = P(w["head"]) if "head" in w else None
+        if self.delayed == "ltd":
+            # limited order (Sec. 7.3): the first layer's product on the input
+            # points and on the centroids, its bias, and the remaining layers
+            if self.dt != F32:
+                raise ValueError("the limited delayed order is built for fp32 networks")
+            self.ltd = []
+            for Ws, bs in w["sa"]:
+                if len(Ws) < 2:
+                    raise ValueError("a one-layer module's limited order is its delayed order")
+                W1 = np.asarray(Ws[0], np.float32)
+                self.ltd.append(dict(
+                    first=ops.MLPParams([W1], [None], device=self.device),
+                    cen=ops.MLPParams([np.ascontiguousarray(W1[:, :3])], [None], device=self.device),
+                    b1=torch.as_tensor(np.asarray(bs[0], np.float32)).to(self.device).contiguous(),
+                    rest=ops.MLPParams(Ws[1:], bs[1:], device=self.device)))
 
     def _search_chain(self, xyz, B):
         """FPS and ball query of every level on the side stream."""
@@ -115,7 +136,20 @@ class PointNet2(Net):
                 main.wait_event(ev_fps[i - 1])          # p = centroids of the previous level
             idx, cx, nit = self._bufs[f"idx{i}"], self._bufs[f"cxyz{i}"], self._bufs[f"nit{i}"]
             out = self._buf(f"f{i}", (B, m["M"], prm.c_out))
-            if self.delayed:
+            if self.delayed == "ltd":
+                L = self.ltd[i]
+                c1 = L["first"].c_out
+                p1 = self._buf(f"p1_{i}", (B, N, c1))
+                ws = self._ws(f"ws_p1_{i}", ops.mlp_workspace_bytes(B * N, L["first"]))
+                ops.pointwise_mlp(p, L["first"], x1=f, relu_mask=0, out=p1, ws=ws)   # overlaps the search chain
+                q = self._buf(f"q_{i}", (B, m["M"], c1))
+                main.wait_event(ev_fps[i])
+                ws = self._ws(f"ws_q_{i}", ops.mlp_workspace_bytes(B * m["M"], L["cen"]))
+                ops.pointwise_mlp(cx, L["cen"], relu_mask=0, out=q, ws=ws)
+                main.wait_event(ev_bq[i])
+                ws = self._ws(f"ws_sa{i}", ops.ltd_workspace_bytes(B, m["M"], m["K"], L["rest"]))
+                ops.ltd_module(p1, q, nit, L["rest"], b1=L["b1"], out=out, ws=ws)
+            elif self.delayed:
                 # F on all N input points -> PFT, overlapping the search chain
                 pft_dt = torch.bfloat16 if self.dt == BF16 else torch.float32
                 pft = self._buf(f"pft{i}", (B, N, prm.c_out), pft_dt)
@@ -221,7 +255,9 @@ class DGCNN(Net):
         return res
 
 
-def build(spec: dict, weights: dict, delayed: bool = True, device="cuda") -> Net:
+def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda") -> Net:
+    """delayed: True (delayed aggregation), False (conventional) or "ltd"
+    (limited delayed aggregation)."""
     if spec["kind"] in ("pointnet2_cls", "pointnet2_seg"):
         return PointNet2(spec, weights, delayed, device)
     if spec["kind"] == "dgcnn":

@@ -205,6 +205,36 @@ def conventional_module(nit: torch.Tensor, p: MLPParams, xyz: torch.Tensor | Non
     return out
 
 
+def ltd_workspace_bytes(B: int, M: int, K: int, p: MLPParams) -> int:
+    d, _, _ = p.abi()
+    return int(_lib.lib().mesorasi_ltd_workspace(B, M, K, p.n, d, p.dtype))
+
+
+def ltd_module(p1: torch.Tensor, q: torch.Tensor, nit: torch.Tensor, p: MLPParams, b1: torch.Tensor | None = None,
+               relu_mask: int | None = None, out: torch.Tensor | None = None, ws: torch.Tensor | None = None):
+    """Limited delayed aggregation (Sec. 7.3): p1 [B, N, >=C1] = the first
+    layer's product on the input points, q [B, M, >=C1] = its centroid
+    term, b1 [C1] the first layer's bias; p = the remaining layers.
+    Returns max_k MLP_rest(ReLU(p1[nit] - q + b1)) [B, M, C_out]."""
+    B, M, K = nit.shape
+    N, C1 = p1.shape[1], p.dims[0]
+    pp, ldp = _rows(p1, C1)
+    pq, ldq = _rows(q, C1)
+    if relu_mask is None:
+        relu_mask = (1 << p.n) - 1
+    if out is None:
+        out = torch.empty((B, M, p.c_out), dtype=torch.float32, device=nit.device)
+    po, ldo = _rows(out)
+    need = ltd_workspace_bytes(B, M, K, p)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=nit.device)
+    d, W, b = p.abi()
+    check(_lib.lib().mesorasi_ltd_module(pp, ldp, pq, ldq, _ptr(b1), nit.data_ptr(), B, N, M, K, C1, p.n, d, W, b,
+                                         relu_mask, p.dtype, po, ldo, ws.data_ptr(), ws.numel(), _stream()),
+          "ltd_module")
+    return out
+
+
 def interpolate3(xyz_dst: torch.Tensor, xyz_src: torch.Tensor, f_src: torch.Tensor,
                  out: torch.Tensor | None = None):
     _check_xyz(xyz_dst, "xyz_dst")

@@ -145,6 +145,22 @@ def test_conventional_validation_and_workspace():
               NULL) == _lib.EUNSUPPORTED   # last layer without ReLU
 
 
+def test_ltd_validation_and_workspace():
+    L = _lib.lib()
+    d, W, b = _mlp_args([64, 64, 128])          # the remaining layers after the hoisted first one
+    f = "mesorasi_ltd_module"
+    args = lambda C1, n, ld_p, ws, relu=3, ws_ptr=FAKE: (FAKE, ld_p, FAKE, 64, NULL, FAKE, 1, 10, 5, 4, C1, n, d, W, b,
+                                                        relu, 0, FAKE, 128, ws_ptr, ws, NULL)
+    need = L.mesorasi_ltd_workspace(1, 5, 4, 2, d, 0)
+    assert need >= 5 * 4 * 64 * 4                                             # the first-layer rows
+    assert st(f, *args(64, 2, 64, need - 1)) == _lib.EWORKSPACE
+    assert st(f, *args(32, 2, 64, need)) == _lib.EINVAL                      # dims[0] != C1
+    assert st(f, *args(64, 2, 32, need)) == _lib.EINVAL                      # ld_p < C1
+    assert st(f, *args(64, 0, 64, need)) == _lib.EUNSUPPORTED                # no remaining layer
+    assert st(f, *args(64, 2, 64, need, relu=1)) == _lib.EUNSUPPORTED        # last layer without ReLU
+    assert L.mesorasi_ltd_workspace(1, 5, 4, 0, d, 0) == 0
+
+
 def test_misc_validation():
     assert st("mesorasi_interpolate3", FAKE, FAKE, FAKE, 8, 1, 10, 2, 8, FAKE, 8, NULL) == _lib.EINVAL  # Ns < 3
     assert st("mesorasi_cast_bf16", FAKE, -1, FAKE, NULL) == _lib.EINVAL

@@ -90,6 +90,20 @@ def test_pointnet2_cls_small_batch(gpu, delayed):
     check_pointnet(spec, run_gpu(spec, xyz, feat, w, delayed), ref, 1e-4)
 
 
+@pytest.mark.parametrize("name,B", [("sa_module", 1), ("pointnet2_cls", 3), ("pointnet2_seg", 1)])
+def test_limited_order(gpu, name, B):
+    """Limited delayed aggregation (Sec. 7.3) end to end against the oracle's
+    limited composition, and against the conventional order it equals."""
+    spec = synth.workload(name, B=B)
+    xyz, feat = synth.make_points(spec)
+    w = synth.make_weights(spec)
+    ref = ON.forward(spec, xyz, feat, w, delayed="ltd")
+    got = run_gpu(spec, xyz, feat, w, "ltd")
+    check_pointnet(spec, got, ref, 1e-4)
+    conv = ON.forward(spec, xyz, feat, w, delayed=False)
+    assert normwise(got["out"], conv["out"]) <= 1e-4
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("delayed", [True, False], ids=["delayed", "conventional"])
 def test_pointnet2_seg(gpu, delayed, dtype):

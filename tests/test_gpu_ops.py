@@ -317,6 +317,27 @@ def test_conventional_edge(gpu):
     assert normwise(host(out), ref) <= 1e-4
 
 
+@pytest.mark.parametrize("C1,bias,dt", [(64, True, F32), (10, True, F32), (64, False, F32), (32, True, BF16)],
+                         ids=["vec4", "scalar_width", "no_bias", "bf16_rest"])
+def test_ltd_module_parity(gpu, C1, bias, dt):
+    """Limited delayed aggregation (first-layer rows from p1 - q + b1, then
+    the remaining layers and the max over K) against the oracle."""
+    rr = g(14)
+    B, N, M, K = 2, 300, 77, 9
+    p1 = rr.standard_normal((B, N, C1)).astype(np.float32)
+    q = rr.standard_normal((B, M, C1)).astype(np.float32)
+    b1 = rr.uniform(-0.2, 0.2, C1).astype(np.float32) if bias else None
+    nit = rr.integers(0, N, size=(B, M, K)).astype(np.int32)
+    dims = [C1, 24, 40]
+    Ws, bs = _weights(rr, dims)
+    h1 = O.ltd_group(p1, q, b1, nit)
+    h = O.mlp(h1, Ws, bs, bf16=dt == BF16)
+    ref = O.rowgroup_max(h.reshape(B, M * K, dims[-1]), K)
+    p = ops.MLPParams(Ws, bs, dtype=dt)
+    out = ops.ltd_module(dev(p1), dev(q), dev(nit), p, b1=None if b1 is None else dev(b1))
+    assert normwise(host(out), ref) <= TOL[dt]
+
+
 @pytest.mark.parametrize("B,Nd,Ns,C", [(2, 4096, 1024, 128), (3, 100, 17, 5), (1, 64, 16, 512), (2, 10, 3, 8),
                                        (1, 300, 2500, 7), (2, 129, 3, 4)])
 def test_interpolate3(gpu, B, Nd, Ns, C):
