@@ -57,6 +57,8 @@ FPS_CASES = [
     ("n9000", 1, 9000, 300, "normal"),
     ("lidar_sa1", 1, 16384, 4096, "lidar"),
     ("n20000", 1, 20000, 64, "normal"),
+    ("n32769_global_path", 1, 32769, 40, "normal"),   # coordinates re-read from memory per iteration
+    ("n_max", 1, 65536, 24, "normal"),                # the documented maximum cloud size
 ]
 
 
@@ -98,6 +100,7 @@ BQ_CASES = [
     ("nohit", 1, 50, 10, 1e-3, 8, "normal"),
     ("grid_boundary", 1, 64, 64, 1.0, 16, "grid"),
     ("lidar_sa1", 1, 16384, 4096, 0.1, 64, "lidar"),
+    ("k_max", 1, 2000, 24, 3.0, 1024, "normal"),      # the documented maximum K
 ]
 
 
@@ -132,6 +135,7 @@ KNN_CASES = [
     ("ties_4ch_groups", 2, 150, 150, 8, 10, "grid"),      # 16-byte channel path with exact ties
     ("c28_scalar_path", 1, 90, 90, 28, 5, "self"),         # 4-channel groups, bank-conflicting stride: scalar path
     ("interp_like", 2, 256, 1024, 3, 3, "other"),
+    ("k_max_c_max", 1, 300, 100, 128, 64, "other"),   # the documented maximum K and width
 ]
 
 
@@ -172,6 +176,7 @@ AGG_CASES = [
     ("odd_channels", 2, 100, 33, 7, 13, "f32", "cidx"),
     ("odd_bf16", 2, 100, 33, 7, 13, "bf16", "cidx"),
     ("wide", 1, 64, 16, 32, 1024, "f32", "cidx"),
+    ("wide_bf16", 1, 64, 16, 32, 2048, "bf16", "cidx"),
     ("none", 2, 80, 20, 5, 24, "f32", "none"),
     ("k1", 2, 50, 50, 1, 8, "f32", "cidx"),
 ]
@@ -233,6 +238,9 @@ MLP_CASES = [
     ("sa2_bf16_two_src", 333, [3, 64], [64, 64, 128], BF16),
     ("fp_bf16", 200, [256, 128], [256, 256], BF16),
     ("odd_bf16", 45, [6, 1], [20, 12], BF16),
+    ("width_max", 40, [4096], [4096, 64], F32),       # the documented maximum width (skinny path)
+    ("width_max_gemm", 200, [4096], [4096, 64], F32), # the same on the tiled GEMM path
+    ("depth_max", 100, [16], [32] * 8, F32),          # the documented maximum depth
 ]
 
 
