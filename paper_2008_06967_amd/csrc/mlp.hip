@@ -9,11 +9,11 @@
 // sources, so the first layer reads xyz and the previous module's features
 // without a concatenated copy).  Workgroup tiles of 64 or 128 rows by 64 or
 // 128 output channels (chosen per layer to fill the 256 CUs), 4 waves each
-// owning up to 2 x 2 blocks of 32 x 32; layers with too few tiles (the FC
-// head's 32 rows) split K and sum the partials in a fixed order:
-//  - fp32: v_mfma_f32_32x32x2_f32 (lane l feeds A[l%32][k + l/32] and
-//    B[k + l/32][l%32]); LDS tiles are k-major so the 32 lanes of a half
-//    wave read consecutive words.
+// owning up to 2 x 2 blocks of 32 x 32; layers with too few tiles split K
+// and sum the partials in a fixed order:
+//  - fp32: v_mfma_f32_32x32x2_f32 (lane l feeds one A and one B value of
+//    the same k); row-major LDS tiles read with 16-byte loads in an MFMA
+//    lane k-order (details at gemm_f32_kernel).
 //  - bf16: v_mfma_f32_32x32x16_bf16 (lane l feeds 8 consecutive k of row
 //    l%32, k offset 8*(l/32)); LDS rows of 32 bf16 padded to 40 so the
 //    16-byte reads of a half wave hit distinct banks.
@@ -23,6 +23,9 @@
 // store or a pooled column max (pool groups of G rows; values are >= 0
 // after ReLU, so the max is an unsigned atomicMax on the float bits, which
 // is exact and order independent).
+// MLPs on at most 64 rows (the classifier head) take a skinny path of
+// 16-column MFMA blocks instead (skinny_f32_kernel); narrow multi-layer fp32
+// MLPs run fused in one kernel (mlp_fused.hip).
 #include "common.h"
 #include "mlp_internal.h"
 
