@@ -59,6 +59,19 @@ struct GemmArgs {
     int64_t ldy;
     int64_t G;           // pool group (EPI_POOL)
     float* part;         // split-K partial sums [splits, rows, N]
+    // two-source first layer with a narrow x0 (the xyz columns): the main
+    // loop runs over x1 alone against W columns cc .. cc + K - 1 (row stride
+    // ldw), and the cc x0 columns are added in the epilogue
+    const float* xc;
+    int64_t ldc;
+    int cc;
+    int ldw;
+};
+
+// 16 bytes at a 4-byte aligned address: gfx950 global loads accept dword
+// alignment, so this is still one 16-byte load.
+struct __attribute__((packed, aligned(4))) f32x4u {
+    float x, y, z, w;
 };
 
 // Element (r, k) of the virtual input [x0 | x1] as float (0 outside).
@@ -304,8 +317,15 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, i
 // of one LDS row, read with 16-byte loads (conflict-free: row stride
 // BK + 4 words puts 8 consecutive lanes on distinct bank quads).  The
 // product is the same sum over k, accumulated in a different order.
-template <int BM, int BN, int BK, int EPI, bool FAST_A, bool FAST_W>
+//
+// SPLIT (first layer [x0 | x1] with x0 at most 4 columns wide and x1
+// 16-byte aligned): the k loop reads x1 like a single fast source and the
+// weight columns after x0 with unaligned 16-byte loads; the x0 columns and
+// their weights are staged in LDS once and added to the accumulators before
+// the epilogue (same sum, different order).
+template <int BM, int BN, int BK, int EPI, bool FAST_A, bool FAST_W, bool SPLIT = false>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
+    static_assert(!SPLIT || FAST_A, "the split form reads x1 as a fast source");
     constexpr int TM = BM / 64, TN = BN / 64;
     constexpr int LW = BK + kPadF;           // LDS row stride in words
     constexpr int CPR = BK / 4;              // 16-byte chunks per tile row
@@ -314,10 +334,28 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     static_assert(QA >= 1 && QB >= 1 && HK % 4 == 0, "tile shape");
     __shared__ __attribute__((aligned(16))) float As[2][BM * LW];
     __shared__ __attribute__((aligned(16))) float Bs[2][BN * LW];
+    __shared__ __attribute__((aligned(16))) float sXc[SPLIT ? BM * 4 : 4];
+    __shared__ __attribute__((aligned(16))) float sWc[SPLIT ? BN * 4 : 4];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t row_t = (int64_t)blockIdx.x * BM;
     const int col_t = blockIdx.y * BN;
+    const int ldw = SPLIT ? a.ldw : a.K;
+    if constexpr (SPLIT) {
+        // x0 rows of this tile and the matching weight columns (zero past
+        // cc, rows or N); read after the first barrier below
+        const float* Wf = static_cast<const float*>(a.W) - a.cc;
+        for (int e = tid; e < BM * 4; e += 256) {
+            const int64_t r = row_t + (e >> 2);
+            const int i = e & 3;
+            sXc[e] = (i < a.cc && r < a.rows) ? a.xc[r * a.ldc + i] : 0.0f;
+        }
+        for (int e = tid; e < BN * 4; e += 256) {
+            const int n = col_t + (e >> 2);
+            const int i = e & 3;
+            sWc[e] = (i < a.cc && n < a.N) ? Wf[(int64_t)n * ldw + i] : 0.0f;
+        }
+    }
     const int k_lo = blockIdx.z * a.kc;
     const int k_hi = min(a.K, k_lo + a.kc);
     // chunk c = tid + 256 p covers tile row c / CPR, words 4 (c % CPR) .. +3
@@ -352,7 +390,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     for (int p = 0; p < QB; ++p) {
         const int n = col_t + crow + RSTEP * p;
         rowb[p] = n < a.N;
-        pb[p] = static_cast<const float*>(a.W) + (int64_t)(rowb[p] ? n : 0) * a.K;
+        pb[p] = static_cast<const float*>(a.W) + (int64_t)(rowb[p] ? n : 0) * ldw;
     }
     auto fetch = [&](float (&ra)[QA][4], bool (&oka)[QA], float (&rb)[QB][4], bool (&okb)[QB], int k0) {
         const bool kin = k0 + ck < a.K;
@@ -369,7 +407,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
         }
 #pragma unroll
         for (int p = 0; p < QB; ++p) {
-            if constexpr (FAST_W) {
+            if constexpr (SPLIT) {
+                const f32x4u u = *reinterpret_cast<const f32x4u*>(pb[p] + ko);
+                rb[p][0] = u.x; rb[p][1] = u.y; rb[p][2] = u.z; rb[p][3] = u.w;
+                okb[p] = rowb[p] && kin;
+            } else if constexpr (FAST_W) {
                 const float4 u = *reinterpret_cast<const float4*>(pb[p] + ko);
                 rb[p][0] = u.x; rb[p][1] = u.y; rb[p][2] = u.z; rb[p][3] = u.w;
                 okb[p] = rowb[p] && kin;
@@ -444,6 +486,32 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
         __syncthreads();
     }
     if (n_slices & 1) compute(0);
+    if constexpr (SPLIT) {
+        // staged columns past cc are zero, so four fused steps add exactly
+        // the cc products
+        if (blockIdx.z == 0) {
+            float4 wc[TN];
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                wc[j] = *reinterpret_cast<const float4*>(&sWc[(wn * (BN / 2) + j * 32 + (lane & 31)) * 4]);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const float4 xr = *reinterpret_cast<const float4*>(
+                        &sXc[(wm * (BM / 2) + i * 32 + 4 * (lane >> 5) + 8 * (r >> 2) + (r & 3)) * 4]);
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        float t = acc[i][j][r];
+                        t = fmaf(xr.x, wc[j].x, t);
+                        t = fmaf(xr.y, wc[j].y, t);
+                        t = fmaf(xr.z, wc[j].z, t);
+                        t = fmaf(xr.w, wc[j].w, t);
+                        acc[i][j][r] = t;
+                    }
+                }
+        }
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -749,6 +817,10 @@ template <int BM, int BN, int EPI>
 static void launch_tile(const GemmArgs& a, bool bf16, bool fast_a, bool fast_w, dim3 grid, hipStream_t s) {
     const dim3 block(256);
     constexpr int BK = (BM / 64) * (BN / 64) >= 2 ? 32 : 64;   // f32_slice(BM, BN)
+    if (a.cc > 0) {
+        gemm_f32_kernel<BM, BN, BK, EPI, true, false, true><<<grid, block, 0, s>>>(a);
+        return;
+    }
     if (bf16) {
         if (fast_a && fast_w) gemm_bf16_kernel<BM, BN, EPI, true, true><<<grid, block, 0, s>>>(a);
         else if (fast_w) gemm_bf16_kernel<BM, BN, EPI, false, true><<<grid, block, 0, s>>>(a);
@@ -771,6 +843,22 @@ static void launch_epi(const GemmArgs& a, const LayerPlan& pl, bool bf16, bool f
 
 // Launch one layer.  epi: EPI_F32 / EPI_BF16 / EPI_POOL.
 static int launch_layer(GemmArgs a, bool bf16, int epi, float* part, hipStream_t s) {
+    a.ldw = a.K;
+    if (!bf16 && !a.a_bf16 && a.x1 && a.c1 > 0 && a.c0 <= 4 && a.c1 % 4 == 0 && a.ld1 % 4 == 0 &&
+        aligned(a.x1, 16) && aligned(a.W, 4)) {
+        // split form: the k loop over x1 alone, x0 added in the epilogue
+        a.xc = static_cast<const float*>(a.x0);
+        a.ldc = a.ld0;
+        a.cc = a.c0;
+        a.x0 = a.x1;
+        a.ld0 = a.ld1;
+        a.c0 = a.c1;
+        a.x1 = nullptr;
+        a.ld1 = 0;
+        a.c1 = 0;
+        a.W = static_cast<const float*>(a.W) + a.cc;
+        a.K = a.c0;
+    }
     const LayerPlan pl = plan_layer(a.rows, a.N, a.K, bf16);
     a.kc = pl.kc;
     // vector loads: 16-byte aligned rows and whole 16-byte chunks (4 fp32

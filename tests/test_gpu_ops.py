@@ -225,6 +225,12 @@ MLP_CASES = [
     ("sa1_f32", 1000, [3], [64, 64, 128], F32),
     ("sa2_two_src", 517, [3, 128], [128, 128, 256], F32),
     ("sa3_groupall", 256, [3, 256], [256, 512, 1024], F32),
+    # [x0 | x1] with x0 at most 4 wide and x1 aligned: the k loop over x1,
+    # x0 added in the epilogue (with split K when the tiles are few)
+    ("two_src_splitk", 100, [3, 256], [512, 64], F32),
+    ("two_src_x0_1", 300, [1, 64], [64], F32),
+    ("two_src_x0_4", 259, [4, 32], [200, 16], F32),
+    ("two_src_x0_5", 130, [5, 32], [48], F32),        # x0 too wide: general loader
     ("fc_head", 32, [1024], [512, 256, 40], F32),
     # at most 64 rows: the skinny path (16-column MFMA blocks, K split over waves)
     ("fc_skinny_1row", 1, [1024], [512, 256, 40], F32),
@@ -281,6 +287,20 @@ def test_mlp_pooled(gpu, dt, G):
     p = ops.MLPParams(Ws, bs, dtype=dt)
     y = ops.pointwise_mlp(dev(x), p, pool_group=G)
     assert normwise(host(y).reshape(groups, 80), ref.reshape(groups, 80)) <= TOL[dt]
+
+
+@pytest.mark.parametrize("G", [32, 16])
+def test_mlp_pooled_two_source(gpu, G):
+    """Group-all shape: [xyz | features] with the max over each cloud fused."""
+    rr = g(10)
+    groups = 9
+    rows = G * groups
+    x0 = rr.standard_normal((rows, 3)).astype(np.float32)
+    x1 = rr.standard_normal((rows, 64)).astype(np.float32)
+    Ws, bs = _weights(rr, [67, 256])
+    ref = O.rowgroup_max(O.mlp(np.concatenate([x0, x1], -1), Ws, bs).reshape(groups, G, 256), G)
+    y = ops.pointwise_mlp(dev(x0), ops.MLPParams(Ws, bs), x1=dev(x1), pool_group=G)
+    assert normwise(host(y).reshape(groups, 256), ref.reshape(groups, 256)) <= 1e-4
 
 
 def test_mlp_strided_input(gpu):
