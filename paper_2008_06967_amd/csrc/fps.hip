@@ -19,12 +19,17 @@
 // the lowest lane holding it and that lane's lowest slot as wave-uniform
 // scalars, and the winner's coordinates are read once with a uniform
 // register index -- per-lane work after the reduction does not grow with
-// P.  One barrier per iteration: the per-wave winners go to a
-// double-buffered LDS slot array indexed by iteration parity, so a wave
-// that runs ahead writes the other buffer while slower waves still read
-// this one.  A single-wave workgroup needs no barrier at all.  The
-// iteration is bound by VALU issue for large P (four waves per SIMD at
-// 16 points per thread) and by the reduction chain for small P.
+// P.  One barrier per iteration: the per-wave winners go to a ring of 128
+// LDS slot rows indexed by iteration, so a wave that runs ahead writes the
+// next row while slower waves still read this one.  The ring also keeps
+// the results: every 64 iterations each lane of wave 0 finds the winner of
+// one past iteration again from its row (highest distance, lowest wave)
+// and stores it, so no wave spends instructions recording the winner on
+// the path to the next barrier (doing it per iteration cost about 10 % at
+// 8 waves).  A single-wave workgroup needs no barrier at all and keeps its
+// results in registers.  The iteration is bound by VALU issue for large P
+// (four waves per SIMD at 16 points per thread) and by the reduction chain
+// for small P.
 #include "common.h"
 
 namespace meso {
@@ -33,9 +38,10 @@ template <int T, int P, bool REG_XYZ>
 __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, int N, int M, int32_t* __restrict__ idx,
                                                 float* __restrict__ cxyz) {
     constexpr int W = T / 64;
-    // per-wave winner of iteration m, double-buffered by m & 1: {dist bits, index, x, y} and z
-    __shared__ int4 s_slot[2][W];
-    __shared__ float s_z[2][W];
+    constexpr int R = W > 1 ? 128 : 1;   // ring rows (two result blocks of 64 iterations)
+    // per-wave winner of iteration m in row m % R: {dist bits, index, x, y} and z
+    __shared__ int4 s_slot[R][W];
+    __shared__ float s_z[R][W];
 
     const int b = blockIdx.x;
     const float* __restrict__ p = xyz + (int64_t)b * N * 3;
@@ -61,9 +67,34 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
     }
 
     float cx = p[0], cy = p[1], cz = p[2];
-    // Results are kept in wave 0, iteration m in lane m % 64, and written
-    // 64 iterations at a time (one coalesced store instead of one
-    // single-lane store per iteration).
+    const float x0 = cx, y0 = cy, z0 = cz;
+    // Multi-wave: lane l of wave 0 resolves iteration (m_last & ~63) + l
+    // from the ring and stores it (iteration 0 is point 0).
+    auto resolve = [&](int m_last) {
+        const int mi = (m_last & ~63) + lane;
+        const int row = mi & (R - 1);
+        int best = s_slot[row][0].x, bw = 0;
+#pragma unroll
+        for (int w = 1; w < W; ++w) {
+            const int d = s_slot[row][w].x;
+            bw = d > best ? w : bw;
+            best = d > best ? d : best;
+        }
+        const int4 sl = s_slot[row][bw];
+        const float sz = s_z[row][bw];
+        if (mi <= m_last) {
+            const bool first = mi == 0;
+            out_idx[mi] = first ? 0 : sl.y;
+            if (out_c) {
+                out_c[3 * mi + 0] = first ? x0 : __int_as_float(sl.z);
+                out_c[3 * mi + 1] = first ? y0 : __int_as_float(sl.w);
+                out_c[3 * mi + 2] = first ? z0 : sz;
+            }
+        }
+    };
+    // Single wave: iteration m is kept in lane m % 64 and written 64
+    // iterations at a time (one coalesced store instead of one single-lane
+    // store per iteration).
     int keep_i = 0;
     float keep_x = cx, keep_y = cy, keep_z = cz;
     auto flush = [&](int m_last) {   // iterations (m_last & ~63) .. m_last
@@ -78,7 +109,8 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
         }
     };
 
-    for (int m = 1; m < M; ++m) {
+    // one iteration: the update, the wave and block reductions, the new centroid
+    auto step = [&](int m) {
         // 1. distance to the newest centroid, running min, this thread's max
         int tmax = INT32_MIN;
 #pragma unroll
@@ -132,7 +164,7 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
             cy = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sy), wl));
             cz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sz), wl));
         } else {
-            const int buf = m & 1;
+            const int buf = m & (R - 1);
             if (lane == wl) {
                 s_slot[buf][wave] = make_int4(wmax, base + sq, __float_as_int(sx), __float_as_int(sy));
                 s_z[buf][wave] = sz;
@@ -155,16 +187,38 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
             cy = __int_as_float(__builtin_amdgcn_readlane(sl.w, ww));
             cz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(slz), ww));
         }
-        if (wave == 0) {
+        if constexpr (W == 1) {
             const bool mine = lane == (m & 63);
             keep_i = mine ? sel : keep_i;
             keep_x = mine ? cx : keep_x;
             keep_y = mine ? cy : keep_y;
             keep_z = mine ? cz : keep_z;
-            if ((m & 63) == 63) flush(m);
+        } else {
+            (void)sel;
         }
+    };
+    auto write_block = [&](int m_last) {
+        if constexpr (W == 1) flush(m_last);
+        else resolve(m_last);
+    };
+    if constexpr (P <= 4) {
+        // blocks of 64 iterations with the results written after each
+        // block: no per-iteration test (a few percent at small P)
+        for (int mb = 1; mb < M;) {
+            const int me = min(M, (mb | 63) + 1);
+            for (int m = mb; m < me; ++m) step(m);
+            if (wave == 0) write_block(me - 1);
+            mb = me;
+        }
+        if (M == 1 && wave == 0) write_block(0);
+    } else {
+        // one flat loop (the blocked form schedules worse at large P)
+        for (int m = 1; m < M; ++m) {
+            step(m);
+            if (wave == 0 && (m & 63) == 63) write_block(m);
+        }
+        if (wave == 0 && ((M - 1) & 63) != 63) write_block(M - 1);
     }
-    if (wave == 0 && ((M - 1) & 63) != 63) flush(M - 1);
 }
 
 template <int T, int P, bool REG>
