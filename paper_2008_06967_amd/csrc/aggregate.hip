@@ -16,6 +16,19 @@
 // contiguous range of clouds.  Nothing N x K x C sized is ever written.  Wider PFTs are split into
 // channel slices processed by different waves -- the column partitioning
 // of the paper's PFT buffer (Sec. 5.2, "PFT Partitioning").
+//
+// LDS form (aggregate_lds_kernel), used when a column slice of one cloud's
+// PFT fits the 160 KB LDS and the batch gives enough workgroups: this is
+// the paper's on-chip PFT buffer with its column partitioning (Sec. 5.2).
+// A 1024-thread workgroup copies slice s (32 or 16 fp32 channels, 64 or 32
+// bf16) of cloud b's PFT into LDS once, with coalesced 16-byte loads, then
+// gathers every NIT row of its share of the cloud's centroids from LDS:
+// lane (g, q) of a wave serves centroid g of the pass and 16 bytes q of
+// the slice, so one LDS read instruction fetches 64 / Q neighbor rows of
+// Q x 16 bytes.  Random-row LDS gathers run at ~117-139 B/clk per CU on
+// gfx950 against ~32 B/clk for the same gathers through the vector L1, which
+// is what bounds the L2 form at batch size.  Neighbor indices come straight
+// from global memory four at a time (16-byte rows of the NIT).
 #include "common.h"
 
 namespace meso {
@@ -151,6 +164,155 @@ __global__ __launch_bounds__(256) void aggregate_kernel(const T* __restrict__ pf
     }
 }
 
+// Slice widths in 16-byte units per row (Q) and the launch shape.
+constexpr int kAggLdsThreads = 1024;
+constexpr int kAggLdsMaxTile = 128 * 1024;   // tile bytes (the NIT stays in global memory)
+
+template <typename T, int Q>
+__global__ __launch_bounds__(kAggLdsThreads) void aggregate_lds_kernel(
+    const T* __restrict__ pft, int64_t ldp, const int32_t* __restrict__ nit, int N, int M, int K, int C, int slices,
+    int parts, int64_t nblocks, int per_xcd, const int32_t* __restrict__ cidx, const T* __restrict__ cfeat,
+    int64_t ldc, int sign, int relu, float* __restrict__ out, int64_t ldo) {
+    constexpr int VEC = 16 / sizeof(T);          // elements per 16 bytes
+    constexpr int CS = Q * VEC;                  // channels per slice
+    constexpr int G = 64 / Q;                    // centroids per wave pass
+    constexpr int NW = kAggLdsThreads / 64;
+    extern __shared__ uint4 tile[];              // [N][Q] 16-byte units
+    // renumber so that each XCD runs one contiguous range of (cloud, slice, part)
+    const int64_t lb = (int64_t)(blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (lb >= nblocks) return;
+    const int part = (int)(lb % parts);
+    const int64_t bs = lb / parts;
+    const int s = (int)(bs % slices);
+    const int64_t b = bs / slices;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int ch0 = s * CS;
+
+    // 1. the slice of the cloud's PFT into LDS (columns past C as zeros)
+    const T* __restrict__ src = pft + b * (int64_t)N * ldp + ch0;
+    constexpr int U = 8;
+    const int total = N * Q;
+    for (int i0 = 0; i0 < total; i0 += kAggLdsThreads * U) {
+        uint4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kAggLdsThreads + tid;
+            const int r = i / Q, qq = i % Q;
+            const bool ok = i < total && ch0 + qq * VEC < C;
+            v[u] = ok ? *reinterpret_cast<const uint4*>(src + (int64_t)r * ldp + qq * VEC) : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kAggLdsThreads + tid;
+            if (i < total) tile[i] = v[u];
+        }
+    }
+    __syncthreads();
+
+    // 2. this part's centroids, G per wave pass
+    const int per = (M + parts - 1) / parts;
+    const int cb = part * per, ce = min(M, cb + per);
+    const int g = lane / Q, q = lane % Q;
+    const bool chok = ch0 + q * VEC < C;
+    const int K4 = K / 4;
+    for (int c0 = cb + wave * G; c0 < ce; c0 += NW * G) {
+        const int c = min(c0 + g, ce - 1);
+        const int64_t gc = b * M + c;
+        const int4* __restrict__ nr = reinterpret_cast<const int4*>(nit + gc * K);
+        float mx[VEC];
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) mx[v] = -__builtin_huge_valf();
+        auto take = [&](int j) {
+            const uint4 w = tile[j * Q + q];
+            float a[VEC];
+            if constexpr (sizeof(T) == 4) {
+                a[0] = __uint_as_float(w.x); a[1] = __uint_as_float(w.y);
+                a[2] = __uint_as_float(w.z); a[3] = __uint_as_float(w.w);
+            } else {
+                const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    a[2 * i] = __uint_as_float(ws[i] << 16);
+                    a[2 * i + 1] = __uint_as_float(ws[i] & 0xffff0000u);
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) mx[v] = fmaxf(mx[v], a[v]);
+        };
+        for (int k4 = 0; k4 < K4; k4 += 2) {
+            const int4 ja = nr[k4];
+            const int4 jb = nr[min(k4 + 1, K4 - 1)];   // a repeated row does not change the max
+            take(ja.x); take(ja.y); take(ja.z); take(ja.w);
+            take(jb.x); take(jb.y); take(jb.z); take(jb.w);
+        }
+        float cen[VEC];
+        if (cidx) {
+            const uint4 w = tile[cidx[gc] * Q + q];
+            if constexpr (sizeof(T) == 4) {
+                cen[0] = __uint_as_float(w.x); cen[1] = __uint_as_float(w.y);
+                cen[2] = __uint_as_float(w.z); cen[3] = __uint_as_float(w.w);
+            } else {
+                const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    cen[2 * i] = __uint_as_float(ws[i] << 16);
+                    cen[2 * i + 1] = __uint_as_float(ws[i] & 0xffff0000u);
+                }
+            }
+        } else if (cfeat && chok) {
+            load_vec<T, VEC>(cfeat + gc * ldc + ch0 + q * VEC, cen);
+        }
+        if (c0 + g >= ce || !chok) continue;
+        float r[VEC];
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            r[v] = mx[v];
+            if (cidx || cfeat) r[v] = sign < 0 ? mx[v] - cen[v] : mx[v] + cen[v];
+            if (relu) r[v] = r[v] > 0.0f ? r[v] : 0.0f;
+        }
+        float* __restrict__ o = out + gc * ldo + ch0 + q * VEC;
+#pragma unroll
+        for (int v = 0; v < VEC; v += 4) *reinterpret_cast<float4*>(o + v) = make_float4(r[v], r[v + 1], r[v + 2], r[v + 3]);
+    }
+}
+
+// LDS form plan: the widest slice (Q = 8, else 4) whose tile fits and
+// that reaches 256 workgroups with at most 2 (Q = 8) or 4 (Q = 4) parts per
+// slice, each part gathering at least twice the tile; none -> L2 form.
+struct AggLdsPlan {
+    int q, slices, parts;
+};
+static AggLdsPlan plan_aggregate_lds(int64_t B, int N, int M, int K, int C, int elem) {
+    const int vec = 16 / elem;
+    for (int q : {8, 4}) {
+        if ((int64_t)N * q * 16 > kAggLdsMaxTile) continue;
+        const int slices = (int)ceil_div(C, q * vec);
+        int parts = 1;
+        while (B * slices * parts < 256 && parts < 64) parts *= 2;
+        if (parts > (q == 8 ? 2 : 4)) continue;
+        const int64_t per = ceil_div(M, parts);
+        if (per * K < 2 * (int64_t)N) continue;
+        return {q, slices, parts};
+    }
+    return {0, 0, 0};
+}
+
+template <typename T, int Q>
+static int launch_aggregate_lds(const T* pft, int64_t ldp, const int32_t* nit, int64_t B, int N, int M, int K, int C,
+                                const AggLdsPlan& pl, const int32_t* cidx, const T* cfeat, int64_t ldc, int sign,
+                                int relu, float* out, int64_t ldo, hipStream_t s) {
+    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&aggregate_lds_kernel<T, Q>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, kAggLdsMaxTile);
+    MESO_REQUIRE(attr == hipSuccess, MESORASI_EHIP, "mesorasi_aggregate_max: LDS size attribute: %s",
+                 hipGetErrorString(attr));
+    const int64_t nb = B * pl.slices * pl.parts;
+    const int per_xcd = (int)ceil_div(nb, 8);
+    const size_t lds = (size_t)N * Q * 16;
+    aggregate_lds_kernel<T, Q><<<dim3((unsigned)(8 * per_xcd)), dim3(kAggLdsThreads), lds, s>>>(
+        pft, ldp, nit, N, M, K, C, pl.slices, pl.parts, nb, per_xcd, cidx, cfeat, ldc, sign, relu, out, ldo);
+    return MESORASI_OK;
+}
+
 template <typename T, int VEC>
 static void launch_aggregate(const T* pft, int64_t ldp, const int32_t* nit, int64_t B, int N, int M, int K, int C,
                              const int32_t* cidx, const T* cfeat, int64_t ldc, int sign, int relu, float* out,
@@ -203,22 +365,46 @@ extern "C" int mesorasi_aggregate_max(const void* pft, int64_t ld_pft, int32_t p
     MESO_REQUIRE(N <= 0x7fffffff && M <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_aggregate_max: size");
     hipStream_t s = as_stream(stream);
     const int n = (int)N, m = (int)M;
+    // the LDS form reads NIT rows as 16-byte vectors
+    const bool lds_ok = K % 4 == 0 && aligned(nit, 16);
     if (pft_dtype == MESORASI_F32) {
         const float* p = static_cast<const float*>(pft);
         const float* cf = static_cast<const float*>(cfeat);
         const bool vec = C % 4 == 0 && ld_pft % 4 == 0 && ld_out % 4 == 0 && aligned(p, 16) && aligned(out, 16) &&
                          (!cf || (ld_c % 4 == 0 && aligned(cf, 16)));
-        if (vec) launch_aggregate<float, 4>(p, ld_pft, nit, B, n, m, K, C, cidx, cf, ld_c, sign, relu, out, ld_out, s);
-        else launch_aggregate<float, 1>(p, ld_pft, nit, B, n, m, K, C, cidx, cf, ld_c, sign, relu, out, ld_out, s);
+        const AggLdsPlan pl = vec && lds_ok ? plan_aggregate_lds(B, n, m, K, C, 4) : AggLdsPlan{0, 0, 0};
+        if (pl.q == 8) {
+            const int rc = launch_aggregate_lds<float, 8>(p, ld_pft, nit, B, n, m, K, C, pl, cidx, cf, ld_c, sign, relu,
+                                                          out, ld_out, s);
+            if (rc != MESORASI_OK) return rc;
+        } else if (pl.q == 4) {
+            const int rc = launch_aggregate_lds<float, 4>(p, ld_pft, nit, B, n, m, K, C, pl, cidx, cf, ld_c, sign, relu,
+                                                          out, ld_out, s);
+            if (rc != MESORASI_OK) return rc;
+        } else if (vec) {
+            launch_aggregate<float, 4>(p, ld_pft, nit, B, n, m, K, C, cidx, cf, ld_c, sign, relu, out, ld_out, s);
+        } else {
+            launch_aggregate<float, 1>(p, ld_pft, nit, B, n, m, K, C, cidx, cf, ld_c, sign, relu, out, ld_out, s);
+        }
     } else {
         const uint16_t* p = static_cast<const uint16_t*>(pft);
         const uint16_t* cf = static_cast<const uint16_t*>(cfeat);
         const bool vec = C % 8 == 0 && ld_pft % 8 == 0 && ld_out % 4 == 0 && aligned(p, 16) && aligned(out, 16) &&
                          (!cf || (ld_c % 8 == 0 && aligned(cf, 16)));
-        if (vec)
+        const AggLdsPlan pl = vec && lds_ok ? plan_aggregate_lds(B, n, m, K, C, 2) : AggLdsPlan{0, 0, 0};
+        if (pl.q == 8) {
+            const int rc = launch_aggregate_lds<uint16_t, 8>(p, ld_pft, nit, B, n, m, K, C, pl, cidx, cf, ld_c, sign,
+                                                             relu, out, ld_out, s);
+            if (rc != MESORASI_OK) return rc;
+        } else if (pl.q == 4) {
+            const int rc = launch_aggregate_lds<uint16_t, 4>(p, ld_pft, nit, B, n, m, K, C, pl, cidx, cf, ld_c, sign,
+                                                             relu, out, ld_out, s);
+            if (rc != MESORASI_OK) return rc;
+        } else if (vec) {
             launch_aggregate<uint16_t, 8>(p, ld_pft, nit, B, n, m, K, C, cidx, cf, ld_c, sign, relu, out, ld_out, s);
-        else
+        } else {
             launch_aggregate<uint16_t, 1>(p, ld_pft, nit, B, n, m, K, C, cidx, cf, ld_c, sign, relu, out, ld_out, s);
+        }
     }
     return after_launch("mesorasi_aggregate_max");
 }

@@ -179,6 +179,13 @@ AGG_CASES = [
     ("wide_bf16", 1, 64, 16, 32, 2048, "bf16", "cidx"),
     ("none", 2, 80, 20, 5, 24, "f32", "none"),
     ("k1", 2, 50, 50, 1, 8, "f32", "cidx"),
+    # batches large enough for the LDS form (a PFT column slice per workgroup)
+    ("lds_cls_sa1", 32, 1024, 512, 32, 128, "f32", "cidx"),
+    ("lds_cls_sa2", 32, 512, 128, 64, 256, "f32", "cidx"),
+    ("lds_dgcnn", 16, 1024, 1024, 20, 64, "f32", "cfeat"),
+    ("lds_bf16", 64, 512, 256, 16, 128, "bf16", "cidx"),
+    ("lds_bf16_cfeat", 16, 1024, 1024, 20, 128, "bf16", "cfeat"),
+    ("lds_ragged_c", 40, 600, 300, 12, 100, "f32", "cidx"),
 ]
 
 
@@ -200,11 +207,12 @@ def test_aggregate_bit_exact(gpu, name, B, N, M, K, C, dt, cen):
     assert np.array_equal(host(out), ref)
 
 
-def test_aggregate_strided_pft_and_out(gpu):
+@pytest.mark.parametrize("B", [2, 16])
+def test_aggregate_strided_pft_and_out(gpu, B):
     """DGCNN layout: PFT = [A | Bm] in one [N, 2C] table, output into a
-    column slice of a wider concat buffer."""
+    column slice of a wider concat buffer (B = 16 takes the LDS form)."""
     rr = g(6)
-    B, N, K, C = 2, 200, 20, 64
+    N, K, C = 200, 20, 64
     P = rr.standard_normal((B, N, 2 * C)).astype(np.float32)
     nit = rr.integers(0, N, (B, N, K)).astype(np.int32)
     ref = O.aggregate_max(np.ascontiguousarray(P[..., C:]), nit, cfeat=np.ascontiguousarray(P[..., :C]), sign=+1,
