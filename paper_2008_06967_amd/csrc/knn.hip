@@ -204,6 +204,164 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_kernel(const float* __rest
     }
 }
 
+// Register form for clouds of at most 64 * NT points: every wave first
+// computes the distances from its 4 queries to all references (reference
+// t * 64 + l in lane l, register t), then selects per query:
+//  1. tau = the K-th smallest of the 64 lane minima.  These are K distinct
+//     references, so tau bounds the K-th smallest distance from above and
+//     every reference of the exact top K has d <= tau; for random layouts
+//     only a few more than K references do.
+//  2. The candidates d <= tau are compacted through LDS (64 at a time),
+//     sorted across the wave in (distance, index) order and merged into
+//     the list: the same exact order as the streaming form, with one sort
+//     and one scan per query instead of a sorted merge or an insert per
+//     improving candidate.
+template <int NT>
+__global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __restrict__ ref, int64_t ldr,
+                                                                 const float* __restrict__ query, int64_t ldq,
+                                                                 int N, int M, int C, int Cs, int K, int qblocks,
+                                                                 int vec4, int32_t* __restrict__ nit,
+                                                                 float* __restrict__ dist) {
+    extern __shared__ float smem[];
+    float* sR = smem;                                    // [kKnnTile][Cs]
+    float* sQ = smem + kKnnTile * Cs;                    // [kKnnQpb][C]
+    float* sCd = sQ + kKnnQpb * C;                       // [kKnnWaves][64] candidate distances
+    int* sCj = reinterpret_cast<int*>(sCd + kKnnWaves * 64);   // [kKnnWaves][64] candidate indices
+    const int64_t b = blockIdx.x / qblocks;
+    const int q0 = (blockIdx.x % qblocks) * kKnnQpb;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float inf = __builtin_huge_valf();
+    const int nt = (N + kKnnTile - 1) / kKnnTile;
+
+    for (int e = tid; e < kKnnQpb * C; e += 64 * kKnnWaves) {
+        const int qq = e / C, c = e - qq * C;
+        const int qi = q0 + qq;
+        sQ[e] = qi < M ? query[(b * M + qi) * ldq + c] : 0.0f;
+    }
+
+    // 1. all distances, in the channel order of the oracle
+    float d[kKnnQpw][NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+#pragma unroll
+        for (int qq = 0; qq < kKnnQpw; ++qq) d[qq][t] = inf;
+        if (t < nt) {
+            const int t0 = t * kKnnTile;
+            __syncthreads();
+            if (vec4) {
+                const int C4 = C >> 2;
+                for (int e = tid; e < kKnnTile * C4; e += 64 * kKnnWaves) {
+                    const int r = e / C4, c = (e - r * C4) << 2;
+                    const int j = t0 + r;
+                    const float4 v = j < N ? *reinterpret_cast<const float4*>(ref + (b * N + j) * ldr + c)
+                                           : make_float4(0.f, 0.f, 0.f, 0.f);
+                    *reinterpret_cast<float4*>(sR + r * Cs + c) = v;
+                }
+            } else {
+                for (int e = tid; e < kKnnTile * C; e += 64 * kKnnWaves) {
+                    const int r = e / C, c = e - r * C;
+                    const int j = t0 + r;
+                    sR[r * Cs + c] = j < N ? ref[(b * N + j) * ldr + c] : 0.0f;
+                }
+            }
+            __syncthreads();
+            float a[kKnnQpw];
+#pragma unroll
+            for (int qq = 0; qq < kKnnQpw; ++qq) a[qq] = 0.0f;
+            const float* rr = sR + lane * Cs;
+            const float* qb = sQ + wave * kKnnQpw * C;
+            if (vec4) {
+                for (int c = 0; c < C; c += 4) {
+                    const float4 r = *reinterpret_cast<const float4*>(rr + c);
+#pragma unroll
+                    for (int qq = 0; qq < kKnnQpw; ++qq) {
+                        const float4 qv = *reinterpret_cast<const float4*>(qb + qq * C + c);
+                        float u = r.x - qv.x;
+                        a[qq] = __builtin_fmaf(u, u, a[qq]);
+                        u = r.y - qv.y;
+                        a[qq] = __builtin_fmaf(u, u, a[qq]);
+                        u = r.z - qv.z;
+                        a[qq] = __builtin_fmaf(u, u, a[qq]);
+                        u = r.w - qv.w;
+                        a[qq] = __builtin_fmaf(u, u, a[qq]);
+                    }
+                }
+            } else {
+                for (int c = 0; c < C; ++c) {
+                    const float r = rr[c];
+#pragma unroll
+                    for (int qq = 0; qq < kKnnQpw; ++qq) {
+                        const float u = r - qb[qq * C + c];
+                        a[qq] = __builtin_fmaf(u, u, a[qq]);
+                    }
+                }
+            }
+            const bool valid = t0 + lane < N;
+#pragma unroll
+            for (int qq = 0; qq < kKnnQpw; ++qq) d[qq][t] = valid ? a[qq] : inf;
+        }
+    }
+
+    // 2. per query: threshold, candidates, exact order
+    float* cd = sCd + wave * 64;
+    int* cj = sCj + wave * 64;
+#pragma unroll
+    for (int qq = 0; qq < kKnnQpw; ++qq) {
+        float mn = inf;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) mn = fminf(mn, d[qq][t]);
+        float sv = mn;
+        int sl = lane;
+        wave_sort_pairs(sv, sl, lane);
+        const float tau = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sv), K - 1));
+        // candidates of this lane and their offsets (exclusive scan over lanes)
+        int cnt = 0;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) cnt += (t * kKnnTile + lane < N && d[qq][t] <= tau) ? 1 : 0;
+        int incl = cnt;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int v = __shfl_up(incl, o);
+            incl += lane >= o ? v : 0;
+        }
+        const int total = __builtin_amdgcn_readlane(incl, 63);
+        const int off = incl - cnt;
+        float td = inf;
+        int tj = 0x7fffffff;
+        for (int base = 0; base < total; base += 64) {
+            int o = off;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int j = t * kKnnTile + lane;
+                if (j < N && d[qq][t] <= tau) {
+                    if (o >= base && o < base + 64) {
+                        cd[o - base] = d[qq][t];
+                        cj[o - base] = j;
+                    }
+                    ++o;
+                }
+            }
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+            const bool have = lane < total - base;
+            float ed = have ? cd[lane] : inf;
+            int ej = have ? cj[lane] : 0x7fffffff;
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+            wave_sort_pairs(ed, ej, lane);
+            if (base == 0) {
+                td = ed;
+                tj = ej;
+            } else {
+                merge_sorted_pairs(td, tj, ed, ej, lane);
+            }
+        }
+        const int qi = q0 + wave * kKnnQpw + qq;
+        if (qi < M && lane < K) {
+            nit[(b * M + qi) * K + lane] = tj;
+            if (dist) dist[(b * M + qi) * K + lane] = td;
+        }
+    }
+}
+
 constexpr int kIpWaves = 4;
 constexpr int kIpDests = 128;    // destinations per workgroup, two per lane
 constexpr int kIpChunk = 1024;   // sources staged in LDS per pass
@@ -403,8 +561,23 @@ extern "C" int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query
     const int vec4 = C % 4 == 0 && ld_ref % 4 == 0 && aligned(ref, 16) && C % 32 != 28;
     const int Cs = vec4 ? C + 4 : (C | 1);
     const size_t lds = sizeof(float) * ((size_t)kKnnTile * Cs + (size_t)kKnnQpb * C);
-    knn_kernel<<<dim3((unsigned)blocks), dim3(64 * kKnnWaves), lds, as_stream(stream)>>>(
-        ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks, vec4, nit, dist);
+    const dim3 grid((unsigned)blocks), block(64 * kKnnWaves);
+    hipStream_t s = as_stream(stream);
+    // clouds of at most 1024 points: all distances in registers, then one
+    // selection per query; larger clouds stream through the running list
+    const size_t lds_reg = lds + sizeof(float) * 2 * 64 * kKnnWaves;
+    if (N <= 4 * kKnnTile)
+        knn_reg_kernel<4><<<grid, block, lds_reg, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks,
+                                                       vec4, nit, dist);
+    else if (N <= 8 * kKnnTile)
+        knn_reg_kernel<8><<<grid, block, lds_reg, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks,
+                                                       vec4, nit, dist);
+    else if (N <= 16 * kKnnTile)
+        knn_reg_kernel<16><<<grid, block, lds_reg, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K,
+                                                        qblocks, vec4, nit, dist);
+    else
+        knn_kernel<<<grid, block, lds, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks, vec4, nit,
+                                            dist);
     return after_launch("mesorasi_knn");
 }
 

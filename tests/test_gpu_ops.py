@@ -136,6 +136,14 @@ KNN_CASES = [
     ("c28_scalar_path", 1, 90, 90, 28, 5, "self"),         # 4-channel groups, bank-conflicting stride: scalar path
     ("interp_like", 2, 256, 1024, 3, 3, "other"),
     ("k_max_c_max", 1, 300, 100, 128, 64, "other"),   # the documented maximum K and width
+    # at most 1024 points: all distances in registers, one selection per query;
+    # few distinct points put far more than 64 candidates at the threshold
+    ("reg_ties_many", 2, 1024, 1024, 2, 20, "grid"),
+    ("reg_k64", 1, 1024, 256, 8, 64, "other"),
+    ("reg_n65", 2, 65, 65, 4, 20, "self"),
+    # more than 1024 points: the streaming running list
+    ("stream_n1500", 1, 1500, 200, 16, 20, "other"),
+    ("stream_ties", 1, 1100, 300, 3, 10, "grid"),
 ]
 
 
