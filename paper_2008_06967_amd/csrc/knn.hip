@@ -64,6 +64,35 @@ __device__ __forceinline__ void merge_sorted_pairs(float& td, int& tj, float sd,
     for (int jm = 32; jm > 0; jm >>= 1) cx_step(td, tj, jm, true, lane);
 }
 
+// K-th smallest (K <= 64) of one non-negative float per lane (+inf
+// allowed), wave-uniform.  Its bits are fixed from the top: a bit stays 0
+// when at least K lanes are <= the largest value with the prefix so far and
+// that bit 0 (non-negative floats order like their bit patterns).  One
+// ballot per bit, no cross-lane data movement.
+__device__ __forceinline__ float wave_kth_smallest(float v, int K) {
+    const uint32_t x = __float_as_uint(v);
+    uint32_t pre = 0;
+#pragma unroll
+    for (int bit = 30; bit >= 0; --bit) {
+        const uint32_t lim = pre | ((1u << bit) - 1u);
+        const int n = __builtin_popcountll(ballot(x <= lim));
+        pre = n >= K ? pre : (pre | (1u << bit));
+    }
+    return __uint_as_float(pre);
+}
+
+// Rank of this lane's (d, j) among lanes 0 .. n-1 in (distance, index)
+// order (indices distinct): the output slot of a candidate, without a sort.
+__device__ __forceinline__ int pair_rank(float d, int j, int n) {
+    int r = 0;
+    for (int l = 0; l < n; ++l) {
+        const float dl = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(d), l));
+        const int jl = __builtin_amdgcn_readlane(j, l);
+        r += (dl < d || (dl == d && jl < j)) ? 1 : 0;
+    }
+    return r;
+}
+
 __global__ __launch_bounds__(64 * kKnnWaves) void knn_kernel(const float* __restrict__ ref, int64_t ldr,
                                                              const float* __restrict__ query, int64_t ldq, int N, int M,
                                                              int C, int Cs, int K, int qblocks, int vec4,
@@ -310,11 +339,10 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __
         float mn = inf;
 #pragma unroll
         for (int t = 0; t < NT; ++t) mn = fminf(mn, d[qq][t]);
-        float sv = mn;
-        int sl = lane;
-        wave_sort_pairs(sv, sl, lane);
-        const float tau = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sv), K - 1));
-        // candidates of this lane and their offsets (exclusive scan over lanes)
+        const float tau = wave_kth_smallest(mn, K);
+        // candidates of this lane and their offsets (exclusive scan over
+        // lanes; ballot slots per register would need NT more registers and
+        // halve the occupancy)
         int cnt = 0;
 #pragma unroll
         for (int t = 0; t < NT; ++t) cnt += (t * kKnnTile + lane < N && d[qq][t] <= tau) ? 1 : 0;
@@ -326,6 +354,31 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __
         }
         const int total = __builtin_amdgcn_readlane(incl, 63);
         const int off = incl - cnt;
+        const int qi = q0 + wave * kKnnQpw + qq;
+        if (total <= 64) {
+            // the usual case: every candidate's output slot from its rank
+            int o = off;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int j = t * kKnnTile + lane;
+                if (j < N && d[qq][t] <= tau) {
+                    cd[o] = d[qq][t];
+                    cj[o] = j;
+                    ++o;
+                }
+            }
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+            const bool have = lane < total;
+            const float ed = have ? cd[lane] : inf;
+            const int ej = have ? cj[lane] : 0x7fffffff;
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+            const int rk = pair_rank(ed, ej, total);
+            if (have && rk < K && qi < M) {
+                nit[(b * M + qi) * K + rk] = ej;
+                if (dist) dist[(b * M + qi) * K + rk] = ed;
+            }
+            continue;
+        }
         float td = inf;
         int tj = 0x7fffffff;
         for (int base = 0; base < total; base += 64) {
@@ -354,7 +407,296 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __
                 merge_sorted_pairs(td, tj, ed, ej, lane);
             }
         }
-        const int qi = q0 + wave * kKnnQpw + qq;
+        if (qi < M && lane < K) {
+            nit[(b * M + qi) * K + lane] = tj;
+            if (dist) dist[(b * M + qi) * K + lane] = td;
+        }
+    }
+}
+
+// MFMA form for C in [32, 128] with C % 8 == 0 and N <= 1024 (the DGCNN
+// feature-space layers).  The distance a = fl(fl(|x|^2 + |y|^2) - 2 fl(x.y))
+// comes from a Gram product on v_mfma_f32_32x32x2_f32; it is only used to
+// bound the exact distance d (the fp32 fma chain in channel order):
+//   |d - D| <= ((1+u)^2 (1 + gamma_C) - 1) D,   D = |x - y|^2 <= 2(|x|^2 + |y|^2)
+//   |a - D| <= (gamma_C + gamma_{C+2} + 3u + O(u^2)) (|x|^2 + |y|^2)
+// for any summation order inside the MFMA (products rounded or not), so
+// |a - d| <= (4C + 12) u (|x|^2 + |y|^2) to first order; eps below takes
+// twice that, plus C * 2^-120 for flushed denormal products, with the
+// computed norms.  Then lower = a - eps <= d <= a + eps = upper, and:
+//  1. tau = the K-th smallest of the 64 lane minima of upper: K distinct
+//     references have d <= tau, so every reference of the exact top K has
+//     d <= tau, hence lower <= tau;
+//  2. the candidates lower <= tau (or NaN) get their exact d, compacted 64 at a
+//     time, and are sorted across the wave in (distance, index) order, as in
+//     the register form.  Results are bit-identical to the exact search.
+// Workgroup: 32 queries (one MFMA row block), 8 waves.  Phase 1: wave w
+// takes reference blocks w, w + 8, ...: its 32 x 32 Gram block from
+// registers (query rows fixed, reference rows streamed from global memory,
+// the k order of each operand split in two halves like the GEMM), turned
+// into a and stored to a 32 x 1032 LDS table.  Phase 2: wave w selects
+// for queries 4w .. 4w + 3, reading 4 references per lane per 16-byte read.
+constexpr int kKnnMfmaLda = 1024 + 8;          // a-table row stride (words)
+constexpr int kKnnMfmaMaxN = 1024;
+
+typedef float knn_f32x16 __attribute__((ext_vector_type(16)));
+
+template <int CH>   // maximum C / 2 (32 or 64)
+__global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* __restrict__ ref, int64_t ldr,
+                                                                  const float* __restrict__ query, int64_t ldq,
+                                                                  int N, int M, int C, int K, int qblocks,
+                                                                  int32_t* __restrict__ nit,
+                                                                  float* __restrict__ dist) {
+    extern __shared__ float smem[];
+    float* sA = smem;                                    // [32][kKnnMfmaLda]
+    float* sQ = sA + kKnnQpb * kKnnMfmaLda;              // [32][C]
+    float* sNy = sQ + kKnnQpb * C;                       // [1024]
+    float* sNx = sNy + kKnnMfmaMaxN;                     // [32]
+    int* sCj = reinterpret_cast<int*>(sNx + kKnnQpb);    // [kKnnWaves][4][64]
+    const int64_t b = blockIdx.x / qblocks;
+    const int q0 = (blockIdx.x % qblocks) * kKnnQpb;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float inf = __builtin_huge_valf();
+    const int HC = C / 2;
+
+    // 0. queries into LDS, their squared norms
+    for (int e = tid; e < kKnnQpb * C; e += 64 * kKnnWaves) {
+        const int qq = e / C, c = e - qq * C;
+        const int qi = q0 + qq;
+        sQ[e] = qi < M ? query[(b * M + qi) * ldq + c] : 0.0f;
+    }
+    __syncthreads();
+    if (tid < kKnnQpb) {
+        float nx = 0.0f;
+        for (int c = 0; c < C; ++c) nx = __builtin_fmaf(sQ[tid * C + c], sQ[tid * C + c], nx);
+        sNx[tid] = nx;
+    }
+    const int half = lane >> 5;
+    // this lane's query operand: row lane % 32, k half `half` (read from LDS
+    // four steps at a time inside the MFMA loop)
+    const float* qa = sQ + (lane & 31) * C + half * HC;
+    __syncthreads();   // sNx visible
+
+    // 1. Gram blocks -> a table; at C <= 64 the next block's reference rows
+    //    are loaded while the current block's MFMAs run (two register sets,
+    //    pairs of blocks per loop turn so nothing rotates across the loop edge)
+    const int nblk = (N + 31) / 32;
+    auto load_b = [&](float (&bv)[CH], int blk) {
+        const int j = blk * 32 + (lane & 31);
+        const float* rr = ref + (b * N + (j < N ? j : N - 1)) * ldr + half * HC;
+#pragma unroll
+        for (int s4 = 0; s4 < CH / 4; ++s4) {
+            const float4 v = s4 * 4 < HC ? *reinterpret_cast<const float4*>(rr + 4 * s4) : make_float4(0.f, 0.f, 0.f, 0.f);
+            bv[4 * s4] = v.x; bv[4 * s4 + 1] = v.y; bv[4 * s4 + 2] = v.z; bv[4 * s4 + 3] = v.w;
+        }
+    };
+    auto gram = [&](const float (&bv)[CH], int blk) {
+        const int j = blk * 32 + (lane & 31);
+        const bool valid = j < N;
+        float nyh = 0.0f;
+#pragma unroll
+        for (int k = 0; k < CH; ++k) nyh = __builtin_fmaf(bv[k], bv[k], nyh);
+        const float ny = nyh + __shfl_xor(nyh, 32);
+        knn_f32x16 acc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+#pragma unroll
+        for (int s4 = 0; s4 < CH / 4; ++s4) {
+            const float4 a = s4 * 4 < HC ? *reinterpret_cast<const float4*>(qa + 4 * s4) : make_float4(0.f, 0.f, 0.f, 0.f);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.x, bv[4 * s4], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.y, bv[4 * s4 + 1], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.z, bv[4 * s4 + 2], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.w, bv[4 * s4 + 3], acc, 0, 0, 0);
+        }
+        if (lane < 32 && valid) sNy[j] = ny;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int i = 8 * (r >> 2) + 4 * half + (r & 3);
+            sA[i * kKnnMfmaLda + j] = valid ? __builtin_fmaf(-2.0f, acc[r], sNx[i] + ny) : inf;
+        }
+    };
+    if constexpr (CH <= 32) {
+        float b0[CH], b1[CH];
+        if (wave < nblk) load_b(b0, wave);
+        for (int blk = wave; blk < nblk; blk += 2 * kKnnWaves) {
+            const int nb1 = blk + kKnnWaves;
+            if (nb1 < nblk) load_b(b1, nb1);
+            gram(b0, blk);
+            if (nb1 >= nblk) break;
+            if (nb1 + kKnnWaves < nblk) load_b(b0, nb1 + kKnnWaves);
+            gram(b1, nb1);
+        }
+    } else {
+        // 64 words per operand half: one register set (two would spill)
+        float b0[CH];
+        for (int blk = wave; blk < nblk; blk += kKnnWaves) {
+            load_b(b0, blk);
+            gram(b0, blk);
+        }
+    }
+    __syncthreads();
+
+    // 2. selection: for each of the wave's 4 queries a threshold and the
+    //    candidate slots (one ballot per register); then the exact distances
+    //    of all 4 queries' candidates together (4 independent chains per
+    //    lane), then each candidate's output slot from its rank.  A query
+    //    with more than 64 candidates is sorted and merged 64 at a time.
+    const float kappa = (float)(8 * C + 32) * 0x1p-24f;
+    const float tiny = (float)C * 0x1p-120f;
+    float nyv[16];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const float4 v = *reinterpret_cast<const float4*>(sNy + 256 * t + 4 * lane);
+        nyv[4 * t] = v.x; nyv[4 * t + 1] = v.y; nyv[4 * t + 2] = v.z; nyv[4 * t + 3] = v.w;
+    }
+    int* cjw = sCj + wave * (kKnnQpw * 64);   // [4][64] candidate indices of this wave
+    int total[kKnnQpw];
+    float tau[kKnnQpw];
+#pragma unroll
+    for (int qq = 0; qq < kKnnQpw; ++qq) {
+        const int i = wave * kKnnQpw + qq;
+        const float nxq = sNx[i];
+        float lo[16];
+        float mn = inf;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const float4 v = *reinterpret_cast<const float4*>(sA + i * kKnnMfmaLda + 256 * t + 4 * lane);
+            const float av4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool valid = 256 * t + 4 * lane + u < N;
+                const float e = __builtin_fmaf(kappa, nxq + nyv[4 * t + u], tiny);
+                const float up = valid ? av4[u] + e : inf;
+                lo[4 * t + u] = av4[u] - e;
+                mn = fminf(mn, up);
+            }
+        }
+        tau[qq] = wave_kth_smallest(mn, K);
+        int tot = 0;
+        int slot[16];
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+            const int j = 256 * (t >> 2) + 4 * lane + (t & 3);
+            const bool c = j < N && !(lo[t] > tau[qq]);   // NaN bounds are candidates
+            const uint64_t m = ballot(c);
+            slot[t] = c ? tot + mask_rank(m) : -1;
+            tot += __builtin_popcountll(m);
+        }
+        total[qq] = tot;
+        if (tot <= 64) {
+#pragma unroll
+            for (int t = 0; t < 16; ++t)
+                if (slot[t] >= 0) cjw[qq * 64 + slot[t]] = 256 * (t >> 2) + 4 * lane + (t & 3);
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    // exact distances (the oracle's channel order) of this lane's candidate
+    // of each query
+    int jc[kKnnQpw];
+    float dx[kKnnQpw];
+#pragma unroll
+    for (int qq = 0; qq < kKnnQpw; ++qq) {
+        jc[qq] = (total[qq] <= 64 && lane < total[qq]) ? cjw[qq * 64 + lane] : 0;
+        dx[qq] = 0.0f;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    {
+        const float* rr[kKnnQpw];
+        const float* qr[kKnnQpw];
+#pragma unroll
+        for (int qq = 0; qq < kKnnQpw; ++qq) {
+            rr[qq] = ref + (b * N + jc[qq]) * ldr;
+            qr[qq] = sQ + (wave * kKnnQpw + qq) * C;
+        }
+#pragma unroll
+        for (int c4 = 0; c4 < CH / 2; ++c4) {
+            if (c4 * 4 < C) {
+#pragma unroll
+                for (int qq = 0; qq < kKnnQpw; ++qq) {
+                    const float4 r = *reinterpret_cast<const float4*>(rr[qq] + 4 * c4);
+                    const float4 qv = *reinterpret_cast<const float4*>(qr[qq] + 4 * c4);
+                    float u = r.x - qv.x;
+                    dx[qq] = __builtin_fmaf(u, u, dx[qq]);
+                    u = r.y - qv.y;
+                    dx[qq] = __builtin_fmaf(u, u, dx[qq]);
+                    u = r.z - qv.z;
+                    dx[qq] = __builtin_fmaf(u, u, dx[qq]);
+                    u = r.w - qv.w;
+                    dx[qq] = __builtin_fmaf(u, u, dx[qq]);
+                }
+            }
+        }
+    }
+    for (int qq = 0; qq < kKnnQpw; ++qq) {
+        const int i = wave * kKnnQpw + qq;
+        const int qi = q0 + i;
+        const int tot = total[qq];
+        if (tot <= 64) {
+            const bool have = lane < tot;
+            const float ed = have ? dx[qq] : inf;
+            const int ej = have ? jc[qq] : 0x7fffffff;
+            const int rk = pair_rank(ed, ej, tot);
+            if (have && rk < K && qi < M) {
+                nit[(b * M + qi) * K + rk] = ej;
+                if (dist) dist[(b * M + qi) * K + rk] = ed;
+            }
+            continue;
+        }
+        // many candidates (near-equal distances under wide margins): recompute
+        // this query's bounds and take the candidates 64 at a time
+        const float nxq = sNx[i];
+        int slot[16];
+        int t2 = 0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const float4 v = *reinterpret_cast<const float4*>(sA + i * kKnnMfmaLda + 256 * t + 4 * lane);
+            const float av4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int j = 256 * t + 4 * lane + u;
+                const float e = __builtin_fmaf(kappa, nxq + nyv[4 * t + u], tiny);
+                const bool c = j < N && !(av4[u] - e > tau[qq]);
+                const uint64_t m = ballot(c);
+                slot[4 * t + u] = c ? t2 + mask_rank(m) : -1;
+                t2 += __builtin_popcountll(m);
+            }
+        }
+        int* cj = cjw + qq * 64;
+        const float* qrow = sQ + i * C;
+        float td = inf;
+        int tj = 0x7fffffff;
+        for (int base = 0; base < tot; base += 64) {
+#pragma unroll
+            for (int t = 0; t < 16; ++t)
+                if (slot[t] >= base && slot[t] < base + 64) cj[slot[t] - base] = 256 * (t >> 2) + 4 * lane + (t & 3);
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+            const bool have = lane < tot - base;
+            const int jj = have ? cj[lane] : 0;
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+            const float* rr = ref + (b * N + jj) * ldr;
+            float d = 0.0f;
+            for (int c4 = 0; c4 < C / 4; ++c4) {
+                const float4 r = *reinterpret_cast<const float4*>(rr + 4 * c4);
+                const float4 qv = *reinterpret_cast<const float4*>(qrow + 4 * c4);
+                float u = r.x - qv.x;
+                d = __builtin_fmaf(u, u, d);
+                u = r.y - qv.y;
+                d = __builtin_fmaf(u, u, d);
+                u = r.z - qv.z;
+                d = __builtin_fmaf(u, u, d);
+                u = r.w - qv.w;
+                d = __builtin_fmaf(u, u, d);
+            }
+            float ed = have ? d : inf;
+            int ej = have ? jj : 0x7fffffff;
+            wave_sort_pairs(ed, ej, lane);
+            if (base == 0) {
+                td = ed;
+                tj = ej;
+            } else {
+                merge_sorted_pairs(td, tj, ed, ej, lane);
+            }
+        }
         if (qi < M && lane < K) {
             nit[(b * M + qi) * K + lane] = tj;
             if (dist) dist[(b * M + qi) * K + lane] = td;
@@ -566,7 +908,24 @@ extern "C" int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query
     // clouds of at most 1024 points: all distances in registers, then one
     // selection per query; larger clouds stream through the running list
     const size_t lds_reg = lds + sizeof(float) * 2 * 64 * kKnnWaves;
-    if (N <= 4 * kKnnTile)
+    const bool mfma = N <= kKnnMfmaMaxN && C >= 32 && C % 8 == 0 && ld_ref % 4 == 0 && aligned(ref, 16);
+    if (mfma) {
+        const size_t lds_m = sizeof(float) * ((size_t)kKnnQpb * kKnnMfmaLda + (size_t)kKnnQpb * C + kKnnMfmaMaxN +
+                                              kKnnQpb + 64 * kKnnQpw * kKnnWaves);
+        if (C <= 64) {
+            static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&knn_mfma_kernel<32>),
+                                                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            MESO_REQUIRE(attr == hipSuccess, MESORASI_EHIP, "mesorasi_knn: LDS size attribute: %s", hipGetErrorString(attr));
+            knn_mfma_kernel<32><<<grid, block, lds_m, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, K, qblocks,
+                                                           nit, dist);
+        } else {
+            static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&knn_mfma_kernel<64>),
+                                                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            MESO_REQUIRE(attr == hipSuccess, MESORASI_EHIP, "mesorasi_knn: LDS size attribute: %s", hipGetErrorString(attr));
+            knn_mfma_kernel<64><<<grid, block, lds_m, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, K, qblocks,
+                                                           nit, dist);
+        }
+    } else if (N <= 4 * kKnnTile)
         knn_reg_kernel<4><<<grid, block, lds_reg, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks,
                                                        vec4, nit, dist);
     else if (N <= 8 * kKnnTile)

@@ -34,7 +34,8 @@ def _rows(t: torch.Tensor, width: int | None = None):
     # all leading dims must be row-contiguous multiples of ld
     expect = ld * t.shape[-2] if t.dim() >= 2 else None
     for d in range(t.dim() - 3, -1, -1):
-        assert t.stride(d) == expect, "leading dimensions must collapse into rows"
+        # the stride of a size-1 dimension is never used
+        assert t.shape[d] == 1 or t.stride(d) == expect, "leading dimensions must collapse into rows"
         expect *= t.shape[d]
     if width is not None:
         assert t.shape[-1] >= width

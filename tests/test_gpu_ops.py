@@ -141,6 +141,13 @@ KNN_CASES = [
     ("reg_ties_many", 2, 1024, 1024, 2, 20, "grid"),
     ("reg_k64", 1, 1024, 256, 8, 64, "other"),
     ("reg_n65", 2, 65, 65, 4, 20, "self"),
+    # C in [32, 128], C % 8 == 0, N <= 1024: Gram distances on MFMA bound the
+    # exact ones; candidates re-ranked with the exact fp32 distance
+    ("mfma_c32_ties", 1, 512, 512, 32, 20, "grid"),
+    ("mfma_c96_ragged", 2, 700, 300, 96, 16, "other"),
+    ("mfma_near_duplicates", 1, 1024, 256, 64, 20, "jitter"),   # far more candidates than K in the margin
+    ("mfma_large_offset", 1, 1000, 200, 128, 20, "offset"),     # norms >> distances: wide margins
+    ("mfma_k64", 1, 1024, 128, 128, 64, "other"),
     # more than 1024 points: the streaming running list
     ("stream_n1500", 1, 1500, 200, 16, 20, "other"),
     ("stream_ties", 1, 1100, 300, 3, 10, "grid"),
@@ -152,9 +159,17 @@ def test_knn_bit_exact(gpu, name, B, N, M, C, K, kind):
     rr = g(3)
     if kind == "grid":
         ref = rr.integers(0, 3, size=(B, N, C)).astype(np.float32)
+    elif kind == "jitter":   # 8 base points, each repeated with 1e-6 noise
+        base = rr.standard_normal((B, 8, C))
+        ref = np.ascontiguousarray(base[:, rr.integers(0, 8, N)] + 1e-6 * rr.standard_normal((B, N, C)), np.float32)
+    elif kind == "offset":   # features around 100: |x|^2 ~ 1e6 C, distances ~ 2C
+        ref = (100.0 + rr.standard_normal((B, N, C))).astype(np.float32)
     else:
         ref = rr.standard_normal((B, N, C)).astype(np.float32)
-    query = ref if kind in ("self", "grid") else rr.standard_normal((B, M, C)).astype(np.float32)
+    if kind in ("self", "grid", "jitter", "offset"):
+        query = ref if M == N else np.ascontiguousarray(ref[:, :M])
+    else:
+        query = rr.standard_normal((B, M, C)).astype(np.float32)
     rn, rd = O.knn(ref, query, K)
     nit, dist = ops.knn(dev(ref), dev(query), K, want_dist=True)
     assert np.array_equal(host(nit), rn)
