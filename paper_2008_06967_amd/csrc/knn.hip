@@ -449,8 +449,10 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
                                                                   float* __restrict__ dist) {
     extern __shared__ float smem[];
     float* sA = smem;                                    // [32][kKnnMfmaLda]
-    float* sQ = sA + kKnnQpb * kKnnMfmaLda;              // [32][C]
-    float* sNy = sQ + kKnnQpb * C;                       // [1024]
+    const int CQ = C + 4;                                // query row stride: 16-byte lane reads of
+                                                         // 32 rows land on distinct bank groups
+    float* sQ = sA + kKnnQpb * kKnnMfmaLda;              // [32][CQ]
+    float* sNy = sQ + kKnnQpb * CQ;                      // [1024]
     float* sNx = sNy + kKnnMfmaMaxN;                     // [32]
     int* sCj = reinterpret_cast<int*>(sNx + kKnnQpb);    // [kKnnWaves][4][64]
     const int64_t b = blockIdx.x / qblocks;
@@ -463,18 +465,18 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
     for (int e = tid; e < kKnnQpb * C; e += 64 * kKnnWaves) {
         const int qq = e / C, c = e - qq * C;
         const int qi = q0 + qq;
-        sQ[e] = qi < M ? query[(b * M + qi) * ldq + c] : 0.0f;
+        sQ[qq * CQ + c] = qi < M ? query[(b * M + qi) * ldq + c] : 0.0f;
     }
     __syncthreads();
     if (tid < kKnnQpb) {
         float nx = 0.0f;
-        for (int c = 0; c < C; ++c) nx = __builtin_fmaf(sQ[tid * C + c], sQ[tid * C + c], nx);
+        for (int c = 0; c < C; ++c) nx = __builtin_fmaf(sQ[tid * CQ + c], sQ[tid * CQ + c], nx);
         sNx[tid] = nx;
     }
     const int half = lane >> 5;
     // this lane's query operand: row lane % 32, k half `half` (read from LDS
     // four steps at a time inside the MFMA loop)
-    const float* qa = sQ + (lane & 31) * C + half * HC;
+    const float* qa = sQ + (lane & 31) * CQ + half * HC;
     __syncthreads();   // sNx visible
 
     // 1. Gram blocks -> a table; at C <= 64 the next block's reference rows
@@ -527,7 +529,7 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
             gram(b1, nb1);
         }
     } else {
-        // 64 words per operand half: one register set (two would spill)
+        // 64 words per operand half: one register set (two measured slower)
         float b0[CH];
         for (int blk = wave; blk < nblk; blk += kKnnWaves) {
             load_b(b0, blk);
@@ -606,7 +608,7 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
 #pragma unroll
         for (int qq = 0; qq < kKnnQpw; ++qq) {
             rr[qq] = ref + (b * N + jc[qq]) * ldr;
-            qr[qq] = sQ + (wave * kKnnQpw + qq) * C;
+            qr[qq] = sQ + (wave * kKnnQpw + qq) * CQ;
         }
 #pragma unroll
         for (int c4 = 0; c4 < CH / 2; ++c4) {
@@ -662,7 +664,7 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
             }
         }
         int* cj = cjw + qq * 64;
-        const float* qrow = sQ + i * C;
+        const float* qrow = sQ + i * CQ;
         float td = inf;
         int tj = 0x7fffffff;
         for (int base = 0; base < tot; base += 64) {
@@ -910,8 +912,8 @@ extern "C" int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query
     const size_t lds_reg = lds + sizeof(float) * 2 * 64 * kKnnWaves;
     const bool mfma = N <= kKnnMfmaMaxN && C >= 32 && C % 8 == 0 && ld_ref % 4 == 0 && aligned(ref, 16);
     if (mfma) {
-        const size_t lds_m = sizeof(float) * ((size_t)kKnnQpb * kKnnMfmaLda + (size_t)kKnnQpb * C + kKnnMfmaMaxN +
-                                              kKnnQpb + 64 * kKnnQpw * kKnnWaves);
+        const size_t lds_m = sizeof(float) * ((size_t)kKnnQpb * kKnnMfmaLda + (size_t)kKnnQpb * (C + 4) +
+                                              kKnnMfmaMaxN + kKnnQpb + 64 * kKnnQpw * kKnnWaves);
         if (C <= 64) {
             static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&knn_mfma_kernel<32>),
                                                                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
