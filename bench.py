@@ -126,8 +126,10 @@ def call_work(name, a, kw):
     fps:            (M-1) * N point updates per cloud, 8 flops each (3 sub,
                     1 mul, 2 fma) -> alu
     ball_query:     B * M * N candidate tests (upper bound; early exit scans
-                    fewer), 8 flops each -> alu
-    knn:            B * M * N pairs, 3 * C flops each (sub, mul, add) -> alu
+                    fewer), 8 flops each -> alu; its compulsory HBM bytes
+                    (points, centroids, NIT and counts) reported beside it
+    knn:            B * M * N pairs, 3 * C flops each (sub, mul, add) -> alu;
+                    compulsory bytes (reference and query rows, NIT) beside it
     pointwise_mlp:  2 * rows * sum(C_l * C_l+1) -> mfma
     aggregate_max:  compulsory HBM bytes -- every PFT row read once, the NIT,
                     the centroid indices or rows, the output -> hbm (the
@@ -143,12 +145,16 @@ def call_work(name, a, kw):
         B, N = xyz.shape[0], xyz.shape[1]
         return ("alu", 8.0 * B * (M - 1) * N / 1e12, None)
     if name == "ball_query":
-        xyz, q = arg(0, "xyz"), arg(1, "qxyz")
-        return ("alu", 8.0 * xyz.shape[0] * q.shape[1] * xyz.shape[1] / 1e12, None)
+        xyz, q, K = arg(0, "xyz"), arg(1, "qxyz"), arg(3, "K")
+        B, N, M = xyz.shape[0], xyz.shape[1], q.shape[1]
+        comp = 12 * B * N + 12 * B * M + 4 * B * M * K + 4 * B * M
+        return ("alu", 8.0 * B * M * N / 1e12, {"compulsory_bytes": comp})
     if name == "knn":
-        ref, q = arg(0, "ref"), arg(1, "query")
+        ref, q, K = arg(0, "ref"), arg(1, "query"), arg(2, "K")
         B, N, C = ref.shape
-        return ("alu", 3.0 * C * B * q.shape[1] * N / 1e12, None)
+        M = q.shape[1]
+        comp = 4 * B * N * C + (0 if q.data_ptr() == ref.data_ptr() else 4 * B * M * C) + 4 * B * M * K
+        return ("alu", 3.0 * C * B * M * N / 1e12, {"compulsory_bytes": comp})
     if name == "pointwise_mlp":
         x0, prm = arg(0, "x0"), arg(1, "p")
         rows = int(np.prod(x0.shape[:-1]))
@@ -341,6 +347,10 @@ def main():
         roofs[k] = {"bound": kd, "achieved": round(rate, 4), "peak": pk, "unit": pu, "frac": round(rate / pk, 5)}
         if extra and "logical_gather_bytes" in extra:
             roofs[k]["logical_gather_GBps"] = round(extra["logical_gather_bytes"] / (ms * 1e-3) / 1e9, 1)
+        if extra and "compulsory_bytes" in extra:
+            gbs = extra["compulsory_bytes"] / (ms * 1e-3) / 1e9
+            roofs[k]["hbm_compulsory_GBps"] = round(gbs, 1)
+            roofs[k]["hbm_frac"] = round(gbs / HBM_PEAK_GBS, 5)
     dom = max((k for k in stages if k in work), key=lambda k: stages[k])
     roof = dict(roofs[dom])
     roof["kernel"] = dom
