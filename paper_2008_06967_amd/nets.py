@@ -132,8 +132,9 @@ class PointNet2(Net):
         for i, m in enumerate(self.spec["sa"]):
             prm = self.sa[i]
             N = p.shape[1]
-            if i > 0:
-                main.wait_event(ev_fps[i - 1])          # p = centroids of the previous level
+            # p = the previous level's centroids: already ordered, since the
+            # previous level waited for its ball query, recorded after its FPS
+            # (a redundant wait would add a cross-stream edge to the graph)
             idx, cx, nit = self._bufs[f"idx{i}"], self._bufs[f"cxyz{i}"], self._bufs[f"nit{i}"]
             out = self._buf(f"f{i}", (B, m["M"], prm.c_out))
             if self.delayed == "ltd":
