@@ -66,7 +66,24 @@ struct GemmArgs {
     int64_t ldc;
     int cc;
     int ldw;
+    // pooled output of the MLP's last layer, cleared by the first layer's
+    // workgroups (null: nothing to clear)
+    float* zy;
+    int64_t zrows, zld;
+    int zcols;
 };
+
+// Clears the pooled output from the first layer's kernel, so the last
+// layer's atomic maxima start from zero without a separate fill launch
+// (kernel order on the stream makes the clear complete first).
+__device__ __forceinline__ void clear_pool_target(const GemmArgs& a) {
+    if (!a.zy) return;
+    const int64_t nb = (int64_t)gridDim.x * gridDim.y * gridDim.z;
+    const int64_t bid = blockIdx.x + (int64_t)gridDim.x * (blockIdx.y + (int64_t)gridDim.y * blockIdx.z);
+    const int64_t n = a.zrows * a.zcols;
+    for (int64_t e = bid * blockDim.x + threadIdx.x; e < n; e += nb * blockDim.x)
+        a.zy[(e / a.zcols) * a.zld + e % a.zcols] = 0.0f;
+}
 
 // 16 bytes at a 4-byte aligned address: gfx950 global loads accept dword
 // alignment, so this is still one 16-byte load.
@@ -341,6 +358,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     const int64_t row_t = (int64_t)blockIdx.x * BM;
     const int col_t = blockIdx.y * BN;
     const int ldw = SPLIT ? a.ldw : a.K;
+    clear_pool_target(a);
     if constexpr (SPLIT) {
         // x0 rows of this tile and the matching weight columns (zero past
         // cc, rows or N); read after the first barrier below
@@ -523,6 +541,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // tiles (8 consecutive k per lane per MFMA operand).
 template <int BM, int BN, int EPI, bool FAST_A, bool FAST_W>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
+    clear_pool_target(a);
     constexpr int BK = BKH;
     constexpr int TM = BM / 64, TN = BN / 64;
     constexpr int PA = BM / 64, PB = BN / 64;   // 8-element runs per thread per slice
@@ -930,7 +949,9 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
         return MESORASI_OK;
     }
     float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + lay.act);
-    if (pool_group > 0) {
+    // a pooled multi-layer MLP clears its output from the first layer's
+    // kernel; a single pooled layer needs the fill launch first
+    if (pool_group > 0 && n_layers == 1) {
         const int rc = zero_rows_f32(static_cast<float*>(y), rows / pool_group, dims[n_layers], ld_y, s);
         if (rc != MESORASI_OK) return rc;
     }
@@ -938,6 +959,12 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
         GemmArgs a{};
         if (l == 0) {
             a.x0 = x0; a.ld0 = ld0; a.x1 = x1; a.ld1 = ld1; a.c0 = c0; a.c1 = c1; a.a_bf16 = 0;
+            if (pool_group > 0 && n_layers > 1) {
+                a.zy = static_cast<float*>(y);
+                a.zrows = rows / pool_group;
+                a.zcols = dims[n_layers];
+                a.zld = ld_y;
+            }
         } else {
             a.x0 = buf[(l - 1) & 1]; a.ld0 = dims[l]; a.x1 = nullptr; a.ld1 = 0; a.c0 = dims[l]; a.c1 = 0;
             a.a_bf16 = bf16 ? 1 : 0;

@@ -334,6 +334,24 @@ def test_mlp_pooled_two_source(gpu, G):
     assert normwise(host(y).reshape(groups, 256), ref.reshape(groups, 256)) <= 1e-4
 
 
+@pytest.mark.parametrize("rows_per_group,groups", [(16, 9), (40, 5)])
+def test_mlp_pooled_multilayer_reuses_output(gpu, rows_per_group, groups):
+    """A pooled multi-layer MLP on the tiled GEMM path clears its output in
+    the first layer's kernel: a second call into the same buffer with
+    smaller activations must not keep the first call's maxima."""
+    rr = g(11)
+    G = rows_per_group
+    rows = G * groups
+    Ws, bs = _weights(rr, [20, 200, 300])
+    p = ops.MLPParams(Ws, bs)
+    y = torch.empty(groups, 300, device="cuda")
+    for scale in (10.0, 0.1):
+        x = (scale * rr.standard_normal((rows, 20))).astype(np.float32)
+        ref = O.rowgroup_max(O.mlp(x, Ws, bs).reshape(groups, G, 300), G)
+        ops.pointwise_mlp(dev(x), p, pool_group=G, out=y)
+        assert normwise(host(y), ref.reshape(groups, 300)) <= 1e-4
+
+
 def test_mlp_strided_input(gpu):
     rr = g(9)
     wide = rr.standard_normal((100, 50)).astype(np.float32)
