@@ -71,7 +71,24 @@ struct GemmArgs {
     float* zy;
     int64_t zrows, zld;
     int zcols;
+    // gathered first layer of the conventional module (split form only):
+    // row r reads point g = (r / gmk) * gn + gnit[r] of the inputs -- x1
+    // row g and, through xc, xyz row g minus centroid row r / gk of gcen
+    const int32_t* gnit;
+    int64_t gmk, gn;
+    int gk;
+    const float* gcen;
+    // gathered layer of the limited order (lq set, single fast source):
+    // input row r is ReLU((x0[g] - lq[r / gk]) + lb1)
+    const float* lq;
+    int64_t ldq;
+    const float* lb1;
 };
+
+// Input row of row r of a gathered layer (see GemmArgs::gnit).
+__device__ __forceinline__ int64_t gather_row(const GemmArgs& a, int64_t r) {
+    return (r / a.gmk) * a.gn + a.gnit[r];
+}
 
 // Clears the pooled output from the first layer's kernel, so the last
 // layer's atomic maxima start from zero without a separate fill launch
@@ -339,10 +356,13 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, i
 // 16-byte aligned): the k loop reads x1 like a single fast source and the
 // weight columns after x0 with unaligned 16-byte loads; the x0 columns and
 // their weights are staged in LDS once and added to the accumulators before
-// the epilogue (same sum, different order).
-template <int BM, int BN, int BK, int EPI, bool FAST_A, bool FAST_W, bool SPLIT = false>
+// the epilogue (same sum, different order).  A gathered split layer (the
+// conventional module's first layer) takes its rows through the neighbor
+// index table, so the neighbor feature matrix is never written to memory.
+template <int BM, int BN, int BK, int EPI, bool FAST_A, bool FAST_W, bool SPLIT = false, bool LTD = false>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     static_assert(!SPLIT || FAST_A, "the split form reads x1 as a fast source");
+    static_assert(!LTD || (FAST_A && FAST_W && !SPLIT), "the limited-order gather reads one fast source");
     constexpr int TM = BM / 64, TN = BN / 64;
     constexpr int LW = BK + kPadF;           // LDS row stride in words
     constexpr int CPR = BK / 4;              // 16-byte chunks per tile row
@@ -366,7 +386,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
         for (int e = tid; e < BM * 4; e += 256) {
             const int64_t r = row_t + (e >> 2);
             const int i = e & 3;
-            sXc[e] = (i < a.cc && r < a.rows) ? a.xc[r * a.ldc + i] : 0.0f;
+            float v = 0.0f;
+            if (i < a.cc && r < a.rows) {
+                if (a.gnit) v = a.xc[gather_row(a, r) * a.ldc + i] - a.gcen[(r / a.gk) * 3 + i];
+                else v = a.xc[r * a.ldc + i];
+            }
+            sXc[e] = v;
         }
         for (int e = tid; e < BN * 4; e += 256) {
             const int n = col_t + (e >> 2);
@@ -396,13 +421,19 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     float ra0[QA][4], rb0[QB][4], ra1[QA][4], rb1[QB][4];
     bool oka0[QA], okb0[QB], oka1[QA], okb1[QB];
     const float* pa[QA];
+    const float* pq[LTD ? QA : 1];
     const float* pb[QB];
     bool rowa[QA], rowb[QB];
 #pragma unroll
     for (int p = 0; p < QA; ++p) {
         const int64_t r = row_t + crow + RSTEP * p;
         rowa[p] = r < a.rows;
-        pa[p] = static_cast<const float*>(a.x0) + (rowa[p] ? r : 0) * a.ld0;
+        int64_t src = rowa[p] ? r : 0;
+        if constexpr (SPLIT || LTD) {
+            if (a.gnit && rowa[p]) src = gather_row(a, r);
+        }
+        pa[p] = static_cast<const float*>(a.x0) + src * a.ld0;
+        if constexpr (LTD) pq[p] = a.lq + (rowa[p] ? r / a.gk : 0) * a.ldq;
     }
 #pragma unroll
     for (int p = 0; p < QB; ++p) {
@@ -415,7 +446,15 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
         const int ko = kin ? k0 + ck : 0;    // columns past K read column 0 of the row
 #pragma unroll
         for (int p = 0; p < QA; ++p) {
-            if constexpr (FAST_A) {
+            if constexpr (LTD) {
+                const float4 u = *reinterpret_cast<const float4*>(pa[p] + ko);
+                const float4 qv = *reinterpret_cast<const float4*>(pq[p] + ko);
+                const float4 bv = a.lb1 ? *reinterpret_cast<const float4*>(a.lb1 + ko) : make_float4(0.f, 0.f, 0.f, 0.f);
+                const float h[4] = {(u.x - qv.x) + bv.x, (u.y - qv.y) + bv.y, (u.z - qv.z) + bv.z, (u.w - qv.w) + bv.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) ra[p][i] = h[i] > 0.0f ? h[i] : 0.0f;
+                oka[p] = rowa[p] && kin;
+            } else if constexpr (FAST_A) {
                 const float4 u = *reinterpret_cast<const float4*>(pa[p] + ko);
                 ra[p][0] = u.x; ra[p][1] = u.y; ra[p][2] = u.z; ra[p][3] = u.w;
                 oka[p] = rowa[p] && kin;
@@ -840,6 +879,10 @@ static void launch_tile(const GemmArgs& a, bool bf16, bool fast_a, bool fast_w, 
         gemm_f32_kernel<BM, BN, BK, EPI, true, false, true><<<grid, block, 0, s>>>(a);
         return;
     }
+    if (a.lq) {
+        gemm_f32_kernel<BM, BN, BK, EPI, true, true, false, true><<<grid, block, 0, s>>>(a);
+        return;
+    }
     if (bf16) {
         if (fast_a && fast_w) gemm_bf16_kernel<BM, BN, EPI, true, true><<<grid, block, 0, s>>>(a);
         else if (fast_w) gemm_bf16_kernel<BM, BN, EPI, false, true><<<grid, block, 0, s>>>(a);
@@ -861,10 +904,16 @@ static void launch_epi(const GemmArgs& a, const LayerPlan& pl, bool bf16, bool f
 }
 
 // Launch one layer.  epi: EPI_F32 / EPI_BF16 / EPI_POOL.
+static bool split_ok(const GemmArgs& a, bool bf16) {
+    return !bf16 && !a.a_bf16 && a.x1 && a.c1 > 0 && a.c0 <= 4 && a.c1 % 4 == 0 && a.ld1 % 4 == 0 &&
+           aligned(a.x1, 16) && aligned(a.W, 4);
+}
+
 static int launch_layer(GemmArgs a, bool bf16, int epi, float* part, hipStream_t s) {
     a.ldw = a.K;
-    if (!bf16 && !a.a_bf16 && a.x1 && a.c1 > 0 && a.c0 <= 4 && a.c1 % 4 == 0 && a.ld1 % 4 == 0 &&
-        aligned(a.x1, 16) && aligned(a.W, 4)) {
+    const bool split = split_ok(a, bf16);
+    MESO_REQUIRE(split || !a.gnit || a.lq, MESORASI_EUNSUPPORTED, "gathered layer without the split form");
+    if (split) {
         // split form: the k loop over x1 alone, x0 added in the epilogue
         a.xc = static_cast<const float*>(a.x0);
         a.ldc = a.ld0;
@@ -887,6 +936,7 @@ static int launch_layer(GemmArgs a, bool bf16, int epi, float* part, hipStream_t
     bool fast_a;
     if (a.a_bf16) fast_a = a.c1 == 0 && a.c0 == a.K && a.K % 8 == 0 && a.ld0 % 8 == 0 && aligned(a.x0, 16);
     else fast_a = a.c1 == 0 && a.c0 == a.K && a.K % kq == 0 && a.ld0 % 4 == 0 && aligned(a.x0, 16);
+    MESO_REQUIRE(!a.lq || (!bf16 && fast_a && fast_w), MESORASI_EUNSUPPORTED, "gathered layer without fast operands");
     if (pl.splits > 1) {
         a.part = part;
         launch_epi<EPI_PARTIAL>(a, pl, bf16, fast_a, fast_w, s);
@@ -923,10 +973,10 @@ static int check_mlp_spec(const char* who, int64_t rows, int n_layers, const int
 static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
                    int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
                    uint32_t relu_mask, int dtype, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, void* ws,
-                   hipStream_t s) {
+                   hipStream_t s, const MlpGather* g = nullptr) {
     if (fused_mlp_supported(n_layers, dims, dtype))
         return run_fused_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, out_dtype, y, ld_y,
-                             pool_group, s);
+                             pool_group, s, g);
     const bool bf16 = dtype == MESORASI_BF16;
     const size_t elem = bf16 ? 2 : 4;
     int64_t w = 0;
@@ -934,7 +984,7 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
     const size_t one = align256((size_t)rows * (size_t)w * elem);
     const MlpWs lay = mlp_ws_layout(rows, n_layers, dims, dtype);
     char* buf[2] = {static_cast<char*>(ws), static_cast<char*>(ws) + one};
-    if (skinny_ok(x0, ld0, x1, c1, rows, n_layers, dims, W, dtype, out_dtype, pool_group)) {
+    if (!g && skinny_ok(x0, ld0, x1, c1, rows, n_layers, dims, W, dtype, out_dtype, pool_group)) {
         // uses only the activation part of the workspace
         for (int l = 0; l < n_layers; ++l) {
             const float* xin = l == 0 ? x0 : reinterpret_cast<const float*>(buf[(l - 1) & 1]);
@@ -959,6 +1009,16 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
         GemmArgs a{};
         if (l == 0) {
             a.x0 = x0; a.ld0 = ld0; a.x1 = x1; a.ld1 = ld1; a.c0 = c0; a.c1 = c1; a.a_bf16 = 0;
+            if (g) {
+                a.gnit = g->nit;
+                a.gmk = g->mk;
+                a.gn = g->n;
+                a.gk = g->k;
+                a.gcen = g->cxyz;
+                a.lq = g->q;
+                a.ldq = g->ldq;
+                a.lb1 = g->b1;
+            }
             if (pool_group > 0 && n_layers > 1) {
                 a.zy = static_cast<float*>(y);
                 a.zrows = rows / pool_group;
@@ -1151,6 +1211,18 @@ extern "C" int mesorasi_conventional_module(const float* xyz, const float* feat,
     MESO_REQUIRE(ws && ws_bytes >= need, MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who, ws_bytes, need);
     MESO_REQUIRE(N <= 0x7fffffff && M <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: size", who);
     hipStream_t s = as_stream(stream);
+    if (grouping == 0 && dtype == MESORASI_F32) {
+        // gather -> MLP -> max without the neighbor matrix: the fused kernel
+        // (every layer narrow) or a split first layer that reads its rows
+        // through nit
+        GemmArgs a0{};
+        a0.x1 = feat; a0.ld1 = ld_f; a0.c0 = 3; a0.c1 = cf; a0.W = W[0];
+        if (fused_mlp_supported(n_layers, dims, dtype) || split_ok(a0, false)) {
+            const MlpGather g{nit, M * K, N, K, cxyz};
+            return run_mlp(xyz, 3, 3, cf > 0 ? feat : nullptr, cf, cf > 0 ? ld_f : 0, rows, n_layers, dims, W, bias,
+                           relu_mask, dtype, MESORASI_F32, out, ld_out, K, static_cast<char*>(ws) + nfm_bytes, s, &g);
+        }
+    }
     float* nfm = static_cast<float*>(ws);
     const int64_t blocks = std::min<int64_t>(ceil_div(rows * cin, 256), 16384);
     if (grouping == 0)
@@ -1198,9 +1270,17 @@ extern "C" int mesorasi_ltd_module(const float* p1, int64_t ld_p, const float* q
     MESO_REQUIRE(ws && ws_bytes >= need, MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who, ws_bytes, need);
     MESO_REQUIRE(N <= 0x7fffffff && M <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: size", who);
     hipStream_t s = as_stream(stream);
-    float* h1 = static_cast<float*>(ws);
     const bool vec = C1 % 4 == 0 && ld_p % 4 == 0 && ld_q % 4 == 0 && aligned(p1, 16) && aligned(q, 16) &&
                      (b1 == nullptr || aligned(b1, 16));
+    if (dtype == MESORASI_F32 &&
+        (fused_mlp_supported(n_layers, dims, dtype) || (vec && aligned(W[0], 16)))) {
+        // the first-layer rows ReLU(p1[j] - q[c] + b1) are formed in the next
+        // layer's loader (fused kernel or gathered GEMM), never in memory
+        const MlpGather g{nit, M * K, N, K, nullptr, q, ld_q, b1};
+        return run_mlp(p1, C1, ld_p, nullptr, 0, 0, rows, n_layers, dims, W, bias, relu_mask, dtype, MESORASI_F32,
+                       out, ld_out, K, static_cast<char*>(ws) + h1_bytes, s, &g);
+    }
+    float* h1 = static_cast<float*>(ws);
     const int64_t work = rows * (vec ? C1 / 4 : C1);
     const int64_t blocks = std::min<int64_t>(ceil_div(work, 256), 16384);
     if (vec)

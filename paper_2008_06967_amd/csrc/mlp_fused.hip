@@ -17,6 +17,9 @@
 // MFMA: v_mfma_f32_32x32x2_f32 (fp32 in, fp32 accumulate).
 // Used for fp32 MLPs whose layer inputs are at most 160 wide and whose
 // outputs are at most 128 wide; other MLPs run layer by layer (mlp.hip).
+// The conventional module's rows can be gathered straight from the inputs
+// through the neighbor index table, which makes that module one kernel:
+// gather, every layer, max pool.
 #include "common.h"
 #include "mlp_internal.h"
 
@@ -48,6 +51,16 @@ struct FusedArgs {
     int out_bf16;
     int64_t G;      // pool group (0: store)
     int hsize;      // floats per activation buffer
+    // gathered rows (MlpGather), read at point (r / gmk) * gn + gnit[r]:
+    // x0 = xyz minus centroid r / gk of gcen, x1 = feat; or, with lq set,
+    // ReLU((x0 - lq[r / gk]) + lb1)
+    const int32_t* gnit;
+    int64_t gmk, gn;
+    int gk;
+    const float* gcen;
+    const float* lq;
+    int64_t ldq;
+    const float* lb1;
 };
 
 __host__ __device__ __forceinline__ int pad16(int x) { return (x + 15) & ~15; }
@@ -224,15 +237,44 @@ void mlp_fused_f32_kernel(FusedArgs a) {
     // layer-0 input tile -> H0 (k-major), zero beyond c0 + c1 up to the slice edge
     {
         const int K0 = a.c0 + a.c1, K0p = pad16(K0);
-        for (int e = tid; e < FBM * K0p; e += 256) {
-            const int r = e / K0p, k = e - r * K0p;
-            const int64_t row = row_t + r;
-            float v = 0.0f;
-            if (row < a.rows) {
-                if (k < a.c0) v = a.x0[row * a.ld0 + k];
-                else if (k < K0) v = a.x1[row * a.ld1 + (k - a.c0)];
+        if (a.gnit) {
+            // gathered rows: each row's input point and centroid once, then
+            // the element loop reads them from LDS
+            __shared__ int64_t s_pt[FBM], s_cen[FBM];
+            if (tid < FBM) {
+                const int64_t row = row_t + tid;
+                const bool ok = row < a.rows;
+                s_pt[tid] = ok ? (row / a.gmk) * a.gn + a.gnit[row] : 0;
+                s_cen[tid] = ok ? row / a.gk : 0;
             }
-            H0[k * FST + r] = v;
+            __syncthreads();
+            for (int e = tid; e < FBM * K0p; e += 256) {
+                const int r = e / K0p, k = e - r * K0p;
+                float v = 0.0f;
+                if (row_t + r < a.rows && k < K0) {
+                    const int64_t j = s_pt[r], c = s_cen[r];
+                    if (a.lq) {
+                        const float h = (a.x0[j * a.ld0 + k] - a.lq[c * a.ldq + k]) + (a.lb1 ? a.lb1[k] : 0.0f);
+                        v = h > 0.0f ? h : 0.0f;
+                    } else if (k < a.c0) {
+                        v = a.x0[j * a.ld0 + k] - a.gcen[c * 3 + k];
+                    } else {
+                        v = a.x1[j * a.ld1 + (k - a.c0)];
+                    }
+                }
+                H0[k * FST + r] = v;
+            }
+        } else {
+            for (int e = tid; e < FBM * K0p; e += 256) {
+                const int r = e / K0p, k = e - r * K0p;
+                const int64_t row = row_t + r;
+                float v = 0.0f;
+                if (row < a.rows) {
+                    if (k < a.c0) v = a.x0[row * a.ld0 + k];
+                    else if (k < K0) v = a.x1[row * a.ld1 + (k - a.c0)];
+                }
+                H0[k * FST + r] = v;
+            }
         }
     }
     __syncthreads();
@@ -257,9 +299,20 @@ bool fused_mlp_supported(int n_layers, const int32_t* dims, int dtype) {
 
 int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
                   int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
-                  uint32_t relu_mask, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, hipStream_t s) {
+                  uint32_t relu_mask, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, hipStream_t s,
+                  const MlpGather* g) {
     FusedArgs a{};
     a.x0 = x0; a.ld0 = ld0; a.x1 = x1; a.ld1 = ld1; a.c0 = c0; a.c1 = c1;
+    if (g) {
+        a.gnit = g->nit;
+        a.gmk = g->mk;
+        a.gn = g->n;
+        a.gk = g->k;
+        a.gcen = g->cxyz;
+        a.lq = g->q;
+        a.ldq = g->ldq;
+        a.lb1 = g->b1;
+    }
     a.rows = rows;
     a.n_layers = n_layers;
     int hmax = 16;

@@ -6,12 +6,30 @@
 
 namespace meso {
 
+// Rows of a gathered first layer, read straight from the inputs instead of
+// a materialized (centroid, neighbor) matrix.  Row r = (cloud b, centroid
+// c, neighbor k), r = (b M + c) K + k, belongs to point j = nit[r] of cloud
+// b and is
+//   q == null (conventional, PointNet++ grouping): [xyz_j - cxyz_c | feat_j]
+//   q != null (limited order): ReLU((p1_j - q_c) + b1), p1 = the x0 rows.
+struct MlpGather {
+    const int32_t* nit;   // [B * M * K]
+    int64_t mk;           // rows per cloud (M * K)
+    int64_t n;            // points per cloud
+    int k;                // rows per centroid
+    const float* cxyz;    // [B * M, 3]
+    const float* q;       // [B * M, ldq]
+    int64_t ldq;
+    const float* b1;      // nullable
+};
+
 // True when every layer input fits the fused kernel's LDS tile.
 bool fused_mlp_supported(int n_layers, const int32_t* dims, int dtype);
 
 // Whole MLP in one launch (no workspace).  pool_group > 0 zero-fills y first.
 int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
                   int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
-                  uint32_t relu_mask, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, hipStream_t s);
+                  uint32_t relu_mask, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, hipStream_t s,
+                  const MlpGather* g = nullptr);
 
 }  // namespace meso

@@ -366,18 +366,36 @@ def test_mlp_strided_input(gpu):
 # conventional module, interpolation, small entry points
 # ----------------------------------------------------------------------------
 
-@pytest.mark.parametrize("dt", [F32, BF16])
-def test_conventional_pointnet(gpu, dt):
+# (B, N, M, K, cf, hidden/output widths, dtype, feature row stride or 0):
+# fp32 rows are gathered straight from the inputs -- in the fused kernel
+# when every layer is narrow, through a split first layer otherwise -- and
+# the neighbor matrix is built only for bf16, for feature widths that are
+# not a multiple of 4, and for unaligned feature rows.
+CONV_CASES = {
+    "fused_gather": (2, 512, 128, 32, 13, [32, 48], F32, 0),
+    "fused_xyz_only": (3, 300, 70, 32, 0, [32, 64], F32, 0),
+    "fused_k20": (2, 256, 50, 20, 8, [40, 24], F32, 0),
+    "split_gather": (2, 256, 64, 32, 128, [128, 256], F32, 0),
+    "split_strided_k24": (3, 200, 45, 24, 64, [96, 160], F32, 72),
+    "nfm_width": (2, 256, 40, 16, 130, [64, 160], F32, 0),
+    "bf16": (2, 512, 128, 32, 13, [32, 48], BF16, 0),
+}
+
+
+@pytest.mark.parametrize("case", list(CONV_CASES), ids=list(CONV_CASES))
+def test_conventional_pointnet(gpu, case):
+    B, N, M, K, cf, widths, dt, ldf = CONV_CASES[case]
     rr = g(10)
-    B, N, M, K, cf = 2, 512, 128, 32, 13
     xyz = synth.mesh_surfaces(rr, B, N)
-    feat = rr.standard_normal((B, N, cf)).astype(np.float32)
+    base = rr.standard_normal((B, N, max(cf, ldf, 1))).astype(np.float32)
+    feat = np.ascontiguousarray(base[:, :, :cf]) if cf else None
     idx, cxyz = O.fps(xyz, M)
     nit, _, _ = O.ball_query(xyz, cxyz, 0.4, K)
-    Ws, bs = _weights(rr, [3 + cf, 32, 48])
+    Ws, bs = _weights(rr, [3 + cf] + widths)
     h = O.mlp(O.group_pointnet(xyz, feat, cxyz, nit), Ws, bs, bf16=dt == BF16)
-    ref = O.rowgroup_max(h.reshape(B, M * K, 48), K)
-    out = ops.conventional_module(dev(nit), ops.MLPParams(Ws, bs, dtype=dt), xyz=dev(xyz), feat=dev(feat),
+    ref = O.rowgroup_max(h.reshape(B, M * K, widths[-1]), K)
+    tf = dev(base)[:, :, :cf] if cf else None   # row stride max(cf, ldf)
+    out = ops.conventional_module(dev(nit), ops.MLPParams(Ws, bs, dtype=dt), xyz=dev(xyz), feat=tf,
                                   cxyz=dev(cxyz), grouping=0)
     assert normwise(host(out), ref) <= TOL[dt]
 
@@ -394,24 +412,41 @@ def test_conventional_edge(gpu):
     assert normwise(host(out), ref) <= 1e-4
 
 
-@pytest.mark.parametrize("C1,bias,dt", [(64, True, F32), (10, True, F32), (64, False, F32), (32, True, BF16)],
-                         ids=["vec4", "scalar_width", "no_bias", "bf16_rest"])
-def test_ltd_module_parity(gpu, C1, bias, dt):
+# (C1, remaining widths, bias, dtype, p1 row stride): fp32 first-layer rows
+# are formed in the next layer's loader -- the fused kernel when every layer
+# is narrow, the gathered GEMM otherwise -- and materialized only for bf16
+# and for widths or strides that are not a multiple of 4.
+LTD_CASES = {
+    "fused_vec4": (64, [24, 40], True, F32, 64),
+    "fused_scalar_width": (10, [24, 40], True, F32, 10),
+    "fused_no_bias": (64, [24, 40], False, F32, 64),
+    "gemm_gather": (128, [128, 256], True, F32, 128),
+    "gemm_gather_no_bias_strided": (64, [96, 160], False, F32, 72),
+    "gemm_materialized": (66, [64, 200], True, F32, 66),
+    "bf16_rest": (32, [24, 40], True, BF16, 32),
+}
+
+
+@pytest.mark.parametrize("case", list(LTD_CASES), ids=list(LTD_CASES))
+def test_ltd_module_parity(gpu, case):
     """Limited delayed aggregation (first-layer rows from p1 - q + b1, then
     the remaining layers and the max over K) against the oracle."""
+    C1, widths, bias, dt, ldp = LTD_CASES[case]
     rr = g(14)
     B, N, M, K = 2, 300, 77, 9
-    p1 = rr.standard_normal((B, N, C1)).astype(np.float32)
+    base = rr.standard_normal((B, N, ldp)).astype(np.float32)
+    p1 = np.ascontiguousarray(base[:, :, :C1])
     q = rr.standard_normal((B, M, C1)).astype(np.float32)
     b1 = rr.uniform(-0.2, 0.2, C1).astype(np.float32) if bias else None
     nit = rr.integers(0, N, size=(B, M, K)).astype(np.int32)
-    dims = [C1, 24, 40]
+    dims = [C1] + widths
     Ws, bs = _weights(rr, dims)
     h1 = O.ltd_group(p1, q, b1, nit)
     h = O.mlp(h1, Ws, bs, bf16=dt == BF16)
     ref = O.rowgroup_max(h.reshape(B, M * K, dims[-1]), K)
     p = ops.MLPParams(Ws, bs, dtype=dt)
-    out = ops.ltd_module(dev(p1), dev(q), dev(nit), p, b1=None if b1 is None else dev(b1))
+    tp = dev(base)[:, :, :C1]   # row stride ldp
+    out = ops.ltd_module(tp, dev(q), dev(nit), p, b1=None if b1 is None else dev(b1))
     assert normwise(host(out), ref) <= TOL[dt]
 
 
