@@ -180,9 +180,14 @@ int mesorasi_aggregate_max(const void* pft, int64_t ld_pft, int32_t pft_dtype, c
 
 /*
  * Conventional module, kept as the comparison path (Eq. (1); Sec. 3.1
- * "Aggregation" and "Feature Computation"): build the neighbor feature
- * matrix (NFM) in the workspace, run the MLP on every (centroid, neighbor)
- * row, and max-reduce over the K rows of each centroid.
+ * "Aggregation" and "Feature Computation"): the neighbor feature matrix
+ * (NFM), the MLP on every (centroid, neighbor) row, and the max over the
+ * K rows of each centroid.  fp32 PointNet++ grouping reads the NFM rows
+ * straight from xyz / feat through nit (inside the fused MLP kernel, or in
+ * the first layer's GEMM when cf and ld_f are multiples of 4 and feat is
+ * 16-byte aligned); otherwise (bf16, DGCNN edge grouping, other widths)
+ * the NFM is built in the workspace first.  Results agree to fp32
+ * rounding either way.
  *   grouping 0 (PointNet++): NFM row = [xyz_j - cxyz_c | feat_j], dims[0] =
  *            3 + cf; needs xyz and cxyz [B, M, 3].
  *   grouping 1 (DGCNN edge): NFM row = [f_i | f_j - f_i] with f = feat
@@ -212,9 +217,12 @@ size_t mesorasi_conventional_workspace(int64_t B, int64_t M, int32_t K, int32_t 
  *   q  = cxyz W1[:, :3]^T on the M centroids      -> [B, M, ld_q], C1 columns
  * and this call forms, for every (centroid c, neighbor k) row,
  *   h1 = ReLU(p1[b, nit[b, c, k], :] - q[b, c, :] + b1)
- * (fp32: the subtraction, then the bias) in the workspace, runs the
- * remaining layers (n_layers >= 1, dims[0] == C1) on those B*M*K rows and
- * max-reduces over the K rows of each centroid into out [B, M, ld_out].
+ * (fp32: the subtraction, then the bias), runs the remaining layers
+ * (n_layers >= 1, dims[0] == C1) on those B*M*K rows and max-reduces over
+ * the K rows of each centroid into out [B, M, ld_out].  In fp32 the h1
+ * rows are formed in the next layer's loader (fused MLP kernel, or a GEMM
+ * when C1, ld_p, ld_q are multiples of 4 and p1, q, b1, W[0] are 16-byte
+ * aligned); otherwise they are written to the workspace first.
  *   b1  [C1] float32 or NULL (no first-layer bias).
  *   nit [B, M, K] int32, per-cloud indices in [0, N).
  *   MLP arguments as in mesorasi_pointwise_mlp (last layer must have ReLU).
