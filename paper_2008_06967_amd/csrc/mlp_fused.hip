@@ -87,10 +87,37 @@ __device__ __forceinline__ void load_w8(const float* __restrict__ W, int n, int 
     }
 }
 
+// Column blocks of layer l owned by this wave: cb = wave + 4 j; blocks past
+// the layer's count repeat a valid block (discarded) so the MFMA chain stays
+// unconditional.
+template <int CB>
+__device__ __forceinline__ void layer_blocks(const FusedArgs& a, int l, int wave, int (&cbs)[CB]) {
+    const int ncb = (a.dims[l + 1] + 31) / 32;
+#pragma unroll
+    for (int j = 0; j < CB; ++j) cbs[j] = (wave + 4 * j < ncb) ? wave + 4 * j : min(wave, ncb - 1);
+}
+
+// This lane's weights of the first k-slice (k = 0 .. 15) of layer l.
+template <int CB>
+__device__ __forceinline__ void load_first_slice(const FusedArgs& a, int l, int wave, int lane, float (&w)[CB][8]) {
+    const int K = a.dims[l], N = a.dims[l + 1];
+    const float* __restrict__ W = a.W[l];
+    const bool vec = (K % 4) == 0 && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
+    int cbs[CB];
+    layer_blocks<CB>(a, l, wave, cbs);
+#pragma unroll
+    for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + (lane & 31), N, 8 * (lane >> 5), K, vec, w[j]);
+}
+
 // One layer: hin [K][FST] (LDS) x W^T -> CB column blocks of 32 per wave.
+// wb[0] holds this layer's first k-slice on entry (requested before the
+// input tile or the previous layer's epilogue, so the weights' round trip
+// overlaps that work) and the next layer's on return; the bias is requested
+// before the k loop for the same reason.
 template <int CB>
 __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const float* __restrict__ hin,
-                                            float* __restrict__ hout, int64_t row_t, int tid, int lane, int wave) {
+                                            float* __restrict__ hout, int64_t row_t, int tid, int lane, int wave,
+                                            float (&wb)[2][CB][8]) {
     const int K = a.dims[l], N = a.dims[l + 1];
     const float* __restrict__ W = a.W[l];
     const int ncb = (N + 31) / 32;
@@ -98,12 +125,15 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
     const bool vec = (K % 4) == 0 && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
     const int kh = 8 * (lane >> 5);              // this lane's half of each 16-slice
     const int cl = lane & 31;
-
-    // column blocks of this wave: cb = wave + 4 j; blocks past ncb repeat a
-    // valid block (discarded) so the MFMA chain stays unconditional
     int cbs[CB];
+    layer_blocks<CB>(a, l, wave, cbs);
+    const float* __restrict__ bias = a.bias[l];
+    float bvs[CB];
 #pragma unroll
-    for (int j = 0; j < CB; ++j) cbs[j] = (wave + 4 * j < ncb) ? wave + 4 * j : min(wave, ncb - 1);
+    for (int j = 0; j < CB; ++j) {
+        const int col = cbs[j] * 32 + cl;
+        bvs[j] = (bias && col < N) ? bias[col] : 0.0f;
+    }
 
     f32x16 acc[CB][2];
 #pragma unroll
@@ -113,9 +143,6 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[j][h][r] = 0.0f;
 
-    float wb[2][CB][8];
-#pragma unroll
-    for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + cl, N, kh, K, vec, wb[0][j]);
     const float* hrow = hin + kh * FST + cl;
 
     for (int k0 = 0; k0 < K; k0 += 32) {
@@ -124,8 +151,10 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
         for (int half = 0; half < 2; ++half) {
             const int ks = k0 + 16 * half;
             if (ks >= K) break;
+            if (ks + 16 < K) {
 #pragma unroll
-            for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + cl, N, ks + 16 + kh, K, vec, wb[half ^ 1][j]);
+                for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + cl, N, ks + 16 + kh, K, vec, wb[half ^ 1][j]);
+            }
             float av[8][2];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
@@ -144,15 +173,16 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
         }
     }
 
+    if (!last) load_first_slice<CB>(a, l + 1, wave, lane, wb[0]);
+
     // epilogue: bias + ReLU, then LDS (next layer's input) or HBM
     const bool relu = (a.relu_mask >> l) & 1u;
-    const float* __restrict__ bias = a.bias[l];
 #pragma unroll
     for (int j = 0; j < CB; ++j) {
         if (wave + 4 * j >= ncb) continue;
         const int col = cbs[j] * 32 + cl;
         const bool col_ok = col < N;
-        const float bv = (col_ok && bias) ? bias[col] : 0.0f;
+        const float bv = bvs[j];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int rbase = h * 32 + 4 * (lane >> 5);
@@ -233,6 +263,8 @@ void mlp_fused_f32_kernel(FusedArgs a) {
     float* H1 = smem + a.hsize;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t row_t = (int64_t)blockIdx.x * FBM;
+    float wb[2][CB][8];
+    load_first_slice<CB>(a, 0, wave, lane, wb[0]);
 
     // layer-0 input tile -> H0 (k-major), zero beyond c0 + c1 up to the slice edge
     {
@@ -282,7 +314,7 @@ void mlp_fused_f32_kernel(FusedArgs a) {
     for (int l = 0; l < a.n_layers; ++l) {
         const float* hin = (l & 1) ? H1 : H0;
         float* hout = (l & 1) ? H0 : H1;
-        fused_layer<CB>(a, l, hin, hout, row_t, tid, lane, wave);
+        fused_layer<CB>(a, l, hin, hout, row_t, tid, lane, wave, wb);
     }
 }
 
