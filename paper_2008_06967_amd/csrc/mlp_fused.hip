@@ -90,9 +90,21 @@ __device__ __forceinline__ void load_w8(const float* __restrict__ W, int n, int 
 // Column blocks of layer l owned by this wave: cb = wave + 4 j; blocks past
 // the layer's count repeat a valid block (discarded) so the MFMA chain stays
 // unconditional.
+// A layer of at most 64 outputs (one or two blocks) is split by rows
+// instead: wave w owns block w / 2 for the 32-row half w % 2, so no wave
+// repeats another's MFMAs.
+template <int CB>
+__device__ __forceinline__ bool row_split(const FusedArgs& a, int l) {
+    return CB == 1 && a.dims[l + 1] <= 64;
+}
+
 template <int CB>
 __device__ __forceinline__ void layer_blocks(const FusedArgs& a, int l, int wave, int (&cbs)[CB]) {
     const int ncb = (a.dims[l + 1] + 31) / 32;
+    if (row_split<CB>(a, l)) {
+        cbs[0] = min(wave >> 1, ncb - 1);
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < CB; ++j) cbs[j] = (wave + 4 * j < ncb) ? wave + 4 * j : min(wave, ncb - 1);
 }
@@ -144,6 +156,8 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
             for (int r = 0; r < 16; ++r) acc[j][h][r] = 0.0f;
 
     const float* hrow = hin + kh * FST + cl;
+    const bool split = row_split<CB>(a, l);
+    const int h0 = wave & 1;
 
     for (int k0 = 0; k0 < K; k0 += 32) {
         // two slices per trip so the double-buffered weights keep static indices
@@ -155,21 +169,33 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
 #pragma unroll
                 for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + cl, N, ks + 16 + kh, K, vec, wb[half ^ 1][j]);
             }
-            float av[8][2];
+            if (split) {
+                // this wave's 32-row half only
+                float av[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                av[i][0] = hrow[(ks + i) * FST];
-                av[i][1] = hrow[(ks + i) * FST + 32];
+                for (int i = 0; i < 8; ++i) av[i] = hrow[(ks + i) * FST + 32 * h0];
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], wb[half][0][i], acc[0][0], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            } else {
+                float av[8][2];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    av[i][0] = hrow[(ks + i) * FST];
+                    av[i][1] = hrow[(ks + i) * FST + 32];
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+#pragma unroll
+                    for (int j = 0; j < CB; ++j)
+#pragma unroll
+                        for (int h = 0; h < 2; ++h)
+                            acc[j][h] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][h], wb[half][j][i], acc[j][h], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-#pragma unroll
-                for (int j = 0; j < CB; ++j)
-#pragma unroll
-                    for (int h = 0; h < 2; ++h)
-                        acc[j][h] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][h], wb[half][j][i], acc[j][h], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
         }
     }
 
@@ -177,71 +203,77 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
 
     // epilogue: bias + ReLU, then LDS (next layer's input) or HBM
     const bool relu = (a.relu_mask >> l) & 1u;
-#pragma unroll
-    for (int j = 0; j < CB; ++j) {
-        if (wave + 4 * j >= ncb) continue;
+    // one 32-row half h of block j from accumulator v
+    auto emit = [&](const f32x16& v, int j, int h) {
         const int col = cbs[j] * 32 + cl;
         const bool col_ok = col < N;
         const float bv = bvs[j];
+        const int rbase = h * 32 + 4 * (lane >> 5);
+        if (!last) {
+            if (col_ok) {
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int rbase = h * 32 + 4 * (lane >> 5);
-            if (!last) {
-                if (col_ok) {
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        float t = acc[j][h][r] + bv;
-                        if (relu) t = t > 0.0f ? t : 0.0f;
-                        hout[col * FST + rbase + 8 * (r >> 2) + (r & 3)] = t;
-                    }
-                }
-            } else if (a.G > 0) {
-                unsigned* yu = static_cast<unsigned*>(a.y);
-                const int64_t half0 = row_t + h * 32;   // 32-row half, a multiple of 32
-                if (a.G % 32 == 0) {
-                    // the whole half lies in one group: fold its 32 rows first.
-                    // ReLU by comparison maps -0 to +0, so every folded value
-                    // has a non-negative bit pattern (unsigned atomicMax order)
-                    float m = 0.0f;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const float t = acc[j][h][r] + bv;
-                        m = fmaxf(m, t > 0.0f ? t : 0.0f);
-                    }
-                    m = fmaxf(m, __shfl_xor(m, 32));
-                    if (lane < 32 && col_ok && half0 < a.rows)
-                        atomicMax(yu + (half0 / a.G) * a.ldy + col, __float_as_uint(m));
-                } else {
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int64_t row = row_t + rbase + 8 * (r >> 2) + (r & 3);
-                        float t = acc[j][h][r] + bv;
-                        t = t > 0.0f ? t : 0.0f;   // pooling requires a final ReLU
-                        if (col_ok && row < a.rows) atomicMax(yu + (row / a.G) * a.ldy + col, __float_as_uint(t));
-                    }
-                }
-            } else {
-                const int64_t row0 = row_t + rbase;
-                if (a.out_bf16) {
-                    uint16_t* yb = static_cast<uint16_t*>(a.y) + row0 * a.ldy + col;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int dr = 8 * (r >> 2) + (r & 3);
-                        float t = acc[j][h][r] + bv;
-                        if (relu) t = t > 0.0f ? t : 0.0f;
-                        if (col_ok && row0 + dr < a.rows) yb[dr * a.ldy] = f32_to_bf16(t);
-                    }
-                } else {
-                    float* yf = static_cast<float*>(a.y) + row0 * a.ldy + col;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int dr = 8 * (r >> 2) + (r & 3);
-                        float t = acc[j][h][r] + bv;
-                        if (relu) t = t > 0.0f ? t : 0.0f;
-                        if (col_ok && row0 + dr < a.rows) yf[dr * a.ldy] = t;
-                    }
+                for (int r = 0; r < 16; ++r) {
+                    float t = v[r] + bv;
+                    if (relu) t = t > 0.0f ? t : 0.0f;
+                    hout[col * FST + rbase + 8 * (r >> 2) + (r & 3)] = t;
                 }
             }
+        } else if (a.G > 0) {
+            unsigned* yu = static_cast<unsigned*>(a.y);
+            const int64_t half0 = row_t + h * 32;   // 32-row half, a multiple of 32
+            if (a.G % 32 == 0) {
+                // the whole half lies in one group: fold its 32 rows first.
+                // ReLU by comparison maps -0 to +0, so every folded value
+                // has a non-negative bit pattern (unsigned atomicMax order)
+                float m = 0.0f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const float t = v[r] + bv;
+                    m = fmaxf(m, t > 0.0f ? t : 0.0f);
+                }
+                m = fmaxf(m, __shfl_xor(m, 32));
+                if (lane < 32 && col_ok && half0 < a.rows)
+                    atomicMax(yu + (half0 / a.G) * a.ldy + col, __float_as_uint(m));
+            } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = row_t + rbase + 8 * (r >> 2) + (r & 3);
+                    float t = v[r] + bv;
+                    t = t > 0.0f ? t : 0.0f;   // pooling requires a final ReLU
+                    if (col_ok && row < a.rows) atomicMax(yu + (row / a.G) * a.ldy + col, __float_as_uint(t));
+                }
+            }
+        } else {
+            const int64_t row0 = row_t + rbase;
+            if (a.out_bf16) {
+                uint16_t* yb = static_cast<uint16_t*>(a.y) + row0 * a.ldy + col;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int dr = 8 * (r >> 2) + (r & 3);
+                    float t = v[r] + bv;
+                    if (relu) t = t > 0.0f ? t : 0.0f;
+                    if (col_ok && row0 + dr < a.rows) yb[dr * a.ldy] = f32_to_bf16(t);
+                }
+            } else {
+                float* yf = static_cast<float*>(a.y) + row0 * a.ldy + col;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int dr = 8 * (r >> 2) + (r & 3);
+                    float t = v[r] + bv;
+                    if (relu) t = t > 0.0f ? t : 0.0f;
+                    if (col_ok && row0 + dr < a.rows) yf[dr * a.ldy] = t;
+                }
+            }
+        }
+    };
+    if (split) {
+        if ((wave >> 1) < ncb) emit(acc[0][0], 0, h0);
+    } else {
+#pragma unroll
+        for (int j = 0; j < CB; ++j) {
+            if (wave + 4 * j >= ncb) continue;
+            emit(acc[j][0], j, 0);
+            emit(acc[j][1], j, 1);
         }
     }
     if (!last) {
@@ -252,11 +284,12 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
     __syncthreads();
 }
 
-// One 32-column block per wave (outputs up to 128 wide); the register budget
-// leaves room for three workgroups per CU, which hide each other's memory
-// latency.  (Wider outputs measured slower than the per-layer GEMMs.)
+// One 32-column block per wave (outputs up to 128 wide), or one block and
+// row half for layers of at most 64 outputs; two workgroups per CU (with a
+// three-workgroup register budget the row-split epilogue spilled).  (Wider
+// outputs measured slower than the per-layer GEMMs.)
 template <int CB>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 void mlp_fused_f32_kernel(FusedArgs a) {
     extern __shared__ float smem[];
     float* H0 = smem;
