@@ -145,7 +145,7 @@ int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query, int64_t l
  *         c0 + c1, a width < 1, ld_y < dims[n], rows % G != 0;
  *         EUNSUPPORTED for n_layers outside [1, MESORASI_MAX_LAYERS], a width
  *         above MESORASI_MAX_WIDTH, pooling without a final ReLU or with
- *         out_dtype BF16;  EWORKSPACE when ws is too small.
+ *         out_dtype BF16, G > 2^31 - 1;  EWORKSPACE when ws is too small.
  */
 int mesorasi_pointwise_mlp(const float* x0, int32_t c0, int64_t ld0, const float* x1, int32_t c1, int64_t ld1,
                            int64_t rows, int32_t n_layers, const int32_t* dims, const void* const* W,

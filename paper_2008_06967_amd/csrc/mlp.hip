@@ -1154,6 +1154,7 @@ extern "C" int mesorasi_pointwise_mlp(const float* x0, int32_t c0, int64_t ld0, 
     MESO_REQUIRE(out_dtype == MESORASI_F32 || out_dtype == MESORASI_BF16, MESORASI_EUNSUPPORTED, "%s: out_dtype %d",
                  who, out_dtype);
     MESO_REQUIRE(pool_group >= 0, MESORASI_EINVAL, "%s: pool_group < 0", who);
+    MESO_REQUIRE(pool_group <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: pool_group > 2^31 - 1", who);
     if (pool_group > 0) {
         MESO_REQUIRE(rows % pool_group == 0, MESORASI_EINVAL, "%s: rows %% pool_group != 0", who);
         MESO_REQUIRE((relu_mask >> (n_layers - 1)) & 1u, MESORASI_EUNSUPPORTED, "%s: pooling needs a final ReLU", who);

@@ -30,6 +30,7 @@ namespace {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int FBM = 64;        // rows per workgroup (two 32-row halves)
+constexpr int kOutF32 = 0, kOutBf16 = 1, kOutPool = 2;   // last layer: store fp32 / bf16, or pooled max
 constexpr int FST = FBM + 1;   // k-major activation stride (odd: conflict-free)
 constexpr int kMaxIn = 160;    // widest layer input kept in LDS (padded to 16)
 constexpr int kMaxOut = 128;   // widest layer output: 4 column blocks, one per wave
@@ -126,7 +127,7 @@ __device__ __forceinline__ void load_first_slice(const FusedArgs& a, int l, int 
 // input tile or the previous layer's epilogue, so the weights' round trip
 // overlaps that work) and the next layer's on return; the bias is requested
 // before the k loop for the same reason.
-template <int CB>
+template <int CB, int OUT>
 __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const float* __restrict__ hin,
                                             float* __restrict__ hout, int64_t row_t, int tid, int lane, int wave,
                                             float (&wb)[2][CB][8]) {
@@ -218,7 +219,7 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
                     hout[col * FST + rbase + 8 * (r >> 2) + (r & 3)] = t;
                 }
             }
-        } else if (a.G > 0) {
+        } else if constexpr (OUT == kOutPool) {
             unsigned* yu = static_cast<unsigned*>(a.y);
             const int64_t half0 = row_t + h * 32;   // 32-row half, a multiple of 32
             if (a.G % 32 == 0) {
@@ -235,17 +236,24 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
                 if (lane < 32 && col_ok && half0 < a.rows)
                     atomicMax(yu + (half0 / a.G) * a.ldy + col, __float_as_uint(m));
             } else {
+                // groups of this lane's rows: one 64-bit division for the
+                // half, then small 32-bit quotients (offsets below G + 32)
+                const int64_t rl = row_t + rbase;
+                const int64_t g0 = rl / a.G;
+                const int off0 = (int)(rl - g0 * a.G);
+                const int G = (int)a.G;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int64_t row = row_t + rbase + 8 * (r >> 2) + (r & 3);
+                    const int dr = 8 * (r >> 2) + (r & 3);
                     float t = v[r] + bv;
                     t = t > 0.0f ? t : 0.0f;   // pooling requires a final ReLU
-                    if (col_ok && row < a.rows) atomicMax(yu + (row / a.G) * a.ldy + col, __float_as_uint(t));
+                    const int64_t grp = g0 + (unsigned)(off0 + dr) / (unsigned)G;
+                    if (col_ok && rl + dr < a.rows) atomicMax(yu + grp * a.ldy + col, __float_as_uint(t));
                 }
             }
         } else {
             const int64_t row0 = row_t + rbase;
-            if (a.out_bf16) {
+            if constexpr (OUT == kOutBf16) {
                 uint16_t* yb = static_cast<uint16_t*>(a.y) + row0 * a.ldy + col;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
@@ -288,7 +296,7 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
 // row half for layers of at most 64 outputs; two workgroups per CU (with a
 // three-workgroup register budget the row-split epilogue spilled).  (Wider
 // outputs measured slower than the per-layer GEMMs.)
-template <int CB>
+template <int CB, bool GATHER, int OUT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 void mlp_fused_f32_kernel(FusedArgs a) {
     extern __shared__ float smem[];
@@ -302,7 +310,7 @@ void mlp_fused_f32_kernel(FusedArgs a) {
     // layer-0 input tile -> H0 (k-major), zero beyond c0 + c1 up to the slice edge
     {
         const int K0 = a.c0 + a.c1, K0p = pad16(K0);
-        if (a.gnit) {
+        if constexpr (GATHER) {
             // gathered rows: each row's input point and centroid once, then
             // the element loop reads them from LDS
             __shared__ int64_t s_pt[FBM], s_cen[FBM];
@@ -347,7 +355,7 @@ void mlp_fused_f32_kernel(FusedArgs a) {
     for (int l = 0; l < a.n_layers; ++l) {
         const float* hin = (l & 1) ? H1 : H0;
         float* hout = (l & 1) ? H0 : H1;
-        fused_layer<CB>(a, l, hin, hout, row_t, tid, lane, wave, wb);
+        fused_layer<CB, OUT>(a, l, hin, hout, row_t, tid, lane, wave, wb);
     }
 }
 
@@ -398,7 +406,20 @@ int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1,
         const int rc = zero_rows_f32(static_cast<float*>(y), rows / pool_group, dims[n_layers], ld_y, s);
         if (rc != MESORASI_OK) return rc;
     }
-    mlp_fused_f32_kernel<1><<<dim3((unsigned)ceil_div(rows, FBM)), dim3(256), lds, s>>>(a);
+    // one instantiation per input and output form keeps each launch's code
+    // (and its instruction-cache footprint) to the path it runs
+    const dim3 grid((unsigned)ceil_div(rows, FBM)), block(256);
+    const bool gather = g != nullptr;
+    if (pool_group > 0) {
+        if (gather) mlp_fused_f32_kernel<1, true, kOutPool><<<grid, block, lds, s>>>(a);
+        else mlp_fused_f32_kernel<1, false, kOutPool><<<grid, block, lds, s>>>(a);
+    } else if (a.out_bf16) {
+        if (gather) mlp_fused_f32_kernel<1, true, kOutBf16><<<grid, block, lds, s>>>(a);
+        else mlp_fused_f32_kernel<1, false, kOutBf16><<<grid, block, lds, s>>>(a);
+    } else {
+        if (gather) mlp_fused_f32_kernel<1, true, kOutF32><<<grid, block, lds, s>>>(a);
+        else mlp_fused_f32_kernel<1, false, kOutF32><<<grid, block, lds, s>>>(a);
+    }
     return after_launch("mesorasi_pointwise_mlp (fused)");
 }
 
