@@ -303,19 +303,24 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, i
             if (lane < 32 && col_ok) atomicMax(yu + (row0 / a.G) * a.ldy + col, __float_as_uint(m));
             return;
         }
+        // this lane's rows rbase + d (d < 32): one 64-bit division, then
+        // 32-bit quotients of offsets below G + 32 (the caller keeps G < 2^31)
+        const int64_t gb = rbase / a.G;
+        const unsigned ob = (unsigned)(rbase - gb * a.G), G = (unsigned)a.G;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int64_t r0 = rbase + 8 * q;  // rows r0 .. r0 + 3 in registers 4q .. 4q+3
             if (!col_ok || r0 >= a.rows) continue;
-            const int64_t g0 = r0 / a.G;
-            const int64_t rl = (r0 + 3 < a.rows) ? r0 + 3 : a.rows - 1;
-            if (rl / a.G == g0) {
+            const unsigned o = ob + 8 * q;
+            const int nr = r0 + 3 < a.rows ? 4 : (int)(a.rows - r0);
+            const int64_t g0 = gb + o / G;
+            if (gb + (o + nr - 1) / G == g0) {
                 float m = v[4 * q];
-                for (int i = 1; i < 4 && r0 + i < a.rows; ++i) m = fmaxf(m, v[4 * q + i]);
+                for (int i = 1; i < nr; ++i) m = fmaxf(m, v[4 * q + i]);
                 atomicMax(yu + g0 * a.ldy + col, __float_as_uint(m));
             } else {
-                for (int i = 0; i < 4 && r0 + i < a.rows; ++i)
-                    atomicMax(yu + ((r0 + i) / a.G) * a.ldy + col, __float_as_uint(v[4 * q + i]));
+                for (int i = 0; i < nr; ++i)
+                    atomicMax(yu + (gb + (o + i) / G) * a.ldy + col, __float_as_uint(v[4 * q + i]));
             }
         }
     } else {
