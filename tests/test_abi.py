@@ -92,6 +92,9 @@ def test_mlp_validation_and_workspace():
         _lib.EUNSUPPORTED
     # rows % pool_group
     assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 128, 3, FAKE, 1 << 20, NULL) == _lib.EINVAL
+    # pool groups are limited to 2^31 - 1 rows
+    assert st(f, FAKE, 3, 3, NULL, 0, 0, 1 << 32, 3, d, W, b, 7, 0, 0, FAKE, 128, 1 << 32, FAKE, 1 << 20, NULL) == \
+        _lib.EUNSUPPORTED
     # narrow fp32 MLPs run fused and need no workspace; wide ones run layer by layer
     assert L.mesorasi_pointwise_mlp_workspace(10, 3, d, 0, 0) == 0
     dw, Ww, bw = _mlp_args([3, 200, 200, 256])
