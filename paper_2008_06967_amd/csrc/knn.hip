@@ -17,6 +17,8 @@
 // over the 3 nearest coarse points (the three_interpolate kernel of the
 // PointNet++ segmentation baseline, Sec. 6 "Software Setup"); layout at the
 // kernel.
+#include <type_traits>
+
 #include "common.h"
 
 namespace meso {
@@ -423,7 +425,10 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __
 // for any summation order inside the MFMA (products rounded or not), so
 // |a - d| <= (4C + 12) u (|x|^2 + |y|^2) to first order; eps below takes
 // twice that, plus C * 2^-120 for flushed denormal products, with the
-// computed norms.  Then lower = a - eps <= d <= a + eps = upper, and:
+// computed norms.  For C <= 64 the table keeps a rounded to bf16 (a' =
+// a(1 + r), |r| <= 2^-8) and the bounds widen by 2^-7 |a'| >= |a' - a|,
+// so lower = a' - eps - 2^-7 |a'| <= d <= a' + eps + 2^-7 |a'| = upper
+// (fp32 table and no extra term for wider C), and:
 //  1. tau = the K-th smallest of the 64 lane minima of upper: K distinct
 //     references have d <= tau, so every reference of the exact top K has
 //     d <= tau, hence lower <= tau;
@@ -434,12 +439,33 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __
 // takes reference blocks w, w + 8, ...: its 32 x 32 Gram block from
 // registers (query rows fixed, reference rows streamed from global memory,
 // the k order of each operand split in two halves like the GEMM), turned
-// into a and stored to a 32 x 1032 LDS table.  Phase 2: wave w selects
-// for queries 4w .. 4w + 3, reading 4 references per lane per 16-byte read.
-constexpr int kKnnMfmaLda = 1024 + 8;          // a-table row stride (words)
+// into a and stored to a 32 x 1032 LDS table: bf16 for C <= 64 (66 KB, so
+// two workgroups fit a CU and one's Gram MFMAs overlap the other's
+// selection), fp32 above (one workgroup per CU either way, and the bf16
+// margin only added candidates).  Phase 2: wave w selects for queries
+// 4w .. 4w + 3, reading 4 references per lane per 8- or 16-byte read; its
+// candidate list reuses the reference-norm buffer once every wave holds
+// its norms in registers.
+constexpr int kKnnMfmaLda = 1024 + 8;          // a-table row stride (entries)
 constexpr int kKnnMfmaMaxN = 1024;
 
 typedef float knn_f32x16 __attribute__((ext_vector_type(16)));
+
+// Four consecutive table entries as float (bf16 or fp32 table).
+__device__ __forceinline__ void load_bounds4(const uint16_t* p, float (&a)[4]) {
+    const uint2 v = *reinterpret_cast<const uint2*>(p);
+    a[0] = bf16_to_f32(v.x & 0xffffu);
+    a[1] = bf16_to_f32(v.x >> 16);
+    a[2] = bf16_to_f32(v.y & 0xffffu);
+    a[3] = bf16_to_f32(v.y >> 16);
+}
+__device__ __forceinline__ void load_bounds4(const float* p, float (&a)[4]) {
+    const float4 v = *reinterpret_cast<const float4*>(p);
+    a[0] = v.x;
+    a[1] = v.y;
+    a[2] = v.z;
+    a[3] = v.w;
+}
 
 template <int CH>   // maximum C / 2 (32 or 64)
 __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* __restrict__ ref, int64_t ldr,
@@ -447,14 +473,16 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
                                                                   int N, int M, int C, int K, int qblocks,
                                                                   int32_t* __restrict__ nit,
                                                                   float* __restrict__ dist) {
+    constexpr bool BF = CH <= 32;                        // bf16 table
+    using TabT = std::conditional_t<BF, uint16_t, float>;
     extern __shared__ float smem[];
-    float* sA = smem;                                    // [32][kKnnMfmaLda]
+    TabT* sA = reinterpret_cast<TabT*>(smem);            // [32][kKnnMfmaLda] bounds
     const int CQ = C + 4;                                // query row stride: 16-byte lane reads of
                                                          // 32 rows land on distinct bank groups
-    float* sQ = sA + kKnnQpb * kKnnMfmaLda;              // [32][CQ]
+    float* sQ = smem + kKnnQpb * kKnnMfmaLda * sizeof(TabT) / sizeof(float);   // [32][CQ]
     float* sNy = sQ + kKnnQpb * CQ;                      // [1024]
     float* sNx = sNy + kKnnMfmaMaxN;                     // [32]
-    int* sCj = reinterpret_cast<int*>(sNx + kKnnQpb);    // [kKnnWaves][4][64]
+    uint16_t* sCj = reinterpret_cast<uint16_t*>(sNy);    // [kKnnWaves][4][64], after the norms are read
     const int64_t b = blockIdx.x / qblocks;
     const int q0 = (blockIdx.x % qblocks) * kKnnQpb;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -514,7 +542,9 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int i = 8 * (r >> 2) + 4 * half + (r & 3);
-            sA[i * kKnnMfmaLda + j] = valid ? __builtin_fmaf(-2.0f, acc[r], sNx[i] + ny) : inf;
+            const float av = valid ? __builtin_fmaf(-2.0f, acc[r], sNx[i] + ny) : inf;
+            if constexpr (BF) sA[i * kKnnMfmaLda + j] = f32_to_bf16(av);
+            else sA[i * kKnnMfmaLda + j] = av;
         }
     };
     if constexpr (CH <= 32) {
@@ -551,7 +581,8 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
         const float4 v = *reinterpret_cast<const float4*>(sNy + 256 * t + 4 * lane);
         nyv[4 * t] = v.x; nyv[4 * t + 1] = v.y; nyv[4 * t + 2] = v.z; nyv[4 * t + 3] = v.w;
     }
-    int* cjw = sCj + wave * (kKnnQpw * 64);   // [4][64] candidate indices of this wave
+    __syncthreads();   // every wave holds its norms: sNy becomes the candidate lists
+    uint16_t* cjw = sCj + wave * (kKnnQpw * 64);   // [4][64] candidate indices of this wave
     int total[kKnnQpw];
     float tau[kKnnQpw];
 #pragma unroll
@@ -562,12 +593,12 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
         float mn = inf;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            const float4 v = *reinterpret_cast<const float4*>(sA + i * kKnnMfmaLda + 256 * t + 4 * lane);
-            const float av4[4] = {v.x, v.y, v.z, v.w};
+            float av4[4];
+            load_bounds4(sA + i * kKnnMfmaLda + 256 * t + 4 * lane, av4);
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const bool valid = 256 * t + 4 * lane + u < N;
-                const float e = __builtin_fmaf(kappa, nxq + nyv[4 * t + u], tiny);
+                const float e = __builtin_fmaf(kappa, nxq + nyv[4 * t + u], tiny) + (BF ? 0x1p-7f * fabsf(av4[u]) : 0.0f);
                 const float up = valid ? av4[u] + e : inf;
                 lo[4 * t + u] = av4[u] - e;
                 mn = fminf(mn, up);
@@ -588,7 +619,7 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
         if (tot <= 64) {
 #pragma unroll
             for (int t = 0; t < 16; ++t)
-                if (slot[t] >= 0) cjw[qq * 64 + slot[t]] = 256 * (t >> 2) + 4 * lane + (t & 3);
+                if (slot[t] >= 0) cjw[qq * 64 + slot[t]] = (uint16_t)(256 * (t >> 2) + 4 * lane + (t & 3));
         }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -651,26 +682,27 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
         int t2 = 0;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            const float4 v = *reinterpret_cast<const float4*>(sA + i * kKnnMfmaLda + 256 * t + 4 * lane);
-            const float av4[4] = {v.x, v.y, v.z, v.w};
+            float av4[4];
+            load_bounds4(sA + i * kKnnMfmaLda + 256 * t + 4 * lane, av4);
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int j = 256 * t + 4 * lane + u;
-                const float e = __builtin_fmaf(kappa, nxq + nyv[4 * t + u], tiny);
+                const float e = __builtin_fmaf(kappa, nxq + nyv[4 * t + u], tiny) + (BF ? 0x1p-7f * fabsf(av4[u]) : 0.0f);
                 const bool c = j < N && !(av4[u] - e > tau[qq]);
                 const uint64_t m = ballot(c);
                 slot[4 * t + u] = c ? t2 + mask_rank(m) : -1;
                 t2 += __builtin_popcountll(m);
             }
         }
-        int* cj = cjw + qq * 64;
+        uint16_t* cj = cjw + qq * 64;
         const float* qrow = sQ + i * CQ;
         float td = inf;
         int tj = 0x7fffffff;
         for (int base = 0; base < tot; base += 64) {
 #pragma unroll
             for (int t = 0; t < 16; ++t)
-                if (slot[t] >= base && slot[t] < base + 64) cj[slot[t] - base] = 256 * (t >> 2) + 4 * lane + (t & 3);
+                if (slot[t] >= base && slot[t] < base + 64)
+                    cj[slot[t] - base] = (uint16_t)(256 * (t >> 2) + 4 * lane + (t & 3));
             __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
             const bool have = lane < tot - base;
             const int jj = have ? cj[lane] : 0;
@@ -912,8 +944,11 @@ extern "C" int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query
     const size_t lds_reg = lds + sizeof(float) * 2 * 64 * kKnnWaves;
     const bool mfma = N <= kKnnMfmaMaxN && C >= 32 && C % 8 == 0 && ld_ref % 4 == 0 && aligned(ref, 16);
     if (mfma) {
-        const size_t lds_m = sizeof(float) * ((size_t)kKnnQpb * kKnnMfmaLda + (size_t)kKnnQpb * (C + 4) +
-                                              kKnnMfmaMaxN + kKnnQpb + 64 * kKnnQpw * kKnnWaves);
+        // bounds table (bf16 for C <= 64), query rows, reference norms
+        // (later the candidate lists), query norms: 79 KB at C = 64, so two
+        // workgroups per CU
+        const size_t lds_m = (C <= 64 ? sizeof(uint16_t) : sizeof(float)) * (size_t)kKnnQpb * kKnnMfmaLda +
+                             sizeof(float) * ((size_t)kKnnQpb * (C + 4) + kKnnMfmaMaxN + kKnnQpb);
         if (C <= 64) {
             static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&knn_mfma_kernel<32>),
                                                                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
