@@ -251,11 +251,13 @@ template <int NT>
 __global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __restrict__ ref, int64_t ldr,
                                                                  const float* __restrict__ query, int64_t ldq,
                                                                  int N, int M, int C, int Cs, int K, int qblocks,
-                                                                 int vec4, int32_t* __restrict__ nit,
+                                                                 int vec4, int whole, int32_t* __restrict__ nit,
                                                                  float* __restrict__ dist) {
+    // whole: the cloud's every reference row is staged once (sR holds NT
+    // tiles), instead of one tile per round trip and two barriers
     extern __shared__ float smem[];
-    float* sR = smem;                                    // [kKnnTile][Cs]
-    float* sQ = smem + kKnnTile * Cs;                    // [kKnnQpb][C]
+    float* sR = smem;                                    // [kKnnTile or NT * kKnnTile][Cs]
+    float* sQ = smem + (whole ? NT : 1) * kKnnTile * Cs; // [kKnnQpb][C]
     float* sCd = sQ + kKnnQpb * C;                       // [kKnnWaves][64] candidate distances
     int* sCj = reinterpret_cast<int*>(sCd + kKnnWaves * 64);   // [kKnnWaves][64] candidate indices
     const int64_t b = blockIdx.x / qblocks;
@@ -270,6 +272,13 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __
         sQ[e] = qi < M ? query[(b * M + qi) * ldq + c] : 0.0f;
     }
 
+    if (whole) {
+        for (int e = tid; e < N * C; e += 64 * kKnnWaves) {
+            const int r = e / C, c = e - r * C;
+            sR[r * Cs + c] = ref[(b * N + r) * ldr + c];
+        }
+    }
+
     // 1. all distances, in the channel order of the oracle
     float d[kKnnQpw][NT];
 #pragma unroll
@@ -278,6 +287,9 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __
         for (int qq = 0; qq < kKnnQpw; ++qq) d[qq][t] = inf;
         if (t < nt) {
             const int t0 = t * kKnnTile;
+            if (whole) {
+                if (t == 0) __syncthreads();
+            } else {
             __syncthreads();
             if (vec4) {
                 const int C4 = C >> 2;
@@ -296,10 +308,13 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_reg_kernel(const float* __
                 }
             }
             __syncthreads();
+            }
             float a[kKnnQpw];
 #pragma unroll
             for (int qq = 0; qq < kKnnQpw; ++qq) a[qq] = 0.0f;
-            const float* rr = sR + lane * Cs;
+            // rows past N in the last whole-cloud tile are never staged:
+            // their distances are discarded below
+            const float* rr = sR + ((whole ? t0 : 0) + lane) * Cs;
             const float* qb = sQ + wave * kKnnQpw * C;
             if (vec4) {
                 for (int c = 0; c < C; c += 4) {
@@ -962,16 +977,23 @@ extern "C" int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query
             knn_mfma_kernel<64><<<grid, block, lds_m, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, K, qblocks,
                                                            nit, dist);
         }
-    } else if (N <= 4 * kKnnTile)
-        knn_reg_kernel<4><<<grid, block, lds_reg, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks,
-                                                       vec4, nit, dist);
-    else if (N <= 8 * kKnnTile)
-        knn_reg_kernel<8><<<grid, block, lds_reg, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks,
-                                                       vec4, nit, dist);
-    else if (N <= 16 * kKnnTile)
-        knn_reg_kernel<16><<<grid, block, lds_reg, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K,
-                                                        qblocks, vec4, nit, dist);
-    else
+    } else if (N <= 16 * kKnnTile) {
+        // a cloud of at most 32 KB is staged whole (one round trip instead of
+        // one per 64-row tile)
+        const int nt_k = N <= 4 * kKnnTile ? 4 : N <= 8 * kKnnTile ? 8 : 16;
+        const size_t whole_rows = sizeof(float) * (size_t)nt_k * kKnnTile * Cs;
+        const int whole = whole_rows <= 32 * 1024 ? 1 : 0;
+        const size_t l = lds_reg + (whole ? whole_rows - sizeof(float) * (size_t)kKnnTile * Cs : 0);
+        if (nt_k == 4)
+            knn_reg_kernel<4><<<grid, block, l, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks,
+                                                     vec4, whole, nit, dist);
+        else if (nt_k == 8)
+            knn_reg_kernel<8><<<grid, block, l, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks,
+                                                     vec4, whole, nit, dist);
+        else
+            knn_reg_kernel<16><<<grid, block, l, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks,
+                                                      vec4, whole, nit, dist);
+    } else
         knn_kernel<<<grid, block, lds, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, Cs, K, qblocks, vec4, nit,
                                             dist);
     return after_launch("mesorasi_knn");
