@@ -364,14 +364,18 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, i
 // the epilogue (same sum, different order).  A gathered split layer (the
 // conventional module's first layer) takes its rows through the neighbor
 // index table, so the neighbor feature matrix is never written to memory.
-template <int BM, int BN, int BK, int EPI, bool FAST_A, bool FAST_W, bool SPLIT = false, bool LTD = false>
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
+template <int BM, int BN, int BK, int EPI, bool FAST_A, bool FAST_W, bool SPLIT = false, bool LTD = false,
+          int NW = 4>
+__global__ __launch_bounds__(64 * NW) void gemm_f32_kernel(GemmArgs a) {
     static_assert(!SPLIT || FAST_A, "the split form reads x1 as a fast source");
     static_assert(!LTD || (FAST_A && FAST_W && !SPLIT), "the limited-order gather reads one fast source");
-    constexpr int TM = BM / 64, TN = BN / 64;
+    constexpr int NTHR = 64 * NW;            // waves in a (NW / 2) x 2 grid, WRM x WRN each
+    constexpr int WRM = BM / (NW / 2), WRN = BN / 2;
+    constexpr int TM = WRM / 32, TN = WRN / 32;
     constexpr int LW = BK + kPadF;           // LDS row stride in words
     constexpr int CPR = BK / 4;              // 16-byte chunks per tile row
-    constexpr int QA = BM * CPR / 256, QB = BN * CPR / 256;   // chunks per thread per slice
+    static_assert(WRM == 64 || NW == 4, "8-wave tiles give each wave 64 rows");
+    constexpr int QA = BM * CPR / NTHR, QB = BN * CPR / NTHR;   // chunks per thread per slice
     constexpr int HK = BK / 2;               // k per lane per slice
     static_assert(QA >= 1 && QB >= 1 && HK % 4 == 0, "tile shape");
     __shared__ __attribute__((aligned(16))) float As[2][BM * LW];
@@ -388,7 +392,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
         // x0 rows of this tile and the matching weight columns (zero past
         // cc, rows or N); read after the first barrier below
         const float* Wf = static_cast<const float*>(a.W) - a.cc;
-        for (int e = tid; e < BM * 4; e += 256) {
+        for (int e = tid; e < BM * 4; e += NTHR) {
             const int64_t r = row_t + (e >> 2);
             const int i = e & 3;
             float v = 0.0f;
@@ -398,7 +402,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
             }
             sXc[e] = v;
         }
-        for (int e = tid; e < BN * 4; e += 256) {
+        for (int e = tid; e < BN * 4; e += NTHR) {
             const int n = col_t + (e >> 2);
             const int i = e & 3;
             sWc[e] = (i < a.cc && n < a.N) ? Wf[(int64_t)n * ldw + i] : 0.0f;
@@ -406,9 +410,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     }
     const int k_lo = blockIdx.z * a.kc;
     const int k_hi = min(a.K, k_lo + a.kc);
-    // chunk c = tid + 256 p covers tile row c / CPR, words 4 (c % CPR) .. +3
+    // chunk c = tid + NTHR p covers tile row c / CPR, words 4 (c % CPR) .. +3
     const int crow = tid / CPR, ck = 4 * (tid % CPR);
-    constexpr int RSTEP = 256 / CPR;         // tile rows between a thread's chunks
+    constexpr int RSTEP = NTHR / CPR;        // tile rows between a thread's chunks
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -499,7 +503,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
         float av[TM][HK], bv[TN][HK];
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
-            const float* src = &As[buf][(wm * (BM / 2) + i * 32 + (lane & 31)) * LW + hk];
+            const float* src = &As[buf][(wm * WRM + i * 32 + (lane & 31)) * LW + hk];
 #pragma unroll
             for (int q = 0; q < HK / 4; ++q) {
                 const float4 u = reinterpret_cast<const float4*>(src)[q];
@@ -508,7 +512,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
         }
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const float* src = &Bs[buf][(wn * (BN / 2) + j * 32 + (lane & 31)) * LW + hk];
+            const float* src = &Bs[buf][(wn * WRN + j * 32 + (lane & 31)) * LW + hk];
 #pragma unroll
             for (int q = 0; q < HK / 4; ++q) {
                 const float4 u = reinterpret_cast<const float4*>(src)[q];
@@ -555,13 +559,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
             float4 wc[TN];
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                wc[j] = *reinterpret_cast<const float4*>(&sWc[(wn * (BN / 2) + j * 32 + (lane & 31)) * 4]);
+                wc[j] = *reinterpret_cast<const float4*>(&sWc[(wn * WRN + j * 32 + (lane & 31)) * 4]);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const float4 xr = *reinterpret_cast<const float4*>(
-                        &sXc[(wm * (BM / 2) + i * 32 + 4 * (lane >> 5) + 8 * (r >> 2) + (r & 3)) * 4]);
+                        &sXc[(wm * WRM + i * 32 + 4 * (lane >> 5) + 8 * (r >> 2) + (r & 3)) * 4]);
 #pragma unroll
                     for (int j = 0; j < TN; ++j) {
                         float t = acc[i][j][r];
@@ -578,7 +582,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-            epilogue<EPI, false>(a, acc[i][j], row_t + wm * (BM / 2) + i * 32, col_t + wn * (BN / 2) + j * 32, lane);
+            epilogue<EPI, false>(a, acc[i][j], row_t + wm * WRM + i * 32, col_t + wn * WRN + j * 32, lane);
 }
 
 // bf16 MFMA GEMM, same structure with k-slices of 32 and row-major LDS
@@ -901,6 +905,14 @@ static void launch_tile(const GemmArgs& a, bool bf16, bool fast_a, bool fast_w, 
 
 template <int EPI>
 static void launch_epi(const GemmArgs& a, const LayerPlan& pl, bool bf16, bool fast_a, bool fast_w, hipStream_t s) {
+    if (pl.bm == 128 && pl.bn == 128 && pl.splits == 1 && !bf16 && fast_a && fast_w && a.cc == 0 && !a.lq &&
+        ceil_div(a.rows, 256) * ceil_div(a.N, 128) >= kTargetTiles) {
+        // enough rows for a full wave of 256 x 128 tiles: eight waves, two
+        // per SIMD, share each staged B slice over twice the rows
+        const dim3 g8((unsigned)ceil_div(a.rows, 256), (unsigned)ceil_div(a.N, 128), 1);
+        gemm_f32_kernel<256, 128, 32, EPI, true, true, false, false, 8><<<g8, dim3(512), 0, s>>>(a);
+        return;
+    }
     const dim3 grid((unsigned)ceil_div(a.rows, pl.bm), (unsigned)ceil_div(a.N, pl.bn), (unsigned)pl.splits);
     if (pl.bm == 128 && pl.bn == 128) launch_tile<128, 128, EPI>(a, bf16, fast_a, fast_w, grid, s);
     else if (pl.bm == 128) launch_tile<128, 64, EPI>(a, bf16, fast_a, fast_w, grid, s);

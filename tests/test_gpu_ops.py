@@ -278,6 +278,8 @@ MLP_CASES = [
     ("width_max", 40, [4096], [4096, 64], F32),       # the documented maximum width (skinny path)
     ("width_max_gemm", 200, [4096], [4096, 64], F32), # the same on the tiled GEMM path
     ("depth_max", 100, [16], [32] * 8, F32),          # the documented maximum depth
+    # a full wave of 256 x 128 tiles (eight-wave kernel), ragged rows and columns
+    ("many_rows_wide", 8525, [64], [1000, 384], F32),
 ]
 
 
@@ -318,6 +320,18 @@ def test_mlp_pooled(gpu, dt, G):
     p = ops.MLPParams(Ws, bs, dtype=dt)
     y = ops.pointwise_mlp(dev(x), p, pool_group=G)
     assert normwise(host(y).reshape(groups, 80), ref.reshape(groups, 80)) <= TOL[dt]
+
+
+def test_mlp_pooled_many_rows(gpu):
+    """Per-point 1x1 convolution with the max over each cloud fused, at a
+    row count that fills the chip with 256 x 128 tiles."""
+    rr = g(12)
+    G, groups = 1024, 9
+    x = rr.standard_normal((G * groups, 96)).astype(np.float32)
+    Ws, bs = _weights(rr, [96, 1024])
+    ref = O.rowgroup_max(O.mlp(x, Ws, bs).reshape(groups, G, 1024), G)
+    y = ops.pointwise_mlp(dev(x), ops.MLPParams(Ws, bs), pool_group=G)
+    assert normwise(host(y).reshape(groups, 1024), ref.reshape(groups, 1024)) <= 1e-4
 
 
 @pytest.mark.parametrize("G", [32, 16])
