@@ -374,7 +374,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_f32_kernel(GemmArgs a) {
     constexpr int TM = WRM / 32, TN = WRN / 32;
     constexpr int LW = BK + kPadF;           // LDS row stride in words
     constexpr int CPR = BK / 4;              // 16-byte chunks per tile row
-    static_assert(WRM == 64 || NW == 4, "8-wave tiles give each wave 64 rows");
+    static_assert(WRM % 32 == 0 && WRN % 32 == 0, "whole 32 x 32 MFMA blocks per wave");
     constexpr int QA = BM * CPR / NTHR, QB = BN * CPR / NTHR;   // chunks per thread per slice
     constexpr int HK = BK / 2;               // k per lane per slice
     static_assert(QA >= 1 && QB >= 1 && HK % 4 == 0, "tile shape");
@@ -498,36 +498,39 @@ __global__ __launch_bounds__(64 * NW) void gemm_f32_kernel(GemmArgs a) {
                 okb[p] ? make_float4(rb[p][0], rb[p][1], rb[p][2], rb[p][3]) : make_float4(0.f, 0.f, 0.f, 0.f);
     };
     const int hk = HK * (lane >> 5);
-    // operands of one slice into registers, then its MFMAs
+    // A slice is consumed in groups of four k steps: the operand reads of
+    // group q + 1 are issued before the MFMAs of group q, so only the first
+    // group's LDS latency is exposed (all waves read right after the barrier).
     auto compute = [&](int buf) {
         float av[TM][HK], bv[TN][HK];
+        auto read = [&](int q) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
-            const float* src = &As[buf][(wm * WRM + i * 32 + (lane & 31)) * LW + hk];
-#pragma unroll
-            for (int q = 0; q < HK / 4; ++q) {
-                const float4 u = reinterpret_cast<const float4*>(src)[q];
+            for (int i = 0; i < TM; ++i) {
+                const float4 u = reinterpret_cast<const float4*>(
+                    &As[buf][(wm * WRM + i * 32 + (lane & 31)) * LW + hk])[q];
                 av[i][4 * q] = u.x; av[i][4 * q + 1] = u.y; av[i][4 * q + 2] = u.z; av[i][4 * q + 3] = u.w;
             }
-        }
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const float* src = &Bs[buf][(wn * WRN + j * 32 + (lane & 31)) * LW + hk];
-#pragma unroll
-            for (int q = 0; q < HK / 4; ++q) {
-                const float4 u = reinterpret_cast<const float4*>(src)[q];
+            for (int j = 0; j < TN; ++j) {
+                const float4 u = reinterpret_cast<const float4*>(
+                    &Bs[buf][(wn * WRN + j * 32 + (lane & 31)) * LW + hk])[q];
                 bv[j][4 * q] = u.x; bv[j][4 * q + 1] = u.y; bv[j][4 * q + 2] = u.z; bv[j][4 * q + 3] = u.w;
             }
+        };
+        read(0);
+#pragma unroll
+        for (int q = 0; q < HK / 4; ++q) {
+            if (q + 1 < HK / 4) read(q + 1);
+            __builtin_amdgcn_sched_barrier(0);   // next group's reads ahead of this group's MFMAs
+#pragma unroll
+            for (int kk = 4 * q; kk < 4 * q + 4; ++kk)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][kk], bv[j][kk], acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);   // and the LDS stores that follow stay after them
         }
-        __builtin_amdgcn_sched_barrier(0);   // keep the operand reads ahead of the MFMAs
-#pragma unroll
-        for (int kk = 0; kk < HK; ++kk)
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][kk], bv[j][kk], acc[i][j], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);   // the LDS stores that follow stay after the MFMAs
     };
 
     // Slices come in pairs (compute from LDS buffer 0 then 1), so buffers
