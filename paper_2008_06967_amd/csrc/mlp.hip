@@ -883,16 +883,17 @@ static size_t mlp_ws_bytes(int64_t rows, int n_layers, const int32_t* dims, int 
     return w.act + w.part;
 }
 
-template <int BM, int BN, int EPI>
+// fp32 tiles run with NW waves in an (NW / 2) x 2 grid; bf16 tiles with four.
+template <int BM, int BN, int EPI, int NW = 4>
 static void launch_tile(const GemmArgs& a, bool bf16, bool fast_a, bool fast_w, dim3 grid, hipStream_t s) {
-    const dim3 block(256);
+    const dim3 block(256), fblock(64 * NW);
     constexpr int BK = (BM / 64) * (BN / 64) >= 2 ? 32 : 64;   // f32_slice(BM, BN)
     if (a.cc > 0) {
-        gemm_f32_kernel<BM, BN, BK, EPI, true, false, true><<<grid, block, 0, s>>>(a);
+        gemm_f32_kernel<BM, BN, BK, EPI, true, false, true, false, NW><<<grid, fblock, 0, s>>>(a);
         return;
     }
     if (a.lq) {
-        gemm_f32_kernel<BM, BN, BK, EPI, true, true, false, true><<<grid, block, 0, s>>>(a);
+        gemm_f32_kernel<BM, BN, BK, EPI, true, true, false, true, NW><<<grid, fblock, 0, s>>>(a);
         return;
     }
     if (bf16) {
@@ -900,24 +901,29 @@ static void launch_tile(const GemmArgs& a, bool bf16, bool fast_a, bool fast_w, 
         else if (fast_w) gemm_bf16_kernel<BM, BN, EPI, false, true><<<grid, block, 0, s>>>(a);
         else gemm_bf16_kernel<BM, BN, EPI, false, false><<<grid, block, 0, s>>>(a);
     } else {
-        if (fast_a && fast_w) gemm_f32_kernel<BM, BN, BK, EPI, true, true><<<grid, block, 0, s>>>(a);
-        else if (fast_w) gemm_f32_kernel<BM, BN, BK, EPI, false, true><<<grid, block, 0, s>>>(a);
-        else gemm_f32_kernel<BM, BN, BK, EPI, false, false><<<grid, block, 0, s>>>(a);
+        if (fast_a && fast_w) gemm_f32_kernel<BM, BN, BK, EPI, true, true, false, false, NW><<<grid, fblock, 0, s>>>(a);
+        else if (fast_w) gemm_f32_kernel<BM, BN, BK, EPI, false, true, false, false, NW><<<grid, fblock, 0, s>>>(a);
+        else gemm_f32_kernel<BM, BN, BK, EPI, false, false, false, false, NW><<<grid, fblock, 0, s>>>(a);
     }
 }
 
+// 128 x 128 fp32 tiles run with eight waves (two per SIMD, 32 x 64 each), so
+// one wave's LDS and barrier waits overlap the other's MFMAs; with a full
+// wave of 256 x 128 tiles (plain fast sources, no split K) the tile doubles
+// to 64 x 64 per wave, halving the staged B traffic per row.
 template <int EPI>
 static void launch_epi(const GemmArgs& a, const LayerPlan& pl, bool bf16, bool fast_a, bool fast_w, hipStream_t s) {
     if (pl.bm == 128 && pl.bn == 128 && pl.splits == 1 && !bf16 && fast_a && fast_w && a.cc == 0 && !a.lq &&
         ceil_div(a.rows, 256) * ceil_div(a.N, 128) >= kTargetTiles) {
-        // enough rows for a full wave of 256 x 128 tiles: eight waves, two
-        // per SIMD, share each staged B slice over twice the rows
         const dim3 g8((unsigned)ceil_div(a.rows, 256), (unsigned)ceil_div(a.N, 128), 1);
         gemm_f32_kernel<256, 128, 32, EPI, true, true, false, false, 8><<<g8, dim3(512), 0, s>>>(a);
         return;
     }
     const dim3 grid((unsigned)ceil_div(a.rows, pl.bm), (unsigned)ceil_div(a.N, pl.bn), (unsigned)pl.splits);
-    if (pl.bm == 128 && pl.bn == 128) launch_tile<128, 128, EPI>(a, bf16, fast_a, fast_w, grid, s);
+    if (pl.bm == 128 && pl.bn == 128) {
+        if (bf16) launch_tile<128, 128, EPI>(a, bf16, fast_a, fast_w, grid, s);
+        else launch_tile<128, 128, EPI, 8>(a, bf16, fast_a, fast_w, grid, s);
+    }
     else if (pl.bm == 128) launch_tile<128, 64, EPI>(a, bf16, fast_a, fast_w, grid, s);
     else if (pl.bn == 128) launch_tile<64, 128, EPI>(a, bf16, fast_a, fast_w, grid, s);
     else launch_tile<64, 64, EPI>(a, bf16, fast_a, fast_w, grid, s);
