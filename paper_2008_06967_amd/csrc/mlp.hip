@@ -907,10 +907,11 @@ static void launch_tile(const GemmArgs& a, bool bf16, bool fast_a, bool fast_w, 
     }
 }
 
-// 128 x 128 fp32 tiles run with eight waves (two per SIMD, 32 x 64 each), so
-// one wave's LDS and barrier waits overlap the other's MFMAs; with a full
-// wave of 256 x 128 tiles (plain fast sources, no split K) the tile doubles
-// to 64 x 64 per wave, halving the staged B traffic per row.
+// 128 x 128 and 128 x 64 fp32 tiles run with eight waves (two per SIMD,
+// 32 x 64 or 32 x 32 each), so one wave's LDS and barrier waits overlap the
+// other's MFMAs; with a full wave of 256 x 128 tiles (plain fast sources, no
+// split K) the tile doubles to 64 x 64 per wave, halving the staged B
+// traffic per row.
 template <int EPI>
 static void launch_epi(const GemmArgs& a, const LayerPlan& pl, bool bf16, bool fast_a, bool fast_w, hipStream_t s) {
     if (pl.bm == 128 && pl.bn == 128 && pl.splits == 1 && !bf16 && fast_a && fast_w && a.cc == 0 && !a.lq &&
@@ -924,7 +925,10 @@ static void launch_epi(const GemmArgs& a, const LayerPlan& pl, bool bf16, bool f
         if (bf16) launch_tile<128, 128, EPI>(a, bf16, fast_a, fast_w, grid, s);
         else launch_tile<128, 128, EPI, 8>(a, bf16, fast_a, fast_w, grid, s);
     }
-    else if (pl.bm == 128) launch_tile<128, 64, EPI>(a, bf16, fast_a, fast_w, grid, s);
+    else if (pl.bm == 128) {
+        if (bf16) launch_tile<128, 64, EPI>(a, bf16, fast_a, fast_w, grid, s);
+        else launch_tile<128, 64, EPI, 8>(a, bf16, fast_a, fast_w, grid, s);
+    }
     else if (pl.bn == 128) launch_tile<64, 128, EPI>(a, bf16, fast_a, fast_w, grid, s);
     else launch_tile<64, 64, EPI>(a, bf16, fast_a, fast_w, grid, s);
 }
