@@ -94,7 +94,8 @@ int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, int32_t* idx
  *   nit   [B, M, K] int32 out
  *   cnt   [B, M] int32 out, nullable: number of real hits (<= K)
  * Errors: EINVAL for NULL xyz/qxyz/nit, B/N/M < 0, N == 0 < M, K < 1,
- *         radius not finite or <= 0;  EUNSUPPORTED for K > MESORASI_MAX_K_BALL.
+ *         radius not finite or <= 0;  EUNSUPPORTED for K > MESORASI_MAX_K_BALL,
+ *         N > 2^31 - 321, M > 2^31 - 1.
  */
 int mesorasi_ball_query(const float* xyz, const float* qxyz, int64_t B, int64_t N, int64_t M, float radius,
                         int32_t K, int32_t* nit, int32_t* cnt, void* stream);
