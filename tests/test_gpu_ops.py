@@ -279,7 +279,12 @@ MLP_CASES = [
     ("width_max_gemm", 200, [4096], [4096, 64], F32), # the same on the tiled GEMM path
     ("depth_max", 100, [16], [32] * 8, F32),          # the documented maximum depth
     # a full wave of 256 x 128 tiles (eight-wave kernel), ragged rows and columns
-    ("many_rows_wide", 8525, [64], [1000, 384], F32),
+    ("many_rows_wide", 16284, [64], [1000, 384], F32),
+    # eight-wave 128 x 128 and 128 x 64 tiles on the split two-source form and
+    # on the general loader (widths not multiples of 4, ragged rows)
+    ("split_8wave_128x128", 16384, [3, 128], [256], F32),
+    ("split_8wave_128x64", 16384, [3, 128], [128], F32),
+    ("general_8wave_128x128", 16383, [6, 125], [256], F32),
 ]
 
 
@@ -326,7 +331,7 @@ def test_mlp_pooled_many_rows(gpu):
     """Per-point 1x1 convolution with the max over each cloud fused, at a
     row count that fills the chip with 256 x 128 tiles."""
     rr = g(12)
-    G, groups = 1024, 9
+    G, groups = 1024, 16
     x = rr.standard_normal((G * groups, 96)).astype(np.float32)
     Ws, bs = _weights(rr, [96, 1024])
     ref = O.rowgroup_max(O.mlp(x, Ws, bs).reshape(groups, G, 1024), G)
@@ -438,6 +443,8 @@ LTD_CASES = {
     "gemm_gather_no_bias_strided": (64, [96, 160], False, F32, 72),
     "gemm_materialized": (66, [64, 200], True, F32, 66),
     "bf16_rest": (32, [24, 40], True, BF16, 32),
+    # 16384 gathered rows into 256 columns: the eight-wave 128 x 128 tile
+    "gemm_gather_8wave": (128, [256, 64], True, F32, 128, (2, 2048, 512, 16)),
 }
 
 
@@ -445,9 +452,9 @@ LTD_CASES = {
 def test_ltd_module_parity(gpu, case):
     """Limited delayed aggregation (first-layer rows from p1 - q + b1, then
     the remaining layers and the max over K) against the oracle."""
-    C1, widths, bias, dt, ldp = LTD_CASES[case]
+    C1, widths, bias, dt, ldp, *sizes = LTD_CASES[case]
     rr = g(14)
-    B, N, M, K = 2, 300, 77, 9
+    B, N, M, K = sizes[0] if sizes else (2, 300, 77, 9)
     base = rr.standard_normal((B, N, ldp)).astype(np.float32)
     p1 = np.ascontiguousarray(base[:, :, :C1])
     q = rr.standard_normal((B, M, C1)).astype(np.float32)
