@@ -8,9 +8,10 @@
 // One launch per layer: Y = phi(X W^T + b) with X = [x0 | x1] (two column
 // sources, so the first layer reads xyz and the previous module's features
 // without a concatenated copy).  Workgroup tiles of 64 or 128 rows by 64 or
-// 128 output channels (chosen per layer to fill the 256 CUs), 4 waves each
-// owning up to 2 x 2 blocks of 32 x 32; layers with too few tiles split K
-// and sum the partials in a fixed order:
+// 128 output channels (chosen per layer to fill the 256 CUs; fp32 tiles of
+// 128 rows run with eight waves, and with 256 rows when a layer has a full
+// wave of those), each wave owning up to 2 x 2 blocks of 32 x 32; layers
+// with too few tiles split K and sum the partials in a fixed order:
 //  - fp32: v_mfma_f32_32x32x2_f32 (lane l feeds one A and one B value of
 //    the same k); row-major LDS tiles read with 16-byte loads in an MFMA
 //    lane k-order (details at gemm_f32_kernel).
@@ -346,7 +347,8 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, const f32x16& acc, i
     }
 }
 
-// fp32 MFMA GEMM.  Workgroup tile BM x BN, 2 x 2 waves, each wave TM x TN
+// fp32 MFMA GEMM.  Workgroup tile BM x BN, NW waves in an (NW / 2) x 2 grid
+// (four or eight: eight put two waves on each SIMD), each wave TM x TN
 // blocks of 32 x 32.  K advances in slices of BK through double-buffered
 // row-major LDS tiles (rows of BK words + 4 pad); the next slice is fetched
 // into registers while the current one feeds the MFMAs, so one barrier per
