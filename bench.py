@@ -47,6 +47,7 @@ DESCRIBE = {
 HBM_PEAK_GBS = 8000.0
 MFMA_F32_PEAK_TFLOPS = 157.3
 MFMA_BF16_PEAK_TFLOPS = 2516.6
+N_CUS = 256   # MI355X compute units (the ALU peak is spread evenly over them)
 
 
 def parse():
@@ -143,7 +144,8 @@ def call_work(name, a, kw):
     if name == "fps":
         xyz, M = arg(0, "xyz"), arg(1, "M")
         B, N = xyz.shape[0], xyz.shape[1]
-        return ("alu", 8.0 * B * (M - 1) * N / 1e12, None)
+        # one workgroup per cloud walks M - 1 dependent iterations
+        return ("alu", 8.0 * B * (M - 1) * N / 1e12, {"serial_iterations": M - 1, "workgroups": B})
     if name == "ball_query":
         xyz, q, K = arg(0, "xyz"), arg(1, "qxyz"), arg(3, "K")
         B, N, M = xyz.shape[0], xyz.shape[1], q.shape[1]
@@ -347,6 +349,12 @@ def main():
         roofs[k] = {"bound": kd, "achieved": round(rate, 4), "peak": pk, "unit": pu, "frac": round(rate / pk, 5)}
         if extra and "logical_gather_bytes" in extra:
             roofs[k]["logical_gather_GBps"] = round(extra["logical_gather_bytes"] / (ms * 1e-3) / 1e9, 1)
+        if extra and "serial_iterations" in extra:
+            # latency view of a sequential kernel: time per dependent
+            # iteration, and the rate against the CUs it can occupy
+            roofs[k]["us_per_iteration"] = round(ms * 1e3 / max(1, extra["serial_iterations"]), 4)
+            cus = min(extra["workgroups"], N_CUS)
+            roofs[k]["frac_of_occupied_cus"] = round(rate / (pk * cus / N_CUS), 5)
         if extra and "compulsory_bytes" in extra:
             gbs = extra["compulsory_bytes"] / (ms * 1e-3) / 1e9
             roofs[k]["hbm_compulsory_GBps"] = round(gbs, 1)
