@@ -114,13 +114,17 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_kernel(const float* __rest
         sQ[e] = qi < M ? query[(b * M + qi) * ldq + c] : 0.0f;
     }
 
+    // (thr, thrj): the list's K-th entry, (+inf, INT_MAX) while the list is
+    // short, so that a candidate whose distance overflowed to +inf is still
+    // admitted then, as by the sequential insertion rule
     float td[kKnnQpw], thr[kKnnQpw];
-    int tj[kKnnQpw];
+    int tj[kKnnQpw], thrj[kKnnQpw];
 #pragma unroll
     for (int qq = 0; qq < kKnnQpw; ++qq) {
         td[qq] = inf;
         tj[qq] = 0x7fffffff;
         thr[qq] = inf;
+        thrj[qq] = 0x7fffffff;
     }
 
     for (int t0 = 0; t0 < N; t0 += kKnnTile) {
@@ -179,7 +183,7 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_kernel(const float* __rest
         }
 #pragma unroll
         for (int qq = 0; qq < kKnnQpw; ++qq) {
-            uint64_t mask = ballot(valid && d[qq] < thr[qq]);
+            uint64_t mask = ballot(valid && pair_before(d[qq], t0 + lane, thr[qq], thrj[qq]));
             if (__builtin_popcountll(mask) > kKnnSerialMax) {
                 // many candidates (the first tiles): sort the tile's (distance,
                 // index) pairs across the wave, then merge them into the list
@@ -193,17 +197,19 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_kernel(const float* __rest
                     tj[qq] = 0x7fffffff;
                 }
                 thr[qq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(td[qq]), K - 1));
+                thrj[qq] = __builtin_amdgcn_readlane(tj[qq], K - 1);
                 mask = 0;
             }
             while (mask) {
                 const int l = __builtin_ctzll(mask);
                 mask &= mask - 1;
                 const float dc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(d[qq]), l));
-                if (dc < thr[qq]) {
-                    const int jc = t0 + l;
-                    // every stored entry has a smaller index, so it precedes the
-                    // candidate iff its distance is <= dc
-                    const int pos = __builtin_popcountll(ballot(td[qq] <= dc));
+                const int jc = t0 + l;
+                if (pair_before(dc, jc, thr[qq], thrj[qq])) {
+                    // a stored entry has a smaller index than the candidate, so it
+                    // precedes it iff its distance is <= dc; an empty slot
+                    // (+inf, INT_MAX) never does
+                    const int pos = __builtin_popcountll(ballot(pair_before(td[qq], tj[qq], dc, jc)));
                     // lane i takes lane i-1's entry: one DPP wave_shr:1 each
                     // (lane 0 never uses it)
                     const float sd = __int_as_float(
@@ -221,6 +227,7 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_kernel(const float* __rest
                         tj[qq] = 0x7fffffff;
                     }
                     thr[qq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(td[qq]), K - 1));
+                    thrj[qq] = __builtin_amdgcn_readlane(tj[qq], K - 1);
                 }
             }
         }
@@ -757,37 +764,16 @@ constexpr int kIpWaves = 4;
 constexpr int kIpDests = 128;    // destinations per workgroup, two per lane
 constexpr int kIpChunk = 1024;   // sources staged in LDS per pass
 
-// insert (d, j) into an ascending top-3 when sources arrive in index order:
-// strict < keeps the earlier index first on equal distances
+// insert (d, j) into an ascending top-3 in (distance, index) order (used
+// both for sources in index order and for merging lists).  An empty slot
+// (+inf, INT_MAX) takes any source, also one whose distance overflowed to
+// +inf; padding sources carry j = INT_MAX and are never inserted.
 __device__ __forceinline__ void top3_insert(float d, int j, float (&e)[3], int (&jj)[3]) {
-    if (d < e[2]) {
-        if (d < e[1]) {
+    if (pair_before(d, j, e[2], jj[2])) {
+        if (pair_before(d, j, e[1], jj[1])) {
             e[2] = e[1];
             jj[2] = jj[1];
-            if (d < e[0]) {
-                e[1] = e[0];
-                jj[1] = jj[0];
-                e[0] = d;
-                jj[0] = j;
-            } else {
-                e[1] = d;
-                jj[1] = j;
-            }
-        } else {
-            e[2] = d;
-            jj[2] = j;
-        }
-    }
-}
-
-// the same for candidates in any order: (distance, index) lexicographic
-__device__ __forceinline__ bool before(float d, int j, float e, int je) { return d < e || (d == e && j < je); }
-__device__ __forceinline__ void top3_merge(float d, int j, float (&e)[3], int (&jj)[3]) {
-    if (before(d, j, e[2], jj[2])) {
-        if (before(d, j, e[1], jj[1])) {
-            e[2] = e[1];
-            jj[2] = jj[1];
-            if (before(d, j, e[0], jj[0])) {
+            if (pair_before(d, j, e[0], jj[0])) {
                 e[1] = e[0];
                 jj[1] = jj[0];
                 e[0] = d;
@@ -847,7 +833,7 @@ __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __r
         __syncthreads();
         const int n = min(kIpChunk, Ns - c0);
         for (int t = tid; t < n + 16; t += 64 * kIpWaves) {
-            float x = inf, y = inf, z = inf;      // padding: infinite distance, never inserted
+            float x = inf, y = inf, z = inf;      // padding: infinite distance and index INT_MAX
             if (t < n) {
                 const float* src = xyz_src + (b * Ns + c0 + t) * 3;
                 x = src[0];
@@ -869,7 +855,7 @@ __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __r
                         az[4] = {vz.x, vz.y, vz.z, vz.w};
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int j = c0 + t + u;
+                const int j = t + u < n ? c0 + t + u : 0x7fffffff;
 #pragma unroll
                 for (int h = 0; h < 2; ++h) top3_insert(dist3(ax[u], ay[u], az[u], qx[h], qy[h], qz[h]), j, e[h], jj[h]);
             }
@@ -888,14 +874,16 @@ __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __r
         int fj[3] = {0x7fffffff, 0x7fffffff, 0x7fffffff};
         for (int w = 0; w < kIpWaves; ++w)
 #pragma unroll
-            for (int k = 0; k < 3; ++k) top3_merge(s_e[w][tid][k], s_jj[w][tid][k], f, fj);
+            for (int k = 0; k < 3; ++k) top3_insert(s_e[w][tid][k], s_jj[w][tid][k], f, fj);
         const float w0 = 1.0f / fmaxf(f[0], 1e-10f);
         const float w1 = 1.0f / fmaxf(f[1], 1e-10f);
         const float w2 = 1.0f / fmaxf(f[2], 1e-10f);
         const float ws = w0 + w1 + w2;
-        s_j[tid][0] = fj[0];
-        s_j[tid][1] = fj[1];
-        s_j[tid][2] = fj[2];
+        // with Ns >= 3 every slot holds a source (any source precedes an empty
+        // slot); the min only keeps the row reads below inside f_src
+        s_j[tid][0] = min(fj[0], Ns - 1);
+        s_j[tid][1] = min(fj[1], Ns - 1);
+        s_j[tid][2] = min(fj[2], Ns - 1);
         s_w[tid][0] = w0 / ws;
         s_w[tid][1] = w1 / ws;
         s_w[tid][2] = w2 / ws;

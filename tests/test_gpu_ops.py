@@ -151,6 +151,11 @@ KNN_CASES = [
     # more than 1024 points: the streaming running list
     ("stream_n1500", 1, 1500, 200, 16, 20, "other"),
     ("stream_ties", 1, 1100, 300, 3, 10, "grid"),
+    # coordinates around 1e20: most squared distances overflow to +inf, and the
+    # list still fills with the lowest such indices (never an empty slot)
+    ("stream_overflow", 1, 1500, 100, 3, 20, "huge"),
+    ("reg_overflow", 1, 1000, 100, 3, 20, "huge"),
+    ("mfma_overflow", 1, 512, 64, 64, 20, "huge"),
 ]
 
 
@@ -164,13 +169,17 @@ def test_knn_bit_exact(gpu, name, B, N, M, C, K, kind):
         ref = np.ascontiguousarray(base[:, rr.integers(0, 8, N)] + 1e-6 * rr.standard_normal((B, N, C)), np.float32)
     elif kind == "offset":   # features around 100: |x|^2 ~ 1e6 C, distances ~ 2C
         ref = (100.0 + rr.standard_normal((B, N, C))).astype(np.float32)
+    elif kind == "huge":     # finite inputs whose squared distances mostly overflow
+        ref = (1e20 * rr.standard_normal((B, N, C))).astype(np.float32)
     else:
         ref = rr.standard_normal((B, N, C)).astype(np.float32)
-    if kind in ("self", "grid", "jitter", "offset"):
+    if kind in ("self", "grid", "jitter", "offset", "huge"):
         query = ref if M == N else np.ascontiguousarray(ref[:, :M])
     else:
         query = rr.standard_normal((B, M, C)).astype(np.float32)
     rn, rd = O.knn(ref, query, K)
+    if kind == "huge":
+        assert np.isinf(rd).mean() > 0.5
     nit, dist = ops.knn(dev(ref), dev(query), K, want_dist=True)
     assert np.array_equal(host(nit), rn)
     assert np.array_equal(host(dist), rd)
@@ -494,6 +503,26 @@ def test_interpolate3_ties_take_lowest_index(gpu, Ns_half):
     src = np.concatenate([base, base], 1)
     dst = rr.uniform(-1, 1, (2, 257, 3)).astype(np.float32)
     f = rr.standard_normal((2, 2 * Ns_half, 6)).astype(np.float32)
+    ref = O.interpolate3(dst, src, f)
+    out = ops.interpolate3(dev(dst), dev(src), dev(f))
+    assert normwise(host(out), ref) <= 1e-5
+
+
+def test_interpolate3_overflowing_distances(gpu):
+    """Sources beyond 1e20 (squared distances +inf, weight 0) beside two
+    near sources: the 3-NN list still takes the lowest-index infinite
+    source as its third entry, and the result is the two near sources'
+    weighted mean."""
+    rr = g(14)
+    Ns, Nd = 1500, 70
+    far = 1e20 * rr.uniform(1, 2, (1, Ns, 3)) * rr.choice([-1.0, 1.0], (1, Ns, 3))
+    src = far.astype(np.float32)
+    src[0, 5] = (0.1, 0.2, 0.3)
+    src[0, 1100] = (-0.4, 0.0, 0.5)           # in the second staged chunk
+    dst = rr.uniform(-1, 1, (1, Nd, 3)).astype(np.float32)
+    f = rr.standard_normal((1, Ns, 8)).astype(np.float32)
+    nn, dd = O.knn(src, dst, 3)
+    assert (nn[..., :2] != 0).all() and np.isinf(dd[..., 2]).all()
     ref = O.interpolate3(dst, src, f)
     out = ops.interpolate3(dev(dst), dev(src), dev(f))
     assert normwise(host(out), ref) <= 1e-5

@@ -431,19 +431,27 @@ def test_eq3_hand_example():
     assert float(conv[0, 0, 0]) == d["conventional"]
 
 
-def test_group_all_same_in_both_orders():
-    spec = synth.workload("pointnet2_cls", B=1)
-    xyz, feat = synth.make_points(spec)
+def test_group_all_matches_float64_chain_and_is_order_free():
+    """Group-all (no centroid term, the same computation in both orders):
+    every point's MLP row by a numpy float64 chain (one fp32 rounding per
+    layer, as the oracle's MLP), then the column max over the cloud; the
+    result does not depend on the order of the points."""
+    spec = synth.workload("pointnet2_cls", B=2)
     w = synth.make_weights(spec)
-    a = ON.forward(spec, xyz, feat, w, delayed=True)
-    c = ON.forward(spec, xyz, feat, w, delayed=False)
-    for ma, mc in zip(a["modules"], c["modules"]):
-        assert np.array_equal(ma["idx"], mc["idx"]) and np.array_equal(ma["nit"], mc["nit"])
-    # group-all on identical inputs is identical
-    m = a["modules"][-1]
-    g1 = ON.group_all(m["cxyz"], m["out"], *w["group_all"])
-    g2 = ON.group_all(m["cxyz"], m["out"], *w["group_all"])
-    assert np.array_equal(g1, g2)
+    Ws, bs = w["group_all"]
+    r = g(16)
+    xyz = r.uniform(-1, 1, (2, 40, 3)).astype(np.float32)
+    feat = np.maximum(r.standard_normal((2, 40, Ws[0].shape[1] - 3)), 0).astype(np.float32)
+    got = ON.group_all(xyz, feat, Ws, bs)
+    h = np.concatenate([xyz, feat], -1).astype(np.float64)
+    for W, b in zip(Ws, bs):
+        h = np.maximum(h @ np.asarray(W, np.float64).T + np.asarray(b, np.float64), 0.0)
+        h = h.astype(np.float32).astype(np.float64)
+    ref = h.max(axis=1).astype(np.float32)
+    assert got.shape == ref.shape
+    assert np.max(np.abs(got - ref)) <= 1e-6 * np.max(np.abs(ref))
+    perm = r.permutation(40)
+    assert np.array_equal(ON.group_all(xyz[:, perm], feat[:, perm], Ws, bs), got)
 
 
 def test_walkthrough_shapes():
@@ -495,3 +503,16 @@ def test_interpolate3_properties():
     s3 = np.array([[[1, 0, 0], [0, 1, 0], [0, 0, 1], [5, 5, 5]]], np.float32)
     f3 = np.array([[[3.0], [6.0], [9.0], [100.0]]], np.float32)
     assert np.allclose(O.interpolate3(np.zeros((1, 1, 3), np.float32), s3, f3), 6.0)
+
+
+def test_interpolate3_hand_example():
+    """Pins the weight law (1/d2, not 1/d) and the 3-source cut-off."""
+    d = gold("interpolate3_weights.json")
+    dst = np.array([d["dst"]], np.float32)
+    src = np.array([d["src"]], np.float32)
+    f = np.array([d["features"]], np.float32)
+    out = O.interpolate3(dst, src, f)[0, 0].astype(np.float64)
+    want = np.array(d["expected_num"], np.float64) / d["expected_den"]
+    assert np.max(np.abs(out - want)) <= 1e-7
+    wrong = np.array(d["inverse_distance_num"], np.float64) / d["inverse_distance_den"]
+    assert np.max(np.abs(out - wrong)) > 0.1
