@@ -159,6 +159,29 @@ size_t mesorasi_pointwise_mlp_workspace(int64_t rows, int32_t n_layers, const in
                                         int64_t pool_group);
 
 /*
+ * mesorasi_pointwise_mlp without a workspace argument and without any
+ * allocation, for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, results and errors as mesorasi_pointwise_mlp, except:
+ *  - the intermediate activations and split-K partials live in a fixed
+ *    device array of MESORASI_NOALLOC_WS_BYTES inside the library, one per
+ *    GPU, held until the process ends;
+ *  - a call whose mesorasi_pointwise_mlp_workspace() exceeds that size is
+ *    rejected with EUNSUPPORTED before any HIP call;
+ *  - EHIP if the array's device address cannot be obtained (looked up once
+ *    per device, with that device current, on the first call that needs it).
+ * Every call on one GPU shares that GPU's array and leaves its last
+ * contents there: calls that overlap on one GPU (different streams or host
+ * threads without ordering between them) race and give wrong results.
+ * Nothing in the array needs to start at zero.
+ */
+#define MESORASI_NOALLOC_WS_BYTES (32u << 20)
+int mesorasi_pointwise_mlp_noalloc(const float* x0, int32_t c0, int64_t ld0, const float* x1, int32_t c1,
+                                   int64_t ld1, int64_t rows, int32_t n_layers, const int32_t* dims,
+                                   const void* const* W, const float* const* bias, uint32_t relu_mask, int32_t dtype,
+                                   int32_t out_dtype, void* y, int64_t ld_y, int64_t pool_group, void* stream);
+
+/*
  * Aggregation A on the PFT (Sec. 5.2 first paragraph; Sec. 4.1 max/subtract
  * distributivity): for each NIT entry, gather the K PFT rows, take the
  * column-wise max (exact), then combine with the centroid row in one fp32

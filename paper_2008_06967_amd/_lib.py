@@ -12,6 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmesorasi.so")
 
 OK, EINVAL, EUNSUPPORTED, EHIP, EWORKSPACE = 0, -1, -2, -3, -4
+NOALLOC_WS_BYTES = 32 << 20    # MESORASI_NOALLOC_WS_BYTES: the allocation-free MLP's fixed scratch
 F32, BF16 = 0, 1
 
 _i64, _i32, _u32, _p, _f = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_float
@@ -28,6 +29,8 @@ SIGNATURES = {
     "mesorasi_pointwise_mlp": (ctypes.c_int, [_p, _i32, _i64, _p, _i32, _i64, _i64, _i32, _p, _p, _p, _u32, _i32,
                                               _i32, _p, _i64, _i64, _p, _size, _p]),
     "mesorasi_pointwise_mlp_workspace": (_size, [_i64, _i32, _p, _i32, _i64]),
+    "mesorasi_pointwise_mlp_noalloc": (ctypes.c_int, [_p, _i32, _i64, _p, _i32, _i64, _i64, _i32, _p, _p, _p, _u32,
+                                                      _i32, _i32, _p, _i64, _i64, _p]),
     "mesorasi_aggregate_max": (ctypes.c_int, [_p, _i64, _i32, _p, _i64, _i64, _i64, _i32, _i32, _p, _p, _i64, _i32,
                                               _i32, _p, _i64, _p]),
     "mesorasi_conventional_module": (ctypes.c_int, [_p, _p, _i32, _i64, _p, _p, _i64, _i64, _i64, _i32, _i32, _i32,

@@ -27,6 +27,8 @@
 // MLPs on at most 64 rows (the classifier head) take a skinny path of
 // 16-column MFMA blocks instead (skinny_f32_kernel); narrow multi-layer fp32
 // MLPs run fused in one kernel (mlp_fused.hip).
+#include <mutex>
+
 #include "common.h"
 #include "mlp_internal.h"
 
@@ -1171,12 +1173,11 @@ extern "C" size_t mesorasi_pointwise_mlp_workspace(int64_t rows, int32_t n_layer
     return mlp_ws_bytes(rows, n_layers, dims, dtype);
 }
 
-extern "C" int mesorasi_pointwise_mlp(const float* x0, int32_t c0, int64_t ld0, const float* x1, int32_t c1,
-                                      int64_t ld1, int64_t rows, int32_t n_layers, const int32_t* dims,
-                                      const void* const* W, const float* const* bias, uint32_t relu_mask,
-                                      int32_t dtype, int32_t out_dtype, void* y, int64_t ld_y, int64_t pool_group,
-                                      void* ws, size_t ws_bytes, void* stream) {
-    const char* who = "mesorasi_pointwise_mlp";
+// Argument checks shared by both MLP entry points (host only, no HIP call).
+static int check_mlp_args(const char* who, const float* x0, int32_t c0, int64_t ld0, const float* x1, int32_t c1,
+                          int64_t ld1, int64_t rows, int32_t n_layers, const int32_t* dims, const void* const* W,
+                          uint32_t relu_mask, int32_t dtype, int32_t out_dtype, void* y, int64_t ld_y,
+                          int64_t pool_group) {
     int rc = check_mlp_spec(who, rows, n_layers, dims, dtype);
     if (rc != MESORASI_OK) return rc;
     MESO_REQUIRE(c0 >= 1 && c1 >= 0, MESORASI_EINVAL, "%s: c0 = %d, c1 = %d", who, c0, c1);
@@ -1196,10 +1197,78 @@ extern "C" int mesorasi_pointwise_mlp(const float* x0, int32_t c0, int64_t ld0, 
     MESO_REQUIRE(x0 && y && W, MESORASI_EINVAL, "%s: NULL x0, y or W", who);
     MESO_REQUIRE(c1 == 0 || x1, MESORASI_EINVAL, "%s: NULL x1 with c1 > 0", who);
     for (int l = 0; l < n_layers; ++l) MESO_REQUIRE(W[l] != nullptr, MESORASI_EINVAL, "%s: W[%d] is NULL", who, l);
+    MESO_REQUIRE(rows / 64 < 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: too many rows", who);
+    return MESORASI_OK;
+}
+
+extern "C" int mesorasi_pointwise_mlp(const float* x0, int32_t c0, int64_t ld0, const float* x1, int32_t c1,
+                                      int64_t ld1, int64_t rows, int32_t n_layers, const int32_t* dims,
+                                      const void* const* W, const float* const* bias, uint32_t relu_mask,
+                                      int32_t dtype, int32_t out_dtype, void* y, int64_t ld_y, int64_t pool_group,
+                                      void* ws, size_t ws_bytes, void* stream) {
+    const char* who = "mesorasi_pointwise_mlp";
+    const int rc = check_mlp_args(who, x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, relu_mask, dtype,
+                                  out_dtype, y, ld_y, pool_group);
+    if (rc != MESORASI_OK || rows == 0) return rc;
     const size_t need = mlp_ws_bytes(rows, n_layers, dims, dtype);
     MESO_REQUIRE(ws_bytes >= need && (need == 0 || ws), MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who,
                  ws_bytes, need);
-    MESO_REQUIRE(rows / 64 < 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: too many rows", who);
+    return run_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, dtype, out_dtype, y, ld_y,
+                   pool_group, ws, as_stream(stream));
+}
+
+// ---------------------------------------------------------------------------
+// allocation-free variant: the workspace is a file-scope device array
+// ---------------------------------------------------------------------------
+
+// Every GPU the library runs on holds its own copy until the process ends.
+// In host code `scratch` names a host-side stand-in: kernels and copies get
+// the device address from hipGetSymbolAddress, kept per device.
+static __device__ __align__(256) unsigned char scratch[MESORASI_NOALLOC_WS_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_dev[kMaxDevices];
+
+// Device address of the current device's scratch array, looked up once per
+// device (with that device current) on its first use.
+static int scratch_on_current_device(const char* who, void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return set_error(MESORASI_EHIP, "%s: hipGetDevice: %s", who, hipGetErrorString(e));
+    MESO_REQUIRE(dev >= 0 && dev < kMaxDevices, MESORASI_EUNSUPPORTED, "%s: device %d", who, dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return set_error(MESORASI_EHIP, "%s: hipGetSymbolAddress(scratch): %s", who, hipGetErrorString(e));
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return MESORASI_OK;
+}
+
+extern "C" int mesorasi_pointwise_mlp_noalloc(const float* x0, int32_t c0, int64_t ld0, const float* x1, int32_t c1,
+                                              int64_t ld1, int64_t rows, int32_t n_layers, const int32_t* dims,
+                                              const void* const* W, const float* const* bias, uint32_t relu_mask,
+                                              int32_t dtype, int32_t out_dtype, void* y, int64_t ld_y,
+                                              int64_t pool_group, void* stream) {
+    const char* who = "mesorasi_pointwise_mlp_noalloc";
+    int rc = check_mlp_args(who, x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, relu_mask, dtype, out_dtype, y,
+                            ld_y, pool_group);
+    if (rc != MESORASI_OK || rows == 0) return rc;
+    const size_t need = mlp_ws_bytes(rows, n_layers, dims, dtype);
+    MESO_REQUIRE(need <= (size_t)MESORASI_NOALLOC_WS_BYTES, MESORASI_EUNSUPPORTED,
+                 "%s: needs %zu bytes of scratch, above the fixed %zu", who, need,
+                 (size_t)MESORASI_NOALLOC_WS_BYTES);
+    void* ws = nullptr;
+    if (need > 0) {
+        rc = scratch_on_current_device(who, &ws);
+        if (rc != MESORASI_OK) return rc;
+    }
+    // the activations and split-K partials are written before they are
+    // read, so nothing in the array needs clearing between calls
     return run_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, dtype, out_dtype, y, ld_y,
                    pool_group, ws, as_stream(stream));
 }

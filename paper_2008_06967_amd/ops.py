@@ -150,6 +150,34 @@ def pointwise_mlp(x0: torch.Tensor, p: MLPParams, x1: torch.Tensor | None = None
     return out
 
 
+def pointwise_mlp_noalloc(x0: torch.Tensor, p: MLPParams, x1: torch.Tensor | None = None,
+                          relu_mask: int | None = None, out_dtype: int = F32, pool_group: int = 0,
+                          out: torch.Tensor | None = None):
+    """pointwise_mlp through the allocation-free entry point: the library's
+    fixed per-GPU scratch array replaces the workspace (calls that overlap
+    on one GPU race).  Only `out` is allocated here, when not given."""
+    p0, ld0 = _rows(x0)
+    c0 = x0.shape[-1]
+    if x1 is not None:
+        p1, ld1 = _rows(x1)
+        c1 = x1.shape[-1]
+    else:
+        p1, ld1, c1 = None, 0, 0
+    rows = math.prod(x0.shape[:-1])
+    if relu_mask is None:
+        relu_mask = (1 << p.n) - 1
+    if out is None:
+        dt = torch.float32 if out_dtype == F32 else torch.bfloat16
+        shape = (rows // pool_group, p.c_out) if pool_group else tuple(x0.shape[:-1]) + (p.c_out,)
+        out = torch.empty(shape, dtype=dt, device=x0.device)
+    py, ldy = _rows(out)
+    d, W, b = p.abi()
+    check(_lib.lib().mesorasi_pointwise_mlp_noalloc(p0, c0, ld0, p1, c1, ld1, rows, p.n, d, W, b, relu_mask,
+                                                    p.dtype, out_dtype, py, ldy, pool_group, _stream()),
+          "pointwise_mlp_noalloc")
+    return out
+
+
 def aggregate_max(pft: torch.Tensor, nit: torch.Tensor, cidx: torch.Tensor | None = None,
                   cfeat: torch.Tensor | None = None, sign: int = -1, relu: bool = False,
                   out: torch.Tensor | None = None):

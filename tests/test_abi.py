@@ -120,6 +120,24 @@ def test_mlp_validation_and_workspace():
     assert st(f, NULL, 3, 3, NULL, 0, 0, 0, 3, d, W, b, 7, 0, 0, NULL, 128, 0, NULL, 0, NULL) == _lib.OK  # rows = 0
 
 
+def test_mlp_noalloc_validation():
+    """The allocation-free MLP checks its arguments like the workspace form
+    and refuses work beyond its fixed scratch array, before any HIP call."""
+    L = _lib.lib()
+    f = "mesorasi_pointwise_mlp_noalloc"
+    d, W, b = _mlp_args([3, 64, 64, 128])
+    assert st(f, FAKE, 4, 4, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 128, 0, NULL) == _lib.EINVAL   # dims[0]
+    assert st(f, FAKE, 3, 3, NULL, 0, 0, 10, 3, d, W, b, 7, 0, 0, FAKE, 128, 3, NULL) == _lib.EINVAL   # rows % G
+    assert st(f, NULL, 3, 3, NULL, 0, 0, 0, 3, d, W, b, 7, 0, 0, NULL, 128, 0, NULL) == _lib.OK        # rows = 0
+    dw, Ww, bw = _mlp_args([3, 200, 200, 256])
+    rows = 1 << 20
+    assert L.mesorasi_pointwise_mlp_workspace(rows, 3, dw, 0, 0) > _lib.NOALLOC_WS_BYTES
+    assert st(f, FAKE, 3, 3, NULL, 0, 0, rows, 3, dw, Ww, bw, 7, 0, 0, FAKE, 256, 0, NULL) == _lib.EUNSUPPORTED
+    assert b"scratch" in L.mesorasi_last_error()
+    m = re.search(r"#define MESORASI_NOALLOC_WS_BYTES \((\d+)u << (\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == _lib.NOALLOC_WS_BYTES
+
+
 def test_aggregate_validation():
     f = "mesorasi_aggregate_max"
     assert st(f, FAKE, 64, 0, FAKE, 1, 10, 5, 4, 64, FAKE, FAKE, 64, -1, 0, FAKE, 64, NULL) == _lib.EINVAL  # both
