@@ -78,11 +78,28 @@ const char* mesorasi_last_error(void);
  *   xyz   [B, N, 3] float32
  *   idx   [B, M] int32 out: selected indices in selection order
  *   cxyz  [B, M, 3] float32 out, nullable: copies of the selected points
- * Errors: EINVAL for NULL xyz/idx, B/N/M < 0, M > N, N == 0 < M;
- *         EUNSUPPORTED for N > MESORASI_MAX_N_FPS.
- * One workgroup per cloud (the M iterations are sequential).
+ *   ws    device workspace of at least mesorasi_fps_workspace(B, N, M)
+ *         bytes, 8-byte aligned (NULL allowed when that size is 0).  Large
+ *         clouds spread each cloud over several workgroups that exchange
+ *         their per-iteration winners through it; it is cleared by the call
+ *         itself (any contents on entry), and its first 4 bytes hold 0 after
+ *         the call, or 1 if a workgroup gave up waiting on the others (it
+ *         then finishes on its own and the indices, though in [0, N), are
+ *         not the sampling's; this needs the call's workgroups to be kept
+ *         from running together, which a working GPU does not do).  Calls
+ *         that overlap in time need separate workspaces.
+ * Errors: EINVAL for NULL xyz/idx, B/N/M < 0, M > N, N == 0 < M, a
+ *         misaligned ws;  EUNSUPPORTED for N > MESORASI_MAX_N_FPS;
+ *         EWORKSPACE when ws is too small.
+ * The M iterations are sequential: one workgroup per cloud for small
+ * clouds, several single-wave workgroups per cloud for large ones.
  */
-int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, int32_t* idx, float* cxyz, void* stream);
+int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, int32_t* idx, float* cxyz, void* ws,
+                 size_t ws_bytes, void* stream);
+
+/* Workspace bytes for mesorasi_fps with these sizes (0 when none is
+ * needed).  Returns 0 for invalid sizes as well. */
+size_t mesorasi_fps_workspace(int64_t B, int64_t N, int64_t M);
 
 /*
  * Ball query: neighbor search N (Sec. 3.1 "Neighbor Search") producing the

@@ -30,6 +30,8 @@
 // results in registers.  The iteration is bound by VALU issue for large P
 // (four waves per SIMD at 16 points per thread) and by the reduction chain
 // for small P.
+#include <algorithm>
+
 #include "common.h"
 
 namespace meso {
@@ -226,12 +228,238 @@ static void launch_fps(const float* xyz, int64_t B, int N, int M, int32_t* idx, 
     fps_kernel<T, P, REG><<<dim3((unsigned)B), dim3(T), 0, s>>>(xyz, N, M, idx, cxyz);
 }
 
+// ---------------------------------------------------------------------------
+// Large clouds: G one-wave workgroups per cloud.
+//
+// One CU's vector ALUs bound the single-workgroup kernel once every thread
+// holds 16 points (16384-point clouds: about 1.3 us per iteration).  Here
+// the points are spread over G single-wave workgroups (workgroup g owns the
+// contiguous points [64 P g, 64 P (g + 1)), lane l the P points from
+// 64 P g + P l), so an iteration's update is P points per lane on G CUs,
+// and the workgroups exchange their local winners through global memory:
+//  * the workspace holds, per cloud, 2 x G slots of four 64-bit words,
+//    cleared by a fill kernel before the launch;
+//  * at iteration m each workgroup stores its winner in slot [m % 2][g]:
+//    word 0 = m << 48 | distance bits << 16 | index, words 1-3 = m << 32 |
+//    x, y, z bits.  Every word carries the tag m, so a reader accepts a
+//    slot only when all four words belong to iteration m, whatever order
+//    the stores land in (aligned 64-bit accesses are single-copy atomic);
+//  * lane h < G of every workgroup polls slot [m % 2][h] (agent-scope
+//    atomic loads) until all G carry tag m, then the largest distance wins
+//    and, on ties, the lowest h -- workgroups order the indices, so that is
+//    the lowest index, as in the sequential rule;
+//  * a workgroup publishes iteration m + 2 into the same parity only after
+//    reading every slot of iteration m + 1, which each workgroup writes
+//    only after reading all of iteration m: two parities never lose a
+//    value, and a cleared slot (tag 0) never matches m >= 1.
+// Every wait is bounded: after kFpsSpinCap polls the workgroup sets the
+// error word in the workspace and continues alone with its local winners
+// (valid indices, wrong results), so the kernel always drains.  Waiting
+// needs the cloud's G workgroups resident at once; a launch has at most
+// 8 x ceil(B / 8) x 64 single-wave workgroups, which fit on the chip beside
+// any other kernel's workgroups (those finish without waiting on this one).
+// Workgroups of one cloud are numbered congruent modulo 8 so that the
+// round-robin dispatch puts them on one XCD and their slots in one L2;
+// correctness does not depend on that placement.
+// ---------------------------------------------------------------------------
+
+constexpr int kFpsMaxGroups = 64;   // one polling lane per group
+constexpr int kFpsSpinCap = 1 << 20;
+constexpr size_t kFpsWsHeader = 256;   // error word, then the slots
+
+__global__ void fps_clear_kernel(uint64_t* __restrict__ w, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        w[i] = 0;
+}
+
+__device__ __forceinline__ void ws_store(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ws_load(const uint64_t* p) {
+    return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int P>
+__global__ __launch_bounds__(64) void fps_multi_kernel(const float* __restrict__ xyz, int B, int N, int M, int G,
+                                                       int32_t* __restrict__ idx, float* __restrict__ cxyz,
+                                                       uint64_t* __restrict__ slots, unsigned* __restrict__ err) {
+    // blockIdx -> (cloud, group): ids congruent mod 8 share a cloud
+    const int i = blockIdx.x;
+    const int xcd = i & 7, k = i >> 3;
+    const int b = xcd + 8 * (k / G);
+    const int g = k - (k / G) * G;
+    if (b >= B) return;
+    const int lane = threadIdx.x;
+    const float* __restrict__ p = xyz + (int64_t)b * N * 3;
+    const int base = g * 64 * P + lane * P;
+    uint64_t* __restrict__ cs = slots + (int64_t)b * 2 * G * 4;   // this cloud's [2][G][4] words
+
+    float px[P], py[P], pz[P], dm[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+        const int j = base + q;
+        const bool ok = j < N;
+        px[q] = ok ? p[3 * j + 0] : 0.0f;
+        py[q] = ok ? p[3 * j + 1] : 0.0f;
+        pz[q] = ok ? p[3 * j + 2] : 0.0f;
+        dm[q] = ok ? __builtin_huge_valf() : -1.0f;   // -1 never wins
+    }
+    float cx = p[0], cy = p[1], cz = p[2];
+    // workgroup 0 records the results: iteration m in lane m % 64, stored
+    // 64 iterations at a time
+    int keep_i = 0;
+    float keep_x = cx, keep_y = cy, keep_z = cz;
+    int32_t* __restrict__ out_idx = idx + (int64_t)b * M;
+    float* __restrict__ out_c = cxyz ? cxyz + (int64_t)b * M * 3 : nullptr;
+    auto flush = [&](int m_last) {
+        const int m0 = m_last & ~63;
+        if (m0 + lane <= m_last) {
+            out_idx[m0 + lane] = keep_i;
+            if (out_c) {
+                out_c[3 * (m0 + lane) + 0] = keep_x;
+                out_c[3 * (m0 + lane) + 1] = keep_y;
+                out_c[3 * (m0 + lane) + 2] = keep_z;
+            }
+        }
+    };
+    bool alone = false;   // set once a wait hit the cap
+
+    for (int m = 1; m < M; ++m) {
+        // 1. running minima and this lane's largest (signed-int min/max on
+        //    the bits: values are >= 0 or the -1 sentinel)
+        int tmax = INT32_MIN;
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            const int nm = min(__float_as_int(dist3(px[q], py[q], pz[q], cx, cy, cz)), __float_as_int(dm[q]));
+            dm[q] = __int_as_float(nm);
+            tmax = max(tmax, nm);
+        }
+        // 2. local winner: the lowest lane holding the max, its lowest slot
+        const int wmax = wave_max_i32(tmax);
+        const int wl = __builtin_ctzll(ballot(tmax == wmax));
+        int sq = P - 1;
+#pragma unroll
+        for (int q = P - 1; q >= 0; --q) {
+            const uint64_t hold = ballot(__float_as_int(dm[q]) == wmax);
+            sq = ((hold >> wl) & 1ull) ? q : sq;
+        }
+        sq = __builtin_amdgcn_readfirstlane(sq);
+        const int lj = __builtin_amdgcn_readlane(base + sq, wl);
+        const int lx = __builtin_amdgcn_readlane(__float_as_int(px[sq]), wl);
+        const int ly = __builtin_amdgcn_readlane(__float_as_int(py[sq]), wl);
+        const int lz = __builtin_amdgcn_readlane(__float_as_int(pz[sq]), wl);
+        int sel = lj;
+        int sx = lx, sy = ly, sz = lz;
+        if (!alone) {
+            // 3. publish (every workgroup holds a real point, so wmax >= 0)
+            uint64_t* mine = cs + ((m & 1) * G + g) * 4;
+            const uint64_t tag = (uint64_t)m;
+            if (lane == 0) {
+                ws_store(mine + 0, (tag << 48) | ((uint64_t)(uint32_t)wmax << 16) | (uint64_t)(uint32_t)lj);
+                ws_store(mine + 1, (tag << 32) | (uint32_t)lx);
+                ws_store(mine + 2, (tag << 32) | (uint32_t)ly);
+                ws_store(mine + 3, (tag << 32) | (uint32_t)lz);
+            }
+            // 4. wait for all G slots of iteration m (lane h reads slot h)
+            const uint64_t* theirs = cs + ((m & 1) * G + min(lane, G - 1)) * 4;
+            uint64_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
+            bool ok = lane >= G;
+            for (int spins = 0;; ++spins) {
+                if (!ok) {
+                    w0 = ws_load(theirs + 0);
+                    w1 = ws_load(theirs + 1);
+                    w2 = ws_load(theirs + 2);
+                    w3 = ws_load(theirs + 3);
+                    ok = (w0 >> 48) == tag && (w1 >> 32) == tag && (w2 >> 32) == tag && (w3 >> 32) == tag;
+                }
+                if (ballot(!ok) == 0ull) break;
+                if (spins >= kFpsSpinCap) {
+                    alone = true;
+                    if (lane == 0) atomicOr(err, 1u);
+                    break;
+                }
+            }
+            if (!alone) {
+                // 5. global winner: the largest distance, then the lowest group
+                const int d = lane < G ? (int)((w0 >> 16) & 0x7fffffffull) : INT32_MIN;
+                const int gmax = wave_max_i32(d);
+                const int ww = __builtin_ctzll(ballot(d == gmax));
+                sel = __builtin_amdgcn_readlane((int)(w0 & 0xffffull), ww);
+                sx = __builtin_amdgcn_readlane((int)(uint32_t)w1, ww);
+                sy = __builtin_amdgcn_readlane((int)(uint32_t)w2, ww);
+                sz = __builtin_amdgcn_readlane((int)(uint32_t)w3, ww);
+            }
+        }
+        cx = __int_as_float(sx);
+        cy = __int_as_float(sy);
+        cz = __int_as_float(sz);
+        if (g == 0) {
+            const bool keep = lane == (m & 63);
+            keep_i = keep ? sel : keep_i;
+            keep_x = keep ? cx : keep_x;
+            keep_y = keep ? cy : keep_y;
+            keep_z = keep ? cz : keep_z;
+            if ((m & 63) == 63) flush(m);
+        }
+    }
+    if (g == 0 && ((M - 1) & 63) != 63) flush(M - 1);
+}
+
+// Shape of the multi-workgroup form: P points per lane, G workgroups per
+// cloud (every workgroup holds at least one real point).
+struct FpsMultiPlan {
+    int P, G;
+};
+static FpsMultiPlan fps_multi_plan(int64_t N) {
+    const int P = N <= 8192 ? 4 : (N <= 16384 ? 8 : 16);
+    return {P, (int)ceil_div(N, 64 * P)};
+}
+// The multi-workgroup form runs for clouds above 32768 points, where the
+// single-workgroup kernel can no longer keep the coordinates in registers
+// and re-reads the cloud every iteration (65536 points: 17.5 us per
+// iteration there, 4.6 us here).  Below, one exchange through global memory
+// (about 0.7 us for one tagged word between CUs, 2-2.5 us for this
+// kernel's four-word slots, measured on MI355X) costs more than a whole
+// single-workgroup iteration (0.63 us at 4096 points, 1.29 us at 16384, 2.66
+// us at 32768 against 2.72 us here).
+constexpr int64_t kFpsMultiMinN = 32769;
+
+static bool fps_use_multi(int64_t N, int64_t M) {
+    return N >= kFpsMultiMinN && M >= 2 && fps_multi_plan(N).G <= kFpsMaxGroups;
+}
+
+static size_t fps_ws_bytes(int64_t B, int64_t N, int64_t M) {
+    if (B <= 0 || !fps_use_multi(N, M)) return 0;
+    return kFpsWsHeader + (size_t)B * 2 * fps_multi_plan(N).G * 4 * sizeof(uint64_t);
+}
+
+template <int P>
+static int launch_fps_multi(const float* xyz, int64_t B, int N, int M, int G, int32_t* idx, float* cxyz, void* ws,
+                            hipStream_t s) {
+    uint64_t* slots = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + kFpsWsHeader);
+    unsigned* err = static_cast<unsigned*>(ws);
+    const int64_t words = (int64_t)B * 2 * G * 4;
+    const int64_t clear = words + kFpsWsHeader / 8;
+    fps_clear_kernel<<<dim3((unsigned)std::min<int64_t>(ceil_div(clear, 256), 1024)), dim3(256), 0, s>>>(
+        static_cast<uint64_t*>(ws), clear);
+    int rc = after_launch("mesorasi_fps");
+    if (rc != MESORASI_OK) return rc;
+    const int64_t grid = 8 * ceil_div(B, 8) * G;
+    fps_multi_kernel<P><<<dim3((unsigned)grid), dim3(64), 0, s>>>(xyz, (int)B, N, M, G, idx, cxyz, slots, err);
+    return after_launch("mesorasi_fps");
+}
+
 }  // namespace meso
 
 using namespace meso;
 
-extern "C" int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, int32_t* idx, float* cxyz,
-                            void* stream) {
+extern "C" size_t mesorasi_fps_workspace(int64_t B, int64_t N, int64_t M) {
+    if (B < 0 || N < 0 || M < 0 || M > N || N > MESORASI_MAX_N_FPS) return 0;
+    return fps_ws_bytes(B, N, M);
+}
+
+extern "C" int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, int32_t* idx, float* cxyz, void* ws,
+                            size_t ws_bytes, void* stream) {
     MESO_REQUIRE(B >= 0 && N >= 0 && M >= 0, MESORASI_EINVAL, "mesorasi_fps: negative size (B=%lld N=%lld M=%lld)",
                  (long long)B, (long long)N, (long long)M);
     MESO_REQUIRE(M <= N, MESORASI_EINVAL, "mesorasi_fps: M = %lld > N = %lld", (long long)M, (long long)N);
@@ -240,8 +468,18 @@ extern "C" int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, i
     MESO_REQUIRE(N <= MESORASI_MAX_N_FPS, MESORASI_EUNSUPPORTED, "mesorasi_fps: N = %lld > %d", (long long)N,
                  MESORASI_MAX_N_FPS);
     MESO_REQUIRE(B <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_fps: B too large");
+    const size_t need = fps_ws_bytes(B, N, M);
+    MESO_REQUIRE(ws_bytes >= need && (need == 0 || ws), MESORASI_EWORKSPACE, "mesorasi_fps: workspace %zu < %zu bytes",
+                 ws_bytes, need);
+    MESO_REQUIRE(need == 0 || aligned(ws, 8), MESORASI_EINVAL, "mesorasi_fps: workspace not 8-byte aligned");
     hipStream_t s = as_stream(stream);
     const int n = (int)N, m = (int)M;
+    if (need > 0) {
+        const FpsMultiPlan pl = fps_multi_plan(N);
+        if (pl.P == 4) return launch_fps_multi<4>(xyz, B, n, m, pl.G, idx, cxyz, ws, s);
+        if (pl.P == 8) return launch_fps_multi<8>(xyz, B, n, m, pl.G, idx, cxyz, ws, s);
+        return launch_fps_multi<16>(xyz, B, n, m, pl.G, idx, cxyz, ws, s);
+    }
     // workgroup shape per cloud size, from a sweep on MI355X: the iteration
     // time is a fixed reduction/barrier chain plus P points of VALU work
     if (n <= 128) launch_fps<64, 2, true>(xyz, B, n, m, idx, cxyz, s);

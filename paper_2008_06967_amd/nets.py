@@ -111,7 +111,8 @@ class PointNet2(Net):
             for i, m in enumerate(self.spec["sa"]):
                 idx = self._buf(f"idx{i}", (B, m["M"]), torch.int32)
                 cx = self._buf(f"cxyz{i}", (B, m["M"], 3))
-                ops.fps(p, m["M"], out_idx=idx, out_xyz=cx)
+                ws = self._ws(f"ws_fps{i}", ops.fps_workspace_bytes(B, p.shape[1], m["M"]))
+                ops.fps(p, m["M"], out_idx=idx, out_xyz=cx, ws=ws)
                 e = torch.cuda.Event()
                 e.record(side)
                 ev_fps.append(e)

@@ -47,14 +47,25 @@ def _check_xyz(x: torch.Tensor, name: str):
         f"{name} must be a contiguous float32 [B, N, 3] tensor"
 
 
+def fps_workspace_bytes(B: int, N: int, M: int) -> int:
+    return int(_lib.lib().mesorasi_fps_workspace(B, N, M))
+
+
 def fps(xyz: torch.Tensor, M: int, want_xyz: bool = True, out_idx: torch.Tensor | None = None,
-        out_xyz: torch.Tensor | None = None):
+        out_xyz: torch.Tensor | None = None, ws: torch.Tensor | None = None):
+    """ws: a uint8 device tensor of at least fps_workspace_bytes(B, N, M)
+    (allocated here when needed and not given); its first 4 bytes read 0
+    after the call unless a workgroup gave up waiting (see the C header)."""
     _check_xyz(xyz, "xyz")
     B, N, _ = xyz.shape
     idx = out_idx if out_idx is not None else torch.empty((B, M), dtype=torch.int32, device=xyz.device)
     cxyz = out_xyz if out_xyz is not None else (
         torch.empty((B, M, 3), dtype=torch.float32, device=xyz.device) if want_xyz else None)
-    check(_lib.lib().mesorasi_fps(xyz.data_ptr(), B, N, M, idx.data_ptr(), _ptr(cxyz), _stream()), "fps")
+    need = fps_workspace_bytes(B, N, M)
+    if need and (ws is None or ws.numel() < need):
+        ws = torch.empty(need, dtype=torch.uint8, device=xyz.device)
+    wp, wn = (ws.data_ptr(), ws.numel()) if need else (None, 0)
+    check(_lib.lib().mesorasi_fps(xyz.data_ptr(), B, N, M, idx.data_ptr(), _ptr(cxyz), wp, wn, _stream()), "fps")
     return idx, cxyz
 
 

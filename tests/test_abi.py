@@ -44,13 +44,33 @@ def st(fn, *args):
 
 
 def test_fps_validation():
-    assert st("mesorasi_fps", FAKE, 1, 10, 11, FAKE, NULL, NULL) == _lib.EINVAL          # M > N
-    assert st("mesorasi_fps", FAKE, -1, 10, 5, FAKE, NULL, NULL) == _lib.EINVAL          # B < 0
-    assert st("mesorasi_fps", NULL, 1, 10, 5, FAKE, NULL, NULL) == _lib.EINVAL           # NULL xyz
-    assert st("mesorasi_fps", FAKE, 1, 70000, 5, FAKE, NULL, NULL) == _lib.EUNSUPPORTED  # N too large
-    assert st("mesorasi_fps", NULL, 0, 10, 5, NULL, NULL, NULL) == _lib.OK               # empty batch
-    st("mesorasi_fps", FAKE, 1, 10, 11, FAKE, NULL, NULL)
+    f = "mesorasi_fps"
+    assert st(f, FAKE, 1, 10, 11, FAKE, NULL, NULL, 0, NULL) == _lib.EINVAL          # M > N
+    assert st(f, FAKE, -1, 10, 5, FAKE, NULL, NULL, 0, NULL) == _lib.EINVAL          # B < 0
+    assert st(f, NULL, 1, 10, 5, FAKE, NULL, NULL, 0, NULL) == _lib.EINVAL           # NULL xyz
+    assert st(f, FAKE, 1, 70000, 5, FAKE, NULL, NULL, 0, NULL) == _lib.EUNSUPPORTED  # N too large
+    assert st(f, NULL, 0, 10, 5, NULL, NULL, NULL, 0, NULL) == _lib.OK               # empty batch
+    st(f, FAKE, 1, 10, 11, FAKE, NULL, NULL, 0, NULL)
     assert b"M = 11" in _lib.lib().mesorasi_last_error()
+
+
+def test_fps_workspace():
+    """Small clouds run one workgroup per cloud and need no workspace; large
+    ones exchange winners through one, which must be big enough and 8-byte
+    aligned."""
+    L = _lib.lib()
+    f = "mesorasi_fps"
+    assert L.mesorasi_fps_workspace(32, 1024, 512) == 0
+    assert L.mesorasi_fps_workspace(4, 16384, 4096) == 0
+    need = L.mesorasi_fps_workspace(4, 40000, 4096)
+    assert need > 0 and need % 8 == 0
+    assert L.mesorasi_fps_workspace(8, 40000, 4096) > need                           # grows with the batch
+    assert L.mesorasi_fps_workspace(4, 40000, 1) == 0                                # nothing to exchange
+    assert L.mesorasi_fps_workspace(4, 100, 200) == 0                                # invalid sizes
+    assert st(f, FAKE, 4, 40000, 4096, FAKE, NULL, NULL, 0, NULL) == _lib.EWORKSPACE
+    assert st(f, FAKE, 4, 40000, 4096, FAKE, NULL, FAKE, need - 8, NULL) == _lib.EWORKSPACE
+    assert st(f, FAKE, 4, 40000, 4096, FAKE, NULL, ctypes.c_void_p(0x1004), need, NULL) == _lib.EINVAL
+    assert b"aligned" in L.mesorasi_last_error()
 
 
 def test_ball_query_validation():

@@ -23,12 +23,23 @@ def test_fps_work_and_latency_fields():
     assert extra == {"serial_iterations": 9, "workgroups": 3}
 
 
-def test_ball_query_work_counts_every_candidate_and_compulsory_bytes():
-    xyz, q = torch.zeros(2, 50, 3), torch.zeros(2, 7, 3)
-    kind, amount, extra = bench.call_work("ball_query", (xyz, q, 0.1, 16), {})
+def test_ball_query_work_counts_the_scanned_pairs():
+    """A query whose K slots fill scans up to its K-th hit; a short list
+    (padded with its first hit) scans all N points.  Without the output
+    the worst case B * M * N is credited."""
+    xyz, q = torch.zeros(2, 50, 3), torch.zeros(2, 3, 3)
+    K = 4
+    nit = torch.tensor([[[0, 3, 9, 12], [5, 5, 5, 5], [1, 2, 3, 4]],
+                        [[7, 7, 7, 7], [10, 20, 30, 49], [0, 1, 2, 3]]], dtype=torch.int32)
+    kind, amount, extra = bench.call_work("ball_query", (xyz, q, 0.1, K), {}, (nit, None))
+    scanned = 13 + 50 + 5 + 50 + 50 + 4
     assert kind == "alu"
-    assert amount == pytest.approx(8.0 * 2 * 7 * 50 / 1e12)
-    assert extra["compulsory_bytes"] == 12 * 2 * 50 + 12 * 2 * 7 + 4 * 2 * 7 * 16 + 4 * 2 * 7
+    assert extra["scanned_pairs"] == scanned
+    assert amount == pytest.approx(8.0 * scanned / 1e12)
+    assert extra["worst_case_pairs"] == 2 * 3 * 50
+    assert extra["compulsory_bytes"] == 12 * 2 * 50 + 12 * 2 * 3 + 4 * 2 * 3 * K
+    _, amount, _ = bench.call_work("ball_query", (xyz, q, 0.1, K), {})
+    assert amount == pytest.approx(8.0 * 2 * 3 * 50 / 1e12)
 
 
 def test_knn_self_query_reads_the_reference_once():
@@ -42,11 +53,15 @@ def test_knn_self_query_reads_the_reference_once():
 
 
 def test_mlp_work_sums_every_layer():
-    prm = types.SimpleNamespace(dims=[3, 64, 64, 128])
+    prm = types.SimpleNamespace(dims=[3, 64, 64, 128], dtype=0)
     x0 = torch.zeros(4, 256, 3)
-    kind, amount, _ = bench.call_work("pointwise_mlp", (x0, prm), {})
+    out = torch.zeros(4, 256, 128)
+    kind, amount, extra = bench.call_work("pointwise_mlp", (x0, prm), {}, out)
     assert kind == "mfma"
     assert amount == pytest.approx(2.0 * 1024 * (3 * 64 + 64 * 64 + 64 * 128) / 1e12)
+    # compulsory bytes of a fused MLP: input rows, output rows, weights
+    assert extra["compulsory_bytes_mlp"] == 1024 * 3 * 4 + 1024 * 128 * 4 + (3 * 64 + 64 * 64 + 64 * 128) * 4
+    assert extra["bf16"] is False
 
 
 def test_aggregation_compulsory_bytes():
@@ -75,3 +90,11 @@ def test_recorded_traffic_matches_its_source_hash():
         else:
             assert got is None
     assert bench.load_traffic("no_such_kernel#0@nowhere") is None
+
+
+def test_cpu_threads_respects_the_job_share(monkeypatch):
+    avail = len(os.sched_getaffinity(0))
+    monkeypatch.setenv("OMP_NUM_THREADS", "1")
+    assert bench.cpu_threads() == (1, avail)
+    monkeypatch.delenv("OMP_NUM_THREADS")
+    assert bench.cpu_threads() == (avail, avail)

@@ -57,8 +57,16 @@ FPS_CASES = [
     ("n9000", 1, 9000, 300, "normal"),
     ("lidar_sa1", 1, 16384, 4096, "lidar"),
     ("n20000", 1, 20000, 64, "normal"),
-    ("n32769_global_path", 1, 32769, 40, "normal"),   # coordinates re-read from memory per iteration
+    ("n32768_global_path", 1, 32768, 40, "normal"),   # coordinates re-read from memory per iteration
     ("n_max", 1, 65536, 24, "normal"),                # the documented maximum cloud size
+    # more than 32768 points: several single-wave workgroups per cloud that
+    # exchange their winners through the workspace
+    ("multi_b9_ragged_last_group", 9, 32769, 100, "normal"),   # batch not a multiple of 8; last group 1 point
+    ("multi_grid_ties", 2, 40000, 500, "grid"),        # equal distances across groups
+    ("multi_dups", 2, 40000, 400, "dups"),            # minima reach 0; re-selection
+    ("multi_m2", 4, 33000, 2, "normal"),
+    ("multi_m65", 3, 33000, 65, "normal"),             # one result block plus one
+    ("multi_n_max", 2, 65536, 300, "normal"),
 ]
 
 
@@ -81,9 +89,14 @@ def _points(kind, B, N, r):
 def test_fps_bit_exact(gpu, name, B, N, M, kind):
     x = _points(kind, B, N, g(1))
     ri, rc = O.fps(x, M)
-    idx, cxyz = ops.fps(dev(x), M)
+    need = ops.fps_workspace_bytes(B, N, M)
+    # a workspace full of stale bytes: the call clears it itself
+    ws = torch.full((max(need, 8),), 0x5A, dtype=torch.uint8, device="cuda")
+    idx, cxyz = ops.fps(dev(x), M, ws=ws)
     assert np.array_equal(host(idx), ri)
     assert np.array_equal(host(cxyz), rc)
+    if need:
+        assert int(ws[:4].view(torch.int32).item()) == 0     # no workgroup gave up waiting
 
 
 # ----------------------------------------------------------------------------
