@@ -84,7 +84,8 @@ class StageTimer:
     """Wraps the ops entry points so every call records a start/end event on
     the stream it is launched on."""
 
-    NAMES = ("fps", "ball_query", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3")
+    NAMES = ("fps", "ball_query", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3",
+             "three_nn", "interpolate3_apply")
 
     def __init__(self, ops):
         import torch
@@ -157,7 +158,9 @@ def call_work(name, a, kw, result=None):
                     the centroid indices or rows, the output -> hbm (the
                     bytes of the gathered rows are reported beside it)
     conventional:   2 * B*M*K * sum(C_l * C_l+1) -> mfma
-    interpolate3:   B * Nd * Ns pairs, 8 flops each -> alu
+    interpolate3, three_nn: B * Nd * Ns pairs, 8 flops each -> alu
+    interpolate3_apply: compulsory HBM bytes (source rows once, neighbours
+                    and distances, output) -> hbm
     """
     def arg(i, key, default=None):
         return a[i] if len(a) > i else kw.get(key, default)
@@ -216,9 +219,16 @@ def call_work(name, a, kw, result=None):
         rows = int(np.prod(nit.shape))
         d = prm.dims
         return ("mfma", 2.0 * rows * sum(x * y for x, y in zip(d[:-1], d[1:])) / 1e12, None)
-    if name == "interpolate3":
+    if name in ("interpolate3", "three_nn"):
         dst, src = arg(0, "xyz_dst"), arg(1, "xyz_src")
         return ("alu", 8.0 * dst.shape[0] * dst.shape[1] * src.shape[1] / 1e12, None)
+    if name == "interpolate3_apply":
+        nit, f = arg(0, "nit"), arg(2, "f_src")
+        B, Nd = nit.shape[0], nit.shape[1]
+        Ns, C = f.shape[1], f.shape[-1]
+        # every source row once, the neighbours and distances, the output
+        comp = 4 * B * Ns * C + 24 * B * Nd + 4 * B * Nd * C
+        return ("hbm", comp / 1e9, {"logical_gather_bytes": 12 * B * Nd * C})
     return None
 
 

@@ -294,6 +294,29 @@ int mesorasi_interpolate3(const float* xyz_dst, const float* xyz_src, const floa
                           int64_t B, int64_t Nd, int64_t Ns, int32_t C, float* f_dst, int64_t ld_dst, void* stream);
 
 /*
+ * The two halves of mesorasi_interpolate3 (three_nn and three_interpolate
+ * of the same baseline, Sec. 6), so that the search, which needs only
+ * coordinates, can run as soon as both levels are sampled, apart from the
+ * interpolation, which waits for the coarse features.
+ * mesorasi_three_nn: for every destination, its 3 nearest sources in
+ * (distance, index) order (the kNN rule, C = 3) and their squared
+ * distances -- the same values mesorasi_knn returns with K = 3.
+ *   xyz_dst [B, Nd, 3], xyz_src [B, Ns, 3] float32
+ *   nit [B, Nd, 3] int32 out, dist [B, Nd, 3] float32 out
+ * Errors: EINVAL for NULL pointers, sizes < 0, Ns < 3.
+ * mesorasi_interpolate3_apply: f_dst = sum_k w_k f_src[nit_k] / sum_k w_k
+ * with w_k = 1 / max(dist_k, 1e-10), in the fp32 operations of
+ * mesorasi_interpolate3 (so the two give identical results).
+ *   nit [B, Nd, 3] int32 (0 <= index < Ns), dist [B, Nd, 3] float32
+ *   f_src [B, Ns, ld_src], f_dst [B, Nd, ld_dst] float32 (first C columns)
+ * Errors: EINVAL for NULL pointers, sizes < 0, Ns < 1, C < 1, ld < C.
+ */
+int mesorasi_three_nn(const float* xyz_dst, const float* xyz_src, int64_t B, int64_t Nd, int64_t Ns, int32_t* nit,
+                      float* dist, void* stream);
+int mesorasi_interpolate3_apply(const int32_t* nit, const float* dist, const float* f_src, int64_t ld_src, int64_t B,
+                                int64_t Nd, int64_t Ns, int32_t C, float* f_dst, int64_t ld_dst, void* stream);
+
+/*
  * float32 -> bf16 bits, round to nearest even (weights and inputs of the
  * bf16 MLP variant).  x [n] float32, y [n] uint16 out.
  * Errors: EINVAL for NULL pointers or n < 0.

@@ -17,6 +17,7 @@
 // over the 3 nearest coarse points (the three_interpolate kernel of the
 // PointNet++ segmentation baseline, Sec. 6 "Software Setup"); layout at the
 // kernel.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -795,11 +796,15 @@ __device__ __forceinline__ void top3_insert(float d, int j, float (&e)[3], int (
 // (sources read four at a time with 16-byte LDS broadcasts).  The four
 // lists are merged per destination in (distance, index) order, then the
 // workgroup interpolates all channels with coalesced row reads.
+// SEARCH_ONLY: stop after the merge and write the three indices and squared
+// distances (nit, dist [B, Nd, 3]) instead of interpolating.
+template <bool SEARCH_ONLY>
 __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __restrict__ xyz_dst,
                                                                 const float* __restrict__ xyz_src,
                                                                 const float* __restrict__ f_src, int64_t lds, int Nd,
                                                                 int Ns, int C, float* __restrict__ f_dst, int64_t ldd,
-                                                                int dblocks, int vec4) {
+                                                                int dblocks, int vec4, int32_t* __restrict__ nn_out,
+                                                                float* __restrict__ d_out) {
     __shared__ __attribute__((aligned(16))) float sx[kIpChunk + 16], sy[kIpChunk + 16], sz[kIpChunk + 16];
     __shared__ float s_e[kIpWaves][kIpDests][3];
     __shared__ int s_jj[kIpWaves][kIpDests][3];
@@ -875,19 +880,31 @@ __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __r
         for (int w = 0; w < kIpWaves; ++w)
 #pragma unroll
             for (int k = 0; k < 3; ++k) top3_insert(s_e[w][tid][k], s_jj[w][tid][k], f, fj);
-        const float w0 = 1.0f / fmaxf(f[0], 1e-10f);
-        const float w1 = 1.0f / fmaxf(f[1], 1e-10f);
-        const float w2 = 1.0f / fmaxf(f[2], 1e-10f);
-        const float ws = w0 + w1 + w2;
-        // with Ns >= 3 every slot holds a source (any source precedes an empty
-        // slot); the min only keeps the row reads below inside f_src
-        s_j[tid][0] = min(fj[0], Ns - 1);
-        s_j[tid][1] = min(fj[1], Ns - 1);
-        s_j[tid][2] = min(fj[2], Ns - 1);
-        s_w[tid][0] = w0 / ws;
-        s_w[tid][1] = w1 / ws;
-        s_w[tid][2] = w2 / ws;
+        if constexpr (SEARCH_ONLY) {
+            const int i = d0 + tid;
+            if (i < Nd) {
+#pragma unroll
+                for (int k = 0; k < 3; ++k) {
+                    nn_out[(b * Nd + i) * 3 + k] = min(fj[k], Ns - 1);
+                    d_out[(b * Nd + i) * 3 + k] = f[k];
+                }
+            }
+        } else {
+            const float w0 = 1.0f / fmaxf(f[0], 1e-10f);
+            const float w1 = 1.0f / fmaxf(f[1], 1e-10f);
+            const float w2 = 1.0f / fmaxf(f[2], 1e-10f);
+            const float ws = w0 + w1 + w2;
+            // with Ns >= 3 every slot holds a source (any source precedes an
+            // empty slot); the min only keeps the row reads below inside f_src
+            s_j[tid][0] = min(fj[0], Ns - 1);
+            s_j[tid][1] = min(fj[1], Ns - 1);
+            s_j[tid][2] = min(fj[2], Ns - 1);
+            s_w[tid][0] = w0 / ws;
+            s_w[tid][1] = w1 / ws;
+            s_w[tid][2] = w2 / ws;
+        }
     }
+    if constexpr (SEARCH_ONLY) return;
     __syncthreads();
     const int nd = min(kIpDests, Nd - d0);
     const float* fs = f_src + b * (int64_t)Ns * lds;
@@ -914,6 +931,46 @@ __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __r
         const float v = s_w[r][0] * fs[(int64_t)s_j[r][0] * lds + c] + s_w[r][1] * fs[(int64_t)s_j[r][1] * lds + c] +
                         s_w[r][2] * fs[(int64_t)s_j[r][2] * lds + c];
         f_dst[(b * Nd + d0 + r) * ldd + c] = v;
+    }
+}
+
+// Interpolation from precomputed neighbours: thread e of the grid-stride
+// loop takes destination e / C4 and four channels (or one channel without
+// 16-byte rows).  The weights are those of interp3_kernel, in the same fp32
+// operations, so the two paths agree bit for bit.
+template <bool VEC4>
+__global__ __launch_bounds__(256) void interp3_apply_kernel(const int32_t* __restrict__ nn, const float* __restrict__ dd,
+                                                            const float* __restrict__ f_src, int64_t lds, int64_t Nd,
+                                                            int Ns, int C, int64_t total, float* __restrict__ f_dst,
+                                                            int64_t ldd) {
+    const int cw = VEC4 ? C >> 2 : C;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = e / cw;                // global destination b * Nd + i
+        const int c = (int)(e - r * cw) * (VEC4 ? 4 : 1);
+        const int64_t b = r / Nd;
+        const float w0 = 1.0f / fmaxf(dd[r * 3 + 0], 1e-10f);
+        const float w1 = 1.0f / fmaxf(dd[r * 3 + 1], 1e-10f);
+        const float w2 = 1.0f / fmaxf(dd[r * 3 + 2], 1e-10f);
+        const float ws = w0 + w1 + w2;
+        const float u0 = w0 / ws, u1 = w1 / ws, u2 = w2 / ws;
+        const float* fs = f_src + b * (int64_t)Ns * lds;
+        const float* a0 = fs + (int64_t)nn[r * 3 + 0] * lds + c;
+        const float* a1 = fs + (int64_t)nn[r * 3 + 1] * lds + c;
+        const float* a2 = fs + (int64_t)nn[r * 3 + 2] * lds + c;
+        float* o = f_dst + r * ldd + c;
+        if constexpr (VEC4) {
+            const float4 x0 = *reinterpret_cast<const float4*>(a0);
+            const float4 x1 = *reinterpret_cast<const float4*>(a1);
+            const float4 x2 = *reinterpret_cast<const float4*>(a2);
+            float4 v;
+            v.x = u0 * x0.x + u1 * x1.x + u2 * x2.x;
+            v.y = u0 * x0.y + u1 * x1.y + u2 * x2.y;
+            v.z = u0 * x0.z + u1 * x1.z + u2 * x2.z;
+            v.w = u0 * x0.w + u1 * x1.w + u2 * x2.w;
+            *reinterpret_cast<float4*>(o) = v;
+        } else {
+            *o = u0 * *a0 + u1 * *a1 + u2 * *a2;
+        }
     }
 }
 
@@ -1000,7 +1057,43 @@ extern "C" int mesorasi_interpolate3(const float* xyz_dst, const float* xyz_src,
     const int64_t blocks = B * dblocks;
     MESO_REQUIRE(blocks <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_interpolate3: too many points");
     const int vec4 = C % 4 == 0 && ld_src % 4 == 0 && ld_dst % 4 == 0 && aligned(f_src, 16) && aligned(f_dst, 16);
-    interp3_kernel<<<dim3((unsigned)blocks), dim3(64 * kIpWaves), 0, as_stream(stream)>>>(
-        xyz_dst, xyz_src, f_src, ld_src, (int)Nd, (int)Ns, C, f_dst, ld_dst, dblocks, vec4);
+    interp3_kernel<false><<<dim3((unsigned)blocks), dim3(64 * kIpWaves), 0, as_stream(stream)>>>(
+        xyz_dst, xyz_src, f_src, ld_src, (int)Nd, (int)Ns, C, f_dst, ld_dst, dblocks, vec4, nullptr, nullptr);
     return after_launch("mesorasi_interpolate3");
+}
+
+extern "C" int mesorasi_three_nn(const float* xyz_dst, const float* xyz_src, int64_t B, int64_t Nd, int64_t Ns,
+                                 int32_t* nit, float* dist, void* stream) {
+    MESO_REQUIRE(B >= 0 && Nd >= 0 && Ns >= 0, MESORASI_EINVAL, "mesorasi_three_nn: negative size");
+    if (B == 0 || Nd == 0) return MESORASI_OK;
+    MESO_REQUIRE(Ns >= 3, MESORASI_EINVAL, "mesorasi_three_nn: Ns = %lld < 3", (long long)Ns);
+    MESO_REQUIRE(xyz_dst && xyz_src && nit && dist, MESORASI_EINVAL, "mesorasi_three_nn: NULL pointer");
+    MESO_REQUIRE(Nd <= 0x7fffffff && Ns <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_three_nn: size");
+    const int dblocks = (int)ceil_div(Nd, kIpDests);
+    const int64_t blocks = B * dblocks;
+    MESO_REQUIRE(blocks <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_three_nn: too many points");
+    interp3_kernel<true><<<dim3((unsigned)blocks), dim3(64 * kIpWaves), 0, as_stream(stream)>>>(
+        xyz_dst, xyz_src, nullptr, 0, (int)Nd, (int)Ns, 1, nullptr, 0, dblocks, 0, nit, dist);
+    return after_launch("mesorasi_three_nn");
+}
+
+extern "C" int mesorasi_interpolate3_apply(const int32_t* nit, const float* dist, const float* f_src, int64_t ld_src,
+                                           int64_t B, int64_t Nd, int64_t Ns, int32_t C, float* f_dst, int64_t ld_dst,
+                                           void* stream) {
+    MESO_REQUIRE(B >= 0 && Nd >= 0 && Ns >= 0, MESORASI_EINVAL, "mesorasi_interpolate3_apply: negative size");
+    MESO_REQUIRE(C >= 1 && ld_src >= C && ld_dst >= C, MESORASI_EINVAL, "mesorasi_interpolate3_apply: C / ld");
+    if (B == 0 || Nd == 0) return MESORASI_OK;
+    MESO_REQUIRE(Ns >= 1, MESORASI_EINVAL, "mesorasi_interpolate3_apply: Ns = 0");
+    MESO_REQUIRE(nit && dist && f_src && f_dst, MESORASI_EINVAL, "mesorasi_interpolate3_apply: NULL pointer");
+    MESO_REQUIRE(Ns <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_interpolate3_apply: size");
+    const bool vec4 = C % 4 == 0 && ld_src % 4 == 0 && ld_dst % 4 == 0 && aligned(f_src, 16) && aligned(f_dst, 16);
+    const int64_t total = B * Nd * (vec4 ? C / 4 : C);
+    const dim3 grid((unsigned)std::min<int64_t>(ceil_div(total, 256), 8192)), block(256);
+    if (vec4)
+        interp3_apply_kernel<true><<<grid, block, 0, as_stream(stream)>>>(nit, dist, f_src, ld_src, Nd, (int)Ns, C,
+                                                                         total, f_dst, ld_dst);
+    else
+        interp3_apply_kernel<false><<<grid, block, 0, as_stream(stream)>>>(nit, dist, f_src, ld_src, Nd, (int)Ns, C,
+                                                                          total, f_dst, ld_dst);
+    return after_launch("mesorasi_interpolate3_apply");
 }

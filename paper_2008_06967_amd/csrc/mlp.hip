@@ -881,8 +881,20 @@ static MlpWs mlp_ws_layout(int64_t rows, int n_layers, const int32_t* dims, int 
     }
     return w;
 }
-static size_t mlp_ws_bytes(int64_t rows, int n_layers, const int32_t* dims, int dtype) {
-    if (fused_mlp_supported(n_layers, dims, dtype)) return 0;
+// The fused narrow kernel or the layer-by-layer GEMM (measured on MI355X):
+// the fused kernel wins on neighbour rows gathered in its loader (the
+// conventional and limited modules) and on up to 32768 plain rows (32768 x
+// 3 -> 64 -> 64 -> 128: 21.0 against 24.2 us); above, the GEMM's larger
+// tiles win (65536 x 131 -> 128 -> 128 -> 128: 102 against 127 us; 65536 x
+// 128 -> 128 -> 13: 45 against 71 us; 65536 x 6 -> 32 -> 32 -> 64: 22.6
+// against 27.2 us).
+constexpr int64_t kFusedMaxPlainRows = 32768;
+static bool use_fused(int64_t rows, int n_layers, const int32_t* dims, int dtype, bool neighbor_rows) {
+    return fused_mlp_supported(n_layers, dims, dtype) && (neighbor_rows || rows <= kFusedMaxPlainRows);
+}
+
+static size_t mlp_ws_bytes(int64_t rows, int n_layers, const int32_t* dims, int dtype, bool neighbor_rows) {
+    if (use_fused(rows, n_layers, dims, dtype, neighbor_rows)) return 0;
     const MlpWs w = mlp_ws_layout(rows, n_layers, dims, dtype);
     return w.act + w.part;
 }
@@ -1007,8 +1019,8 @@ static int check_mlp_spec(const char* who, int64_t rows, int n_layers, const int
 static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
                    int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
                    uint32_t relu_mask, int dtype, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, void* ws,
-                   hipStream_t s, const MlpGather* g = nullptr) {
-    if (fused_mlp_supported(n_layers, dims, dtype))
+                   hipStream_t s, bool neighbor_rows, const MlpGather* g = nullptr) {
+    if (use_fused(rows, n_layers, dims, dtype, neighbor_rows))
         return run_fused_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, out_dtype, y, ld_y,
                              pool_group, s, g);
     const bool bf16 = dtype == MESORASI_BF16;
@@ -1170,7 +1182,7 @@ extern "C" size_t mesorasi_pointwise_mlp_workspace(int64_t rows, int32_t n_layer
                                                    int64_t pool_group) {
     (void)pool_group;
     if (check_mlp_spec("mesorasi_pointwise_mlp_workspace", rows, n_layers, dims, dtype) != MESORASI_OK) return 0;
-    return mlp_ws_bytes(rows, n_layers, dims, dtype);
+    return mlp_ws_bytes(rows, n_layers, dims, dtype, false);
 }
 
 // Argument checks shared by both MLP entry points (host only, no HIP call).
@@ -1210,11 +1222,11 @@ extern "C" int mesorasi_pointwise_mlp(const float* x0, int32_t c0, int64_t ld0, 
     const int rc = check_mlp_args(who, x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, relu_mask, dtype,
                                   out_dtype, y, ld_y, pool_group);
     if (rc != MESORASI_OK || rows == 0) return rc;
-    const size_t need = mlp_ws_bytes(rows, n_layers, dims, dtype);
+    const size_t need = mlp_ws_bytes(rows, n_layers, dims, dtype, false);
     MESO_REQUIRE(ws_bytes >= need && (need == 0 || ws), MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who,
                  ws_bytes, need);
     return run_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, dtype, out_dtype, y, ld_y,
-                   pool_group, ws, as_stream(stream));
+                   pool_group, ws, as_stream(stream), false);
 }
 
 // ---------------------------------------------------------------------------
@@ -1258,7 +1270,7 @@ extern "C" int mesorasi_pointwise_mlp_noalloc(const float* x0, int32_t c0, int64
     int rc = check_mlp_args(who, x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, relu_mask, dtype, out_dtype, y,
                             ld_y, pool_group);
     if (rc != MESORASI_OK || rows == 0) return rc;
-    const size_t need = mlp_ws_bytes(rows, n_layers, dims, dtype);
+    const size_t need = mlp_ws_bytes(rows, n_layers, dims, dtype, false);
     MESO_REQUIRE(need <= (size_t)MESORASI_NOALLOC_WS_BYTES, MESORASI_EUNSUPPORTED,
                  "%s: needs %zu bytes of scratch, above the fixed %zu", who, need,
                  (size_t)MESORASI_NOALLOC_WS_BYTES);
@@ -1270,7 +1282,7 @@ extern "C" int mesorasi_pointwise_mlp_noalloc(const float* x0, int32_t c0, int64
     // the activations and split-K partials are written before they are
     // read, so nothing in the array needs clearing between calls
     return run_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, dtype, out_dtype, y, ld_y,
-                   pool_group, ws, as_stream(stream));
+                   pool_group, ws, as_stream(stream), false);
 }
 
 extern "C" size_t mesorasi_conventional_workspace(int64_t B, int64_t M, int32_t K, int32_t n_layers,
@@ -1278,7 +1290,7 @@ extern "C" size_t mesorasi_conventional_workspace(int64_t B, int64_t M, int32_t 
     if (B < 0 || M < 0 || K < 1) return 0;
     const int64_t rows = B * M * K;
     if (check_mlp_spec("mesorasi_conventional_workspace", rows, n_layers, dims, dtype) != MESORASI_OK) return 0;
-    return align256((size_t)rows * (size_t)dims[0] * 4) + mlp_ws_bytes(rows, n_layers, dims, dtype);
+    return align256((size_t)rows * (size_t)dims[0] * 4) + mlp_ws_bytes(rows, n_layers, dims, dtype, true);
 }
 
 extern "C" int mesorasi_conventional_module(const float* xyz, const float* feat, int32_t cf, int64_t ld_f,
@@ -1309,7 +1321,7 @@ extern "C" int mesorasi_conventional_module(const float* xyz, const float* feat,
     else MESO_REQUIRE(feat != nullptr, MESORASI_EINVAL, "%s: NULL feat", who);
     for (int l = 0; l < n_layers; ++l) MESO_REQUIRE(W[l] != nullptr, MESORASI_EINVAL, "%s: W[%d] is NULL", who, l);
     const size_t nfm_bytes = align256((size_t)rows * (size_t)cin * 4);
-    const size_t need = nfm_bytes + mlp_ws_bytes(rows, n_layers, dims, dtype);
+    const size_t need = nfm_bytes + mlp_ws_bytes(rows, n_layers, dims, dtype, true);
     MESO_REQUIRE(ws && ws_bytes >= need, MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who, ws_bytes, need);
     MESO_REQUIRE(N <= 0x7fffffff && M <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: size", who);
     hipStream_t s = as_stream(stream);
@@ -1322,7 +1334,8 @@ extern "C" int mesorasi_conventional_module(const float* xyz, const float* feat,
         if (fused_mlp_supported(n_layers, dims, dtype) || split_ok(a0, false)) {
             const MlpGather g{nit, M * K, N, K, cxyz};
             return run_mlp(xyz, 3, 3, cf > 0 ? feat : nullptr, cf, cf > 0 ? ld_f : 0, rows, n_layers, dims, W, bias,
-                           relu_mask, dtype, MESORASI_F32, out, ld_out, K, static_cast<char*>(ws) + nfm_bytes, s, &g);
+                           relu_mask, dtype, MESORASI_F32, out, ld_out, K, static_cast<char*>(ws) + nfm_bytes, s, true,
+                           &g);
         }
     }
     float* nfm = static_cast<float*>(ws);
@@ -1335,7 +1348,7 @@ extern "C" int mesorasi_conventional_module(const float* xyz, const float* feat,
     rc = after_launch(who);
     if (rc != MESORASI_OK) return rc;
     return run_mlp(nfm, cin, cin, nullptr, 0, 0, rows, n_layers, dims, W, bias, relu_mask, dtype, MESORASI_F32, out,
-                   ld_out, K, static_cast<char*>(ws) + nfm_bytes, s);
+                   ld_out, K, static_cast<char*>(ws) + nfm_bytes, s, true);
 }
 
 extern "C" size_t mesorasi_ltd_workspace(int64_t B, int64_t M, int32_t K, int32_t n_layers, const int32_t* dims,
@@ -1343,7 +1356,7 @@ extern "C" size_t mesorasi_ltd_workspace(int64_t B, int64_t M, int32_t K, int32_
     if (B < 0 || M < 0 || K < 1 || n_layers < 1) return 0;
     const int64_t rows = B * M * K;
     if (check_mlp_spec("mesorasi_ltd_workspace", rows, n_layers, dims, dtype) != MESORASI_OK) return 0;
-    return align256((size_t)rows * (size_t)dims[0] * 4) + mlp_ws_bytes(rows, n_layers, dims, dtype);
+    return align256((size_t)rows * (size_t)dims[0] * 4) + mlp_ws_bytes(rows, n_layers, dims, dtype, true);
 }
 
 extern "C" int mesorasi_ltd_module(const float* p1, int64_t ld_p, const float* q, int64_t ld_q, const float* b1,
@@ -1368,7 +1381,7 @@ extern "C" int mesorasi_ltd_module(const float* p1, int64_t ld_p, const float* q
     MESO_REQUIRE(p1 && q && nit && out && W, MESORASI_EINVAL, "%s: NULL p1, q, nit, out or W", who);
     for (int l = 0; l < n_layers; ++l) MESO_REQUIRE(W[l] != nullptr, MESORASI_EINVAL, "%s: W[%d] is NULL", who, l);
     const size_t h1_bytes = align256((size_t)rows * (size_t)C1 * 4);
-    const size_t need = h1_bytes + mlp_ws_bytes(rows, n_layers, dims, dtype);
+    const size_t need = h1_bytes + mlp_ws_bytes(rows, n_layers, dims, dtype, true);
     MESO_REQUIRE(ws && ws_bytes >= need, MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who, ws_bytes, need);
     MESO_REQUIRE(N <= 0x7fffffff && M <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: size", who);
     hipStream_t s = as_stream(stream);
@@ -1380,7 +1393,7 @@ extern "C" int mesorasi_ltd_module(const float* p1, int64_t ld_p, const float* q
         // layer's loader (fused kernel or gathered GEMM), never in memory
         const MlpGather g{nit, M * K, N, K, nullptr, q, ld_q, b1};
         return run_mlp(p1, C1, ld_p, nullptr, 0, 0, rows, n_layers, dims, W, bias, relu_mask, dtype, MESORASI_F32,
-                       out, ld_out, K, static_cast<char*>(ws) + h1_bytes, s, &g);
+                       out, ld_out, K, static_cast<char*>(ws) + h1_bytes, s, true, &g);
     }
     float* h1 = static_cast<float*>(ws);
     const int64_t work = rows * (vec ? C1 / 4 : C1);
@@ -1394,5 +1407,5 @@ extern "C" int mesorasi_ltd_module(const float* p1, int64_t ld_p, const float* q
     rc = after_launch(who);
     if (rc != MESORASI_OK) return rc;
     return run_mlp(h1, C1, C1, nullptr, 0, 0, rows, n_layers, dims, W, bias, relu_mask, dtype, MESORASI_F32, out,
-                   ld_out, K, static_cast<char*>(ws) + h1_bytes, s);
+                   ld_out, K, static_cast<char*>(ws) + h1_bytes, s, true);
 }

@@ -122,6 +122,19 @@ class PointNet2(Net):
                 e.record(side)
                 ev_bq.append(e)
                 p = cx
+            # the feature-propagation searches need only the sampled
+            # coordinates: done here, off the critical path (three_nn)
+            self.ev_nn = []
+            if self.fp:
+                lv = [xyz] + [self._bufs[f"cxyz{i}"] for i in range(len(self.spec["sa"]))]
+                for i in range(len(self.fp)):
+                    fine, coarse = lv[len(lv) - 2 - i], lv[len(lv) - 1 - i]
+                    nn = self._buf(f"nn{i}", (B, fine.shape[1], 3), torch.int32)
+                    nd = self._buf(f"nnd{i}", (B, fine.shape[1], 3))
+                    ops.three_nn(fine, coarse, out_nit=nn, out_dist=nd)
+                    e = torch.cuda.Event()
+                    e.record(side)
+                    self.ev_nn.append(e)
         return ev_fps, ev_bq
 
     def _sa_levels(self, xyz, feat):
@@ -187,12 +200,14 @@ class PointNet2(Net):
                 ops.pointwise_mlp(g, self.fc, relu_mask=(1 << (self.fc.n - 1)) - 1, out=logits, ws=ws)
                 res["out"] = logits
         if self.fp:
+            main = torch.cuda.current_stream(self.device)
             coarse_xyz, coarse_f = levels[-1]
             for i, prm in enumerate(self.fp):
                 fine_xyz, fine_f = levels[len(levels) - 2 - i]
                 Nf = fine_xyz.shape[1]
                 interp = self._buf(f"interp{i}", (B, Nf, coarse_f.shape[-1]))
-                ops.interpolate3(fine_xyz, coarse_xyz, coarse_f, out=interp)
+                main.wait_event(self.ev_nn[i])
+                ops.interpolate3_apply(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], coarse_f, out=interp)
                 y = self._buf(f"fp{i}", (B, Nf, prm.c_out))
                 ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, prm))
                 ops.pointwise_mlp(interp, prm, x1=fine_f, out=y, ws=ws)

@@ -291,6 +291,35 @@ def interpolate3(xyz_dst: torch.Tensor, xyz_src: torch.Tensor, f_src: torch.Tens
     return out
 
 
+def three_nn(xyz_dst: torch.Tensor, xyz_src: torch.Tensor, out_nit: torch.Tensor | None = None,
+             out_dist: torch.Tensor | None = None):
+    """The 3 nearest sources of every destination (indices, squared
+    distances), as mesorasi_knn with K = 3."""
+    _check_xyz(xyz_dst, "xyz_dst")
+    _check_xyz(xyz_src, "xyz_src")
+    B, Nd, _ = xyz_dst.shape
+    Ns = xyz_src.shape[1]
+    nit = out_nit if out_nit is not None else torch.empty((B, Nd, 3), dtype=torch.int32, device=xyz_dst.device)
+    dist = out_dist if out_dist is not None else torch.empty((B, Nd, 3), dtype=torch.float32, device=xyz_dst.device)
+    check(_lib.lib().mesorasi_three_nn(xyz_dst.data_ptr(), xyz_src.data_ptr(), B, Nd, Ns, nit.data_ptr(),
+                                       dist.data_ptr(), _stream()), "three_nn")
+    return nit, dist
+
+
+def interpolate3_apply(nit: torch.Tensor, dist: torch.Tensor, f_src: torch.Tensor, out: torch.Tensor | None = None):
+    """Inverse-distance interpolation from precomputed 3-NN (three_nn)."""
+    assert nit.dtype == torch.int32 and nit.is_contiguous() and dist.dtype == torch.float32 and dist.is_contiguous()
+    B, Nd, _ = nit.shape
+    Ns, C = f_src.shape[1], f_src.shape[-1]
+    ps, lds = _rows(f_src)
+    if out is None:
+        out = torch.empty((B, Nd, C), dtype=torch.float32, device=f_src.device)
+    po, ldo = _rows(out)
+    check(_lib.lib().mesorasi_interpolate3_apply(nit.data_ptr(), dist.data_ptr(), ps, lds, B, Nd, Ns, C, po, ldo,
+                                                 _stream()), "interpolate3_apply")
+    return out
+
+
 def cast_bf16(x: torch.Tensor) -> torch.Tensor:
     """float32 -> bfloat16 (round to nearest even) on the device."""
     assert x.dtype == torch.float32 and x.is_contiguous()

@@ -217,3 +217,14 @@ def test_product_path_does_not_touch_the_oracle():
             if fn.endswith((".py", ".hip", ".h", ".cpp")):
                 src = open(os.path.join(dirpath, fn)).read()
                 assert "import oracle" not in src and "from oracle" not in src and "liboracle" not in src, fn
+
+
+def test_three_nn_and_apply_validation():
+    assert st("mesorasi_three_nn", FAKE, FAKE, 1, 10, 2, FAKE, FAKE, NULL) == _lib.EINVAL         # Ns < 3
+    assert st("mesorasi_three_nn", FAKE, NULL, 1, 10, 5, FAKE, FAKE, NULL) == _lib.EINVAL         # NULL src
+    assert st("mesorasi_three_nn", NULL, NULL, 0, 10, 5, NULL, NULL, NULL) == _lib.OK             # empty batch
+    f = "mesorasi_interpolate3_apply"
+    assert st(f, FAKE, FAKE, FAKE, 4, 1, 10, 5, 8, FAKE, 8, NULL) == _lib.EINVAL                  # ld_src < C
+    assert st(f, FAKE, NULL, FAKE, 8, 1, 10, 5, 8, FAKE, 8, NULL) == _lib.EINVAL                  # NULL dist
+    assert st(f, FAKE, FAKE, FAKE, 8, 1, 10, 0, 8, FAKE, 8, NULL) == _lib.EINVAL                  # Ns = 0
+    assert st(f, NULL, NULL, NULL, 8, 1, 0, 5, 8, NULL, 8, NULL) == _lib.OK                       # Nd = 0

@@ -6,6 +6,9 @@ identical PFT are bit-exact (values compared as numbers, so +0 == -0);
 MLP features are within a normwise relative error of 1e-4 (fp32) or 2e-2
 (bf16): max|gpu - oracle| / max|oracle| per output tensor.
 """
+import json
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -15,6 +18,8 @@ from paper_2008_06967_amd import ops, synth
 from paper_2008_06967_amd._lib import F32, BF16
 
 pytestmark = pytest.mark.gpu
+
+GOLD = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 TOL = {F32: 1e-4, BF16: 2e-2}
 
@@ -519,6 +524,40 @@ def test_interpolate3_ties_take_lowest_index(gpu, Ns_half):
     ref = O.interpolate3(dst, src, f)
     out = ops.interpolate3(dev(dst), dev(src), dev(f))
     assert normwise(host(out), ref) <= 1e-5
+
+
+@pytest.mark.parametrize("B,Nd,Ns,C", [(2, 4096, 1024, 128), (3, 100, 17, 5), (2, 10, 3, 8), (1, 300, 2500, 7),
+                                       (16, 64, 16, 512)])
+def test_three_nn_and_apply(gpu, B, Nd, Ns, C):
+    """The split form: the search is the oracle's 3-NN bit for bit (indices
+    and squared distances), and the interpolation from it equals the fused
+    kernel's output bit for bit and the oracle's within 1e-5."""
+    rr = g(15)
+    dst = rr.uniform(-1, 1, (B, Nd, 3)).astype(np.float32)
+    src = np.concatenate([dst[:, :min(Ns, Nd) // 2], rr.uniform(-1, 1, (B, Ns - min(Ns, Nd) // 2, 3))], 1)
+    src = src.astype(np.float32)
+    f = rr.standard_normal((B, Ns, C)).astype(np.float32)
+    rn, rd = O.knn(src, dst, 3)
+    nit, dist = ops.three_nn(dev(dst), dev(src))
+    assert np.array_equal(host(nit), rn)
+    assert np.array_equal(host(dist), rd)
+    out = ops.interpolate3_apply(nit, dist, dev(f))
+    fused = ops.interpolate3(dev(dst), dev(src), dev(f))
+    assert torch.equal(out, fused)
+    assert normwise(host(out), O.interpolate3(dst, src, f)) <= 1e-5
+
+
+def test_three_nn_hand_example(gpu):
+    """The hand-worked interpolation (weights 1/d2 over the 3 nearest)
+    through the split GPU form."""
+    d = json.load(open(os.path.join(GOLD, "interpolate3_weights.json")))
+    dst = np.array([d["dst"]], np.float32)
+    src = np.array([d["src"]], np.float32)
+    f = np.array([d["features"]], np.float32)
+    nit, dist = ops.three_nn(dev(dst), dev(src))
+    assert host(nit).tolist() == [[[0, 1, 2]]]
+    out = host(ops.interpolate3_apply(nit, dist, dev(f)))[0, 0].astype(np.float64)
+    assert np.max(np.abs(out - np.array(d["expected_num"]) / d["expected_den"])) <= 1e-6
 
 
 def test_interpolate3_overflowing_distances(gpu):
