@@ -336,6 +336,17 @@ int mesorasi_cast_bf16(const float* x, int64_t n, uint16_t* y, void* stream);
 int mesorasi_edgeconv_fold(const float* W, const float* b, int32_t C, int32_t C_out, float* W_out, float* b_out,
                            void* stream);
 
+/*
+ * Debug check of an index array (the NIT, FPS or 3-NN indices before they
+ * are used to read rows): *count = the number of entries of idx outside
+ * [0, bound).  The library's gathers trust their index arrays (an index out
+ * of range there is undefined behaviour); this check reads only idx and
+ * writes only *count, so it is safe on any input.
+ *   idx [n] int32, count: one device int32 out (overwritten)
+ * Errors: EINVAL for NULL count, NULL idx with n > 0, n < 0.
+ */
+int mesorasi_count_out_of_range(const int32_t* idx, int64_t n, int32_t bound, int32_t* count, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

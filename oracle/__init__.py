@@ -29,9 +29,11 @@ _p = ctypes.c_void_p
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
+        # MESORASI_ORACLE_LIBRARY: the same oracle.c built with sanitizers
+        path = os.environ.get("MESORASI_ORACLE_LIBRARY") or LIB_PATH
+        if path == LIB_PATH and not os.path.exists(LIB_PATH):
             _build()
-        L = ctypes.CDLL(LIB_PATH)
+        L = ctypes.CDLL(path)
         L.orc_dist2.restype = ctypes.c_float
         L.orc_dist2.argtypes = [_p, _p, ctypes.c_int]
         L.orc_bf16_round.restype = ctypes.c_float

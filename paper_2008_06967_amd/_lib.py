@@ -9,7 +9,9 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libmesorasi.so")
+# MESORASI_LIBRARY names another build of the same sources (the host
+# sanitizer build of the test suite); unset, the in-tree library loads
+LIB_PATH = os.environ.get("MESORASI_LIBRARY") or os.path.join(HERE, "libmesorasi.so")
 
 OK, EINVAL, EUNSUPPORTED, EHIP, EWORKSPACE = 0, -1, -2, -3, -4
 NOALLOC_WS_BYTES = 32 << 20    # MESORASI_NOALLOC_WS_BYTES: the allocation-free MLP's fixed scratch
@@ -45,6 +47,7 @@ SIGNATURES = {
     "mesorasi_interpolate3_apply": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i32, _p, _i64, _p]),
     "mesorasi_cast_bf16": (ctypes.c_int, [_p, _i64, _p, _p]),
     "mesorasi_edgeconv_fold": (ctypes.c_int, [_p, _p, _i32, _i32, _p, _p, _p]),
+    "mesorasi_count_out_of_range": (ctypes.c_int, [_p, _i64, _i32, _p, _p]),
 }
 
 _lib = None

@@ -63,6 +63,19 @@ __global__ void edgeconv_fold_kernel(const float* __restrict__ W, const float* _
     }
 }
 
+// Entries of idx outside [0, bound): one atomic per wave (ballot count).
+__global__ void count_out_of_range_kernel(const int32_t* __restrict__ idx, int64_t n, int32_t bound,
+                                          int32_t* __restrict__ count) {
+    for (int64_t i0 = blockIdx.x * (int64_t)blockDim.x; i0 < n; i0 += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = i0 + threadIdx.x;
+        const bool bad = i < n && (idx[i] < 0 || idx[i] >= bound);
+        const uint64_t m = ballot(bad);
+        if ((threadIdx.x & 63) == 0 && m) atomicAdd(count, (int32_t)__builtin_popcountll(m));
+    }
+}
+
+__global__ void zero_i32_kernel(int32_t* p) { *p = 0; }
+
 }  // namespace meso
 
 using namespace meso;
@@ -99,4 +112,15 @@ extern "C" int mesorasi_edgeconv_fold(const float* W, const float* b, int32_t C,
     const int64_t blocks = std::min<int64_t>(ceil_div(std::max<int64_t>(n, C_out), 256), 4096);
     edgeconv_fold_kernel<<<dim3((unsigned)blocks), dim3(256), 0, as_stream(stream)>>>(W, b, C, C_out, W_out, b_out);
     return after_launch("mesorasi_edgeconv_fold");
+}
+
+extern "C" int mesorasi_count_out_of_range(const int32_t* idx, int64_t n, int32_t bound, int32_t* count, void* stream) {
+    MESO_REQUIRE(n >= 0, MESORASI_EINVAL, "mesorasi_count_out_of_range: n = %lld < 0", (long long)n);
+    MESO_REQUIRE(count && (idx || n == 0), MESORASI_EINVAL, "mesorasi_count_out_of_range: NULL pointer");
+    zero_i32_kernel<<<dim3(1), dim3(1), 0, as_stream(stream)>>>(count);
+    int rc = after_launch("mesorasi_count_out_of_range");
+    if (rc != MESORASI_OK || n == 0) return rc;
+    const int64_t blocks = std::min<int64_t>(ceil_div(n, 256), 4096);
+    count_out_of_range_kernel<<<dim3((unsigned)blocks), dim3(256), 0, as_stream(stream)>>>(idx, n, bound, count);
+    return after_launch("mesorasi_count_out_of_range");
 }

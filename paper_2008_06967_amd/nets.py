@@ -29,14 +29,30 @@ from ._lib import F32, BF16
 
 
 class Net:
-    def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda"):
+    def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda", debug: bool = False):
         self.spec = spec
         self.delayed = delayed
         self.device = torch.device(device)
         self.dt = BF16 if spec.get("dtype") == "bf16" else F32
         self.side = torch.cuda.Stream(device=self.device)
         self._bufs: dict[str, torch.Tensor] = {}
+        self.debug = debug
+        self._range_counts: dict[str, torch.Tensor] = {}
         self._params(weights)
+
+    # -- debug index checks ---------------------------------------------------
+    def _check_range(self, name, idx, bound):
+        """debug: count entries of a search output outside [0, bound) on the
+        stream that produced it (read back by index_errors())."""
+        if self.debug:
+            self._range_counts[name] = ops.count_out_of_range(idx, bound, out=self._buf(f"rc_{name}", (),
+                                                                                         torch.int32))
+
+    def index_errors(self) -> dict:
+        """After a debug forward: {output name: entries out of range}, only
+        the nonzero ones (synchronises)."""
+        torch.cuda.synchronize(self.device)
+        return {k: int(v.item()) for k, v in self._range_counts.items() if int(v.item())}
 
     # -- buffers ------------------------------------------------------------
     def _buf(self, name, shape, dtype=torch.float32):
@@ -113,11 +129,13 @@ class PointNet2(Net):
                 cx = self._buf(f"cxyz{i}", (B, m["M"], 3))
                 ws = self._ws(f"ws_fps{i}", ops.fps_workspace_bytes(B, p.shape[1], m["M"]))
                 ops.fps(p, m["M"], out_idx=idx, out_xyz=cx, ws=ws)
+                self._check_range(f"idx{i}", idx, p.shape[1])
                 e = torch.cuda.Event()
                 e.record(side)
                 ev_fps.append(e)
                 nit = self._buf(f"nit{i}", (B, m["M"], m["K"]), torch.int32)
                 ops.ball_query(p, cx, m["radius"], m["K"], out=nit)
+                self._check_range(f"nit{i}", nit, p.shape[1])
                 e = torch.cuda.Event()
                 e.record(side)
                 ev_bq.append(e)
@@ -132,6 +150,7 @@ class PointNet2(Net):
                     nn = self._buf(f"nn{i}", (B, fine.shape[1], 3), torch.int32)
                     nd = self._buf(f"nnd{i}", (B, fine.shape[1], 3))
                     ops.three_nn(fine, coarse, out_nit=nn, out_dist=nd)
+                    self._check_range(f"nn{i}", nn, coarse.shape[1])
                     e = torch.cuda.Event()
                     e.record(side)
                     self.ev_nn.append(e)
@@ -249,6 +268,7 @@ class DGCNN(Net):
             side.wait_stream(main)                       # X of this layer is ready
             with torch.cuda.stream(side):
                 ops.knn(X, X, self.k, out=nit)
+                self._check_range(f"nit{l}", nit, N)
                 ev = torch.cuda.Event()
                 ev.record(side)
             dst = cat[..., off:off + cout]
@@ -272,11 +292,12 @@ class DGCNN(Net):
         return res
 
 
-def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda") -> Net:
+def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", debug: bool = False) -> Net:
     """delayed: True (delayed aggregation), False (conventional) or "ltd"
-    (limited delayed aggregation)."""
+    (limited delayed aggregation).  debug: every search output is checked
+    to lie in range before anything reads through it (index_errors())."""
     if spec["kind"] in ("pointnet2_cls", "pointnet2_seg"):
-        return PointNet2(spec, weights, delayed, device)
+        return PointNet2(spec, weights, delayed, device, debug)
     if spec["kind"] == "dgcnn":
-        return DGCNN(spec, weights, delayed, device)
+        return DGCNN(spec, weights, delayed, device, debug)
     raise ValueError(spec["kind"])

@@ -337,3 +337,12 @@ def edgeconv_fold(W: torch.Tensor, b: torch.Tensor | None):
     check(_lib.lib().mesorasi_edgeconv_fold(W.data_ptr(), _ptr(b), C, Cout, Wo.data_ptr(), bo.data_ptr(), _stream()),
           "edgeconv_fold")
     return Wo, bo
+
+
+def count_out_of_range(idx: torch.Tensor, bound: int, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Device int32 scalar: entries of idx outside [0, bound) (debug check)."""
+    assert idx.dtype == torch.int32 and idx.is_contiguous()
+    count = out if out is not None else torch.empty((), dtype=torch.int32, device=idx.device)
+    check(_lib.lib().mesorasi_count_out_of_range(idx.data_ptr(), idx.numel(), int(bound), count.data_ptr(),
+                                                 _stream()), "count_out_of_range")
+    return count

@@ -228,3 +228,10 @@ def test_three_nn_and_apply_validation():
     assert st(f, FAKE, NULL, FAKE, 8, 1, 10, 5, 8, FAKE, 8, NULL) == _lib.EINVAL                  # NULL dist
     assert st(f, FAKE, FAKE, FAKE, 8, 1, 10, 0, 8, FAKE, 8, NULL) == _lib.EINVAL                  # Ns = 0
     assert st(f, NULL, NULL, NULL, 8, 1, 0, 5, 8, NULL, 8, NULL) == _lib.OK                       # Nd = 0
+
+
+def test_count_out_of_range_validation():
+    f = "mesorasi_count_out_of_range"
+    assert st(f, FAKE, -1, 10, FAKE, NULL) == _lib.EINVAL         # n < 0
+    assert st(f, FAKE, 5, 10, NULL, NULL) == _lib.EINVAL          # NULL count
+    assert st(f, NULL, 5, 10, FAKE, NULL) == _lib.EINVAL          # NULL idx with n > 0
