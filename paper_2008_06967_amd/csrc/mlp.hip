@@ -39,7 +39,14 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int BKH = 32;      // bf16 k-slice
 constexpr int kPadF = 4;     // fp32 k-major LDS rows: tile width + 4 words
-constexpr int kRowH = 40;    // bf16 LDS rows: 32 k + 8 pad (80 bytes)
+constexpr int kRowH = 32;    // bf16 LDS rows: 32 k (64 bytes, four 16-byte chunks), unpadded
+
+// Chunk c of LDS row r of the bf16 tiles sits at chunk position c ^ s(r):
+// the eight (or sixteen) lanes of one 16-byte LDS access phase then touch
+// every bank once, both for the tile stores (four lanes per row) and for
+// the operand reads (one row per lane, one chunk), with 32 or with 64
+// banks of 4 bytes.
+__device__ __forceinline__ int bf16_chunk(int r, int c) { return 8 * (c ^ (((r >> 1) + (r >> 3)) & 3)); }
 constexpr int kTargetTiles = 256;   // one tile per CU
 
 enum { EPI_F32 = 0, EPI_BF16 = 1, EPI_POOL = 2, EPI_PARTIAL = 3 };
@@ -606,7 +613,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t row_t = (int64_t)blockIdx.x * BM;
     const int col_t = blockIdx.y * BN;
-    const int lr = tid >> 2, lk = (tid & 3) * 8;   // 64 rows x 32 k per pass
+    const int lr = tid >> 2, lc = tid & 3, lk = lc * 8;   // 64 rows x 32 k per pass
     const int k_lo = blockIdx.z * a.kc;
     const int k_hi = min(a.K, k_lo + a.kc);
 
@@ -625,9 +632,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
     for (int p = 0; p < PB; ++p) qb[p] = load_w8_bf16<FAST_W>(a, col_t + lr + 64 * p, k_lo + lk, okb[p]);
 #pragma unroll
-    for (int p = 0; p < PA; ++p) *reinterpret_cast<uint4*>(&As[0][(lr + 64 * p) * kRowH + lk]) = select_u4(oka[p], qa[p]);
+    for (int p = 0; p < PA; ++p)
+        *reinterpret_cast<uint4*>(&As[0][(lr + 64 * p) * kRowH + bf16_chunk(lr + 64 * p, lc)]) = select_u4(oka[p], qa[p]);
 #pragma unroll
-    for (int p = 0; p < PB; ++p) *reinterpret_cast<uint4*>(&Bs[0][(lr + 64 * p) * kRowH + lk]) = select_u4(okb[p], qb[p]);
+    for (int p = 0; p < PB; ++p)
+        *reinterpret_cast<uint4*>(&Bs[0][(lr + 64 * p) * kRowH + bf16_chunk(lr + 64 * p, lc)]) = select_u4(okb[p], qb[p]);
     __syncthreads();
 
     int cur = 0;
@@ -641,13 +650,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                av[kk][i] = *reinterpret_cast<const bf16x8*>(
-                    &As[cur][(wm * (BM / 2) + i * 32 + (lane & 31)) * kRowH + 16 * kk + 8 * (lane >> 5)]);
+            for (int i = 0; i < TM; ++i) {
+                const int r = wm * (BM / 2) + i * 32 + (lane & 31);
+                av[kk][i] = *reinterpret_cast<const bf16x8*>(&As[cur][r * kRowH + bf16_chunk(r, 2 * kk + (lane >> 5))]);
+            }
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-                bv[kk][j] = *reinterpret_cast<const bf16x8*>(
-                    &Bs[cur][(wn * (BN / 2) + j * 32 + (lane & 31)) * kRowH + 16 * kk + 8 * (lane >> 5)]);
+            for (int j = 0; j < TN; ++j) {
+                const int r = wn * (BN / 2) + j * 32 + (lane & 31);
+                bv[kk][j] = *reinterpret_cast<const bf16x8*>(&Bs[cur][r * kRowH + bf16_chunk(r, 2 * kk + (lane >> 5))]);
+            }
         }
         __builtin_amdgcn_sched_barrier(0);   // keep the operand reads ahead of the MFMAs
 #pragma unroll
@@ -660,10 +671,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
         __builtin_amdgcn_sched_barrier(0);   // next slice's LDS stores after all MFMAs
 #pragma unroll
         for (int p = 0; p < PA; ++p)
-            *reinterpret_cast<uint4*>(&As[cur ^ 1][(lr + 64 * p) * kRowH + lk]) = select_u4(oka[p], qa[p]);
+            *reinterpret_cast<uint4*>(&As[cur ^ 1][(lr + 64 * p) * kRowH + bf16_chunk(lr + 64 * p, lc)]) =
+                select_u4(oka[p], qa[p]);
 #pragma unroll
         for (int p = 0; p < PB; ++p)
-            *reinterpret_cast<uint4*>(&Bs[cur ^ 1][(lr + 64 * p) * kRowH + lk]) = select_u4(okb[p], qb[p]);
+            *reinterpret_cast<uint4*>(&Bs[cur ^ 1][(lr + 64 * p) * kRowH + bf16_chunk(lr + 64 * p, lc)]) =
+                select_u4(okb[p], qb[p]);
         __syncthreads();
         cur ^= 1;
     }
