@@ -110,12 +110,22 @@ size_t mesorasi_fps_workspace(int64_t B, int64_t N, int64_t M);
  *   xyz   [B, N, 3] float32 points;  qxyz [B, M, 3] float32 queries
  *   nit   [B, M, K] int32 out
  *   cnt   [B, M] int32 out, nullable: number of real hits (<= K)
+ *   ws    device workspace of at least mesorasi_ball_query_workspace(B, N,
+ *         M) bytes, 256-byte aligned (NULL allowed when that size is 0).
+ *         Clouds of 8192 points or more are binned into a grid of cells of
+ *         edge >= radius in it (rebuilt by every call; any contents on
+ *         entry); calls that overlap in time need separate workspaces.
  * Errors: EINVAL for NULL xyz/qxyz/nit, B/N/M < 0, N == 0 < M, K < 1,
- *         radius not finite or <= 0;  EUNSUPPORTED for K > MESORASI_MAX_K_BALL,
- *         N > 2^31 - 321, M > 2^31 - 1.
+ *         radius not finite or <= 0, a misaligned ws;  EUNSUPPORTED for
+ *         K > MESORASI_MAX_K_BALL, N > 2^31 - 321 (N > MESORASI_MAX_N_FPS
+ *         with a workspace), M > 2^31 - 1;  EWORKSPACE when ws is too small.
  */
 int mesorasi_ball_query(const float* xyz, const float* qxyz, int64_t B, int64_t N, int64_t M, float radius,
-                        int32_t K, int32_t* nit, int32_t* cnt, void* stream);
+                        int32_t K, int32_t* nit, int32_t* cnt, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes for mesorasi_ball_query with these sizes (0 when none is
+ * needed, and for invalid sizes). */
+size_t mesorasi_ball_query_workspace(int64_t B, int64_t N, int64_t M);
 
 /*
  * k nearest neighbours in C-dimensional feature space (the DGCNN search in

@@ -134,7 +134,8 @@ class PointNet2(Net):
                 e.record(side)
                 ev_fps.append(e)
                 nit = self._buf(f"nit{i}", (B, m["M"], m["K"]), torch.int32)
-                ops.ball_query(p, cx, m["radius"], m["K"], out=nit)
+                ws = self._ws(f"ws_bq{i}", ops.ball_query_workspace_bytes(B, p.shape[1], m["M"]))
+                ops.ball_query(p, cx, m["radius"], m["K"], out=nit, ws=ws)
                 self._check_range(f"nit{i}", nit, p.shape[1])
                 e = torch.cuda.Event()
                 e.record(side)

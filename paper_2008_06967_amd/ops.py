@@ -69,16 +69,26 @@ def fps(xyz: torch.Tensor, M: int, want_xyz: bool = True, out_idx: torch.Tensor 
     return idx, cxyz
 
 
+def ball_query_workspace_bytes(B: int, N: int, M: int) -> int:
+    return int(_lib.lib().mesorasi_ball_query_workspace(B, N, M))
+
+
 def ball_query(xyz: torch.Tensor, qxyz: torch.Tensor, radius: float, K: int, want_cnt: bool = False,
-               out: torch.Tensor | None = None):
+               out: torch.Tensor | None = None, ws: torch.Tensor | None = None):
+    """ws: a uint8 device tensor of at least ball_query_workspace_bytes(B, N,
+    M) (allocated here when needed and not given)."""
     _check_xyz(xyz, "xyz")
     _check_xyz(qxyz, "qxyz")
     B, N, _ = xyz.shape
     M = qxyz.shape[1]
     nit = out if out is not None else torch.empty((B, M, K), dtype=torch.int32, device=xyz.device)
     cnt = torch.empty((B, M), dtype=torch.int32, device=xyz.device) if want_cnt else None
+    need = ball_query_workspace_bytes(B, N, M)
+    if need and (ws is None or ws.numel() < need):
+        ws = torch.empty(need, dtype=torch.uint8, device=xyz.device)
+    wp, wn = (ws.data_ptr(), ws.numel()) if need else (None, 0)
     check(_lib.lib().mesorasi_ball_query(xyz.data_ptr(), qxyz.data_ptr(), B, N, M, float(radius), K, nit.data_ptr(),
-                                         _ptr(cnt), _stream()), "ball_query")
+                                         _ptr(cnt), wp, wn, _stream()), "ball_query")
     return nit, cnt
 
 

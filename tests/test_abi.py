@@ -75,14 +75,31 @@ def test_fps_workspace():
 
 def test_ball_query_validation():
     f = "mesorasi_ball_query"
-    assert st(f, FAKE, FAKE, 1, 10, 5, 0.2, 0, FAKE, NULL, NULL) == _lib.EINVAL              # K < 1
-    assert st(f, FAKE, FAKE, 1, 10, 5, -0.2, 4, FAKE, NULL, NULL) == _lib.EINVAL             # radius <= 0
-    assert st(f, FAKE, FAKE, 1, 10, 5, float("nan"), 4, FAKE, NULL, NULL) == _lib.EINVAL
-    assert st(f, FAKE, FAKE, 1, 10, 5, float("inf"), 4, FAKE, NULL, NULL) == _lib.EINVAL
-    assert st(f, FAKE, FAKE, 1, 10, 5, 0.2, 2000, FAKE, NULL, NULL) == _lib.EUNSUPPORTED
-    assert st(f, FAKE, FAKE, 1, 0, 5, 0.2, 4, FAKE, NULL, NULL) == _lib.EINVAL               # N = 0 < M
-    assert st(f, NULL, FAKE, 1, 10, 5, 0.2, 4, FAKE, NULL, NULL) == _lib.EINVAL
-    assert st(f, NULL, NULL, 1, 10, 0, 0.2, 4, NULL, NULL, NULL) == _lib.OK                  # M = 0
+    z = (NULL, 0, NULL)        # ws, ws_bytes, stream
+    assert st(f, FAKE, FAKE, 1, 10, 5, 0.2, 0, FAKE, NULL, *z) == _lib.EINVAL              # K < 1
+    assert st(f, FAKE, FAKE, 1, 10, 5, -0.2, 4, FAKE, NULL, *z) == _lib.EINVAL             # radius <= 0
+    assert st(f, FAKE, FAKE, 1, 10, 5, float("nan"), 4, FAKE, NULL, *z) == _lib.EINVAL
+    assert st(f, FAKE, FAKE, 1, 10, 5, float("inf"), 4, FAKE, NULL, *z) == _lib.EINVAL
+    assert st(f, FAKE, FAKE, 1, 10, 5, 0.2, 2000, FAKE, NULL, *z) == _lib.EUNSUPPORTED
+    assert st(f, FAKE, FAKE, 1, 0, 5, 0.2, 4, FAKE, NULL, *z) == _lib.EINVAL               # N = 0 < M
+    assert st(f, NULL, FAKE, 1, 10, 5, 0.2, 4, FAKE, NULL, *z) == _lib.EINVAL
+    assert st(f, NULL, NULL, 1, 10, 0, 0.2, 4, NULL, NULL, *z) == _lib.OK                  # M = 0
+
+
+def test_ball_query_workspace():
+    """Clouds of 8192 points or more are binned into a grid in a workspace,
+    which must be large enough and 256-byte aligned."""
+    L = _lib.lib()
+    f = "mesorasi_ball_query"
+    assert L.mesorasi_ball_query_workspace(32, 1024, 512) == 0
+    need = L.mesorasi_ball_query_workspace(4, 16384, 4096)
+    assert need > 4 * 16384 * 16
+    assert L.mesorasi_ball_query_workspace(8, 16384, 4096) > need
+    assert L.mesorasi_ball_query_workspace(4, 16384, 0) == 0
+    assert st(f, FAKE, FAKE, 4, 16384, 4096, 0.1, 64, FAKE, NULL, NULL, 0, NULL) == _lib.EWORKSPACE
+    assert st(f, FAKE, FAKE, 4, 16384, 4096, 0.1, 64, FAKE, NULL, FAKE, need - 1, NULL) == _lib.EWORKSPACE
+    assert st(f, FAKE, FAKE, 4, 16384, 4096, 0.1, 64, FAKE, NULL, ctypes.c_void_p(0x1080), need, NULL) == _lib.EINVAL
+    assert b"aligned" in L.mesorasi_last_error()
 
 
 def test_knn_validation():

@@ -119,21 +119,48 @@ BQ_CASES = [
     ("grid_boundary", 1, 64, 64, 1.0, 16, "grid"),
     ("lidar_sa1", 1, 16384, 4096, 0.1, 64, "lidar"),
     ("k_max", 1, 2000, 24, 3.0, 1024, "normal"),      # the documented maximum K
+    # 8192 points and more: the grid form (cells of edge >= r, a hit bitmap
+    # per query, the first K set bits)
+    ("grid_lidar_sa1", 2, 16384, 4096, 0.1, 64, "lidar"),
+    ("grid_uniform", 2, 9000, 700, 0.15, 32, "cube"),
+    ("grid_boundary_ties", 1, 8192, 512, 1.0, 40, "grid"),   # integer points: d2 == r2 exactly must not hit
+    ("grid_dups", 2, 10000, 300, 0.3, 64, "dups"),
+    ("grid_k_max", 1, 8200, 50, 2.0, 1024, "normal"),
+    ("grid_nohit", 1, 8192, 64, 1e-4, 8, "normal"),
+    ("grid_two_far_clusters", 1, 12000, 400, 0.05, 16, "clusters"),   # 32 cells per axis cap: cells wider than r
+    ("grid_queries_outside", 2, 8192, 300, 0.5, 32, "outside"),
+    ("grid_n_max", 1, 65536, 256, 0.1, 64, "normal"),
 ]
 
 
 @pytest.mark.parametrize("name,B,N,M,r,K,kind", BQ_CASES, ids=[c[0] for c in BQ_CASES])
 def test_ball_query_bit_exact(gpu, name, B, N, M, r, K, kind):
     rr = g(2)
-    x = _points(kind, B, N, rr)
+    if kind == "clusters":     # two tight clusters 100 apart: the grid's cells are far wider than r
+        x = np.concatenate([rr.normal(0.0, 0.1, (B, N // 2, 3)), rr.normal(100.0, 0.1, (B, N - N // 2, 3))], 1)
+        x = x.astype(np.float32)
+    elif kind == "outside":
+        x = rr.standard_normal((B, N, 3)).astype(np.float32)
+    else:
+        x = _points(kind, B, N, rr)
     if kind in ("grid", "normal") and name != "nohit":
         q = x[:, rr.choice(N, M, replace=False)]
     elif name == "nohit":
         q = rr.standard_normal((B, M, 3)).astype(np.float32) + 50.0
+    elif kind == "outside":    # queries beyond the cloud's box, some within r of it
+        q = x[:, rr.choice(N, M, replace=False)].copy()
+        far = q[..., 0] > 1.0
+        q[..., 0] = np.where(far, x[..., 0].max(1, keepdims=True) + rr.uniform(0, 0.8, far.shape), q[..., 0])
+        q = q.astype(np.float32)
     else:
         _, q = O.fps(x, M)
     rn, rc, _ = O.ball_query(x, q, r, K)
     nit, cnt = ops.ball_query(dev(x), dev(q), r, K, want_cnt=True)
+    if ops.ball_query_workspace_bytes(B, N, M):
+        # a workspace of stale bytes: the grid is rebuilt by the call
+        ws = torch.full((ops.ball_query_workspace_bytes(B, N, M),), 0x7F, dtype=torch.uint8, device="cuda")
+        n2, c2 = ops.ball_query(dev(x), dev(q), r, K, want_cnt=True, ws=ws)
+        assert torch.equal(n2, nit) and torch.equal(c2, cnt)
     assert np.array_equal(host(nit), rn)
     assert np.array_equal(host(cnt), rc)
 
