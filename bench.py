@@ -85,7 +85,7 @@ class StageTimer:
     the stream it is launched on."""
 
     NAMES = ("fps", "ball_query", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3",
-             "three_nn", "interpolate3_apply")
+             "three_nn", "interpolate3_apply", "aggregate_mlp")
 
     def __init__(self, ops):
         import torch
@@ -214,6 +214,14 @@ def call_work(name, a, kw, result=None):
         if cfeat is not None:
             comp += B * M * C * s
         return ("hbm", comp / 1e9, {"logical_gather_bytes": B * M * K * C * s})
+    if name == "aggregate_mlp":
+        # the MLP's flops (its aggregation's bytes beside it)
+        pft, nit, prm = arg(1, "pft"), arg(2, "nit"), arg(4, "p")
+        B, N, C = pft.shape
+        M, K = nit.shape[1], nit.shape[2]
+        d = prm.dims
+        return ("mfma", 2.0 * B * M * sum(x * y for x, y in zip(d[:-1], d[1:])) / 1e12,
+                {"bf16": False, "aggregation_compulsory_bytes": 4 * B * N * C + 4 * B * M * K + 4 * B * M * C})
     if name == "conventional_module":
         nit, prm = arg(0, "nit"), arg(1, "p")
         rows = int(np.prod(nit.shape))

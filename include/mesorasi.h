@@ -230,6 +230,32 @@ int mesorasi_aggregate_max(const void* pft, int64_t ld_pft, int32_t pft_dtype, c
                            int64_t ld_c, int32_t sign, int32_t relu, float* out, int64_t ld_out, void* stream);
 
 /*
+ * Aggregation fused into the next module's MLP (the GPU analogue of the
+ * aggregation unit writing into the NPU's global buffer, Sec. 5.2): for the
+ * B * M centroids of module i (delayed order), the first-layer input rows
+ * of module i + 1 are [cxyz_c | max_k pft[b, nit[c, k]] - pft[b, cidx[c]]]
+ * -- mesorasi_aggregate_max's result with sign -1, bit for bit -- built in
+ * the MLP kernel's loader instead of going through HBM; then the MLP of
+ * mesorasi_pointwise_mlp on them.
+ *   cxyz [B, M, 3] float32 (module i's centroids = module i + 1's points)
+ *   pft  [B, N, ld_pft] float32 (module i's PFT), nit [B, M, K] int32,
+ *   cidx [B, M] int32 (module i's FPS indices)
+ *   MLP arguments as in mesorasi_pointwise_mlp with dtype F32 and
+ *   dims[0] == 3 + C;  y [B * M, ld_y] float32 out
+ *   agg_out [B, M, ld_agg] float32 out, nullable: the aggregated rows as
+ *   well (module i's output, e.g. a skip connection)
+ * Errors: EINVAL for NULL pointers, sizes < 0, K < 1, C < 1, ld < width,
+ *         dims[0] != 3 + C;  EUNSUPPORTED unless the MLP has at least two
+ *         layers with inputs <= 160 and outputs <= 128 channels, C and the
+ *         leading dimensions are multiples of 4 and pft / agg_out are
+ *         16-byte aligned.
+ */
+int mesorasi_aggregate_mlp(const float* cxyz, const float* pft, int64_t ld_pft, const int32_t* nit,
+                           const int32_t* cidx, int64_t B, int64_t N, int64_t M, int32_t K, int32_t C, int32_t n_layers,
+                           const int32_t* dims, const void* const* W, const float* const* bias, uint32_t relu_mask,
+                           float* y, int64_t ld_y, float* agg_out, int64_t ld_agg, void* stream);
+
+/*
  * Conventional module, kept as the comparison path (Eq. (1); Sec. 3.1
  * "Aggregation" and "Feature Computation"): the neighbor feature matrix
  * (NFM), the MLP on every (centroid, neighbor) row, and the max over the

@@ -1298,6 +1298,35 @@ extern "C" int mesorasi_pointwise_mlp_noalloc(const float* x0, int32_t c0, int64
                    pool_group, ws, as_stream(stream), false);
 }
 
+extern "C" int mesorasi_aggregate_mlp(const float* cxyz, const float* pft, int64_t ld_pft, const int32_t* nit,
+                                     const int32_t* cidx, int64_t B, int64_t N, int64_t M, int32_t K, int32_t C,
+                                     int32_t n_layers, const int32_t* dims, const void* const* W,
+                                     const float* const* bias, uint32_t relu_mask, float* y, int64_t ld_y,
+                                     float* agg_out, int64_t ld_agg, void* stream) {
+    const char* who = "mesorasi_aggregate_mlp";
+    MESO_REQUIRE(B >= 0 && N >= 0 && M >= 0, MESORASI_EINVAL, "%s: negative size", who);
+    MESO_REQUIRE(K >= 1, MESORASI_EINVAL, "%s: K = %d < 1", who, K);
+    MESO_REQUIRE(C >= 1 && ld_pft >= C, MESORASI_EINVAL, "%s: C = %d, ld_pft = %lld", who, C, (long long)ld_pft);
+    int rc = check_mlp_spec(who, B * M, n_layers, dims, MESORASI_F32);
+    if (rc != MESORASI_OK) return rc;
+    MESO_REQUIRE(dims[0] == 3 + C, MESORASI_EINVAL, "%s: dims[0] = %d != 3 + C = %d", who, dims[0], 3 + C);
+    MESO_REQUIRE(ld_y >= dims[n_layers], MESORASI_EINVAL, "%s: ld_y < dims[n_layers]", who);
+    MESO_REQUIRE(!agg_out || ld_agg >= C, MESORASI_EINVAL, "%s: ld_agg < C", who);
+    MESO_REQUIRE(fused_mlp_supported(n_layers, dims, MESORASI_F32), MESORASI_EUNSUPPORTED,
+                 "%s: the MLP is not a narrow fused one (at least 2 layers, inputs <= 160, outputs <= 128)", who);
+    MESO_REQUIRE(C % 4 == 0 && ld_pft % 4 == 0 && (!agg_out || ld_agg % 4 == 0), MESORASI_EUNSUPPORTED,
+                 "%s: C and the leading dimensions must be multiples of 4", who);
+    if (B == 0 || M == 0) return MESORASI_OK;
+    MESO_REQUIRE(N >= 1, MESORASI_EINVAL, "%s: N = 0 with M > 0", who);
+    MESO_REQUIRE(cxyz && pft && nit && cidx && y && W, MESORASI_EINVAL, "%s: NULL pointer", who);
+    for (int l = 0; l < n_layers; ++l) MESO_REQUIRE(W[l] != nullptr, MESORASI_EINVAL, "%s: W[%d] is NULL", who, l);
+    MESO_REQUIRE(aligned(pft, 16) && (!agg_out || aligned(agg_out, 16)), MESORASI_EUNSUPPORTED,
+                 "%s: pft and agg_out must be 16-byte aligned", who);
+    MESO_REQUIRE((B * M) / 64 < 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: too many rows", who);
+    MlpAggregate ag{pft, ld_pft, N, M, nit, cidx, K, C, agg_out, ld_agg};
+    return run_fused_aggregate_mlp(cxyz, ag, B * M, n_layers, dims, W, bias, relu_mask, y, ld_y, as_stream(stream));
+}
+
 extern "C" size_t mesorasi_conventional_workspace(int64_t B, int64_t M, int32_t K, int32_t n_layers,
                                                   const int32_t* dims, int32_t dtype) {
     if (B < 0 || M < 0 || K < 1) return 0;

@@ -62,7 +62,19 @@ struct FusedArgs {
     const float* lq;
     int64_t ldq;
     const float* lb1;
+    // aggregated rows (MlpAggregate): x0 = centroid xyz, x1 = max over the
+    // aK rows anit[r, :] of the PFT apft [B, aN, apld] minus its row acidx[r];
+    // also stored to aout [rows, aldo] when that is not null
+    const float* apft;
+    int64_t apld, aN, aM;
+    const int32_t* anit;
+    const int32_t* acidx;
+    int aK;
+    float* aout;
+    int64_t aldo;
 };
+
+constexpr int kInPlain = 0, kInGather = 1, kInAgg = 2;   // layer-0 input forms
 
 __host__ __device__ __forceinline__ int pad16(int x) { return (x + 15) & ~15; }
 
@@ -296,7 +308,7 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
 // row half for layers of at most 64 outputs; two workgroups per CU (with a
 // three-workgroup register budget the row-split epilogue spilled).  (Wider
 // outputs measured slower than the per-layer GEMMs.)
-template <int CB, bool GATHER, int OUT>
+template <int CB, int IN, int OUT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 void mlp_fused_f32_kernel(FusedArgs a) {
     extern __shared__ float smem[];
@@ -310,7 +322,62 @@ void mlp_fused_f32_kernel(FusedArgs a) {
     // layer-0 input tile -> H0 (k-major), zero beyond c0 + c1 up to the slice edge
     {
         const int K0 = a.c0 + a.c1, K0p = pad16(K0);
-        if constexpr (GATHER) {
+        if constexpr (IN == kInAgg) {
+            // the previous module's aggregation, done here (Sec. 5.2: the
+            // aggregation unit writes into the feature buffer of the next
+            // MLP): thread t takes row r and four channels, keeps their
+            // running max over the row's neighbors (fmaxf from -inf, exact
+            // and order-free), subtracts the centroid's row once, and
+            // writes the four values into the k-major tile (and to aout)
+            const int C4 = a.c1 >> 2;
+            for (int e = tid; e < FBM * C4; e += 256) {
+                const int r = e / C4, g4 = e - r * C4;
+                const int64_t row = row_t + r;
+                float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (row < a.rows) {
+                    const int64_t b = row / a.aM;
+                    const float* __restrict__ base = a.apft + b * a.aN * a.apld + 4 * g4;
+                    const int32_t* __restrict__ nr = a.anit + row * a.aK;
+                    const float ninf = -__builtin_huge_valf();
+                    float4 m = make_float4(ninf, ninf, ninf, ninf);
+                    int k = 0;
+                    for (; k + 4 <= a.aK; k += 4) {
+                        float4 t[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) t[u] = *reinterpret_cast<const float4*>(base + (int64_t)nr[k + u] * a.apld);
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            m.x = fmaxf(m.x, t[u].x);
+                            m.y = fmaxf(m.y, t[u].y);
+                            m.z = fmaxf(m.z, t[u].z);
+                            m.w = fmaxf(m.w, t[u].w);
+                        }
+                    }
+                    for (; k < a.aK; ++k) {
+                        const float4 t = *reinterpret_cast<const float4*>(base + (int64_t)nr[k] * a.apld);
+                        m.x = fmaxf(m.x, t.x);
+                        m.y = fmaxf(m.y, t.y);
+                        m.z = fmaxf(m.z, t.z);
+                        m.w = fmaxf(m.w, t.w);
+                    }
+                    const float4 c = *reinterpret_cast<const float4*>(base + (int64_t)a.acidx[row] * a.apld);
+                    v = make_float4(m.x - c.x, m.y - c.y, m.z - c.z, m.w - c.w);
+                    if (a.aout) *reinterpret_cast<float4*>(a.aout + row * a.aldo + 4 * g4) = v;
+                }
+                const int k0 = a.c0 + 4 * g4;
+                H0[(k0 + 0) * FST + r] = v.x;
+                H0[(k0 + 1) * FST + r] = v.y;
+                H0[(k0 + 2) * FST + r] = v.z;
+                H0[(k0 + 3) * FST + r] = v.w;
+            }
+            // the centroid coordinates, and zeros up to the slice edge
+            for (int e = tid; e < FBM * (K0p - a.c1); e += 256) {
+                const int r = e / (K0p - a.c1), kk = e - r * (K0p - a.c1);
+                const int k = kk < a.c0 ? kk : a.c1 + kk;
+                const int64_t row = row_t + r;
+                H0[k * FST + r] = (kk < a.c0 && row < a.rows) ? a.x0[row * a.ld0 + kk] : 0.0f;
+            }
+        } else if constexpr (IN == kInGather) {
             // gathered rows: each row's input point and centroid once, then
             // the element loop reads them from LDS
             __shared__ int64_t s_pt[FBM], s_cen[FBM];
@@ -411,16 +478,42 @@ int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1,
     const dim3 grid((unsigned)ceil_div(rows, FBM)), block(256);
     const bool gather = g != nullptr;
     if (pool_group > 0) {
-        if (gather) mlp_fused_f32_kernel<1, true, kOutPool><<<grid, block, lds, s>>>(a);
-        else mlp_fused_f32_kernel<1, false, kOutPool><<<grid, block, lds, s>>>(a);
+        if (gather) mlp_fused_f32_kernel<1, kInGather, kOutPool><<<grid, block, lds, s>>>(a);
+        else mlp_fused_f32_kernel<1, kInPlain, kOutPool><<<grid, block, lds, s>>>(a);
     } else if (a.out_bf16) {
-        if (gather) mlp_fused_f32_kernel<1, true, kOutBf16><<<grid, block, lds, s>>>(a);
-        else mlp_fused_f32_kernel<1, false, kOutBf16><<<grid, block, lds, s>>>(a);
+        if (gather) mlp_fused_f32_kernel<1, kInGather, kOutBf16><<<grid, block, lds, s>>>(a);
+        else mlp_fused_f32_kernel<1, kInPlain, kOutBf16><<<grid, block, lds, s>>>(a);
     } else {
-        if (gather) mlp_fused_f32_kernel<1, true, kOutF32><<<grid, block, lds, s>>>(a);
-        else mlp_fused_f32_kernel<1, false, kOutF32><<<grid, block, lds, s>>>(a);
+        if (gather) mlp_fused_f32_kernel<1, kInGather, kOutF32><<<grid, block, lds, s>>>(a);
+        else mlp_fused_f32_kernel<1, kInPlain, kOutF32><<<grid, block, lds, s>>>(a);
     }
     return after_launch("mesorasi_pointwise_mlp (fused)");
+}
+
+int run_fused_aggregate_mlp(const float* cxyz, const MlpAggregate& ag, int64_t rows, int n_layers,
+                            const int32_t* dims, const void* const* W, const float* const* bias, uint32_t relu_mask,
+                            float* y, int64_t ld_y, hipStream_t s) {
+    FusedArgs a{};
+    a.x0 = cxyz; a.ld0 = 3; a.c0 = 3; a.c1 = ag.C;
+    a.apft = ag.pft; a.apld = ag.ld_pft; a.aN = ag.n; a.aM = ag.m;
+    a.anit = ag.nit; a.acidx = ag.cidx; a.aK = ag.k; a.aout = ag.out; a.aldo = ag.ld_out;
+    a.rows = rows;
+    a.n_layers = n_layers;
+    int hmax = 16;
+    for (int l = 0; l <= n_layers; ++l) a.dims[l] = dims[l];
+    for (int l = 0; l < n_layers; ++l) {
+        a.W[l] = static_cast<const float*>(W[l]);
+        a.bias[l] = bias ? bias[l] : nullptr;
+        hmax = std::max(hmax, pad16(dims[l]));
+    }
+    a.relu_mask = relu_mask;
+    a.y = y;
+    a.ldy = ld_y;
+    a.hsize = hmax * FST;
+    const size_t lds = sizeof(float) * 2 * (size_t)a.hsize;
+    const dim3 grid((unsigned)ceil_div(rows, FBM)), block(256);
+    mlp_fused_f32_kernel<1, kInAgg, kOutF32><<<grid, block, lds, s>>>(a);
+    return after_launch("mesorasi_aggregate_mlp");
 }
 
 }  // namespace meso

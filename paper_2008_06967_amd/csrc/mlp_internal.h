@@ -23,6 +23,22 @@ struct MlpGather {
     const float* b1;      // nullable
 };
 
+// Rows of an aggregated first layer (the previous module's aggregation
+// done in the loader): row r = (cloud b, centroid c), r = b M + c, is
+// [cxyz_r | max_k pft[b, nit[r, k]] - pft[b, cidx[r]]] over C channels.
+struct MlpAggregate {
+    const float* pft;     // [B, n, ld_pft]
+    int64_t ld_pft;
+    int64_t n;            // points per cloud of the PFT
+    int64_t m;            // centroids per cloud
+    const int32_t* nit;   // [B * m, k]
+    const int32_t* cidx;  // [B * m]
+    int k;
+    int C;
+    float* out;           // nullable: the aggregated rows [B * m, ld_out]
+    int64_t ld_out;
+};
+
 // True when every layer input fits the fused kernel's LDS tile.
 bool fused_mlp_supported(int n_layers, const int32_t* dims, int dtype);
 
@@ -31,5 +47,10 @@ int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1,
                   int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
                   uint32_t relu_mask, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, hipStream_t s,
                   const MlpGather* g = nullptr);
+
+// The aggregated-rows form of the fused MLP (fp32 in and out).
+int run_fused_aggregate_mlp(const float* cxyz, const MlpAggregate& ag, int64_t rows, int n_layers,
+                            const int32_t* dims, const void* const* W, const float* const* bias, uint32_t relu_mask,
+                            float* y, int64_t ld_y, hipStream_t s);
 
 }  // namespace meso

@@ -29,8 +29,10 @@ from ._lib import F32, BF16
 
 
 class Net:
-    def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda", debug: bool = False):
+    def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda", debug: bool = False,
+                 fuse_aggregation: bool = True):
         self.spec = spec
+        self.fuse_aggregation = fuse_aggregation
         self.delayed = delayed
         self.device = torch.device(device)
         self.dt = BF16 if spec.get("dtype") == "bf16" else F32
@@ -157,6 +159,11 @@ class PointNet2(Net):
                     self.ev_nn.append(e)
         return ev_fps, ev_bq
 
+    def _fused_into(self, i):
+        """Level i's MLP takes level i - 1's aggregation in its loader."""
+        return (self.fuse_aggregation and self.dt == F32 and self.delayed is True
+                and ops.aggregate_mlp_supported(self.sa[i], self.sa[i - 1].c_out))
+
     def _sa_levels(self, xyz, feat):
         B = xyz.shape[0]
         main = torch.cuda.current_stream(self.device)
@@ -188,10 +195,19 @@ class PointNet2(Net):
                 # F on all N input points -> PFT, overlapping the search chain
                 pft_dt = torch.bfloat16 if self.dt == BF16 else torch.float32
                 pft = self._buf(f"pft{i}", (B, N, prm.c_out), pft_dt)
-                ws = self._ws(f"ws_sa{i}", ops.mlp_workspace_bytes(B * N, prm))
-                ops.pointwise_mlp(p, prm, x1=f, out_dtype=self.dt, out=pft, ws=ws)
-                main.wait_event(ev_bq[i])
-                ops.aggregate_max(pft, nit, cidx=idx, sign=-1, out=out)
+                if i > 0 and self._fused_into(i):
+                    # the previous level's aggregation happens in this MLP's
+                    # loader (Sec. 5.2), which also stores it (f, the level's
+                    # output, is the next point set's features and a skip)
+                    main.wait_event(ev_bq[i - 1])
+                    ops.aggregate_mlp(p, self._bufs[f"pft{i - 1}"], self._bufs[f"nit{i - 1}"],
+                                      self._bufs[f"idx{i - 1}"], prm, out=pft, agg_out=f)
+                else:
+                    ws = self._ws(f"ws_sa{i}", ops.mlp_workspace_bytes(B * N, prm))
+                    ops.pointwise_mlp(p, prm, x1=f, out_dtype=self.dt, out=pft, ws=ws)
+                if not (i + 1 < len(self.spec["sa"]) and self._fused_into(i + 1)):
+                    main.wait_event(ev_bq[i])
+                    ops.aggregate_max(pft, nit, cidx=idx, sign=-1, out=out)
             else:
                 main.wait_event(ev_bq[i])
                 ws = self._ws(f"ws_sa{i}", ops.conventional_workspace_bytes(B, m["M"], m["K"], prm))
@@ -293,12 +309,15 @@ class DGCNN(Net):
         return res
 
 
-def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", debug: bool = False) -> Net:
+def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", debug: bool = False,
+          fuse_aggregation: bool = True) -> Net:
     """delayed: True (delayed aggregation), False (conventional) or "ltd"
     (limited delayed aggregation).  debug: every search output is checked
-    to lie in range before anything reads through it (index_errors())."""
+    to lie in range before anything reads through it (index_errors()).
+    fuse_aggregation: where the next level's MLP allows it, a level's
+    aggregation runs inside that MLP's loader (mesorasi_aggregate_mlp)."""
     if spec["kind"] in ("pointnet2_cls", "pointnet2_seg"):
-        return PointNet2(spec, weights, delayed, device, debug)
+        return PointNet2(spec, weights, delayed, device, debug, fuse_aggregation)
     if spec["kind"] == "dgcnn":
-        return DGCNN(spec, weights, delayed, device, debug)
+        return DGCNN(spec, weights, delayed, device, debug, fuse_aggregation)
     raise ValueError(spec["kind"])

@@ -199,6 +199,36 @@ def pointwise_mlp_noalloc(x0: torch.Tensor, p: MLPParams, x1: torch.Tensor | Non
     return out
 
 
+def aggregate_mlp_supported(p: MLPParams, C: int) -> bool:
+    """The fused aggregate-into-MLP form applies: an fp32 MLP of at least two
+    layers, inputs <= 160 and outputs <= 128 channels, first layer 3 + C."""
+    return (p.dtype == F32 and p.n >= 2 and p.dims[0] == 3 + C and C % 4 == 0
+            and all(((d + 15) // 16) * 16 <= 160 for d in p.dims[:-1]) and all(d <= 128 for d in p.dims[1:]))
+
+
+def aggregate_mlp(cxyz: torch.Tensor, pft: torch.Tensor, nit: torch.Tensor, cidx: torch.Tensor, p: MLPParams,
+                  relu_mask: int | None = None, out: torch.Tensor | None = None, agg_out: torch.Tensor | None = None):
+    """MLP of module i + 1 on [cxyz | module i's aggregation] with the
+    aggregation done in the MLP's loader; agg_out (optional) also receives
+    the aggregated rows.  cxyz [B, M, 3], pft [B, N, >=C] float32, nit
+    [B, M, K], cidx [B, M]."""
+    _check_xyz(cxyz, "cxyz")
+    B, M, K = nit.shape
+    N, C = pft.shape[1], pft.shape[-1]
+    assert pft.dtype == torch.float32 and nit.is_contiguous() and cidx.is_contiguous()
+    pp, ldp = _rows(pft)
+    if relu_mask is None:
+        relu_mask = (1 << p.n) - 1
+    if out is None:
+        out = torch.empty((B, M, p.c_out), dtype=torch.float32, device=pft.device)
+    py, ldy = _rows(out)
+    pa, lda = _rows(agg_out) if agg_out is not None else (None, 0)
+    d, W, b = p.abi()
+    check(_lib.lib().mesorasi_aggregate_mlp(cxyz.data_ptr(), pp, ldp, nit.data_ptr(), cidx.data_ptr(), B, N, M, K, C,
+                                            p.n, d, W, b, relu_mask, py, ldy, pa, lda, _stream()), "aggregate_mlp")
+    return out
+
+
 def aggregate_max(pft: torch.Tensor, nit: torch.Tensor, cidx: torch.Tensor | None = None,
                   cfeat: torch.Tensor | None = None, sign: int = -1, relu: bool = False,
                   out: torch.Tensor | None = None):

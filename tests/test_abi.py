@@ -252,3 +252,23 @@ def test_count_out_of_range_validation():
     assert st(f, FAKE, -1, 10, FAKE, NULL) == _lib.EINVAL         # n < 0
     assert st(f, FAKE, 5, 10, NULL, NULL) == _lib.EINVAL          # NULL count
     assert st(f, NULL, 5, 10, FAKE, NULL) == _lib.EINVAL          # NULL idx with n > 0
+
+
+def test_aggregate_mlp_validation():
+    L = _lib.lib()
+    f = "mesorasi_aggregate_mlp"
+    d, W, b = _mlp_args([67, 64, 64, 128])
+    args = lambda **k: [k.get("cxyz", FAKE), FAKE, k.get("ldp", 64), FAKE, FAKE, 2, 100, 10, k.get("K", 8),
+                        k.get("C", 64), k.get("n", 3), k.get("d", d), W, b, 7, FAKE, k.get("ldy", 128), NULL, 0, NULL]
+    assert st(f, *args(K=0)) == _lib.EINVAL                         # K < 1
+    assert st(f, *args(C=60)) == _lib.EINVAL                        # dims[0] != 3 + C
+    assert st(f, *args(ldp=32)) == _lib.EINVAL                      # ld_pft < C
+    assert st(f, *args(cxyz=NULL)) == _lib.EINVAL                   # NULL cxyz
+    dw, Ww, bw = _mlp_args([67, 64, 256])
+    assert st(f, *args(d=dw, n=2, ldy=256)) == _lib.EUNSUPPORTED     # output wider than the fused kernel's
+    assert b"narrow" in L.mesorasi_last_error()
+    d1, _, _ = _mlp_args([67, 64])
+    assert st(f, *args(d=d1, n=1)) == _lib.EUNSUPPORTED              # one layer
+    d3, _, _ = _mlp_args([65, 64, 64])
+    assert st(f, FAKE, FAKE, 62, FAKE, FAKE, 2, 100, 10, 8, 62, 2, d3, W, b, 7, FAKE, 128, NULL, 0, NULL) == \
+        _lib.EUNSUPPORTED                                            # C not a multiple of 4

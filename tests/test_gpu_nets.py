@@ -237,3 +237,21 @@ def test_deterministic(gpu):
     b = run_gpu(spec, xyz, None, w, True)
     for k in a:
         assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("name,B", [("pointnet2_seg", 2), ("pointnet2_cls", 3)])
+def test_fused_aggregation_changes_nothing(gpu, name, B):
+    """Levels whose aggregation runs in the next MLP's loader give the same
+    outputs, bit for bit, as the separate aggregation kernel."""
+    spec = synth.workload(name, B=B)
+    xyz, feat = synth.make_points(spec)
+    w = synth.make_weights(spec)
+    tx = torch.from_numpy(xyz).cuda()
+    tf = None if feat is None else torch.from_numpy(feat).cuda()
+    a = nets.build(spec, w, delayed=True, fuse_aggregation=True)
+    b = nets.build(spec, w, delayed=True, fuse_aggregation=False)
+    oa = {k: v.clone() for k, v in a.forward(tx, tf).items()}
+    ob = b.forward(tx, tf)
+    torch.cuda.synchronize()
+    for k in ob:
+        assert torch.equal(oa[k], ob[k]), k

@@ -630,3 +630,39 @@ def test_empty_batches_are_noops(gpu):
     assert idx.shape == (0, 5)
     nit, _ = ops.ball_query(torch.zeros((2, 10, 3), device="cuda"), torch.zeros((2, 0, 3), device="cuda"), 0.1, 4)
     assert nit.shape == (2, 0, 4)
+
+
+# ----------------------------------------------------------------------------
+# aggregation fused into the next module's MLP loader
+# ----------------------------------------------------------------------------
+
+AGG_MLP_CASES = {
+    "seg_sa1_to_sa2": (16, 4096, 1024, 32, 64, [67, 64, 64, 128]),
+    "ragged": (3, 500, 77, 5, 32, [35, 48, 40]),
+    "c128_k64": (2, 1024, 300, 64, 128, [131, 128, 128, 128]),
+}
+
+
+@pytest.mark.parametrize("case", list(AGG_MLP_CASES), ids=list(AGG_MLP_CASES))
+def test_aggregate_mlp_equals_aggregate_then_mlp(gpu, case):
+    """The loader-side aggregation stores exactly mesorasi_aggregate_max's
+    rows and feeds the same MLP kernel, so both outputs are identical to the
+    two-kernel composition; the MLP output meets the oracle's tolerance."""
+    B, N, M, K, C, dims = AGG_MLP_CASES[case]
+    rr = g(16)
+    pft = np.maximum(rr.standard_normal((B, N, C)), 0).astype(np.float32)
+    nit = rr.integers(0, N, (B, M, K)).astype(np.int32)
+    cidx = rr.integers(0, N, (B, M)).astype(np.int32)
+    cxyz = rr.uniform(-1, 1, (B, M, 3)).astype(np.float32)
+    Ws, bs = _weights(rr, dims)
+    p = ops.MLPParams(Ws, bs)
+    agg = torch.empty((B, M, C), device="cuda")
+    y = ops.aggregate_mlp(dev(cxyz), dev(pft), dev(nit), dev(cidx), p, agg_out=agg)
+    ref_agg = ops.aggregate_max(dev(pft), dev(nit), cidx=dev(cidx))
+    ref_y = ops.pointwise_mlp(dev(cxyz), p, x1=ref_agg)
+    assert torch.equal(agg, ref_agg)
+    assert torch.equal(y.view(B * M, -1), ref_y.view(B * M, -1))
+    o_agg = O.aggregate_max(pft, nit, cidx=cidx, sign=-1)
+    assert np.array_equal(host(agg), o_agg)
+    o_y = O.mlp(np.concatenate([cxyz, o_agg], -1), Ws, bs)
+    assert normwise(host(y), o_y) <= 1e-4
