@@ -38,6 +38,7 @@ class Net:
         self.dt = BF16 if spec.get("dtype") == "bf16" else F32
         self.side = torch.cuda.Stream(device=self.device)
         self._bufs: dict[str, torch.Tensor] = {}
+        self._views: dict[str, torch.Tensor] = {}
         self.debug = debug
         self._range_counts: dict[str, torch.Tensor] = {}
         self._params(weights)
@@ -103,6 +104,27 @@ class PointNet2(Net):
         self.fc = P(w["fc"]) if "fc" in w else None
         self.fp = [P(Wb) for Wb in w.get("fp", [])]
         self.head = P(w["head"]) if "head" in w else None
+        # Feature propagation reads [interpolated | skip] rows.  The skip of
+        # FP level k is SA level L - 2 - k's output, which that level writes
+        # straight into the columns after the interpolation of one buffer,
+        # so the MLP reads one contiguous source; the last level's skip is
+        # the input features, taken first (with the first layer's weight
+        # columns permuted to match) so that the layer's wide source is a
+        # plain row-major one.
+        L = len(self.spec["sa"])
+        self.skip_of = {}
+        for k in range(len(self.fp)):
+            s = L - 2 - k
+            ci = self.sa[L - 1].c_out if k == 0 else self.fp[k - 1].c_out
+            if s >= 0:
+                self.skip_of[s] = (k, ci)
+        self.fp_last_feat_first = None
+        if self.fp and self.spec.get("n_feat"):
+            Ws, bs = w["fp"][-1]
+            W0 = np.asarray(Ws[0], np.float32)
+            ci = self.fp[-2].c_out if len(self.fp) > 1 else self.sa[L - 1].c_out
+            W0p = np.ascontiguousarray(np.concatenate([W0[:, ci:], W0[:, :ci]], 1))
+            self.fp_last_feat_first = P(([W0p] + list(Ws[1:]), bs))
         if self.delayed == "ltd":
             # limited order (Sec. 7.3): the first layer's product on the input
             # points and on the centroids, its bias, and the remaining layers
@@ -177,7 +199,13 @@ class PointNet2(Net):
             # previous level waited for its ball query, recorded after its FPS
             # (a redundant wait would add a cross-stream edge to the graph)
             idx, cx, nit = self._bufs[f"idx{i}"], self._bufs[f"cxyz{i}"], self._bufs[f"nit{i}"]
-            out = self._buf(f"f{i}", (B, m["M"], prm.c_out))
+            if i in self.skip_of:
+                k, ci = self.skip_of[i]
+                cat = self._buf(f"cat{k}", (B, m["M"], ci + prm.c_out))
+                out = cat[..., ci:]
+            else:
+                out = self._buf(f"f{i}", (B, m["M"], prm.c_out))
+            self._views[f"f{i}"] = out
             if self.delayed == "ltd":
                 L = self.ltd[i]
                 c1 = L["first"].c_out
@@ -221,8 +249,9 @@ class PointNet2(Net):
         levels = self._sa_levels(xyz, feat)
         res = {}
         for i in range(len(self.spec["sa"])):
-            for k in ("idx", "nit", "cxyz", "f"):
+            for k in ("idx", "nit", "cxyz"):
                 res[f"{k}{i}"] = self._bufs[f"{k}{i}"]
+            res[f"f{i}"] = self._views[f"f{i}"]
         p, f = levels[-1]
         res["out"] = f
         if self.ga is not None:
@@ -238,15 +267,26 @@ class PointNet2(Net):
         if self.fp:
             main = torch.cuda.current_stream(self.device)
             coarse_xyz, coarse_f = levels[-1]
+            L = len(self.spec["sa"])
             for i, prm in enumerate(self.fp):
                 fine_xyz, fine_f = levels[len(levels) - 2 - i]
                 Nf = fine_xyz.shape[1]
-                interp = self._buf(f"interp{i}", (B, Nf, coarse_f.shape[-1]))
+                ci = coarse_f.shape[-1]
+                s = L - 2 - i
+                if s >= 0:   # [interp | skip] in one buffer, the skip already in place
+                    cat = self._bufs[f"cat{i}"]
+                    interp, x0, x1, p_mlp = cat[..., :ci], cat, None, prm
+                elif fine_f is not None and self.fp_last_feat_first is not None:
+                    interp = self._buf(f"interp{i}", (B, Nf, ci))
+                    x0, x1, p_mlp = fine_f, interp, self.fp_last_feat_first
+                else:
+                    interp = self._buf(f"interp{i}", (B, Nf, ci))
+                    x0, x1, p_mlp = interp, fine_f, prm
                 main.wait_event(self.ev_nn[i])
                 ops.interpolate3_apply(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], coarse_f, out=interp)
                 y = self._buf(f"fp{i}", (B, Nf, prm.c_out))
-                ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, prm))
-                ops.pointwise_mlp(interp, prm, x1=fine_f, out=y, ws=ws)
+                ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, p_mlp))
+                ops.pointwise_mlp(x0, p_mlp, x1=x1, out=y, ws=ws)
                 res[f"fp{i}"] = y
                 coarse_xyz, coarse_f = fine_xyz, y
             logits = self._buf("logits", (B, coarse_f.shape[1], self.head.c_out))
