@@ -48,6 +48,16 @@ int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1,
                   uint32_t relu_mask, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, hipStream_t s,
                   const MlpGather* g = nullptr);
 
+// True when every layer is at most 128 wide and the permuted weights fit
+// the LDS of one workgroup (the register-resident MLP, mlp_rr.hip).
+bool rr_mlp_supported(int n_layers, const int32_t* dims);
+
+// The register-resident MLP: fp32 rows [x0 | x1] in, fp32 y out, no
+// workspace, no pooling.
+int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
+               int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
+               uint32_t relu_mask, float* y, int64_t ld_y, hipStream_t s);
+
 // The aggregated-rows form of the fused MLP (fp32 in and out).
 int run_fused_aggregate_mlp(const float* cxyz, const MlpAggregate& ag, int64_t rows, int n_layers,
                             const int32_t* dims, const void* const* W, const float* const* bias, uint32_t relu_mask,

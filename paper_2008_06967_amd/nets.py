@@ -142,10 +142,18 @@ class PointNet2(Net):
                     rest=ops.MLPParams(Ws[1:], bs[1:], device=self.device)))
 
     def _search_chain(self, xyz, B):
-        """FPS and ball query of every level on the side stream."""
+        """Every level's FPS on the side stream (a level samples the previous
+        level's centroids and waits for nothing else), then the
+        feature-propagation 3-NN searches, which need only the sampled
+        coordinates.  The ball queries run on the main stream (_ball_query)
+        right before the aggregations that read them, so no FPS waits for
+        one.  (Two branches: a graph replay maps further branches onto
+        shared hardware queues, which can put a main-stream MLP behind an
+        FPS.)"""
         main, side = torch.cuda.current_stream(self.device), self.side
         side.wait_stream(main)
-        ev_fps, ev_bq = [], []
+        ev_fps = []
+        self._bq_done = set()
         with torch.cuda.stream(side):
             p = xyz
             for i, m in enumerate(self.spec["sa"]):
@@ -157,29 +165,41 @@ class PointNet2(Net):
                 e = torch.cuda.Event()
                 e.record(side)
                 ev_fps.append(e)
-                nit = self._buf(f"nit{i}", (B, m["M"], m["K"]), torch.int32)
-                ws = self._ws(f"ws_bq{i}", ops.ball_query_workspace_bytes(B, p.shape[1], m["M"]))
-                ops.ball_query(p, cx, m["radius"], m["K"], out=nit, ws=ws)
-                self._check_range(f"nit{i}", nit, p.shape[1])
-                e = torch.cuda.Event()
-                e.record(side)
-                ev_bq.append(e)
                 p = cx
-            # the feature-propagation searches need only the sampled
-            # coordinates: done here, off the critical path (three_nn)
-            self.ev_nn = []
+            # one event for the searches of every level but the last (all
+            # done long before the first level reads them) and one for the
+            # last, largest search: each cross-stream wait costs the main
+            # stream several microseconds in a graph replay
+            self.ev_nn = [None] * len(self.fp)
             if self.fp:
+                n = len(self.fp)
                 lv = [xyz] + [self._bufs[f"cxyz{i}"] for i in range(len(self.spec["sa"]))]
-                for i in range(len(self.fp)):
+                for i in range(n):
                     fine, coarse = lv[len(lv) - 2 - i], lv[len(lv) - 1 - i]
                     nn = self._buf(f"nn{i}", (B, fine.shape[1], 3), torch.int32)
                     nd = self._buf(f"nnd{i}", (B, fine.shape[1], 3))
                     ops.three_nn(fine, coarse, out_nit=nn, out_dist=nd)
                     self._check_range(f"nn{i}", nn, coarse.shape[1])
-                    e = torch.cuda.Event()
-                    e.record(side)
-                    self.ev_nn.append(e)
-        return ev_fps, ev_bq
+                    if i == n - 1 or i == n - 2:
+                        e = torch.cuda.Event()
+                        e.record(side)
+                        self.ev_nn[0 if i < n - 1 else i] = e
+        self._ev_fps = ev_fps
+        return ev_fps
+
+    def _ball_query(self, i, p):
+        """Level i's ball query, on the main stream after level i's FPS
+        (issued once per forward, at its first reader)."""
+        if i in self._bq_done:
+            return
+        self._bq_done.add(i)
+        m = self.spec["sa"][i]
+        B, N = p.shape[0], p.shape[1]
+        torch.cuda.current_stream(self.device).wait_event(self._ev_fps[i])
+        nit = self._buf(f"nit{i}", (B, m["M"], m["K"]), torch.int32)
+        ws = self._ws(f"ws_bq{i}", ops.ball_query_workspace_bytes(B, N, m["M"]))
+        ops.ball_query(p, self._bufs[f"cxyz{i}"], m["radius"], m["K"], out=nit, ws=ws)
+        self._check_range(f"nit{i}", nit, N)
 
     def _fused_into(self, i):
         """Level i's MLP takes level i - 1's aggregation in its loader."""
@@ -189,16 +209,17 @@ class PointNet2(Net):
     def _sa_levels(self, xyz, feat):
         B = xyz.shape[0]
         main = torch.cuda.current_stream(self.device)
-        ev_fps, ev_bq = self._search_chain(xyz, B)
+        ev_fps = self._search_chain(xyz, B)
         levels = [(xyz, feat)]
         p, f = xyz, feat
         for i, m in enumerate(self.spec["sa"]):
             prm = self.sa[i]
             N = p.shape[1]
             # p = the previous level's centroids: already ordered, since the
-            # previous level waited for its ball query, recorded after its FPS
-            # (a redundant wait would add a cross-stream edge to the graph)
-            idx, cx, nit = self._bufs[f"idx{i}"], self._bufs[f"cxyz{i}"], self._bufs[f"nit{i}"]
+            # previous level's ball query (main stream) waited for its FPS (a
+            # redundant wait would add a cross-stream edge to the graph)
+            idx, cx = self._bufs[f"idx{i}"], self._bufs[f"cxyz{i}"]
+            nit = self._buf(f"nit{i}", (B, m["M"], m["K"]), torch.int32)
             if i in self.skip_of:
                 k, ci = self.skip_of[i]
                 cat = self._buf(f"cat{k}", (B, m["M"], ci + prm.c_out))
@@ -216,7 +237,7 @@ class PointNet2(Net):
                 main.wait_event(ev_fps[i])
                 ws = self._ws(f"ws_q_{i}", ops.mlp_workspace_bytes(B * m["M"], L["cen"]))
                 ops.pointwise_mlp(cx, L["cen"], relu_mask=0, out=q, ws=ws)
-                main.wait_event(ev_bq[i])
+                self._ball_query(i, p)
                 ws = self._ws(f"ws_sa{i}", ops.ltd_workspace_bytes(B, m["M"], m["K"], L["rest"]))
                 ops.ltd_module(p1, q, nit, L["rest"], b1=L["b1"], out=out, ws=ws)
             elif self.delayed:
@@ -227,17 +248,17 @@ class PointNet2(Net):
                     # the previous level's aggregation happens in this MLP's
                     # loader (Sec. 5.2), which also stores it (f, the level's
                     # output, is the next point set's features and a skip)
-                    main.wait_event(ev_bq[i - 1])
+                    self._ball_query(i - 1, levels[i - 1][0])
                     ops.aggregate_mlp(p, self._bufs[f"pft{i - 1}"], self._bufs[f"nit{i - 1}"],
                                       self._bufs[f"idx{i - 1}"], prm, out=pft, agg_out=f)
                 else:
                     ws = self._ws(f"ws_sa{i}", ops.mlp_workspace_bytes(B * N, prm))
                     ops.pointwise_mlp(p, prm, x1=f, out_dtype=self.dt, out=pft, ws=ws)
                 if not (i + 1 < len(self.spec["sa"]) and self._fused_into(i + 1)):
-                    main.wait_event(ev_bq[i])
+                    self._ball_query(i, p)
                     ops.aggregate_max(pft, nit, cidx=idx, sign=-1, out=out)
             else:
-                main.wait_event(ev_bq[i])
+                self._ball_query(i, p)
                 ws = self._ws(f"ws_sa{i}", ops.conventional_workspace_bytes(B, m["M"], m["K"], prm))
                 ops.conventional_module(nit, prm, xyz=p, feat=f, cxyz=cx, grouping=0, out=out, ws=ws)
             p, f = cx, out
@@ -282,7 +303,8 @@ class PointNet2(Net):
                 else:
                     interp = self._buf(f"interp{i}", (B, Nf, ci))
                     x0, x1, p_mlp = interp, fine_f, prm
-                main.wait_event(self.ev_nn[i])
+                if self.ev_nn[i] is not None:
+                    main.wait_event(self.ev_nn[i])
                 ops.interpolate3_apply(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], coarse_f, out=interp)
                 y = self._buf(f"fp{i}", (B, Nf, prm.c_out))
                 ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, p_mlp))

@@ -339,6 +339,14 @@ MLP_CASES = [
     ("split_8wave_128x128", 16384, [3, 128], [256], F32),
     ("split_8wave_128x64", 16384, [3, 128], [128], F32),
     ("general_8wave_128x128", 16383, [6, 125], [256], F32),
+    # above 32768 rows with every layer at most 128 wide: the register-resident
+    # MLP (persistent workgroups, activations in registers between layers)
+    ("rr_two_layers", 65536, [128], [128, 128], F32),
+    ("rr_head_ragged", 65537, [128], [128, 13], F32),      # last tile of one row; linear last layer
+    ("rr_two_src", 40000, [3, 3], [32, 32, 64], F32),      # element loads of [x0 | x1]
+    ("rr_odd_widths", 33001, [5, 2], [33, 17, 9], F32),    # partial 32-channel blocks
+    ("rr_depth_max", 32769, [16], [32] * 8, F32),
+    ("rr_unaligned_out", 40000, [128], [98], F32),        # 98-float output rows: element stores
 ]
 
 
@@ -355,7 +363,7 @@ def test_mlp_parity(gpu, name, rows, srcs, widths, dt):
     xs = [rr.standard_normal((rows, c)).astype(np.float32) for c in srcs]
     dims = [sum(srcs)] + widths
     Ws, bs = _weights(rr, dims)
-    relu_mask = (1 << (len(widths) - 1)) - 1 if name.startswith("fc") or name == "seg_head" else (1 << len(widths)) - 1
+    relu_mask = (1 << (len(widths) - 1)) - 1 if name.startswith("fc") or "head" in name else (1 << len(widths)) - 1
     ref = O.mlp(np.concatenate(xs, -1), Ws, bs, relu_mask=relu_mask, bf16=dt == BF16)
     p = ops.MLPParams(Ws, bs, dtype=dt)
     y = ops.pointwise_mlp(dev(xs[0]), p, x1=dev(xs[1]) if len(xs) > 1 else None, relu_mask=relu_mask)
