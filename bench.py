@@ -85,7 +85,7 @@ class StageTimer:
     the stream it is launched on."""
 
     NAMES = ("fps", "ball_query", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3",
-             "three_nn", "interpolate3_apply", "aggregate_mlp")
+             "three_nn", "interpolate3_apply", "interpolate3_add", "aggregate_mlp")
 
     def __init__(self, ops):
         import torch
@@ -161,6 +161,7 @@ def call_work(name, a, kw, result=None):
     interpolate3, three_nn: B * Nd * Ns pairs, 8 flops each -> alu
     interpolate3_apply: compulsory HBM bytes (source rows once, neighbours
                     and distances, output) -> hbm
+    interpolate3_add: the same plus the added rows -> hbm
     """
     def arg(i, key, default=None):
         return a[i] if len(a) > i else kw.get(key, default)
@@ -230,12 +231,15 @@ def call_work(name, a, kw, result=None):
     if name in ("interpolate3", "three_nn"):
         dst, src = arg(0, "xyz_dst"), arg(1, "xyz_src")
         return ("alu", 8.0 * dst.shape[0] * dst.shape[1] * src.shape[1] / 1e12, None)
-    if name == "interpolate3_apply":
+    if name in ("interpolate3_apply", "interpolate3_add"):
         nit, f = arg(0, "nit"), arg(2, "f_src")
         B, Nd = nit.shape[0], nit.shape[1]
         Ns, C = f.shape[1], f.shape[-1]
         # every source row once, the neighbours and distances, the output
+        # (and the added rows)
         comp = 4 * B * Ns * C + 24 * B * Nd + 4 * B * Nd * C
+        if name == "interpolate3_add":
+            comp += 4 * B * Nd * C
         return ("hbm", comp / 1e9, {"logical_gather_bytes": 12 * B * Nd * C})
     return None
 

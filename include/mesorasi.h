@@ -353,6 +353,29 @@ int mesorasi_interpolate3_apply(const int32_t* nit, const float* dist, const flo
                                 int64_t Nd, int64_t Ns, int32_t C, float* f_dst, int64_t ld_dst, void* stream);
 
 /*
+ * A feature-propagation layer's first product taken on the coarse points.
+ * The 3-NN interpolation is a convex combination, so for the first layer
+ * of the feature-propagation MLP on [interpolated | skip] rows,
+ *   W1 [interp(f) | s] + b1 = interp(W1a f) + (W1b s + b1),
+ * with W1a the columns of W1 that read the interpolated features: W1a f is
+ * then computed on the coarse points (4x fewer rows here) and W1b s + b1
+ * ahead of time, and this call forms the layer's output:
+ *   f_dst = phi(sum_k w_k f_src[nit_k] / sum_k w_k + add),
+ * the interpolation in the fp32 operations of mesorasi_interpolate3_apply
+ * followed by one fp32 addition; phi = ReLU when relu != 0, else identity.
+ *   nit, dist as for mesorasi_interpolate3_apply
+ *   f_src [B, Ns, ld_src] float32 (W1a f on the coarse points)
+ *   add   [B, Nd, ld_add] float32 (W1b s + b1 on the fine points); may be
+ *         f_dst itself when ld_add == ld_dst (in-place update)
+ *   f_dst [B, Nd, ld_dst] float32 out (first C columns written)
+ * Errors: EINVAL for NULL pointers, sizes < 0, Ns < 1, C < 1, ld < C, or
+ * add aliasing f_dst with another leading dimension.
+ */
+int mesorasi_interpolate3_add(const int32_t* nit, const float* dist, const float* f_src, int64_t ld_src, int64_t B,
+                              int64_t Nd, int64_t Ns, int32_t C, const float* add, int64_t ld_add, int32_t relu,
+                              float* f_dst, int64_t ld_dst, void* stream);
+
+/*
  * float32 -> bf16 bits, round to nearest even (weights and inputs of the
  * bf16 MLP variant).  x [n] float32, y [n] uint16 out.
  * Errors: EINVAL for NULL pointers or n < 0.

@@ -937,12 +937,15 @@ __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __r
 // Interpolation from precomputed neighbours: thread e of the grid-stride
 // loop takes destination e / C4 and four channels (or one channel without
 // 16-byte rows).  The weights are those of interp3_kernel, in the same fp32
-// operations, so the two paths agree bit for bit.
-template <bool VEC4>
+// operations, so the two paths agree bit for bit.  ADD: f_dst =
+// phi(interpolation + add), phi = ReLU when relu is set (add may be f_dst
+// itself: every element is read before the same thread writes it).
+template <bool VEC4, bool ADD = false>
 __global__ __launch_bounds__(256) void interp3_apply_kernel(const int32_t* __restrict__ nn, const float* __restrict__ dd,
                                                             const float* __restrict__ f_src, int64_t lds, int64_t Nd,
-                                                            int Ns, int C, int64_t total, float* __restrict__ f_dst,
-                                                            int64_t ldd) {
+                                                            int Ns, int C, int64_t total, float* f_dst, int64_t ldd,
+                                                            const float* add = nullptr, int64_t lda = 0,
+                                                            int relu = 0) {
     const int cw = VEC4 ? C >> 2 : C;
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
         const int64_t r = e / cw;                // global destination b * Nd + i
@@ -967,9 +970,27 @@ __global__ __launch_bounds__(256) void interp3_apply_kernel(const int32_t* __res
             v.y = u0 * x0.y + u1 * x1.y + u2 * x2.y;
             v.z = u0 * x0.z + u1 * x1.z + u2 * x2.z;
             v.w = u0 * x0.w + u1 * x1.w + u2 * x2.w;
+            if constexpr (ADD) {
+                const float4 p = *reinterpret_cast<const float4*>(add + r * lda + c);
+                v.x += p.x;
+                v.y += p.y;
+                v.z += p.z;
+                v.w += p.w;
+                if (relu) {
+                    v.x = v.x > 0.0f ? v.x : 0.0f;
+                    v.y = v.y > 0.0f ? v.y : 0.0f;
+                    v.z = v.z > 0.0f ? v.z : 0.0f;
+                    v.w = v.w > 0.0f ? v.w : 0.0f;
+                }
+            }
             *reinterpret_cast<float4*>(o) = v;
         } else {
-            *o = u0 * *a0 + u1 * *a1 + u2 * *a2;
+            float v = u0 * *a0 + u1 * *a1 + u2 * *a2;
+            if constexpr (ADD) {
+                v += add[r * lda + c];
+                if (relu) v = v > 0.0f ? v : 0.0f;
+            }
+            *o = v;
         }
     }
 }
@@ -1096,4 +1117,29 @@ extern "C" int mesorasi_interpolate3_apply(const int32_t* nit, const float* dist
         interp3_apply_kernel<false><<<grid, block, 0, as_stream(stream)>>>(nit, dist, f_src, ld_src, Nd, (int)Ns, C,
                                                                           total, f_dst, ld_dst);
     return after_launch("mesorasi_interpolate3_apply");
+}
+
+extern "C" int mesorasi_interpolate3_add(const int32_t* nit, const float* dist, const float* f_src, int64_t ld_src,
+                                         int64_t B, int64_t Nd, int64_t Ns, int32_t C, const float* add,
+                                         int64_t ld_add, int32_t relu, float* f_dst, int64_t ld_dst, void* stream) {
+    MESO_REQUIRE(B >= 0 && Nd >= 0 && Ns >= 0, MESORASI_EINVAL, "mesorasi_interpolate3_add: negative size");
+    MESO_REQUIRE(C >= 1 && ld_src >= C && ld_dst >= C && ld_add >= C, MESORASI_EINVAL,
+                 "mesorasi_interpolate3_add: C / ld");
+    if (B == 0 || Nd == 0) return MESORASI_OK;
+    MESO_REQUIRE(Ns >= 1, MESORASI_EINVAL, "mesorasi_interpolate3_add: Ns = 0");
+    MESO_REQUIRE(nit && dist && f_src && add && f_dst, MESORASI_EINVAL, "mesorasi_interpolate3_add: NULL pointer");
+    MESO_REQUIRE(add != f_dst || ld_add == ld_dst, MESORASI_EINVAL,
+                 "mesorasi_interpolate3_add: add aliases f_dst with another leading dimension");
+    MESO_REQUIRE(Ns <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_interpolate3_add: size");
+    const bool vec4 = C % 4 == 0 && ld_src % 4 == 0 && ld_dst % 4 == 0 && ld_add % 4 == 0 && aligned(f_src, 16) &&
+                      aligned(f_dst, 16) && aligned(add, 16);
+    const int64_t total = B * Nd * (vec4 ? C / 4 : C);
+    const dim3 grid((unsigned)std::min<int64_t>(ceil_div(total, 256), 8192)), block(256);
+    if (vec4)
+        interp3_apply_kernel<true, true><<<grid, block, 0, as_stream(stream)>>>(
+            nit, dist, f_src, ld_src, Nd, (int)Ns, C, total, f_dst, ld_dst, add, ld_add, relu);
+    else
+        interp3_apply_kernel<false, true><<<grid, block, 0, as_stream(stream)>>>(
+            nit, dist, f_src, ld_src, Nd, (int)Ns, C, total, f_dst, ld_dst, add, ld_add, relu);
+    return after_launch("mesorasi_interpolate3_add");
 }

@@ -30,9 +30,10 @@ from ._lib import F32, BF16
 
 class Net:
     def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda", debug: bool = False,
-                 fuse_aggregation: bool = True):
+                 fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384):
         self.spec = spec
         self.fuse_aggregation = fuse_aggregation
+        self.fp_coarse_min_rows = fp_coarse_min_rows
         self.delayed = delayed
         self.device = torch.device(device)
         self.dt = BF16 if spec.get("dtype") == "bf16" else F32
@@ -125,6 +126,24 @@ class PointNet2(Net):
             ci = self.fp[-2].c_out if len(self.fp) > 1 else self.sa[L - 1].c_out
             W0p = np.ascontiguousarray(np.concatenate([W0[:, ci:], W0[:, :ci]], 1))
             self.fp_last_feat_first = P(([W0p] + list(Ws[1:]), bs))
+        # Feature propagation's first layer on [interp(f) | s] rows is
+        # W1a interp(f) + W1b s + b1 = interp(W1a f) + (W1b s + b1): the
+        # interpolation is a convex combination.  So W1a f can be taken on
+        # the coarse points (4x fewer rows), W1b s + b1 as soon as the skip
+        # features exist (off the critical path), and one kernel forms the
+        # layer (mesorasi_interpolate3_add).  fp32 levels of two or more
+        # layers with a skip.
+        self.fp_split = [None] * len(self.fp)
+        if self.dt == F32:
+            for k, (Ws, bs) in enumerate(w.get("fp", [])):
+                ci = self.sa[L - 1].c_out if k == 0 else self.fp[k - 1].c_out
+                W1 = np.asarray(Ws[0], np.float32)
+                if len(Ws) < 2 or W1.shape[1] <= ci:
+                    continue
+                self.fp_split[k] = dict(
+                    a=ops.MLPParams([np.ascontiguousarray(W1[:, :ci])], [None], device=self.device),
+                    b=ops.MLPParams([np.ascontiguousarray(W1[:, ci:])], [bs[0]], device=self.device),
+                    rest=ops.MLPParams(Ws[1:], bs[1:], device=self.device))
         if self.delayed == "ltd":
             # limited order (Sec. 7.3): the first layer's product on the input
             # points and on the centroids, its bias, and the remaining layers
@@ -201,6 +220,26 @@ class PointNet2(Net):
         ops.ball_query(p, self._bufs[f"cxyz{i}"], m["radius"], m["K"], out=nit, ws=ws)
         self._check_range(f"nit{i}", nit, N)
 
+    def _fp_coarse(self, k, rows):
+        """FP level k takes its first product on the coarse points."""
+        return self.fp_split[k] is not None and rows >= self.fp_coarse_min_rows
+
+    def _fp_pre(self, s, skip):
+        """W1b s + b1 of the FP level whose skip is SA level s's output (s =
+        -1: the input features), issued as soon as that output exists."""
+        if not self.fp or skip is None:
+            return
+        k = len(self.spec["sa"]) - 2 - s
+        if not 0 <= k < len(self.fp):      # the last SA level's output is no skip
+            return
+        B, Nf = skip.shape[0], skip.shape[1]
+        if not self._fp_coarse(k, B * Nf):
+            return
+        sp = self.fp_split[k]
+        pre = self._buf(f"fpp{k}", (B, Nf, sp["b"].c_out))
+        ws = self._ws(f"ws_fpp{k}", ops.mlp_workspace_bytes(B * Nf, sp["b"]))
+        ops.pointwise_mlp(skip, sp["b"], relu_mask=0, out=pre, ws=ws)
+
     def _fused_into(self, i):
         """Level i's MLP takes level i - 1's aggregation in its loader."""
         return (self.fuse_aggregation and self.dt == F32 and self.delayed is True
@@ -210,6 +249,7 @@ class PointNet2(Net):
         B = xyz.shape[0]
         main = torch.cuda.current_stream(self.device)
         ev_fps = self._search_chain(xyz, B)
+        self._fp_pre(-1, feat)
         levels = [(xyz, feat)]
         p, f = xyz, feat
         for i, m in enumerate(self.spec["sa"]):
@@ -240,6 +280,7 @@ class PointNet2(Net):
                 self._ball_query(i, p)
                 ws = self._ws(f"ws_sa{i}", ops.ltd_workspace_bytes(B, m["M"], m["K"], L["rest"]))
                 ops.ltd_module(p1, q, nit, L["rest"], b1=L["b1"], out=out, ws=ws)
+                self._fp_pre(i, out)
             elif self.delayed:
                 # F on all N input points -> PFT, overlapping the search chain
                 pft_dt = torch.bfloat16 if self.dt == BF16 else torch.float32
@@ -251,16 +292,19 @@ class PointNet2(Net):
                     self._ball_query(i - 1, levels[i - 1][0])
                     ops.aggregate_mlp(p, self._bufs[f"pft{i - 1}"], self._bufs[f"nit{i - 1}"],
                                       self._bufs[f"idx{i - 1}"], prm, out=pft, agg_out=f)
+                    self._fp_pre(i - 1, f)
                 else:
                     ws = self._ws(f"ws_sa{i}", ops.mlp_workspace_bytes(B * N, prm))
                     ops.pointwise_mlp(p, prm, x1=f, out_dtype=self.dt, out=pft, ws=ws)
                 if not (i + 1 < len(self.spec["sa"]) and self._fused_into(i + 1)):
                     self._ball_query(i, p)
                     ops.aggregate_max(pft, nit, cidx=idx, sign=-1, out=out)
+                    self._fp_pre(i, out)
             else:
                 self._ball_query(i, p)
                 ws = self._ws(f"ws_sa{i}", ops.conventional_workspace_bytes(B, m["M"], m["K"], prm))
                 ops.conventional_module(nit, prm, xyz=p, feat=f, cxyz=cx, grouping=0, out=out, ws=ws)
+                self._fp_pre(i, out)
             p, f = cx, out
             levels.append((p, f))
         return levels
@@ -294,6 +338,23 @@ class PointNet2(Net):
                 Nf = fine_xyz.shape[1]
                 ci = coarse_f.shape[-1]
                 s = L - 2 - i
+                y = self._buf(f"fp{i}", (B, Nf, prm.c_out))
+                if self._fp_coarse(i, B * Nf) and (s >= 0 or fine_f is not None):
+                    # first product on the coarse points, then the layer as
+                    # interp + (W1b s + b1), ReLU (in place), then the rest
+                    sp = self.fp_split[i]
+                    g = self._buf(f"fpg{i}", (B, coarse_f.shape[1], sp["a"].c_out))
+                    ws = self._ws(f"ws_fpg{i}", ops.mlp_workspace_bytes(B * coarse_f.shape[1], sp["a"]))
+                    ops.pointwise_mlp(coarse_f, sp["a"], relu_mask=0, out=g, ws=ws)
+                    h = self._bufs[f"fpp{i}"]
+                    if self.ev_nn[i] is not None:
+                        main.wait_event(self.ev_nn[i])
+                    ops.interpolate3_add(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], g, h, relu=True, out=h)
+                    ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, sp["rest"]))
+                    ops.pointwise_mlp(h, sp["rest"], out=y, ws=ws)
+                    res[f"fp{i}"] = y
+                    coarse_xyz, coarse_f = fine_xyz, y
+                    continue
                 if s >= 0:   # [interp | skip] in one buffer, the skip already in place
                     cat = self._bufs[f"cat{i}"]
                     interp, x0, x1, p_mlp = cat[..., :ci], cat, None, prm
@@ -306,7 +367,6 @@ class PointNet2(Net):
                 if self.ev_nn[i] is not None:
                     main.wait_event(self.ev_nn[i])
                 ops.interpolate3_apply(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], coarse_f, out=interp)
-                y = self._buf(f"fp{i}", (B, Nf, prm.c_out))
                 ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, p_mlp))
                 ops.pointwise_mlp(x0, p_mlp, x1=x1, out=y, ws=ws)
                 res[f"fp{i}"] = y
@@ -372,14 +432,17 @@ class DGCNN(Net):
 
 
 def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", debug: bool = False,
-          fuse_aggregation: bool = True) -> Net:
+          fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384) -> Net:
     """delayed: True (delayed aggregation), False (conventional) or "ltd"
     (limited delayed aggregation).  debug: every search output is checked
     to lie in range before anything reads through it (index_errors()).
     fuse_aggregation: where the next level's MLP allows it, a level's
-    aggregation runs inside that MLP's loader (mesorasi_aggregate_mlp)."""
+    aggregation runs inside that MLP's loader (mesorasi_aggregate_mlp).
+    fp_coarse_min_rows: feature-propagation levels of at least this many
+    fine rows take their first product on the coarse points
+    (mesorasi_interpolate3_add)."""
     if spec["kind"] in ("pointnet2_cls", "pointnet2_seg"):
-        return PointNet2(spec, weights, delayed, device, debug, fuse_aggregation)
+        return PointNet2(spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows)
     if spec["kind"] == "dgcnn":
-        return DGCNN(spec, weights, delayed, device, debug, fuse_aggregation)
+        return DGCNN(spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows)
     raise ValueError(spec["kind"])

@@ -360,6 +360,25 @@ def interpolate3_apply(nit: torch.Tensor, dist: torch.Tensor, f_src: torch.Tenso
     return out
 
 
+def interpolate3_add(nit: torch.Tensor, dist: torch.Tensor, f_src: torch.Tensor, add: torch.Tensor,
+                     relu: bool = True, out: torch.Tensor | None = None):
+    """phi(interpolation of f_src from precomputed 3-NN + add), phi = ReLU
+    when relu: a feature-propagation first layer whose interpolated part
+    was multiplied on the coarse points.  out may be add itself."""
+    assert nit.dtype == torch.int32 and nit.is_contiguous() and dist.dtype == torch.float32 and dist.is_contiguous()
+    B, Nd, _ = nit.shape
+    Ns, C = f_src.shape[1], f_src.shape[-1]
+    assert add.shape[:2] == (B, Nd) and add.shape[-1] == C and add.dtype == torch.float32
+    ps, lds = _rows(f_src)
+    pa, lda = _rows(add)
+    if out is None:
+        out = torch.empty((B, Nd, C), dtype=torch.float32, device=f_src.device)
+    po, ldo = _rows(out)
+    check(_lib.lib().mesorasi_interpolate3_add(nit.data_ptr(), dist.data_ptr(), ps, lds, B, Nd, Ns, C, pa, lda,
+                                               1 if relu else 0, po, ldo, _stream()), "interpolate3_add")
+    return out
+
+
 def cast_bf16(x: torch.Tensor) -> torch.Tensor:
     """float32 -> bfloat16 (round to nearest even) on the device."""
     assert x.dtype == torch.float32 and x.is_contiguous()

@@ -247,6 +247,16 @@ def test_three_nn_and_apply_validation():
     assert st(f, NULL, NULL, NULL, 8, 1, 0, 5, 8, NULL, 8, NULL) == _lib.OK                       # Nd = 0
 
 
+def test_interpolate3_add_validation():
+    f = "mesorasi_interpolate3_add"
+    A = ctypes.c_void_p(0x2000)                     # another buffer (never dereferenced either)
+    assert st(f, FAKE, FAKE, FAKE, 8, 1, 10, 5, 8, A, 4, 1, FAKE, 8, NULL) == _lib.EINVAL          # ld_add < C
+    assert st(f, FAKE, FAKE, FAKE, 8, 1, 10, 5, 8, NULL, 8, 1, FAKE, 8, NULL) == _lib.EINVAL        # NULL add
+    assert st(f, FAKE, FAKE, FAKE, 8, 1, 10, 5, 8, FAKE, 12, 1, FAKE, 8, NULL) == _lib.EINVAL      # aliased, other ld
+    assert st(f, FAKE, FAKE, FAKE, 8, 1, 10, 0, 8, A, 8, 1, FAKE, 8, NULL) == _lib.EINVAL          # Ns = 0
+    assert st(f, NULL, NULL, NULL, 8, 1, 0, 5, 8, NULL, 8, 1, NULL, 8, NULL) == _lib.OK            # Nd = 0
+
+
 def test_count_out_of_range_validation():
     f = "mesorasi_count_out_of_range"
     assert st(f, FAKE, -1, 10, FAKE, NULL) == _lib.EINVAL         # n < 0

@@ -98,3 +98,16 @@ def test_cpu_threads_respects_the_job_share(monkeypatch):
     assert bench.cpu_threads() == (1, avail)
     monkeypatch.delenv("OMP_NUM_THREADS")
     assert bench.cpu_threads() == (avail, avail)
+
+
+def test_interpolation_bytes():
+    """Source rows once, 3 neighbours and distances per destination, the
+    output; the add form also reads the added rows."""
+    nit = torch.zeros(2, 100, 3, dtype=torch.int32)
+    f = torch.zeros(2, 25, 16)
+    kind, amount, extra = bench.call_work("interpolate3_apply", (nit, None, f), {})
+    base = 4 * 2 * 25 * 16 + 24 * 2 * 100 + 4 * 2 * 100 * 16
+    assert kind == "hbm" and amount == pytest.approx(base / 1e9)
+    assert extra["logical_gather_bytes"] == 12 * 2 * 100 * 16
+    kind, amount, _ = bench.call_work("interpolate3_add", (nit, None, f, torch.zeros(2, 100, 16)), {})
+    assert kind == "hbm" and amount == pytest.approx((base + 4 * 2 * 100 * 16) / 1e9)

@@ -22,8 +22,8 @@ def normwise(g, r):
     return float(np.max(np.abs(g - r)) / max(np.max(np.abs(r)), 1e-30))
 
 
-def run_gpu(spec, xyz, feat, w, delayed, graph=False):
-    net = nets.build(spec, w, delayed=delayed)
+def run_gpu(spec, xyz, feat, w, delayed, graph=False, **build_kw):
+    net = nets.build(spec, w, delayed=delayed, **build_kw)
     tx = torch.from_numpy(xyz).cuda()
     tf = None if feat is None else torch.from_numpy(feat).cuda()
     if graph:
@@ -205,6 +205,23 @@ def test_dgcnn_full_batch_graph_sampled_clouds(gpu):
     ref = ON.forward(sub, xyz[pick], None, w, delayed=True)
     check_knn_near_ties(got_s, ref, spec["k"], "full batch, graph")
     assert normwise(got_s["out"], ref["out"]) <= 1e-4
+
+
+@pytest.mark.parametrize("delayed", [True, False], ids=["delayed", "conventional"])
+def test_fp_first_product_on_coarse_points(gpu, delayed):
+    """Every feature-propagation level takes W1a interp(f) as interp(W1a f)
+    on the coarse points plus W1b s + b1 (forced at a small batch): the
+    oracle's interpolate-then-MLP within 1e-4, and close to the plain
+    order."""
+    spec = synth.workload("pointnet2_seg", B=2)
+    xyz, feat = synth.make_points(spec)
+    w = synth.make_weights(spec)
+    ref = ON.forward(spec, xyz, feat, w, delayed=delayed)
+    got = run_gpu(spec, xyz, feat, w, delayed, fp_coarse_min_rows=0)
+    check_pointnet(spec, got, ref, 1e-4)
+    plain = run_gpu(spec, xyz, feat, w, delayed, fp_coarse_min_rows=1 << 40)
+    for k in ("out", "fp0", "fp3"):
+        assert normwise(got[k], plain[k]) <= 1e-5, k
 
 
 def test_graph_replay_matches_eager(gpu):

@@ -582,6 +582,30 @@ def test_three_nn_and_apply(gpu, B, Nd, Ns, C):
     assert normwise(host(out), O.interpolate3(dst, src, f)) <= 1e-5
 
 
+@pytest.mark.parametrize("B,Nd,Ns,C,relu,inplace", [(2, 4096, 1024, 128, True, True), (3, 100, 17, 5, True, False),
+                                                    (2, 300, 50, 12, False, False), (1, 64, 16, 256, True, True)])
+def test_interpolate3_add(gpu, B, Nd, Ns, C, relu, inplace):
+    """phi(interpolation + add): the apply form's interpolation plus one
+    addition, against the oracle's interpolation (1e-5); in place on add
+    when asked, elementwise and strided (C = 5: element path)."""
+    rr = g(16)
+    dst = rr.uniform(-1, 1, (B, Nd, 3)).astype(np.float32)
+    src = rr.uniform(-1, 1, (B, Ns, 3)).astype(np.float32)
+    f = rr.standard_normal((B, Ns, C)).astype(np.float32)
+    a = rr.standard_normal((B, Nd, C)).astype(np.float32)
+    ref = O.interpolate3(dst, src, f).astype(np.float64) + a
+    if relu:
+        ref = np.maximum(ref, 0.0)
+    nit, dist = ops.three_nn(dev(dst), dev(src))
+    add = dev(a)
+    out = ops.interpolate3_add(nit, dist, dev(f), add, relu=relu, out=add if inplace else None)
+    assert (out.data_ptr() == add.data_ptr()) == inplace
+    assert normwise(host(out), ref) <= 1e-5
+    # the same as the apply form's output plus the addition, in fp32
+    plain = host(ops.interpolate3_apply(nit, dist, dev(f))) + a
+    assert np.array_equal(host(out), np.maximum(plain, 0.0) if relu else plain)
+
+
 def test_three_nn_hand_example(gpu):
     """The hand-worked interpolation (weights 1/d2 over the 3 nearest)
     through the split GPU form."""
