@@ -906,15 +906,20 @@ static bool use_fused(int64_t rows, int n_layers, const int32_t* dims, int dtype
     return fused_mlp_supported(n_layers, dims, dtype) && (neighbor_rows || rows <= kFusedMaxPlainRows);
 }
 
-// The register-resident MLP (mlp_rr.hip) for plain fp32 rows above that
-// count when every layer is at most 128 wide.
+// The register-resident MLP (mlp_rr.hip, mlp_rr_bf16.hip) for plain rows
+// above that count when every layer is at most 128 wide; in bf16 only for
+// first layers of at most 32 inputs, where the GEMM's per-layer launches
+// and HBM round trips dominate (65536 x 3 -> 32 -> 32 -> 64: 16.6 against
+// 20.8 us); on 128-wide rows the bf16 GEMM is faster (65536 x 128 -> 128
+// -> 128: 28.5 against 34.7 us), its MFMA work being a sixteenth of fp32's.
 #ifndef MESO_RR_MIN_ROWS
 #define MESO_RR_MIN_ROWS (kFusedMaxPlainRows + 1)
 #endif
 static bool use_rr(int64_t rows, int n_layers, const int32_t* dims, int dtype, int out_dtype, int64_t pool_group,
                    bool neighbor_rows) {
-    return dtype == MESORASI_F32 && out_dtype == MESORASI_F32 && pool_group == 0 && !neighbor_rows &&
-           rows >= MESO_RR_MIN_ROWS && rr_mlp_supported(n_layers, dims);
+    if (pool_group != 0 || neighbor_rows || rows < MESO_RR_MIN_ROWS) return false;
+    if (dtype == MESORASI_F32) return out_dtype == MESORASI_F32 && rr_mlp_supported(n_layers, dims);
+    return dtype == MESORASI_BF16 && dims[0] <= 32 && rb_mlp_supported(n_layers, dims);
 }
 
 static size_t mlp_ws_bytes(int64_t rows, int n_layers, const int32_t* dims, int dtype, bool neighbor_rows) {
@@ -1044,9 +1049,13 @@ static int run_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1
                    int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
                    uint32_t relu_mask, int dtype, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, void* ws,
                    hipStream_t s, bool neighbor_rows, const MlpGather* g = nullptr) {
-    if (!g && use_rr(rows, n_layers, dims, dtype, out_dtype, pool_group, neighbor_rows))
+    if (!g && use_rr(rows, n_layers, dims, dtype, out_dtype, pool_group, neighbor_rows)) {
+        if (dtype == MESORASI_BF16)
+            return run_rb_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, out_dtype, y, ld_y,
+                              s);
         return run_rr_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, static_cast<float*>(y),
                           ld_y, s);
+    }
     if (use_fused(rows, n_layers, dims, dtype, neighbor_rows))
         return run_fused_mlp(x0, c0, ld0, x1, c1, ld1, rows, n_layers, dims, W, bias, relu_mask, out_dtype, y, ld_y,
                              pool_group, s, g);

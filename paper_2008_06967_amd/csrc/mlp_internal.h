@@ -58,6 +58,13 @@ int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, in
                int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
                uint32_t relu_mask, float* y, int64_t ld_y, hipStream_t s);
 
+// The same for bf16 MLPs (mlp_rr_bf16.hip): every layer at most 128 wide;
+// fp32 rows in, fp32 or bf16 y out (bf16-rounded values either way).
+bool rb_mlp_supported(int n_layers, const int32_t* dims);
+int run_rb_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
+               int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
+               uint32_t relu_mask, int out_dtype, void* y, int64_t ld_y, hipStream_t s);
+
 // The aggregated-rows form of the fused MLP (fp32 in and out).
 int run_fused_aggregate_mlp(const float* cxyz, const MlpAggregate& ag, int64_t rows, int n_layers,
                             const int32_t* dims, const void* const* W, const float* const* bias, uint32_t relu_mask,

@@ -347,6 +347,12 @@ MLP_CASES = [
     ("rr_odd_widths", 33001, [5, 2], [33, 17, 9], F32),    # partial 32-channel blocks
     ("rr_depth_max", 32769, [16], [32] * 8, F32),
     ("rr_unaligned_out", 40000, [128], [98], F32),        # 98-float output rows: element stores
+    # the bf16 form (v_mfma_f32_32x32x16_bf16, activations packed in
+    # registers), used for first layers of at most 32 inputs
+    ("rr_bf16_two_src", 65536, [3, 3], [32, 32, 64], BF16),
+    ("rr_bf16_wide_ragged", 40001, [32], [128, 128, 13], BF16),
+    ("rr_bf16_odd_widths", 33001, [5, 2], [33, 17, 9], BF16),
+    ("rr_bf16_depth_max", 32769, [16], [32] * 8, BF16),
 ]
 
 
