@@ -85,7 +85,7 @@ class StageTimer:
     the stream it is launched on."""
 
     NAMES = ("fps", "ball_query", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3",
-             "three_nn", "interpolate3_apply", "interpolate3_add", "aggregate_mlp")
+             "three_nn", "interpolate3_apply", "interpolate3_add", "interpolate3_mlp", "aggregate_mlp")
 
     def __init__(self, ops):
         import torch
@@ -162,6 +162,7 @@ def call_work(name, a, kw, result=None):
     interpolate3_apply: compulsory HBM bytes (source rows once, neighbours
                     and distances, output) -> hbm
     interpolate3_add: the same plus the added rows -> hbm
+    interpolate3_mlp: the MLP's flops on the interpolated rows -> mfma
     """
     def arg(i, key, default=None):
         return a[i] if len(a) > i else kw.get(key, default)
@@ -223,6 +224,11 @@ def call_work(name, a, kw, result=None):
         d = prm.dims
         return ("mfma", 2.0 * B * M * sum(x * y for x, y in zip(d[:-1], d[1:])) / 1e12,
                 {"bf16": False, "aggregation_compulsory_bytes": 4 * B * N * C + 4 * B * M * K + 4 * B * M * C})
+    if name == "interpolate3_mlp":
+        nit, prm = arg(0, "nit"), arg(4, "p")
+        rows = nit.shape[0] * nit.shape[1]
+        d = prm.dims
+        return ("mfma", 2.0 * rows * sum(x * y for x, y in zip(d[:-1], d[1:])) / 1e12, {"bf16": False})
     if name == "conventional_module":
         nit, prm = arg(0, "nit"), arg(1, "p")
         rows = int(np.prod(nit.shape))

@@ -376,6 +376,31 @@ int mesorasi_interpolate3_add(const int32_t* nit, const float* dist, const float
                               float* f_dst, int64_t ld_dst, void* stream);
 
 /*
+ * mesorasi_interpolate3_add followed by an MLP on its rows, in one kernel:
+ * the interpolation, the addition and phi are done in the register-resident
+ * MLP's row loader, so the layer's output never goes to memory (the
+ * feature-propagation level of mesorasi_interpolate3_add, its remaining
+ * layers included).
+ *   y = MLP(phi(sum_k w_k f_src[nit_k] / sum_k w_k + add))
+ * with the interpolation, addition and phi in the fp32 operations of
+ * mesorasi_interpolate3_add and the MLP as in mesorasi_pointwise_mlp (fp32).
+ *   nit, dist, f_src, add as for mesorasi_interpolate3_add, over C = dims[0]
+ *         channels; f_src and add 16-byte aligned
+ *   W, bias, relu_mask: the MLP as in mesorasi_pointwise_mlp (dims[0] = C)
+ *   y [B, Nd, ld_y] float32 out; must not overlap add
+ * No workspace.
+ * Errors: EINVAL for NULL pointers, sizes < 0, Ns = 0 with points, ld < C
+ * or ld_y < dims[n_layers]; EUNSUPPORTED unless every layer is at most 128
+ * wide (its permuted weights fitting 160 KB), dims[0], ld_src and ld_add are
+ * multiples of 4 and f_src and add are 16-byte aligned -- callers fall back
+ * to mesorasi_interpolate3_add + mesorasi_pointwise_mlp.
+ */
+int mesorasi_interpolate3_mlp(const int32_t* nit, const float* dist, const float* f_src, int64_t ld_src, int64_t B,
+                              int64_t Nd, int64_t Ns, const float* add, int64_t ld_add, int32_t relu,
+                              int32_t n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
+                              uint32_t relu_mask, float* y, int64_t ld_y, void* stream);
+
+/*
  * float32 -> bf16 bits, round to nearest even (weights and inputs of the
  * bf16 MLP variant).  x [n] float32, y [n] uint16 out.
  * Errors: EINVAL for NULL pointers or n < 0.

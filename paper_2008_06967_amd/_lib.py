@@ -48,6 +48,8 @@ SIGNATURES = {
     "mesorasi_interpolate3_apply": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i32, _p, _i64, _p]),
     "mesorasi_interpolate3_add": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i32, _p, _i64, _i32, _p, _i64,
                                                  _p]),
+    "mesorasi_interpolate3_mlp": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _p, _i64, _i32, _i32, _p, _p, _p,
+                                                 _u32, _p, _i64, _p]),
     "mesorasi_cast_bf16": (ctypes.c_int, [_p, _i64, _p, _p]),
     "mesorasi_edgeconv_fold": (ctypes.c_int, [_p, _p, _i32, _i32, _p, _p, _p]),
     "mesorasi_count_out_of_range": (ctypes.c_int, [_p, _i64, _i32, _p, _p]),

@@ -1350,6 +1350,33 @@ extern "C" int mesorasi_aggregate_mlp(const float* cxyz, const float* pft, int64
     return run_fused_aggregate_mlp(cxyz, ag, B * M, n_layers, dims, W, bias, relu_mask, y, ld_y, as_stream(stream));
 }
 
+extern "C" int mesorasi_interpolate3_mlp(const int32_t* nit, const float* dist, const float* f_src, int64_t ld_src,
+                                         int64_t B, int64_t Nd, int64_t Ns, const float* add, int64_t ld_add,
+                                         int32_t relu, int32_t n_layers, const int32_t* dims, const void* const* W,
+                                         const float* const* bias, uint32_t relu_mask, float* y, int64_t ld_y,
+                                         void* stream) {
+    const char* who = "mesorasi_interpolate3_mlp";
+    MESO_REQUIRE(B >= 0 && Nd >= 0 && Ns >= 0, MESORASI_EINVAL, "%s: negative size", who);
+    int rc = check_mlp_spec(who, B * Nd, n_layers, dims, MESORASI_F32);
+    if (rc != MESORASI_OK) return rc;
+    const int C = dims[0];
+    MESO_REQUIRE(ld_src >= C && ld_add >= C && ld_y >= dims[n_layers], MESORASI_EINVAL, "%s: leading dimension", who);
+    MESO_REQUIRE(rr_mlp_supported(n_layers, dims), MESORASI_EUNSUPPORTED,
+                 "%s: every layer must be at most 128 wide (the register-resident MLP)", who);
+    MESO_REQUIRE(C % 4 == 0 && ld_src % 4 == 0 && ld_add % 4 == 0, MESORASI_EUNSUPPORTED,
+                 "%s: dims[0] and the leading dimensions of f_src and add must be multiples of 4", who);
+    if (B == 0 || Nd == 0) return MESORASI_OK;
+    MESO_REQUIRE(Ns >= 1, MESORASI_EINVAL, "%s: Ns = 0", who);
+    MESO_REQUIRE(nit && dist && f_src && add && y && W, MESORASI_EINVAL, "%s: NULL pointer", who);
+    for (int l = 0; l < n_layers; ++l) MESO_REQUIRE(W[l] != nullptr, MESORASI_EINVAL, "%s: W[%d] is NULL", who, l);
+    MESO_REQUIRE(aligned(f_src, 16) && aligned(add, 16), MESORASI_EUNSUPPORTED,
+                 "%s: f_src and add must be 16-byte aligned", who);
+    MESO_REQUIRE(Ns <= 0x7fffffff && Nd <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: size", who);
+    const RrInterp ip{nit, dist, f_src, ld_src, Nd, Ns, add, ld_add, relu ? 1 : 0};
+    return run_rr_mlp(nullptr, C, 0, nullptr, 0, 0, B * Nd, n_layers, dims, W, bias, relu_mask, y, ld_y,
+                      as_stream(stream), &ip);
+}
+
 extern "C" size_t mesorasi_conventional_workspace(int64_t B, int64_t M, int32_t K, int32_t n_layers,
                                                   const int32_t* dims, int32_t dtype) {
     if (B < 0 || M < 0 || K < 1) return 0;

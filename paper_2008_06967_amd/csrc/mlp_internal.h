@@ -52,11 +52,24 @@ int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1,
 // the LDS of one workgroup (the register-resident MLP, mlp_rr.hip).
 bool rr_mlp_supported(int n_layers, const int32_t* dims);
 
-// The register-resident MLP: fp32 rows [x0 | x1] in, fp32 y out, no
-// workspace, no pooling.
+// First-layer rows made by interpolation (mesorasi_interpolate3_mlp): row r
+// = b nd + i is phi(sum_k u_k g[b, nit[r, k]] + add[r]); every row and
+// pointer 16-byte aligned, dims[0] % 4 == 0.
+struct RrInterp {
+    const int32_t* nit;   // [rows, 3]
+    const float* dist;    // [rows, 3]
+    const float* g;       // [B, ns, ldg]
+    int64_t ldg, nd, ns;
+    const float* add;     // [rows, lda]
+    int64_t lda;
+    int relu;
+};
+
+// The register-resident MLP: fp32 rows [x0 | x1] (or interpolated rows) in,
+// fp32 y out, no workspace, no pooling.
 int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
                int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
-               uint32_t relu_mask, float* y, int64_t ld_y, hipStream_t s);
+               uint32_t relu_mask, float* y, int64_t ld_y, hipStream_t s, const RrInterp* ip = nullptr);
 
 // The same for bf16 MLPs (mlp_rr_bf16.hip): every layer at most 128 wide;
 // fp32 rows in, fp32 or bf16 y out (bf16-rounded values either way).

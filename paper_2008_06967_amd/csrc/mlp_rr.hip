@@ -58,6 +58,11 @@ struct RrArgs {
     int k0h;     // layer-0 k values per lane half (a multiple of 16, at most 64)
     int vec0;    // layer-0 rows read as aligned float4 (one source, C0 % 4 == 0)
     int vecy;    // output rows stored as aligned float4
+    // interpolated first-layer rows (instead of [x0 | x1]): row r = b Nd + i
+    // is phi(sum_k u_k g[b, nn[r, k]] + add[r]) over the first dims[0]
+    // channels, u_k the normalised inverse squared distances
+    int interp;
+    RrInterp ip;
 };
 
 __host__ __device__ inline int rr_blocks(int n) { return (n + 31) / 32; }
@@ -151,7 +156,46 @@ void mlp_rr_kernel(RrArgs a) {
         // some hundred registers for its whole length)
         int kb = 4 * hk;
         asm volatile("" : "+v"(kb));
-        if (a.vec0) {
+        if (a.interp) {
+            // the interpolation of mesorasi_interpolate3_add, in its fp32
+            // operations, then the addition and phi
+            const RrInterp& q = a.ip;
+            const int64_t r0 = rok ? row : 0;
+            const int64_t b = r0 / q.nd;
+            const float w0 = 1.0f / fmaxf(q.dist[r0 * 3 + 0], 1e-10f);
+            const float w1 = 1.0f / fmaxf(q.dist[r0 * 3 + 1], 1e-10f);
+            const float w2 = 1.0f / fmaxf(q.dist[r0 * 3 + 2], 1e-10f);
+            const float ws = w0 + w1 + w2;
+            const float u0 = w0 / ws, u1 = w1 / ws, u2 = w2 / ws;
+            const float* gs = q.g + b * q.ns * q.ldg;
+            const float* g0 = gs + (int64_t)q.nit[r0 * 3 + 0] * q.ldg;
+            const float* g1 = gs + (int64_t)q.nit[r0 * 3 + 1] * q.ldg;
+            const float* g2 = gs + (int64_t)q.nit[r0 * 3 + 2] * q.ldg;
+            const float* ad = q.add + r0 * q.lda;
+#pragma unroll
+            for (int i = 0; i < kRrMaxSteps / 4; ++i) {
+                if (4 * i < a.k0h) {
+                    const int k = kb + 8 * i;
+                    const bool ok = rok && k < a.c0;
+                    const int kk = ok ? k : 0;
+                    const float4 x0 = *reinterpret_cast<const float4*>(g0 + kk);
+                    const float4 x1 = *reinterpret_cast<const float4*>(g1 + kk);
+                    const float4 x2 = *reinterpret_cast<const float4*>(g2 + kk);
+                    const float4 p = *reinterpret_cast<const float4*>(ad + kk);
+                    float v[4] = {u0 * x0.x + u1 * x1.x + u2 * x2.x, u0 * x0.y + u1 * x1.y + u2 * x2.y,
+                                  u0 * x0.z + u1 * x1.z + u2 * x2.z, u0 * x0.w + u1 * x1.w + u2 * x2.w};
+                    v[0] += p.x;
+                    v[1] += p.y;
+                    v[2] += p.z;
+                    v[3] += p.w;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if (q.relu) v[e] = v[e] > 0.0f ? v[e] : 0.0f;
+                        dst[4 * i + e] = ok ? v[e] : 0.0f;
+                    }
+                }
+            }
+        } else if (a.vec0) {
             const float* src = a.x0 + (rok ? row : 0) * a.ld0;
 #pragma unroll
             for (int i = 0; i < kRrMaxSteps / 4; ++i) {
@@ -333,7 +377,7 @@ bool rr_mlp_supported(int n_layers, const int32_t* dims) { return rr_plan(n_laye
 
 int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
                int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
-               uint32_t relu_mask, float* y, int64_t ld_y, hipStream_t s) {
+               uint32_t relu_mask, float* y, int64_t ld_y, hipStream_t s, const RrInterp* ip) {
     const RrPlan pl = rr_plan(n_layers, dims);
     MESO_REQUIRE(pl.ok, MESORASI_EUNSUPPORTED, "mesorasi_pointwise_mlp: layers too wide for the register MLP");
     if (rows == 0) return MESORASI_OK;
@@ -359,6 +403,12 @@ int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, in
     a.ldy = ld_y;
     a.k0h = pl.k0h;
     a.vec0 = a.c1 == 0 && c0 % 4 == 0 && ld0 % 4 == 0 && aligned(x0, 16);
+    if (ip) {
+        a.interp = 1;
+        a.ip = *ip;
+        a.c0 = dims[0];
+        a.c1 = 0;
+    }
     a.vecy = ld_y % 4 == 0 && aligned(y, 16);
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess) {

@@ -349,9 +349,13 @@ class PointNet2(Net):
                     h = self._bufs[f"fpp{i}"]
                     if self.ev_nn[i] is not None:
                         main.wait_event(self.ev_nn[i])
-                    ops.interpolate3_add(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], g, h, relu=True, out=h)
-                    ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, sp["rest"]))
-                    ops.pointwise_mlp(h, sp["rest"], out=y, ws=ws)
+                    if B * Nf > 32768 and ops.interpolate3_mlp_supported(sp["rest"]):
+                        # the layer formed in the register MLP's row loader
+                        ops.interpolate3_mlp(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], g, h, sp["rest"], out=y)
+                    else:
+                        ops.interpolate3_add(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], g, h, relu=True, out=h)
+                        ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, sp["rest"]))
+                        ops.pointwise_mlp(h, sp["rest"], out=y, ws=ws)
                     res[f"fp{i}"] = y
                     coarse_xyz, coarse_f = fine_xyz, y
                     continue

@@ -379,6 +379,41 @@ def interpolate3_add(nit: torch.Tensor, dist: torch.Tensor, f_src: torch.Tensor,
     return out
 
 
+def interpolate3_mlp_supported(p: MLPParams) -> bool:
+    """mesorasi_interpolate3_mlp applies: an fp32 MLP whose layers are all at
+    most 128 wide (the register-resident MLP), first layer a multiple of 4."""
+    if p.dtype != F32 or p.dims[0] % 4 != 0 or any(d > 128 for d in p.dims):
+        return False
+    h0 = ((p.dims[0] + 1) // 2 + 15) // 16 * 16     # first-layer k steps, as the library pads them
+    lds = 0
+    for l in range(p.n):
+        nob = (p.dims[l + 1] + 31) // 32
+        steps = h0 if l == 0 else 16 * ((p.dims[l] + 31) // 32)
+        lds += 4 * (nob * steps * 64 + nob * 32)
+    return lds <= 160 * 1024
+
+
+def interpolate3_mlp(nit: torch.Tensor, dist: torch.Tensor, f_src: torch.Tensor, add: torch.Tensor, p: MLPParams,
+                     relu: bool = True, relu_mask: int | None = None, out: torch.Tensor | None = None):
+    """MLP on the rows phi(interpolation of f_src + add) in one kernel
+    (mesorasi_interpolate3_mlp)."""
+    assert nit.dtype == torch.int32 and nit.is_contiguous() and dist.dtype == torch.float32 and dist.is_contiguous()
+    B, Nd, _ = nit.shape
+    Ns = f_src.shape[1]
+    assert add.shape[:2] == (B, Nd) and add.shape[-1] == p.dims[0] and f_src.shape[-1] == p.dims[0]
+    ps, lds = _rows(f_src)
+    pa, lda = _rows(add)
+    if out is None:
+        out = torch.empty((B, Nd, p.c_out), dtype=torch.float32, device=f_src.device)
+    po, ldo = _rows(out)
+    d, W, b = p.abi()
+    rm = (1 << p.n) - 1 if relu_mask is None else relu_mask
+    check(_lib.lib().mesorasi_interpolate3_mlp(nit.data_ptr(), dist.data_ptr(), ps, lds, B, Nd, Ns, pa, lda,
+                                               1 if relu else 0, p.n, d, W, b, rm, po, ldo, _stream()),
+          "interpolate3_mlp")
+    return out
+
+
 def cast_bf16(x: torch.Tensor) -> torch.Tensor:
     """float32 -> bfloat16 (round to nearest even) on the device."""
     assert x.dtype == torch.float32 and x.is_contiguous()

@@ -257,6 +257,27 @@ def test_interpolate3_add_validation():
     assert st(f, NULL, NULL, NULL, 8, 1, 0, 5, 8, NULL, 8, 1, NULL, 8, NULL) == _lib.OK            # Nd = 0
 
 
+def test_interpolate3_mlp_validation():
+    f = "mesorasi_interpolate3_mlp"
+    A = ctypes.c_void_p(0x2000)
+    d, W, b = _mlp_args([128, 128, 128])
+    args = lambda **k: [FAKE, FAKE, FAKE, k.get("lds", 128), 2, 100, 50, A, k.get("lda", 128), 1, k.get("n", 2),
+                        k.get("d", d), W, b, 3, FAKE, k.get("ldy", 128), NULL]
+    assert st(f, *args(lda=64)) == _lib.EINVAL                                   # ld_add < C
+    assert st(f, *args(ldy=100)) == _lib.EINVAL                                  # ld_y < output width
+    dw, Ww, bw = _mlp_args([128, 256, 64])
+    assert st(f, *args(d=dw)) == _lib.EUNSUPPORTED                               # a layer wider than 128
+    d6, W6, b6 = _mlp_args([6, 32])
+    assert st(f, *args(d=d6, n=1, lds=8, lda=8, ldy=32)) == _lib.EUNSUPPORTED     # dims[0] % 4 != 0
+    assert st(f, *args(lds=130)) == _lib.EUNSUPPORTED                            # ld_src % 4 != 0
+    a = args()
+    a[5] = 0
+    assert st(f, *a) == _lib.OK                                                  # Nd = 0: nothing to do
+    a = args()
+    a[0] = NULL
+    assert st(f, *a) == _lib.EINVAL                                              # NULL nit
+
+
 def test_count_out_of_range_validation():
     f = "mesorasi_count_out_of_range"
     assert st(f, FAKE, -1, 10, FAKE, NULL) == _lib.EINVAL         # n < 0

@@ -111,3 +111,10 @@ def test_interpolation_bytes():
     assert extra["logical_gather_bytes"] == 12 * 2 * 100 * 16
     kind, amount, _ = bench.call_work("interpolate3_add", (nit, None, f, torch.zeros(2, 100, 16)), {})
     assert kind == "hbm" and amount == pytest.approx((base + 4 * 2 * 100 * 16) / 1e9)
+
+
+def test_interpolate3_mlp_work_is_the_mlp():
+    prm = types.SimpleNamespace(dims=[128, 128, 128], dtype=0)
+    nit = torch.zeros(2, 1000, 3, dtype=torch.int32)
+    kind, amount, _ = bench.call_work("interpolate3_mlp", (nit, None, None, None, prm), {})
+    assert kind == "mfma" and amount == pytest.approx(2.0 * 2000 * (128 * 128 * 2) / 1e12)

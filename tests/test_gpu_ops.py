@@ -612,6 +612,34 @@ def test_interpolate3_add(gpu, B, Nd, Ns, C, relu, inplace):
     assert np.array_equal(host(out), np.maximum(plain, 0.0) if relu else plain)
 
 
+@pytest.mark.parametrize("B,Nd,Ns,widths", [(16, 4096, 1024, [128, 128, 128]), (3, 1000, 77, [20, 33, 9]),
+                                             (2, 20000, 500, [64, 128, 13])])
+def test_interpolate3_mlp(gpu, B, Nd, Ns, widths):
+    """The interpolate-add in the register MLP's loader: the two-call form's
+    rows (mesorasi_interpolate3_add) bit for bit, so the same MLP gives the
+    same output when that form also runs the register MLP (more than 32768
+    rows); the oracle's interpolation + add + ReLU + MLP within 1e-4."""
+    rr = g(17)
+    C = widths[0]
+    dst = rr.uniform(-1, 1, (B, Nd, 3)).astype(np.float32)
+    src = rr.uniform(-1, 1, (B, Ns, 3)).astype(np.float32)
+    f = rr.standard_normal((B, Ns, C)).astype(np.float32)
+    a = rr.standard_normal((B, Nd, C)).astype(np.float32)
+    Ws, bs = _weights(rr, widths)
+    relu_mask = (1 << (len(widths) - 2)) - 1       # last layer linear
+    p = ops.MLPParams(Ws, bs)
+    assert ops.interpolate3_mlp_supported(p)
+    nit, dist = ops.three_nn(dev(dst), dev(src))
+    y = ops.interpolate3_mlp(nit, dist, dev(f), dev(a), p, relu_mask=relu_mask)
+    h = ops.interpolate3_add(nit, dist, dev(f), dev(a))
+    y2 = ops.pointwise_mlp(h, p, relu_mask=relu_mask)
+    if B * Nd > 32768:
+        assert torch.equal(y, y2)
+    hr = np.maximum(O.interpolate3(dst, src, f).astype(np.float64) + a, 0.0).astype(np.float32)
+    ref = O.mlp(hr.reshape(-1, C), Ws, bs, relu_mask=relu_mask).reshape(B, Nd, -1)
+    assert normwise(host(y), ref) <= 1e-4
+
+
 def test_three_nn_hand_example(gpu):
     """The hand-worked interpolation (weights 1/d2 over the 3 nearest)
     through the split GPU form."""
