@@ -4,7 +4,11 @@
 // outputs are small enough to stay on chip (Sec. 4.2: layer outputs shrink
 // from 8-32 MB to 512 KB-1 MB).  A workgroup keeps one 64-row tile's
 // activations in LDS through all layers (k-major, odd stride); only the last
-// layer goes to HBM (or is pooled).
+// layer goes to HBM (or is pooled).  Below 32768 rows, where 64-row tiles
+// would leave the CUs one workgroup each, the tiles are 32 rows (one MFMA
+// row block), so two workgroups share a CU and overlap each other's loads,
+// barriers and epilogues (16384 x 67 -> 64 -> 64 -> 128: 25.6 -> 22.6 us;
+// 4096 x 131 -> 128 -> 128 -> 128: 38.8 -> 23.2 us).
 //
 // Weights never pass through LDS.  Within each 16-wide k-slice the MFMA
 // steps use a permuted k order -- lane l at step i takes k = 8*(l/32) + i --
@@ -20,6 +24,8 @@
 // The conventional module's rows can be gathered straight from the inputs
 // through the neighbor index table, which makes that module one kernel:
 // gather, every layer, max pool.
+#include <type_traits>
+
 #include "common.h"
 #include "mlp_internal.h"
 
@@ -29,9 +35,11 @@ namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int FBM = 64;        // rows per workgroup (two 32-row halves)
+// H 32-row halves per workgroup tile: 64 rows (H = 2), or 32 rows (H = 1)
+// when 64-row tiles would leave the CUs with one workgroup each
 constexpr int kOutF32 = 0, kOutBf16 = 1, kOutPool = 2;   // last layer: store fp32 / bf16, or pooled max
-constexpr int FST = FBM + 1;   // k-major activation stride (odd: conflict-free)
+template <int H>
+constexpr int fst() { return 32 * H + 1; }   // k-major activation stride (odd: conflict-free)
 constexpr int kMaxIn = 160;    // widest layer input kept in LDS (padded to 16)
 constexpr int kMaxOut = 128;   // widest layer output: 4 column blocks, one per wave
 
@@ -106,15 +114,15 @@ __device__ __forceinline__ void load_w8(const float* __restrict__ W, int n, int 
 // A layer of at most 64 outputs (one or two blocks) is split by rows
 // instead: wave w owns block w / 2 for the 32-row half w % 2, so no wave
 // repeats another's MFMAs.
-template <int CB>
+template <int CB, int H>
 __device__ __forceinline__ bool row_split(const FusedArgs& a, int l) {
-    return CB == 1 && a.dims[l + 1] <= 64;
+    return H == 2 && CB == 1 && a.dims[l + 1] <= 64;
 }
 
-template <int CB>
+template <int CB, int H>
 __device__ __forceinline__ void layer_blocks(const FusedArgs& a, int l, int wave, int (&cbs)[CB]) {
     const int ncb = (a.dims[l + 1] + 31) / 32;
-    if (row_split<CB>(a, l)) {
+    if (row_split<CB, H>(a, l)) {
         cbs[0] = min(wave >> 1, ncb - 1);
         return;
     }
@@ -123,13 +131,13 @@ __device__ __forceinline__ void layer_blocks(const FusedArgs& a, int l, int wave
 }
 
 // This lane's weights of the first k-slice (k = 0 .. 15) of layer l.
-template <int CB>
+template <int CB, int H>
 __device__ __forceinline__ void load_first_slice(const FusedArgs& a, int l, int wave, int lane, float (&w)[CB][8]) {
     const int K = a.dims[l], N = a.dims[l + 1];
     const float* __restrict__ W = a.W[l];
     const bool vec = (K % 4) == 0 && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
     int cbs[CB];
-    layer_blocks<CB>(a, l, wave, cbs);
+    layer_blocks<CB, H>(a, l, wave, cbs);
 #pragma unroll
     for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + (lane & 31), N, 8 * (lane >> 5), K, vec, w[j]);
 }
@@ -139,7 +147,7 @@ __device__ __forceinline__ void load_first_slice(const FusedArgs& a, int l, int 
 // input tile or the previous layer's epilogue, so the weights' round trip
 // overlaps that work) and the next layer's on return; the bias is requested
 // before the k loop for the same reason.
-template <int CB, int OUT>
+template <int CB, int OUT, int H>
 __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const float* __restrict__ hin,
                                             float* __restrict__ hout, int64_t row_t, int tid, int lane, int wave,
                                             float (&wb)[2][CB][8]) {
@@ -151,7 +159,8 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
     const int kh = 8 * (lane >> 5);              // this lane's half of each 16-slice
     const int cl = lane & 31;
     int cbs[CB];
-    layer_blocks<CB>(a, l, wave, cbs);
+    constexpr int FST = fst<H>(), FBM = 32 * H;
+    layer_blocks<CB, H>(a, l, wave, cbs);
     const float* __restrict__ bias = a.bias[l];
     float bvs[CB];
 #pragma unroll
@@ -160,16 +169,16 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
         bvs[j] = (bias && col < N) ? bias[col] : 0.0f;
     }
 
-    f32x16 acc[CB][2];
+    f32x16 acc[CB][H];
 #pragma unroll
     for (int j = 0; j < CB; ++j)
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < H; ++h)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[j][h][r] = 0.0f;
 
     const float* hrow = hin + kh * FST + cl;
-    const bool split = row_split<CB>(a, l);
+    const bool split = row_split<CB, H>(a, l);
     const int h0 = wave & 1;
 
     for (int k0 = 0; k0 < K; k0 += 32) {
@@ -182,7 +191,7 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
 #pragma unroll
                 for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + cl, N, ks + 16 + kh, K, vec, wb[half ^ 1][j]);
             }
-            if (split) {
+            if (H == 2 && split) {
                 // this wave's 32-row half only
                 float av[8];
 #pragma unroll
@@ -193,26 +202,25 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
                     acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], wb[half][0][i], acc[0][0], 0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
             } else {
-                float av[8][2];
+                float av[8][H];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    av[i][0] = hrow[(ks + i) * FST];
-                    av[i][1] = hrow[(ks + i) * FST + 32];
-                }
+                for (int i = 0; i < 8; ++i)
+#pragma unroll
+                    for (int h = 0; h < H; ++h) av[i][h] = hrow[(ks + i) * FST + 32 * h];
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int i = 0; i < 8; ++i)
 #pragma unroll
                     for (int j = 0; j < CB; ++j)
 #pragma unroll
-                        for (int h = 0; h < 2; ++h)
+                        for (int h = 0; h < H; ++h)
                             acc[j][h] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][h], wb[half][j][i], acc[j][h], 0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
     }
 
-    if (!last) load_first_slice<CB>(a, l + 1, wave, lane, wb[0]);
+    if (!last) load_first_slice<CB, H>(a, l + 1, wave, lane, wb[0]);
 
     // epilogue: bias + ReLU, then LDS (next layer's input) or HBM
     const bool relu = (a.relu_mask >> l) & 1u;
@@ -286,14 +294,14 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
             }
         }
     };
-    if (split) {
+    if (H == 2 && split) {
         if ((wave >> 1) < ncb) emit(acc[0][0], 0, h0);
     } else {
 #pragma unroll
         for (int j = 0; j < CB; ++j) {
             if (wave + 4 * j >= ncb) continue;
-            emit(acc[j][0], j, 0);
-            emit(acc[j][1], j, 1);
+#pragma unroll
+            for (int h = 0; h < H; ++h) emit(acc[j][h], j, h);
         }
     }
     if (!last) {
@@ -308,16 +316,17 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
 // row half for layers of at most 64 outputs; two workgroups per CU (with a
 // three-workgroup register budget the row-split epilogue spilled).  (Wider
 // outputs measured slower than the per-layer GEMMs.)
-template <int CB, int IN, int OUT>
+template <int CB, int IN, int OUT, int H>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 void mlp_fused_f32_kernel(FusedArgs a) {
+    constexpr int FBM = 32 * H, FST = fst<H>();
     extern __shared__ float smem[];
     float* H0 = smem;
     float* H1 = smem + a.hsize;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t row_t = (int64_t)blockIdx.x * FBM;
     float wb[2][CB][8];
-    load_first_slice<CB>(a, 0, wave, lane, wb[0]);
+    load_first_slice<CB, H>(a, 0, wave, lane, wb[0]);
 
     // layer-0 input tile -> H0 (k-major), zero beyond c0 + c1 up to the slice edge
     {
@@ -422,11 +431,18 @@ void mlp_fused_f32_kernel(FusedArgs a) {
     for (int l = 0; l < a.n_layers; ++l) {
         const float* hin = (l & 1) ? H1 : H0;
         float* hout = (l & 1) ? H0 : H1;
-        fused_layer<CB, OUT>(a, l, hin, hout, row_t, tid, lane, wave, wb);
+        fused_layer<CB, OUT, H>(a, l, hin, hout, row_t, tid, lane, wave, wb);
     }
 }
 
 }  // namespace
+
+// 32-row tiles when 64-row ones would give fewer than two workgroups per
+// CU (256 CUs)
+#ifndef MESO_FUSED_H1_BELOW
+#define MESO_FUSED_H1_BELOW (64 * 2 * 256)
+#endif
+static int fused_halves(int64_t rows) { return rows < MESO_FUSED_H1_BELOW ? 1 : 2; }
 
 bool fused_mlp_supported(int n_layers, const int32_t* dims, int dtype) {
     if (dtype != MESORASI_F32 || n_layers < 2) return false;
@@ -467,7 +483,8 @@ int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1,
     a.ldy = ld_y;
     a.out_bf16 = out_dtype == MESORASI_BF16;
     a.G = pool_group;
-    a.hsize = hmax * FST;
+    const int H = fused_halves(rows);
+    a.hsize = hmax * (32 * H + 1);
     const size_t lds = sizeof(float) * 2 * (size_t)a.hsize;
     if (pool_group > 0) {
         const int rc = zero_rows_f32(static_cast<float*>(y), rows / pool_group, dims[n_layers], ld_y, s);
@@ -475,18 +492,23 @@ int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1,
     }
     // one instantiation per input and output form keeps each launch's code
     // (and its instruction-cache footprint) to the path it runs
-    const dim3 grid((unsigned)ceil_div(rows, FBM)), block(256);
+    const dim3 grid((unsigned)ceil_div(rows, 32 * H)), block(256);
     const bool gather = g != nullptr;
-    if (pool_group > 0) {
-        if (gather) mlp_fused_f32_kernel<1, kInGather, kOutPool><<<grid, block, lds, s>>>(a);
-        else mlp_fused_f32_kernel<1, kInPlain, kOutPool><<<grid, block, lds, s>>>(a);
-    } else if (a.out_bf16) {
-        if (gather) mlp_fused_f32_kernel<1, kInGather, kOutBf16><<<grid, block, lds, s>>>(a);
-        else mlp_fused_f32_kernel<1, kInPlain, kOutBf16><<<grid, block, lds, s>>>(a);
-    } else {
-        if (gather) mlp_fused_f32_kernel<1, kInGather, kOutF32><<<grid, block, lds, s>>>(a);
-        else mlp_fused_f32_kernel<1, kInPlain, kOutF32><<<grid, block, lds, s>>>(a);
-    }
+    auto go = [&](auto h) {
+        constexpr int HH = decltype(h)::value;
+        if (pool_group > 0) {
+            if (gather) mlp_fused_f32_kernel<1, kInGather, kOutPool, HH><<<grid, block, lds, s>>>(a);
+            else mlp_fused_f32_kernel<1, kInPlain, kOutPool, HH><<<grid, block, lds, s>>>(a);
+        } else if (a.out_bf16) {
+            if (gather) mlp_fused_f32_kernel<1, kInGather, kOutBf16, HH><<<grid, block, lds, s>>>(a);
+            else mlp_fused_f32_kernel<1, kInPlain, kOutBf16, HH><<<grid, block, lds, s>>>(a);
+        } else {
+            if (gather) mlp_fused_f32_kernel<1, kInGather, kOutF32, HH><<<grid, block, lds, s>>>(a);
+            else mlp_fused_f32_kernel<1, kInPlain, kOutF32, HH><<<grid, block, lds, s>>>(a);
+        }
+    };
+    if (H == 1) go(std::integral_constant<int, 1>{});
+    else go(std::integral_constant<int, 2>{});
     return after_launch("mesorasi_pointwise_mlp (fused)");
 }
 
@@ -509,10 +531,12 @@ int run_fused_aggregate_mlp(const float* cxyz, const MlpAggregate& ag, int64_t r
     a.relu_mask = relu_mask;
     a.y = y;
     a.ldy = ld_y;
-    a.hsize = hmax * FST;
+    const int H = fused_halves(rows);
+    a.hsize = hmax * (32 * H + 1);
     const size_t lds = sizeof(float) * 2 * (size_t)a.hsize;
-    const dim3 grid((unsigned)ceil_div(rows, FBM)), block(256);
-    mlp_fused_f32_kernel<1, kInAgg, kOutF32><<<grid, block, lds, s>>>(a);
+    const dim3 grid((unsigned)ceil_div(rows, 32 * H)), block(256);
+    if (H == 1) mlp_fused_f32_kernel<1, kInAgg, kOutF32, 1><<<grid, block, lds, s>>>(a);
+    else mlp_fused_f32_kernel<1, kInAgg, kOutF32, 2><<<grid, block, lds, s>>>(a);
     return after_launch("mesorasi_aggregate_mlp");
 }
 
