@@ -86,25 +86,31 @@ constexpr int kInPlain = 0, kInGather = 1, kInAgg = 2;   // layer-0 input forms
 
 __host__ __device__ __forceinline__ int pad16(int x) { return (x + 15) & ~15; }
 
-// 8 consecutive weights W[n][k .. k+7] of a row, zero where k >= K or n >= N.
-// 16-byte loads when the row is aligned and fully inside; element loads
-// (from clamped, in-bounds addresses) otherwise.
-__device__ __forceinline__ void load_w8(const float* __restrict__ W, int n, int N, int k, int K, bool vec,
-                                        float (&v)[8]) {
-    const bool nok = n < N;
-    const float* row = W + (int64_t)(nok ? n : 0) * K;
-    if (vec && k + 8 <= K) {
-        const float4 a = *reinterpret_cast<const float4*>(row + k);
-        const float4 b = *reinterpret_cast<const float4*>(row + k + 4);
-        v[0] = nok ? a.x : 0.0f; v[1] = nok ? a.y : 0.0f; v[2] = nok ? a.z : 0.0f; v[3] = nok ? a.w : 0.0f;
-        v[4] = nok ? b.x : 0.0f; v[5] = nok ? b.y : 0.0f; v[6] = nok ? b.z : 0.0f; v[7] = nok ? b.w : 0.0f;
+// 8 consecutive weights W[n][k .. k+7] of a row, from in-bounds addresses:
+// a row n >= N reads row 0 and columns k >= K read the row's last column.
+// Those values are never used as such -- a column n >= N is never stored,
+// and k >= K meets the zeroed k padding of the activation tile (finite
+// weights times zero) -- so no select touches the loaded values, and the
+// loads stay in flight until the MFMAs of the slice that uses them (a
+// select right after the loads made the compiler wait for every slice's
+// weights as soon as it requested them, exposing an L2 round trip per
+// slice).
+// VEC (rows 16-byte aligned, K % 8 == 0): two 16-byte loads, a group past
+// K read from the row's last full group (such a group is wholly past K:
+// its values meet zero activations); otherwise eight element loads from
+// clamped addresses.
+template <bool VEC>
+__device__ __forceinline__ void load_w8(const float* __restrict__ W, int n, int N, int k, int K, float (&v)[8]) {
+    const float* row = W + (int64_t)(n < N ? n : 0) * K;
+    if constexpr (VEC) {
+        const int kk = min(k, K - 8);
+        const float4 a = *reinterpret_cast<const float4*>(row + kk);
+        const float4 b = *reinterpret_cast<const float4*>(row + kk + 4);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
     } else {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const bool ok = nok && k + i < K;
-            const float w = row[ok ? k + i : 0];
-            v[i] = ok ? w : 0.0f;
-        }
+        for (int i = 0; i < 8; ++i) v[i] = row[min(k + i, K - 1)];
     }
 }
 
@@ -130,16 +136,24 @@ __device__ __forceinline__ void layer_blocks(const FusedArgs& a, int l, int wave
     for (int j = 0; j < CB; ++j) cbs[j] = (wave + 4 * j < ncb) ? wave + 4 * j : min(wave, ncb - 1);
 }
 
+__device__ __forceinline__ bool w_vec(const float* W, int K) {
+    return K % 8 == 0 && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
+}
+
 // This lane's weights of the first k-slice (k = 0 .. 15) of layer l.
 template <int CB, int H>
 __device__ __forceinline__ void load_first_slice(const FusedArgs& a, int l, int wave, int lane, float (&w)[CB][8]) {
     const int K = a.dims[l], N = a.dims[l + 1];
     const float* __restrict__ W = a.W[l];
-    const bool vec = (K % 4) == 0 && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
     int cbs[CB];
     layer_blocks<CB, H>(a, l, wave, cbs);
+    if (w_vec(W, K)) {
 #pragma unroll
-    for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + (lane & 31), N, 8 * (lane >> 5), K, vec, w[j]);
+        for (int j = 0; j < CB; ++j) load_w8<true>(W, cbs[j] * 32 + (lane & 31), N, 8 * (lane >> 5), K, w[j]);
+    } else {
+#pragma unroll
+        for (int j = 0; j < CB; ++j) load_w8<false>(W, cbs[j] * 32 + (lane & 31), N, 8 * (lane >> 5), K, w[j]);
+    }
 }
 
 // One layer: hin [K][FST] (LDS) x W^T -> CB column blocks of 32 per wave.
@@ -155,7 +169,6 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
     const float* __restrict__ W = a.W[l];
     const int ncb = (N + 31) / 32;
     const bool last = l + 1 == a.n_layers;
-    const bool vec = (K % 4) == 0 && ((reinterpret_cast<uintptr_t>(W) & 15) == 0);
     const int kh = 8 * (lane >> 5);              // this lane's half of each 16-slice
     const int cl = lane & 31;
     int cbs[CB];
@@ -181,44 +194,56 @@ __device__ __forceinline__ void fused_layer(const FusedArgs& a, int l, const flo
     const bool split = row_split<CB, H>(a, l);
     const int h0 = wave & 1;
 
-    for (int k0 = 0; k0 < K; k0 += 32) {
-        // two slices per trip so the double-buffered weights keep static indices
+    // the k loop, one copy per weight-load form so the compiler knows how
+    // many loads are in flight at every MFMA
+    auto kloop = [&](auto vec_c) {
+        constexpr bool VEC = decltype(vec_c)::value;
+        for (int k0 = 0; k0 < K; k0 += 32) {
+            // two slices per trip so the double-buffered weights keep static indices
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const int ks = k0 + 16 * half;
-            if (ks >= K) break;
-            if (ks + 16 < K) {
+            for (int half = 0; half < 2; ++half) {
+                const int ks = k0 + 16 * half;
+                if (ks >= K) break;
+                // the next slice's weights, requested unconditionally (past
+                // K the loads are in-bounds and unused): under a condition
+                // the compiler could not count the loads in flight and made
+                // every MFMA of the following slice wait for these as well
+                if (VEC || ks + 16 < K) {
 #pragma unroll
-                for (int j = 0; j < CB; ++j) load_w8(W, cbs[j] * 32 + cl, N, ks + 16 + kh, K, vec, wb[half ^ 1][j]);
-            }
-            if (H == 2 && split) {
-                // this wave's 32-row half only
-                float av[8];
+                    for (int j = 0; j < CB; ++j) load_w8<VEC>(W, cbs[j] * 32 + cl, N, ks + 16 + kh, K, wb[half ^ 1][j]);
+                }
+                if (H == 2 && split) {
+                    // this wave's 32-row half only
+                    float av[8];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) av[i] = hrow[(ks + i) * FST + 32 * h0];
-                __builtin_amdgcn_sched_barrier(0);
+                    for (int i = 0; i < 8; ++i) av[i] = hrow[(ks + i) * FST + 32 * h0];
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], wb[half][0][i], acc[0][0], 0, 0, 0);
-                __builtin_amdgcn_sched_barrier(0);
-            } else {
-                float av[8][H];
+                    for (int i = 0; i < 8; ++i)
+                        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], wb[half][0][i], acc[0][0], 0, 0, 0);
+                    __builtin_amdgcn_sched_barrier(0);
+                } else {
+                    float av[8][H];
 #pragma unroll
-                for (int i = 0; i < 8; ++i)
+                    for (int i = 0; i < 8; ++i)
 #pragma unroll
-                    for (int h = 0; h < H; ++h) av[i][h] = hrow[(ks + i) * FST + 32 * h];
-                __builtin_amdgcn_sched_barrier(0);
+                        for (int h = 0; h < H; ++h) av[i][h] = hrow[(ks + i) * FST + 32 * h];
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int i = 0; i < 8; ++i)
+                    for (int i = 0; i < 8; ++i)
 #pragma unroll
-                    for (int j = 0; j < CB; ++j)
+                        for (int j = 0; j < CB; ++j)
 #pragma unroll
-                        for (int h = 0; h < H; ++h)
-                            acc[j][h] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][h], wb[half][j][i], acc[j][h], 0, 0, 0);
-                __builtin_amdgcn_sched_barrier(0);
+                            for (int h = 0; h < H; ++h)
+                                acc[j][h] =
+                                    __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][h], wb[half][j][i], acc[j][h], 0, 0, 0);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
         }
-    }
+    };
+    if (w_vec(W, K)) kloop(std::true_type{});
+    else kloop(std::false_type{});
 
     if (!last) load_first_slice<CB, H>(a, l + 1, wave, lane, wb[0]);
 
