@@ -84,7 +84,7 @@ class StageTimer:
     """Wraps the ops entry points so every call records a start/end event on
     the stream it is launched on."""
 
-    NAMES = ("fps", "ball_query", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3",
+    NAMES = ("fps", "fps_prefix", "ball_query", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3",
              "three_nn", "interpolate3_apply", "interpolate3_add", "interpolate3_mlp", "aggregate_mlp")
 
     def __init__(self, ops):
@@ -144,6 +144,8 @@ def call_work(name, a, kw, result=None):
 
     fps:            (M-1) * N point updates per cloud, 8 flops each (3 sub,
                     1 mul, 2 fma) -> alu
+    fps_prefix:     the nested sampling as a prefix: compulsory HBM bytes
+                    (indices and coordinates read and written) -> hbm
     ball_query:     the candidate pairs the search rule scans, 8 flops each
                     -> alu: a query that fills its K slots scans up to its
                     K-th hit (index nit[K-1] + 1), otherwise all N points;
@@ -172,6 +174,9 @@ def call_work(name, a, kw, result=None):
         B, N = xyz.shape[0], xyz.shape[1]
         # one workgroup per cloud walks M - 1 dependent iterations
         return ("alu", 8.0 * B * (M - 1) * N / 1e12, {"serial_iterations": M - 1, "workgroups": B})
+    if name == "fps_prefix":
+        ip, M = arg(0, "idx_prev"), arg(2, "M")
+        return ("hbm", 32.0 * ip.shape[0] * M / 1e9, None)
     if name == "ball_query":
         xyz, q, K = arg(0, "xyz"), arg(1, "qxyz"), arg(3, "K")
         B, N, M = xyz.shape[0], xyz.shape[1], q.shape[1]
@@ -443,6 +448,7 @@ def measure(tag, args, dev, headline=False):
     for i, m in enumerate(spec.get("sa", [])):
         per_module[f"sa{i + 1}"] = B * m["M"] / t_step
         ms = sum(stages.get(f"{n}#{i}", 0.0) for n in ("fps", "ball_query", "pointwise_mlp", "aggregate_max"))
+        ms += stages.get(f"fps_prefix#{i - 1}", 0.0) if i else 0.0
         module_ms[f"sa{i + 1}"] = round(ms, 5)
     if spec["kind"] == "dgcnn":
         for l in range(len(spec["edge"])):

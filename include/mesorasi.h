@@ -102,6 +102,34 @@ int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, int32_t* idx
 size_t mesorasi_fps_workspace(int64_t B, int64_t N, int64_t M);
 
 /*
+ * Farthest-point sampling of a sampled set: the nested sampling of stacked
+ * set-abstraction modules, where each module samples its centroids from the
+ * previous module's centroids (Sec. 6 "Software Setup"; Sec. 3.1, each
+ * module's output points are the next module's input points).
+ * The greedy sampling above is a greedy permutation: run from index 0 on
+ * the ordered output of an earlier run (M_prev points), it selects exactly
+ * the first M of them.  (At step k the earlier run chose the point of
+ * largest min-distance to the points chosen so far among all points; that
+ * point is in the subset, with the same fp32 min-distance, and every other
+ * subset point of that value comes later in the subset.  A step whose
+ * largest min-distance is 0 -- the cloud's distinct points used up -- chose
+ * point 0 in the earlier run and chooses subset point 0 here.)  So no
+ * distance is computed:
+ *   idx[b][k]  = k, or 0 where k > 0 and idx_prev[b][k] == 0
+ *   cxyz[b][k] = cxyz_prev[b][k]
+ * which equals mesorasi_fps(cxyz_prev, B, M_prev, M) bit for bit when
+ * (idx_prev, cxyz_prev) is an output of mesorasi_fps or of this call; for
+ * any other input the result is not a sampling of it.
+ *   idx_prev  [B, M_prev] int32, cxyz_prev [B, M_prev, 3] float32 (nullable
+ *             when cxyz is NULL)
+ *   idx       [B, M] int32 out; cxyz [B, M, 3] float32 out, nullable
+ * Errors: EINVAL for sizes < 0, M > M_prev, NULL idx_prev/idx, cxyz
+ *         without cxyz_prev; EUNSUPPORTED for M_prev > MESORASI_MAX_N_FPS.
+ */
+int mesorasi_fps_prefix(const int32_t* idx_prev, const float* cxyz_prev, int64_t B, int64_t M_prev, int64_t M,
+                        int32_t* idx, float* cxyz, void* stream);
+
+/*
  * Ball query: neighbor search N (Sec. 3.1 "Neighbor Search") producing the
  * NIT (Sec. 4.1 walk-through).  For each query q, the first K point indices
  * in ascending order with squared distance (same rule as FPS) strictly

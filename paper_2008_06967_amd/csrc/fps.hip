@@ -449,6 +449,27 @@ static int launch_fps_multi(const float* xyz, int64_t B, int N, int M, int G, in
     return after_launch("mesorasi_fps");
 }
 
+// Sampling of an already sampled, ordered set: the first M points of that
+// order (one thread per output point and coordinate triple).
+__global__ __launch_bounds__(256) void fps_prefix_kernel(const int32_t* __restrict__ idx_prev,
+                                                        const float* __restrict__ cxyz_prev, int64_t B, int Mp, int M,
+                                                        int32_t* __restrict__ idx, float* __restrict__ cxyz) {
+    const int64_t total = B * M;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t b = e / M;
+        const int k = (int)(e - b * M);
+        const int64_t src = b * Mp + k;
+        // a step whose largest min-distance was 0 took point 0 in the earlier
+        // run (index 0 there) and takes subset point 0 here
+        idx[e] = (k == 0 || idx_prev[src] != 0) ? k : 0;
+        if (cxyz) {
+            cxyz[3 * e + 0] = cxyz_prev[3 * src + 0];
+            cxyz[3 * e + 1] = cxyz_prev[3 * src + 1];
+            cxyz[3 * e + 2] = cxyz_prev[3 * src + 2];
+        }
+    }
+}
+
 }  // namespace meso
 
 using namespace meso;
@@ -493,4 +514,24 @@ extern "C" int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, i
     else if (n <= 32768) launch_fps<1024, 32, false>(xyz, B, n, m, idx, cxyz, s);
     else launch_fps<1024, 64, false>(xyz, B, n, m, idx, cxyz, s);
     return after_launch("mesorasi_fps");
+}
+
+extern "C" int mesorasi_fps_prefix(const int32_t* idx_prev, const float* cxyz_prev, int64_t B, int64_t M_prev,
+                                   int64_t M, int32_t* idx, float* cxyz, void* stream) {
+    MESO_REQUIRE(B >= 0 && M_prev >= 0 && M >= 0, MESORASI_EINVAL,
+                 "mesorasi_fps_prefix: negative size (B=%lld M_prev=%lld M=%lld)", (long long)B, (long long)M_prev,
+                 (long long)M);
+    MESO_REQUIRE(M <= M_prev, MESORASI_EINVAL, "mesorasi_fps_prefix: M = %lld > M_prev = %lld", (long long)M,
+                 (long long)M_prev);
+    if (B == 0 || M == 0) return MESORASI_OK;
+    MESO_REQUIRE(idx_prev && idx, MESORASI_EINVAL, "mesorasi_fps_prefix: NULL idx_prev or idx");
+    MESO_REQUIRE(!cxyz || cxyz_prev, MESORASI_EINVAL, "mesorasi_fps_prefix: cxyz requested without cxyz_prev");
+    MESO_REQUIRE(M_prev <= MESORASI_MAX_N_FPS, MESORASI_EUNSUPPORTED, "mesorasi_fps_prefix: M_prev = %lld > %d",
+                 (long long)M_prev, MESORASI_MAX_N_FPS);
+    MESO_REQUIRE(B <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_fps_prefix: B too large");
+    const int64_t total = B * M;
+    const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
+    fps_prefix_kernel<<<dim3(grid), dim3(256), 0, as_stream(stream)>>>(idx_prev, cxyz_prev, B, (int)M_prev, (int)M,
+                                                                       idx, cxyz);
+    return after_launch("mesorasi_fps_prefix");
 }

@@ -765,10 +765,9 @@ constexpr int kIpWaves = 4;
 constexpr int kIpDests = 128;    // destinations per workgroup, two per lane
 constexpr int kIpChunk = 1024;   // sources staged in LDS per pass
 
-// insert (d, j) into an ascending top-3 in (distance, index) order (used
-// both for sources in index order and for merging lists).  An empty slot
-// (+inf, INT_MAX) takes any source, also one whose distance overflowed to
-// +inf; padding sources carry j = INT_MAX and are never inserted.
+// insert (d, j) into an ascending top-3 in (distance, index) order (the
+// merge of the waves' lists).  An empty slot (+inf, INT_MAX) takes any
+// entry, also one whose distance overflowed to +inf.
 __device__ __forceinline__ void top3_insert(float d, int j, float (&e)[3], int (&jj)[3]) {
     if (pair_before(d, j, e[2], jj[2])) {
         if (pair_before(d, j, e[1], jj[1])) {
@@ -787,6 +786,29 @@ __device__ __forceinline__ void top3_insert(float d, int j, float (&e)[3], int (
             e[2] = d;
             jj[2] = j;
         }
+    }
+}
+
+// The scan's top-3 of one destination, as distance bits: sources arrive in
+// ascending index order, so a source enters only with a strictly smaller
+// distance (an equal one has the larger index) and one unsigned compare of
+// the bits (distances are >= +0) is the (distance, index) order.  An empty
+// slot holds kTopOpen, above the bits of every distance, +inf included (so
+// it takes any source, also one whose distance overflowed), and below
+// those of the NaN that padding sources carry (never inserted).
+constexpr unsigned kTopOpen = 0x7f800001u;
+
+__device__ __forceinline__ void top3_scan_insert(unsigned db, int j, unsigned (&eb)[3], int (&jj)[3]) {
+    if (db < eb[2]) {
+        const bool b0 = db < eb[0], b1 = db < eb[1];
+        const unsigned e0 = eb[0], e1 = eb[1];
+        const int j0 = jj[0], j1 = jj[1];
+        eb[2] = b1 ? e1 : db;
+        jj[2] = b1 ? j1 : j;
+        eb[1] = b0 ? e0 : (b1 ? db : e1);
+        jj[1] = b0 ? j0 : (b1 ? j : j1);
+        eb[0] = b0 ? db : e0;
+        jj[0] = b0 ? j : j0;
     }
 }
 
@@ -824,13 +846,13 @@ __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __r
         qy[h] = xyz_dst[(b * Nd + ic) * 3 + 1];
         qz[h] = xyz_dst[(b * Nd + ic) * 3 + 2];
     }
-    float e[2][3];
+    unsigned eb[2][3];
     int jj[2][3];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int k = 0; k < 3; ++k) {
-            e[h][k] = inf;
+            eb[h][k] = kTopOpen;
             jj[h][k] = 0x7fffffff;
         }
 
@@ -838,7 +860,8 @@ __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __r
         __syncthreads();
         const int n = min(kIpChunk, Ns - c0);
         for (int t = tid; t < n + 16; t += 64 * kIpWaves) {
-            float x = inf, y = inf, z = inf;      // padding: infinite distance and index INT_MAX
+            // padding: NaN coordinates, so a NaN distance that never enters
+            float x = __builtin_nanf(""), y = x, z = x;
             if (t < n) {
                 const float* src = xyz_src + (b * Ns + c0 + t) * 3;
                 x = src[0];
@@ -860,17 +883,20 @@ __global__ __launch_bounds__(64 * kIpWaves) void interp3_kernel(const float* __r
                         az[4] = {vz.x, vz.y, vz.z, vz.w};
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int j = t + u < n ? c0 + t + u : 0x7fffffff;
+                const int j = c0 + t + u;
 #pragma unroll
-                for (int h = 0; h < 2; ++h) top3_insert(dist3(ax[u], ay[u], az[u], qx[h], qy[h], qz[h]), j, e[h], jj[h]);
+                for (int h = 0; h < 2; ++h)
+                    top3_scan_insert(__float_as_uint(dist3(ax[u], ay[u], az[u], qx[h], qy[h], qz[h])), j, eb[h],
+                                     jj[h]);
             }
         }
     }
+    // back to (distance, index) pairs, an empty slot as (+inf, INT_MAX)
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int k = 0; k < 3; ++k) {
-            s_e[wave][64 * h + lane][k] = e[h][k];
+            s_e[wave][64 * h + lane][k] = eb[h][k] == kTopOpen ? inf : __uint_as_float(eb[h][k]);
             s_jj[wave][64 * h + lane][k] = jj[h][k];
         }
     __syncthreads();

@@ -30,10 +30,11 @@ from ._lib import F32, BF16
 
 class Net:
     def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda", debug: bool = False,
-                 fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384):
+                 fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True):
         self.spec = spec
         self.fuse_aggregation = fuse_aggregation
         self.fp_coarse_min_rows = fp_coarse_min_rows
+        self.fps_prefix = fps_prefix
         self.delayed = delayed
         self.device = torch.device(device)
         self.dt = BF16 if spec.get("dtype") == "bf16" else F32
@@ -161,64 +162,92 @@ class PointNet2(Net):
                     rest=ops.MLPParams(Ws[1:], bs[1:], device=self.device)))
 
     def _search_chain(self, xyz, B):
-        """Every level's FPS on the side stream (a level samples the previous
-        level's centroids and waits for nothing else), then the
+        """The sampling on the side stream, then (with fps_prefix) the ball
+        queries of every level after the first, then the
         feature-propagation 3-NN searches, which need only the sampled
-        coordinates.  The ball queries run on the main stream (_ball_query)
-        right before the aggregations that read them, so no FPS waits for
-        one.  (Two branches: a graph replay maps further branches onto
-        shared hardware queues, which can put a main-stream MLP behind an
-        FPS.)"""
+        coordinates.  With fps_prefix every level's centroids are a prefix
+        of the first level's, so the whole chain waits only for the first
+        sampling; the first level's ball query runs on the main stream right
+        after it.  Without it, each level samples the previous level's
+        centroids with the sampling kernel and every ball query runs on the
+        main stream right before the aggregation that reads it (no sampling
+        waits for a ball query).  Each cross-stream wait costs the main
+        stream several microseconds in a graph replay, so the main stream
+        waits at most once per event; the side stream is joined once more
+        at the start of feature propagation.  (Two branches: a graph replay
+        maps further branches onto shared hardware queues, which can put a
+        main-stream MLP behind an FPS.)"""
         main, side = torch.cuda.current_stream(self.device), self.side
         side.wait_stream(main)
         ev_fps = []
         self._bq_done = set()
+        self._waited = set()
+        L = len(self.spec["sa"])
         with torch.cuda.stream(side):
             p = xyz
+            lv = [xyz]
             for i, m in enumerate(self.spec["sa"]):
                 idx = self._buf(f"idx{i}", (B, m["M"]), torch.int32)
                 cx = self._buf(f"cxyz{i}", (B, m["M"], 3))
-                ws = self._ws(f"ws_fps{i}", ops.fps_workspace_bytes(B, p.shape[1], m["M"]))
-                ops.fps(p, m["M"], out_idx=idx, out_xyz=cx, ws=ws)
+                if i > 0 and self.fps_prefix:
+                    # level i samples level i-1's centroids, themselves a
+                    # sampling in selection order: its first M, exactly
+                    ops.fps_prefix(self._bufs[f"idx{i - 1}"], p, m["M"], out_idx=idx, out_xyz=cx)
+                else:
+                    ws = self._ws(f"ws_fps{i}", ops.fps_workspace_bytes(B, p.shape[1], m["M"]))
+                    ops.fps(p, m["M"], out_idx=idx, out_xyz=cx, ws=ws)
                 self._check_range(f"idx{i}", idx, p.shape[1])
+                if i == 0 or not self.fps_prefix:
+                    e = torch.cuda.Event()
+                    e.record(side)
+                    ev_fps.append(e)
+                p = cx
+                lv.append(cx)
+            if self.fps_prefix and L > 1:
+                for i in range(1, L):
+                    self._issue_ball_query(i, lv[i])
+                    self._bq_done.add(i)
                 e = torch.cuda.Event()
                 e.record(side)
-                ev_fps.append(e)
-                p = cx
-            # one event for the searches of every level but the last (all
-            # done long before the first level reads them) and one for the
-            # last, largest search: each cross-stream wait costs the main
-            # stream several microseconds in a graph replay
-            self.ev_nn = [None] * len(self.fp)
+                ev_fps += [e] * (L - 1)
             if self.fp:
                 n = len(self.fp)
-                lv = [xyz] + [self._bufs[f"cxyz{i}"] for i in range(len(self.spec["sa"]))]
                 for i in range(n):
                     fine, coarse = lv[len(lv) - 2 - i], lv[len(lv) - 1 - i]
                     nn = self._buf(f"nn{i}", (B, fine.shape[1], 3), torch.int32)
                     nd = self._buf(f"nnd{i}", (B, fine.shape[1], 3))
                     ops.three_nn(fine, coarse, out_nit=nn, out_dist=nd)
                     self._check_range(f"nn{i}", nn, coarse.shape[1])
-                    if i == n - 1 or i == n - 2:
-                        e = torch.cuda.Event()
-                        e.record(side)
-                        self.ev_nn[0 if i < n - 1 else i] = e
         self._ev_fps = ev_fps
         return ev_fps
 
-    def _ball_query(self, i, p):
-        """Level i's ball query, on the main stream after level i's FPS
-        (issued once per forward, at its first reader)."""
-        if i in self._bq_done:
-            return
-        self._bq_done.add(i)
+    def _issue_ball_query(self, i, p):
+        """Level i's ball query on the current stream."""
         m = self.spec["sa"][i]
         B, N = p.shape[0], p.shape[1]
-        torch.cuda.current_stream(self.device).wait_event(self._ev_fps[i])
         nit = self._buf(f"nit{i}", (B, m["M"], m["K"]), torch.int32)
         ws = self._ws(f"ws_bq{i}", ops.ball_query_workspace_bytes(B, N, m["M"]))
         ops.ball_query(p, self._bufs[f"cxyz{i}"], m["radius"], m["K"], out=nit, ws=ws)
         self._check_range(f"nit{i}", nit, N)
+
+    def _ball_query(self, i, p):
+        """Level i's ball query: on the main stream after level i's sampling
+        (issued once per forward, at its first reader), or, when the search
+        chain already issued it, the wait for it."""
+        if i in self._bq_done:
+            self._wait_fps(i)
+            return
+        self._bq_done.add(i)
+        self._wait_fps(i)
+        self._issue_ball_query(i, p)
+
+    def _wait_fps(self, i):
+        """The main stream waits for level i's sampling, once per event per
+        forward (a repeated wait would add a cross-stream edge to the graph)."""
+        e = self._ev_fps[i]
+        if id(e) not in self._waited:
+            self._waited.add(id(e))
+            torch.cuda.current_stream(self.device).wait_event(e)
 
     def _fp_coarse(self, k, rows):
         """FP level k takes its first product on the coarse points."""
@@ -226,7 +255,11 @@ class PointNet2(Net):
 
     def _fp_pre(self, s, skip):
         """W1b s + b1 of the FP level whose skip is SA level s's output (s =
-        -1: the input features), issued as soon as that output exists."""
+        -1: the input features), issued as soon as that output exists: on
+        the main stream for the input features (idle while the first
+        sampling runs), on the side stream for an SA level's output (off
+        the main stream's path; joined at the start of feature
+        propagation)."""
         if not self.fp or skip is None:
             return
         k = len(self.spec["sa"]) - 2 - s
@@ -238,7 +271,15 @@ class PointNet2(Net):
         sp = self.fp_split[k]
         pre = self._buf(f"fpp{k}", (B, Nf, sp["b"].c_out))
         ws = self._ws(f"ws_fpp{k}", ops.mlp_workspace_bytes(B * Nf, sp["b"]))
-        ops.pointwise_mlp(skip, sp["b"], relu_mask=0, out=pre, ws=ws)
+        if s < 0:
+            ops.pointwise_mlp(skip, sp["b"], relu_mask=0, out=pre, ws=ws)
+            return
+        main, side = torch.cuda.current_stream(self.device), self.side
+        e = torch.cuda.Event()
+        e.record(main)
+        with torch.cuda.stream(side):
+            side.wait_event(e)
+            ops.pointwise_mlp(skip, sp["b"], relu_mask=0, out=pre, ws=ws)
 
     def _fused_into(self, i):
         """Level i's MLP takes level i - 1's aggregation in its loader."""
@@ -274,7 +315,7 @@ class PointNet2(Net):
                 ws = self._ws(f"ws_p1_{i}", ops.mlp_workspace_bytes(B * N, L["first"]))
                 ops.pointwise_mlp(p, L["first"], x1=f, relu_mask=0, out=p1, ws=ws)   # overlaps the search chain
                 q = self._buf(f"q_{i}", (B, m["M"], c1))
-                main.wait_event(ev_fps[i])
+                self._wait_fps(i)
                 ws = self._ws(f"ws_q_{i}", ops.mlp_workspace_bytes(B * m["M"], L["cen"]))
                 ops.pointwise_mlp(cx, L["cen"], relu_mask=0, out=q, ws=ws)
                 self._ball_query(i, p)
@@ -331,6 +372,11 @@ class PointNet2(Net):
                 res["out"] = logits
         if self.fp:
             main = torch.cuda.current_stream(self.device)
+            # the side stream's searches and skip products, all done long
+            # before: one join
+            e = torch.cuda.Event()
+            e.record(self.side)
+            main.wait_event(e)
             coarse_xyz, coarse_f = levels[-1]
             L = len(self.spec["sa"])
             for i, prm in enumerate(self.fp):
@@ -347,8 +393,6 @@ class PointNet2(Net):
                     ws = self._ws(f"ws_fpg{i}", ops.mlp_workspace_bytes(B * coarse_f.shape[1], sp["a"]))
                     ops.pointwise_mlp(coarse_f, sp["a"], relu_mask=0, out=g, ws=ws)
                     h = self._bufs[f"fpp{i}"]
-                    if self.ev_nn[i] is not None:
-                        main.wait_event(self.ev_nn[i])
                     if B * Nf > 32768 and ops.interpolate3_mlp_supported(sp["rest"]):
                         # the layer formed in the register MLP's row loader
                         ops.interpolate3_mlp(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], g, h, sp["rest"], out=y)
@@ -368,8 +412,6 @@ class PointNet2(Net):
                 else:
                     interp = self._buf(f"interp{i}", (B, Nf, ci))
                     x0, x1, p_mlp = interp, fine_f, prm
-                if self.ev_nn[i] is not None:
-                    main.wait_event(self.ev_nn[i])
                 ops.interpolate3_apply(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], coarse_f, out=interp)
                 ws = self._ws(f"ws_fp{i}", ops.mlp_workspace_bytes(B * Nf, p_mlp))
                 ops.pointwise_mlp(x0, p_mlp, x1=x1, out=y, ws=ws)
@@ -436,7 +478,7 @@ class DGCNN(Net):
 
 
 def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", debug: bool = False,
-          fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384) -> Net:
+          fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True) -> Net:
     """delayed: True (delayed aggregation), False (conventional) or "ltd"
     (limited delayed aggregation).  debug: every search output is checked
     to lie in range before anything reads through it (index_errors()).
@@ -444,9 +486,11 @@ def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", 
     aggregation runs inside that MLP's loader (mesorasi_aggregate_mlp).
     fp_coarse_min_rows: feature-propagation levels of at least this many
     fine rows take their first product on the coarse points
-    (mesorasi_interpolate3_add)."""
+    (mesorasi_interpolate3_add).  fps_prefix: the sampling of every level
+    after the first, which samples the previous level's centroids, is taken
+    as their first M (mesorasi_fps_prefix, the same result)."""
     if spec["kind"] in ("pointnet2_cls", "pointnet2_seg"):
-        return PointNet2(spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows)
+        return PointNet2(spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows, fps_prefix)
     if spec["kind"] == "dgcnn":
-        return DGCNN(spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows)
+        return DGCNN(spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows, fps_prefix)
     raise ValueError(spec["kind"])

@@ -69,6 +69,26 @@ def fps(xyz: torch.Tensor, M: int, want_xyz: bool = True, out_idx: torch.Tensor 
     return idx, cxyz
 
 
+def fps_prefix(idx_prev: torch.Tensor, cxyz_prev: torch.Tensor | None, M: int, out_idx: torch.Tensor | None = None,
+               out_xyz: torch.Tensor | None = None, want_xyz: bool = True):
+    """The sampling of M points from (idx_prev, cxyz_prev), an earlier
+    fps() (or fps_prefix()) output: its first M points (see the C header)."""
+    if idx_prev.dtype != torch.int32 or idx_prev.dim() != 2 or not idx_prev.is_contiguous():
+        raise ValueError("idx_prev must be a contiguous [B, M_prev] int32 tensor")
+    B, Mp = idx_prev.shape
+    if cxyz_prev is not None:
+        _check_xyz(cxyz_prev, "cxyz_prev")
+        if tuple(cxyz_prev.shape[:2]) != (B, Mp):
+            raise ValueError("cxyz_prev must be [B, M_prev, 3]")
+    idx = out_idx if out_idx is not None else torch.empty((B, M), dtype=torch.int32, device=idx_prev.device)
+    cxyz = out_xyz if out_xyz is not None else (
+        torch.empty((B, M, 3), dtype=torch.float32, device=idx_prev.device)
+        if want_xyz and cxyz_prev is not None else None)
+    check(_lib.lib().mesorasi_fps_prefix(idx_prev.data_ptr(), _ptr(cxyz_prev), B, Mp, M, idx.data_ptr(), _ptr(cxyz),
+                                         _stream()), "fps_prefix")
+    return idx, cxyz
+
+
 def ball_query_workspace_bytes(B: int, N: int, M: int) -> int:
     return int(_lib.lib().mesorasi_ball_query_workspace(B, N, M))
 

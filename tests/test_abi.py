@@ -54,6 +54,20 @@ def test_fps_validation():
     assert b"M = 11" in _lib.lib().mesorasi_last_error()
 
 
+def test_fps_prefix_validation():
+    f = "mesorasi_fps_prefix"
+    assert st(f, FAKE, FAKE, 1, 10, 11, FAKE, FAKE, NULL) == _lib.EINVAL          # M > M_prev
+    assert st(f, FAKE, FAKE, -1, 10, 5, FAKE, FAKE, NULL) == _lib.EINVAL          # B < 0
+    assert st(f, NULL, FAKE, 1, 10, 5, FAKE, FAKE, NULL) == _lib.EINVAL           # NULL idx_prev
+    assert st(f, FAKE, FAKE, 1, 10, 5, NULL, FAKE, NULL) == _lib.EINVAL           # NULL idx
+    assert st(f, FAKE, NULL, 1, 10, 5, FAKE, FAKE, NULL) == _lib.EINVAL           # cxyz without cxyz_prev
+    assert st(f, FAKE, FAKE, 1, 70000, 5, FAKE, FAKE, NULL) == _lib.EUNSUPPORTED  # M_prev too large
+    assert st(f, NULL, NULL, 0, 10, 5, NULL, NULL, NULL) == _lib.OK               # empty batch
+    assert st(f, NULL, NULL, 3, 10, 0, NULL, NULL, NULL) == _lib.OK               # nothing to select
+    st(f, FAKE, FAKE, 1, 10, 11, FAKE, FAKE, NULL)
+    assert b"M_prev = 10" in _lib.lib().mesorasi_last_error()
+
+
 def test_fps_workspace():
     """Small clouds run one workgroup per cloud and need no workspace; large
     ones exchange winners through one, which must be big enough and 8-byte

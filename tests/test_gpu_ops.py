@@ -104,6 +104,39 @@ def test_fps_bit_exact(gpu, name, B, N, M, kind):
         assert int(ws[:4].view(torch.int32).item()) == 0     # no workgroup gave up waiting
 
 
+FPS_PREFIX_CASES = [
+    # name, B, N, levels (M of each nested sampling), cloud kind
+    ("seg_levels", 2, 4096, [1024, 256, 64, 16], "mesh"),
+    ("cls_levels", 3, 1024, [512, 128], "mesh"),
+    ("lidar_levels", 1, 16384, [4096, 1024, 256], "lidar"),
+    ("grid_ties", 2, 3000, [900, 300, 31], "grid"),          # 64 distinct points: zero steps from 64 on
+    ("dups", 3, 2000, [700, 699, 1], "dups"),
+    ("ragged_b5", 5, 777, [333, 333, 65, 2], "normal"),     # M = M_prev, one result block plus one
+]
+
+
+@pytest.mark.parametrize("name,B,N,levels,kind", FPS_PREFIX_CASES, ids=[c[0] for c in FPS_PREFIX_CASES])
+def test_fps_prefix_bit_exact(gpu, name, B, N, levels, kind):
+    """The nested sampling equals the oracle's sampling of each level's
+    input points, and the sampling kernel's own run on them, bit for bit."""
+    x = _points(kind, B, N, g(7))
+    idx, cxyz = ops.fps(dev(x), levels[0])
+    prev_i, prev_c = idx, cxyz
+    zero_steps = False
+    for M in levels[1:]:
+        pc = host(prev_c)
+        ri, rc = O.fps(pc, M)
+        i2, c2 = ops.fps_prefix(prev_i, prev_c, M)
+        assert np.array_equal(host(i2), ri), (name, M)
+        assert np.array_equal(host(c2), rc), (name, M)
+        fi, fc = ops.fps(prev_c, M)
+        assert torch.equal(fi, i2) and torch.equal(fc, c2)
+        zero_steps |= bool((host(i2)[:, 1:] == 0).any())
+        prev_i, prev_c = i2, c2
+    if kind in ("grid", "dups"):
+        assert zero_steps      # the distinct points ran out: steps that take point 0
+
+
 # ----------------------------------------------------------------------------
 # ball query
 # ----------------------------------------------------------------------------

@@ -109,6 +109,35 @@ def test_fps_matches_bruteforce_recompute():
         assert np.array_equal(cxyz, np.take_along_axis(xyz, idx[..., None].astype(np.int64), 1))
 
 
+def test_fps_of_a_sampled_set_is_its_prefix():
+    """Greedy max-min sampling is a greedy permutation: run from index 0 on
+    the ordered output of an earlier run, it picks that output's first M
+    points (at step k the earlier run took the point of largest
+    min-distance among all points, and that point lies in the subset with
+    the same min-distance and the lowest subset index). A step where every
+    min-distance is 0 (the cloud's distinct points used up) picks index 0
+    in both runs. Checked on the oracle's own sampling, three levels deep,
+    on clouds with exact ties and with few distinct points."""
+    r = g(31)
+    clouds = [
+        r.standard_normal((3, 300, 3)).astype(np.float32),
+        r.integers(0, 3, size=(3, 300, 3)).astype(np.float32),        # 27 distinct points: zero steps
+        np.repeat(r.standard_normal((3, 5, 3)).astype(np.float32), 40, axis=1),   # 5 distinct, repeated
+        np.zeros((2, 50, 3), np.float32),                               # one distinct point
+    ]
+    for xyz in clouds:
+        N = xyz.shape[1]
+        ms = [min(N, 200), 64, 17] if N > 64 else [40, 20, 7]
+        idx, c = O.fps(xyz, ms[0])
+        for m in ms[1:]:
+            idx2, c2 = O.fps(c, m)
+            k = np.arange(m)[None, :]
+            expect = np.where((k == 0) | (idx[:, :m] != 0), k, 0)
+            assert np.array_equal(idx2, expect)
+            assert np.array_equal(c2, c[:, :m])
+            idx, c = idx2, c2
+
+
 def test_fps_invariants():
     r = g(3)
     xyz = r.standard_normal((3, 200, 3)).astype(np.float32)
