@@ -30,6 +30,11 @@
 // results in registers.  The iteration is bound by VALU issue for large P
 // (four waves per SIMD at 16 points per thread) and by the reduction chain
 // for small P.
+//
+// From 1025 to 16384 points fps_lds_kernel keeps a copy of the coordinates
+// in LDS as well, so the winners are exchanged as (distance, index) and the
+// new centroid is read from LDS after the block reduction; above 32768
+// points fps_multi_kernel spreads a cloud over several workgroups.
 #include <algorithm>
 
 #include "common.h"
@@ -221,6 +226,136 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
         }
         if (wave == 0 && ((M - 1) & 63) != 63) write_block(M - 1);
     }
+}
+
+// Clouds of 1025 to 16384 points: a copy of the cloud's coordinates in LDS.
+// A wave's winner is then published as (distance bits, index) -- by lane
+// 0, both values being wave-uniform -- and after the block reduction every
+// wave reads the new centroid's coordinates from LDS at the winning index
+// (one broadcast read), instead of the winning lane selecting them among
+// its P register slots before the barrier (a chain of selects on the
+// iteration's critical path: 15 % of an iteration at 4096 points, 27 % at
+// 8192).  Above 8192 points the whole cloud does not fit beside the ring:
+// x and y live in LDS and the winning lane publishes z with its slot.
+// Everything else -- the update, the wave reduction, the slot search, the
+// ring of per-wave winners resolved every 64 iterations -- is as in
+// fps_kernel.
+template <int T, int P, bool Z_SLOT>
+__global__ __launch_bounds__(T) void fps_lds_kernel(const float* __restrict__ xyz, int N, int M,
+                                                    int32_t* __restrict__ idx, float* __restrict__ cxyz) {
+    constexpr int W = T / 64;
+    constexpr int R = 128;                 // ring rows (two result blocks of 64 iterations)
+    constexpr int NC = Z_SLOT ? 2 : 3;     // coordinates per point held in LDS
+    __shared__ int2 s_slot[R][W];          // per-wave winner of iteration m in row m % R: distance bits, index
+    __shared__ float s_z[Z_SLOT ? R : 1][W];
+    __shared__ float s_c[T * P * NC];
+
+    const int b = blockIdx.x;
+    const float* __restrict__ p = xyz + (int64_t)b * N * 3;
+    int32_t* __restrict__ out_idx = idx + (int64_t)b * M;
+    float* __restrict__ out_c = cxyz ? cxyz + (int64_t)b * M * 3 : nullptr;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int base = tid * P;
+
+    float px[P], py[P], pz[P], dm[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+        const int j = base + q;
+        const bool ok = j < N;
+        px[q] = ok ? p[3 * j + 0] : 0.0f;
+        py[q] = ok ? p[3 * j + 1] : 0.0f;
+        pz[q] = ok ? p[3 * j + 2] : 0.0f;
+        dm[q] = ok ? __builtin_huge_valf() : -1.0f;  // +inf for real points; -1 never wins
+        s_c[NC * j + 0] = px[q];
+        s_c[NC * j + 1] = py[q];
+        if constexpr (!Z_SLOT) s_c[NC * j + 2] = pz[q];
+    }
+    __syncthreads();
+    float cx = p[0], cy = p[1], cz = p[2];
+    const float z0 = cz;
+
+    // lane l of wave 0 resolves iteration (m_last & ~63) + l from the ring
+    // and stores it (iteration 0 is point 0)
+    auto resolve = [&](int m_last) {
+        const int mi = (m_last & ~63) + lane;
+        const int row = mi & (R - 1);
+        int best = s_slot[row][0].x, bw = 0;
+#pragma unroll
+        for (int w = 1; w < W; ++w) {
+            const int d = s_slot[row][w].x;
+            bw = d > best ? w : bw;
+            best = d > best ? d : best;
+        }
+        if (mi <= m_last) {
+            const bool first = mi == 0;
+            const int sel = first ? 0 : s_slot[row][bw].y;
+            out_idx[mi] = sel;
+            if (out_c) {
+                out_c[3 * mi + 0] = s_c[NC * sel + 0];
+                out_c[3 * mi + 1] = s_c[NC * sel + 1];
+                if constexpr (Z_SLOT) out_c[3 * mi + 2] = first ? z0 : s_z[row][bw];
+                else out_c[3 * mi + 2] = s_c[NC * sel + 2];
+            }
+        }
+    };
+
+    for (int m = 1; m < M; ++m) {
+        // 1. distance to the newest centroid, running min, this thread's max
+        int tmax = INT32_MIN;
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            const int nm = min(__float_as_int(dist3(px[q], py[q], pz[q], cx, cy, cz)), __float_as_int(dm[q]));
+            dm[q] = __int_as_float(nm);
+            tmax = max(tmax, nm);
+        }
+        // 2. wave max, the lowest lane holding it, that lane's lowest slot
+        const int wmax = wave_max_i32(tmax);
+        const int wl = __builtin_ctzll(ballot(tmax == wmax));
+        int sq = P - 1;
+#pragma unroll
+        for (int q = P - 1; q >= 0; --q) {
+            const uint64_t hold = ballot(__float_as_int(dm[q]) == wmax);
+            sq = ((hold >> wl) & 1ull) ? q : sq;
+        }
+        sq = __builtin_amdgcn_readfirstlane(sq);
+        const int buf = m & (R - 1);
+        if constexpr (Z_SLOT) {
+            if (lane == wl) {
+                s_slot[buf][wave] = make_int2(wmax, base + sq);
+                s_z[buf][wave] = pz[sq];
+            }
+        } else {
+            if (lane == 0) s_slot[buf][wave] = make_int2(wmax, wave * 64 * P + wl * P + sq);
+        }
+        __syncthreads();
+        // 3. block winner: lane w < W inspects wave w's slot; the new
+        //    centroid's coordinates from LDS
+        int2 sl = make_int2(INT32_MIN, 0);
+        float slz = 0.0f;
+        if (lane < W) {
+            sl = s_slot[buf][lane];
+            if constexpr (Z_SLOT) slz = s_z[buf][lane];
+        }
+        int gm;
+        if constexpr (W <= 8) gm = __builtin_amdgcn_readlane(oct_max_i32(sl.x), 7);
+        else gm = __builtin_amdgcn_readlane(row_max_i32(sl.x), 0);
+        const int ww = __builtin_ctzll(ballot(sl.x == gm));
+        const int sel = __builtin_amdgcn_readlane(sl.y, ww);
+        cx = s_c[NC * sel + 0];
+        cy = s_c[NC * sel + 1];
+        if constexpr (Z_SLOT) cz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(slz), ww));
+        else cz = s_c[NC * sel + 2];
+        if (wave == 0 && (m & 63) == 63) resolve(m);
+    }
+    if (wave == 0 && ((M - 1) & 63) != 63) resolve(M - 1);
+}
+
+template <int T, int P, bool Z_SLOT>
+static void launch_fps_lds(const float* xyz, int64_t B, int N, int M, int32_t* idx, float* cxyz, hipStream_t s) {
+    static_assert(T >= 512 && T <= 1024 && T % 64 == 0, "8 or 16 waves");
+    fps_lds_kernel<T, P, Z_SLOT><<<dim3((unsigned)B), dim3(T), 0, s>>>(xyz, N, M, idx, cxyz);
 }
 
 template <int T, int P, bool REG>
@@ -507,10 +642,10 @@ extern "C" int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, i
     else if (n <= 256) launch_fps<64, 4, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 512) launch_fps<256, 2, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 1024) launch_fps<512, 2, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 2048) launch_fps<512, 4, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 4096) launch_fps<512, 8, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 8192) launch_fps<1024, 8, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 16384) launch_fps<1024, 16, true>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 2048) launch_fps_lds<512, 4, false>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 4096) launch_fps_lds<512, 8, false>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 8192) launch_fps_lds<1024, 8, false>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 16384) launch_fps_lds<1024, 16, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 32768) launch_fps<1024, 32, false>(xyz, B, n, m, idx, cxyz, s);
     else launch_fps<1024, 64, false>(xyz, B, n, m, idx, cxyz, s);
     return after_launch("mesorasi_fps");

@@ -60,6 +60,14 @@ FPS_CASES = [
     ("seg_sa1", 2, 4096, 1024, "normal"),
     ("n2000", 2, 2000, 700, "normal"),
     ("n9000", 1, 9000, 300, "normal"),
+    # 1025 .. 16384 points: the cloud's coordinates in LDS
+    ("lds_smallest_m_eq_n", 3, 1025, 1025, "normal"),
+    ("lds_m1", 2, 3000, 1, "normal"),
+    ("lds_m65", 2, 2048, 65, "mesh"),                  # one result block plus one
+    ("lds_grid_ties", 2, 4096, 1500, "grid"),          # 64 distinct points: ties across waves, zero steps
+    ("lds_dups", 1, 8192, 2048, "dups"),
+    ("lds_z_slot_grid", 1, 12000, 700, "grid"),        # above 8192 points: z published with the slot
+    ("lds_z_slot_ragged", 3, 8193, 300, "normal"),
     ("lidar_sa1", 1, 16384, 4096, "lidar"),
     ("n20000", 1, 20000, 64, "normal"),
     ("n32768_global_path", 1, 32768, 40, "normal"),   # coordinates re-read from memory per iteration
