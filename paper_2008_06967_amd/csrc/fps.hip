@@ -14,12 +14,13 @@
 //
 // An iteration: each thread updates its P running minima (as float bits:
 // every value is >= 0 or the -1 padding sentinel, so a signed-int min is
-// the strict-less minimum in one instruction) and keeps their max; a
-// fused-DPP butterfly gives the wave max; one ballot per slot then finds
-// the lowest lane holding it and that lane's lowest slot as wave-uniform
-// scalars, and the winner's coordinates are read once with a uniform
-// register index -- per-lane work after the reduction does not grow with
-// P.  One barrier per iteration: the per-wave winners go to a ring of 128
+// the strict-less minimum in one instruction) and keeps their max and the
+// lowest slot holding it (found while the wave max is reduced); a
+// fused-DPP butterfly gives the wave max, one ballot the lowest lane
+// holding it, and that lane's slot is read out, both wave-uniform, so the
+// winner's coordinates are read once with a uniform register index --
+// per-lane work after the reduction does not grow with P.  One barrier per
+// iteration: the per-wave winners go to a ring of 128
 // LDS slot rows indexed by iteration, so a wave that runs ahead writes the
 // next row while slower waves still read this one.  The ring also keeps
 // the results: every 64 iterations each lane of wave 0 finds the winner of
@@ -141,18 +142,17 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
             tmax = max(tmax, nm);
         }
         // 2. wave max; the lowest lane holding it; that lane's lowest slot.
-        //    One ballot per slot, then a scalar search: the slot and the
-        //    lane are wave-uniform, so only the winning lane's point is read
-        //    (no per-lane select chain over the P slots).
+        //    Every lane finds the lowest of its slots holding its own
+        //    maximum while the wave maximum is reduced (the selects fill
+        //    the DPP chain's latency), and the winning lane's answer is
+        //    read out: the slot and the lane are wave-uniform, so only the
+        //    winning lane's point is read.
+        int ls = P - 1;
+#pragma unroll
+        for (int q = P - 2; q >= 0; --q) ls = __float_as_int(dm[q]) == tmax ? q : ls;
         const int wmax = wave_max_i32(tmax);
         const int wl = __builtin_ctzll(ballot(tmax == wmax));
-        int sq = P - 1;
-#pragma unroll
-        for (int q = P - 1; q >= 0; --q) {
-            const uint64_t hold = ballot(__float_as_int(dm[q]) == wmax);
-            sq = ((hold >> wl) & 1ull) ? q : sq;
-        }
-        sq = __builtin_amdgcn_readfirstlane(sq);
+        const int sq = __builtin_amdgcn_readlane(ls, wl);
         float sx, sy, sz;
         if constexpr (REG_XYZ) {
             sx = px[sq];   // wave-uniform index into the register arrays
@@ -311,15 +311,14 @@ __global__ __launch_bounds__(T) void fps_lds_kernel(const float* __restrict__ xy
             tmax = max(tmax, nm);
         }
         // 2. wave max, the lowest lane holding it, that lane's lowest slot
+        //    (each lane's lowest slot holding its own maximum, found while
+        //    the wave maximum is reduced)
+        int ls = P - 1;
+#pragma unroll
+        for (int q = P - 2; q >= 0; --q) ls = __float_as_int(dm[q]) == tmax ? q : ls;
         const int wmax = wave_max_i32(tmax);
         const int wl = __builtin_ctzll(ballot(tmax == wmax));
-        int sq = P - 1;
-#pragma unroll
-        for (int q = P - 1; q >= 0; --q) {
-            const uint64_t hold = ballot(__float_as_int(dm[q]) == wmax);
-            sq = ((hold >> wl) & 1ull) ? q : sq;
-        }
-        sq = __builtin_amdgcn_readfirstlane(sq);
+        const int sq = __builtin_amdgcn_readlane(ls, wl);
         const int buf = m & (R - 1);
         if constexpr (Z_SLOT) {
             if (lane == wl) {
