@@ -2,11 +2,15 @@
 // that fills the neighbor index table (NIT, Sec. 4.1 walk-through).
 //
 // One wave per query.  The wave walks the cloud in 64-point chunks in index
-// order (coordinates fetched four chunks at a time); each lane tests one point, a ballot collects the chunk's hits and
-// mbcnt gives every hit its rank, so hits land in ascending index order with
-// no sorting.  The walk stops as soon as K hits are found (the early exit is
-// what makes surface-like clouds cheap), then the tail of the row is padded
-// with the first hit.
+// order, eight chunks per step (coordinates fetched together, every chunk's
+// test and ballot formed before its hits are placed); each lane tests one
+// point, a ballot collects the chunk's hits and mbcnt gives every hit its
+// rank, so hits land in ascending index order with no sorting.  The walk
+// stops after the step that completes K hits (the early exit is what makes
+// dense surface-like clouds cheap), then the tail of the row is padded with
+// the first hit.  Clouds of 2048 to 8191 points are first copied into LDS
+// by a workgroup that serves 16 queries; from 8192 points a grid of cells
+// bounds the candidates.
 #include <algorithm>
 #include <cmath>
 
@@ -15,39 +19,40 @@
 namespace meso {
 
 constexpr int kBqWaves = 4;
-constexpr int kBqChunks = 4;   // 64-point chunks per memory round trip
+constexpr int kBqChunks = 8;   // 64-point chunks per walk step
 
 // The index-order walk of one query by one wave: fills row[0 .. K) and
-// returns the number of real hits (<= K).
-__device__ __forceinline__ int bq_walk(const float* __restrict__ p, int N, float qx, float qy, float qz, float r2,
-                                       int K, int32_t* __restrict__ row, int lane) {
+// returns the number of real hits (<= K).  pt(j, x, y, z) reads point j
+// (from memory, or from the LDS copy of the cloud).
+template <class PT>
+__device__ __forceinline__ int bq_walk(PT pt, int N, float qx, float qy, float qz, float r2, int K,
+                                       int32_t* __restrict__ row, int lane) {
     int n = 0;
     int first = 0;
     for (int base0 = 0; base0 < N && n < K; base0 += 64 * kBqChunks) {
-        // the coordinates of kBqChunks chunks are requested together (lanes
-        // past N read point N - 1 and never hit), so one memory round trip
-        // serves several chunks; the chunks are still tested in index order
-        // and the walk stops after the chunk that completes K hits
+        // kBqChunks chunks per step, straight-line: the coordinates are
+        // requested together (lanes past N read point N - 1 and never hit)
+        // and every chunk's test and ballot is formed before the hits are
+        // placed, in index order; hits past the K-th are counted but not
+        // stored, and the walk stops after the step that completes K
         float cx[kBqChunks], cy[kBqChunks], cz[kBqChunks];
 #pragma unroll
+        for (int u = 0; u < kBqChunks; ++u) pt(min(base0 + 64 * u + lane, N - 1), cx[u], cy[u], cz[u]);
+        bool hit[kBqChunks];
+        uint64_t mask[kBqChunks];
+#pragma unroll
         for (int u = 0; u < kBqChunks; ++u) {
-            const int64_t j = min(base0 + 64 * u + lane, N - 1);
-            cx[u] = p[3 * j + 0];
-            cy[u] = p[3 * j + 1];
-            cz[u] = p[3 * j + 2];
+            hit[u] = base0 + 64 * u + lane < N && dist3(cx[u], cy[u], cz[u], qx, qy, qz) < r2;
+            mask[u] = ballot(hit[u]);
         }
 #pragma unroll
         for (int u = 0; u < kBqChunks; ++u) {
-            const int base = base0 + 64 * u;
-            if (base >= N || n >= K) break;
-            const int j = base + lane;
-            const bool hit = j < N && dist3(cx[u], cy[u], cz[u], qx, qy, qz) < r2;
-            const uint64_t mask = ballot(hit);
-            if (mask) {
-                if (n == 0) first = base + __builtin_ctzll(mask);
-                const int pos = n + mask_rank(mask);
-                if (hit && pos < K) row[pos] = j;
-                n += __builtin_popcountll(mask);
+            if (mask[u]) {
+                const int base = base0 + 64 * u;
+                if (n == 0) first = base + __builtin_ctzll(mask[u]);
+                const int pos = n + mask_rank(mask[u]);
+                if (hit[u] && pos < K) row[pos] = base + lane;
+                n += __builtin_popcountll(mask[u]);
             }
         }
     }
@@ -65,8 +70,54 @@ __global__ __launch_bounds__(64 * kBqWaves) void ball_query_kernel(const float* 
     if (gq >= BM) return;  // whole wave leaves together; no barriers below
     const int lane = threadIdx.x & 63;
     const int64_t b = gq / M;
-    const int n = bq_walk(xyz + b * (int64_t)N * 3, N, qxyz[gq * 3 + 0], qxyz[gq * 3 + 1], qxyz[gq * 3 + 2], r2, K,
-                          nit + gq * K, lane);
+    const float* __restrict__ p = xyz + b * (int64_t)N * 3;
+    auto pt = [&](int j, float& x, float& y, float& z) {
+        x = p[3 * j + 0];
+        y = p[3 * j + 1];
+        z = p[3 * j + 2];
+    };
+    const int n = bq_walk(pt, N, qxyz[gq * 3 + 0], qxyz[gq * 3 + 1], qxyz[gq * 3 + 2], r2, K, nit + gq * K, lane);
+    if (cnt && lane == 0) cnt[gq] = n;
+}
+
+// Mid-size clouds (kBqLdsMinN .. kBqGridMinN - 1 points): a workgroup of
+// kBqLdsWaves waves serves as many queries of one cloud and first copies
+// the cloud into LDS (coordinate planes x, y, z).  Surface-like clouds at
+// small radii leave most balls short of K, so nearly every query walks the
+// whole cloud; one wave per query re-reading the cloud through the caches
+// then moves N x 12 bytes per query from L2 (4096 points, 16384 queries:
+// 805 MB), here once per workgroup.  After the copy no wave waits for
+// another: each walks its query and leaves.
+constexpr int kBqLdsWaves = 16;
+constexpr int64_t kBqLdsMinN = 2048;
+
+__global__ __launch_bounds__(64 * kBqLdsWaves) void ball_query_lds_kernel(const float* __restrict__ xyz,
+                                                                          const float* __restrict__ qxyz, int N, int M,
+                                                                          int qblocks, float r2, int K,
+                                                                          int32_t* __restrict__ nit,
+                                                                          int32_t* __restrict__ cnt) {
+    extern __shared__ float s_pts[];   // [3][N]: x, then y, then z
+    const int64_t b = blockIdx.x / qblocks;
+    const int q0 = (int)(blockIdx.x - b * qblocks) * kBqLdsWaves;
+    const float* __restrict__ p = xyz + b * (int64_t)N * 3;
+    for (int e = threadIdx.x; e < 3 * N; e += 64 * kBqLdsWaves) {
+        const int j = e / 3;
+        s_pts[(e - 3 * j) * N + j] = p[e];
+    }
+    __syncthreads();
+    const int qi = q0 + (int)(threadIdx.x >> 6);
+    if (qi >= M) return;   // whole waves leave; no barrier follows
+    const int lane = threadIdx.x & 63;
+    const int64_t gq = b * M + qi;
+    const float* sx = s_pts;
+    const float* sy = s_pts + N;
+    const float* sz = s_pts + 2 * N;
+    auto pt = [&](int j, float& x, float& y, float& z) {
+        x = sx[j];
+        y = sy[j];
+        z = sz[j];
+    };
+    const int n = bq_walk(pt, N, qxyz[gq * 3 + 0], qxyz[gq * 3 + 1], qxyz[gq * 3 + 2], r2, K, nit + gq * K, lane);
     if (cnt && lane == 0) cnt[gq] = n;
 }
 
@@ -267,7 +318,13 @@ __global__ __launch_bounds__(64 * kGridQWaves) void grid_query_kernel(const floa
     for (int o = 8; o > 0; o >>= 1) cand += __shfl_xor(cand, o);
     cand = __shfl(cand, 0);
     if (cand > walk_above) {
-        const int n = bq_walk(xyz + b * (int64_t)N * 3, N, qx, qy, qz, r2, K, nit + gq * K, lane);
+        const float* __restrict__ p = xyz + b * (int64_t)N * 3;
+        auto pt = [&](int j, float& x, float& y, float& z) {
+            x = p[3 * j + 0];
+            y = p[3 * j + 1];
+            z = p[3 * j + 2];
+        };
+        const int n = bq_walk(pt, N, qx, qy, qz, r2, K, nit + gq * K, lane);
         if (cnt && lane == 0) cnt[gq] = n;
         return;
     }
@@ -389,6 +446,14 @@ extern "C" int mesorasi_ball_query(const float* xyz, const float* qxyz, int64_t 
         const int walk_above = (int)std::min(std::sqrt(6.45 * (double)K * (double)N), 2.0e9);
         grid_query_kernel<<<dim3((unsigned)qblocks), dim3(64 * kGridQWaves), lds, s>>>(
             xyz, qxyz, BM, (int)N, (int)M, r2, K, walk_above, w, nit, cnt);
+        return after_launch("mesorasi_ball_query");
+    }
+    if (N >= kBqLdsMinN) {
+        // below kBqGridMinN points: 3 N floats of LDS, at most 96 KB
+        const int64_t qb = ceil_div(M, kBqLdsWaves);
+        MESO_REQUIRE(B * qb <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_ball_query: too many queries");
+        ball_query_lds_kernel<<<dim3((unsigned)(B * qb)), dim3(64 * kBqLdsWaves), (size_t)N * 12, s>>>(
+            xyz, qxyz, (int)N, (int)M, (int)qb, r2, K, nit, cnt);
         return after_launch("mesorasi_ball_query");
     }
     const int64_t blocks = ceil_div(BM, kBqWaves);

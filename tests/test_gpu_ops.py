@@ -160,6 +160,13 @@ BQ_CASES = [
     ("grid_boundary", 1, 64, 64, 1.0, 16, "grid"),
     ("lidar_sa1", 1, 16384, 4096, 0.1, 64, "lidar"),
     ("k_max", 1, 2000, 24, 3.0, 1024, "normal"),      # the documented maximum K
+    # 2048 .. 8191 points: the cloud copied into LDS, 16 queries per workgroup
+    ("lds_seg_sa1", 2, 4096, 1024, 0.1, 32, "mesh"),
+    ("lds_smallest_ragged_m", 3, 2048, 37, 0.3, 16, "normal"),   # queries not a multiple of 16
+    ("lds_k_max", 1, 3000, 20, 3.0, 1024, "normal"),
+    ("lds_boundary_ties", 1, 4096, 256, 1.0, 40, "grid"),
+    ("lds_dups", 2, 5000, 300, 0.3, 64, "dups"),
+    ("lds_largest_nohit", 1, 8191, 64, 1e-4, 8, "normal"),
     # 8192 points and more: the grid form (cells of edge >= r, a hit bitmap
     # per query, the first K set bits)
     ("grid_lidar_sa1", 2, 16384, 4096, 0.1, 64, "lidar"),
