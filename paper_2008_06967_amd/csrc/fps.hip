@@ -32,7 +32,7 @@
 // (four waves per SIMD at 16 points per thread) and by the reduction chain
 // for small P.
 //
-// From 1025 to 16384 points fps_lds_kernel keeps a copy of the coordinates
+// From 513 to 16384 points fps_lds_kernel keeps a copy of the coordinates
 // in LDS as well, so the winners are exchanged as (distance, index) and the
 // new centroid is read from LDS after the block reduction; above 32768
 // points fps_multi_kernel spreads a cloud over several workgroups.
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
     }
 }
 
-// Clouds of 1025 to 16384 points: a copy of the cloud's coordinates in LDS.
+// Clouds of 513 to 16384 points: a copy of the cloud's coordinates in LDS.
 // A wave's winner is then published as (distance bits, index) -- by lane
 // 0, both values being wave-uniform -- and after the block reduction every
 // wave reads the new centroid's coordinates from LDS at the winning index
@@ -353,7 +353,7 @@ __global__ __launch_bounds__(T) void fps_lds_kernel(const float* __restrict__ xy
 
 template <int T, int P, bool Z_SLOT>
 static void launch_fps_lds(const float* xyz, int64_t B, int N, int M, int32_t* idx, float* cxyz, hipStream_t s) {
-    static_assert(T >= 512 && T <= 1024 && T % 64 == 0, "8 or 16 waves");
+    static_assert(T >= 256 && T <= 1024 && T % 64 == 0, "4 to 16 waves");
     fps_lds_kernel<T, P, Z_SLOT><<<dim3((unsigned)B), dim3(T), 0, s>>>(xyz, N, M, idx, cxyz);
 }
 
@@ -640,7 +640,7 @@ extern "C" int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, i
     if (n <= 128) launch_fps<64, 2, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 256) launch_fps<64, 4, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 512) launch_fps<256, 2, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 1024) launch_fps<512, 2, true>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 1024) launch_fps_lds<256, 4, false>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 2048) launch_fps_lds<512, 4, false>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 4096) launch_fps_lds<512, 8, false>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 8192) launch_fps_lds<1024, 8, false>(xyz, B, n, m, idx, cxyz, s);

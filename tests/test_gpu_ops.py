@@ -60,8 +60,10 @@ FPS_CASES = [
     ("seg_sa1", 2, 4096, 1024, "normal"),
     ("n2000", 2, 2000, 700, "normal"),
     ("n9000", 1, 9000, 300, "normal"),
-    # 1025 .. 16384 points: the cloud's coordinates in LDS
-    ("lds_smallest_m_eq_n", 3, 1025, 1025, "normal"),
+    # 513 .. 16384 points: the cloud's coordinates in LDS
+    ("lds_smallest_m_eq_n", 3, 513, 513, "normal"),
+    ("lds_four_waves_grid", 2, 1000, 1000, "grid"),     # four waves: the block max over four slots
+    ("lds_1025_m_eq_n", 3, 1025, 1025, "normal"),
     ("lds_m1", 2, 3000, 1, "normal"),
     ("lds_m65", 2, 2048, 65, "mesh"),                  # one result block plus one
     ("lds_grid_ties", 2, 4096, 1500, "grid"),          # 64 distinct points: ties across waves, zero steps
