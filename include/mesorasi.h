@@ -416,12 +416,17 @@ int mesorasi_interpolate3_add(const int32_t* nit, const float* dist, const float
  *         channels; f_src and add 16-byte aligned
  *   W, bias, relu_mask: the MLP as in mesorasi_pointwise_mlp (dims[0] = C)
  *   y [B, Nd, ld_y] float32 out; must not overlap add
- * No workspace.
+ * No workspace.  The layers' permuted weights live in LDS; when they do not
+ * all fit its 160 KB at once (e.g. the level's layers followed by the
+ * per-point head) they are staged in phases, which needs every wave of the
+ * device to hold at most one 32-row tile: B * Nd <= 32 x 8 x (compute
+ * units), 65536 rows on MI355X.
  * Errors: EINVAL for NULL pointers, sizes < 0, Ns = 0 with points, ld < C
  * or ld_y < dims[n_layers]; EUNSUPPORTED unless every layer is at most 128
- * wide (its permuted weights fitting 160 KB), dims[0], ld_src and ld_add are
- * multiples of 4 and f_src and add are 16-byte aligned -- callers fall back
- * to mesorasi_interpolate3_add + mesorasi_pointwise_mlp.
+ * wide (its own permuted weights fitting 160 KB), the row bound above holds
+ * when phases are needed, dims[0], ld_src and ld_add are multiples of 4 and
+ * f_src and add are 16-byte aligned -- callers fall back to
+ * mesorasi_interpolate3_add + mesorasi_pointwise_mlp.
  */
 int mesorasi_interpolate3_mlp(const int32_t* nit, const float* dist, const float* f_src, int64_t ld_src, int64_t B,
                               int64_t Nd, int64_t Ns, const float* add, int64_t ld_add, int32_t relu,

@@ -918,7 +918,7 @@ static bool use_fused(int64_t rows, int n_layers, const int32_t* dims, int dtype
 static bool use_rr(int64_t rows, int n_layers, const int32_t* dims, int dtype, int out_dtype, int64_t pool_group,
                    bool neighbor_rows) {
     if (pool_group != 0 || neighbor_rows || rows < MESO_RR_MIN_ROWS) return false;
-    if (dtype == MESORASI_F32) return out_dtype == MESORASI_F32 && rr_mlp_supported(n_layers, dims);
+    if (dtype == MESORASI_F32) return out_dtype == MESORASI_F32 && rr_mlp_supported(n_layers, dims, rows);
     return dtype == MESORASI_BF16 && dims[0] <= 32 && rb_mlp_supported(n_layers, dims);
 }
 
@@ -1361,8 +1361,9 @@ extern "C" int mesorasi_interpolate3_mlp(const int32_t* nit, const float* dist, 
     if (rc != MESORASI_OK) return rc;
     const int C = dims[0];
     MESO_REQUIRE(ld_src >= C && ld_add >= C && ld_y >= dims[n_layers], MESORASI_EINVAL, "%s: leading dimension", who);
-    MESO_REQUIRE(rr_mlp_supported(n_layers, dims), MESORASI_EUNSUPPORTED,
-                 "%s: every layer must be at most 128 wide (the register-resident MLP)", who);
+    MESO_REQUIRE(rr_mlp_supported(n_layers, dims, B * Nd), MESORASI_EUNSUPPORTED,
+                 "%s: every layer must be at most 128 wide (the register-resident MLP), and layers whose "
+                 "weights do not fit the LDS together need at most 32 rows per wave of the device", who);
     MESO_REQUIRE(C % 4 == 0 && ld_src % 4 == 0 && ld_add % 4 == 0, MESORASI_EUNSUPPORTED,
                  "%s: dims[0] and the leading dimensions of f_src and add must be multiples of 4", who);
     if (B == 0 || Nd == 0) return MESORASI_OK;

@@ -48,9 +48,11 @@ int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1,
                   uint32_t relu_mask, int out_dtype, void* y, int64_t ld_y, int64_t pool_group, hipStream_t s,
                   const MlpGather* g = nullptr);
 
-// True when every layer is at most 128 wide and the permuted weights fit
-// the LDS of one workgroup (the register-resident MLP, mlp_rr.hip).
-bool rr_mlp_supported(int n_layers, const int32_t* dims);
+// True when every layer is at most 128 wide (the register-resident MLP,
+// mlp_rr.hip) and either the permuted weights of all layers fit the LDS of
+// one workgroup, or each fits and the rows make at most one 32-row tile
+// per wave (the weights are then staged in phases).
+bool rr_mlp_supported(int n_layers, const int32_t* dims, int64_t rows);
 
 // First-layer rows made by interpolation (mesorasi_interpolate3_mlp): row r
 // = b nd + i is phi(sum_k u_k g[b, nit[r, k]] + add[r]); every row and

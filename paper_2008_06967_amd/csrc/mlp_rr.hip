@@ -52,6 +52,11 @@ struct RrArgs {
     int woff[MESORASI_MAX_LAYERS];   // float offset of layer l's permuted weights in LDS
     int boff[MESORASI_MAX_LAYERS];   // float offset of its padded bias
     int lds_floats;
+    // weights staged in phases when all layers do not fit at once: phase p
+    // holds layers phase_first[p] .. phase_first[p + 1] - 1 (offsets above
+    // relative to the phase); then every wave holds at most one tile
+    int nphase;
+    int phase_first[MESORASI_MAX_LAYERS + 1];
     uint32_t relu_mask;
     float* y;
     int64_t ldy;
@@ -138,6 +143,8 @@ __device__ __forceinline__ void rr_products_nob(int nob, const float4* __restric
 // epilogue, the other keeps the SIMD's MFMA pipe busy.  (A four-wave form
 // with 512 registers per wave that requested its next tile's rows before
 // computing the current one measured 9-18 % slower.)
+// PHASED: the weights staged in phases, at most one tile per wave.
+template <bool PHASED>
 __global__ __launch_bounds__(64 * kRrWaves) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void mlp_rr_kernel(RrArgs a) {
     extern __shared__ float4 smem4[];
@@ -237,110 +244,133 @@ void mlp_rr_kernel(RrArgs a) {
     // groups x 64 lanes), each 4 consecutive k of one weight row; all of a
     // layer's loads are in flight before the first LDS store
     constexpr int kPer = 4 * 16 * 64 / (64 * kRrWaves);
-    for (int l = 0; l < a.n_layers; ++l) {
-        const int K = a.dims[l], N = a.dims[l + 1];
-        const int ng = rr_steps(a.dims, l, a.k0h) / 4;
-        const int total = rr_blocks(N) * ng * 64;
-        const unsigned inv = (65536u + ng - 1) / ng;   // gg / ng exactly for gg < 64
-        const float* __restrict__ W = a.W[l];
-        const bool wvec = (K % 4) == 0 && (reinterpret_cast<uintptr_t>(W) & 15) == 0;
-        float4 v[kPer];
+    auto stage = [&](int l0, int l1) {
+        for (int l = l0; l < l1; ++l) {
+            const int K = a.dims[l], N = a.dims[l + 1];
+            const int ng = rr_steps(a.dims, l, a.k0h) / 4;
+            const int total = rr_blocks(N) * ng * 64;
+            const unsigned inv = (65536u + ng - 1) / ng;   // gg / ng exactly for gg < 64
+            const float* __restrict__ W = a.W[l];
+            const bool wvec = (K % 4) == 0 && (reinterpret_cast<uintptr_t>(W) & 15) == 0;
+            float4 v[kPer];
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int i = tid + 64 * kRrWaves * u;
-            const int ln = i & 63, gg = i >> 6;
-            const int ob = (int)(((unsigned)gg * inv) >> 16), g = gg - ob * ng;
-            const int n = ob * 32 + (ln & 31);
-            const int k = rr_k(l, 4 * g, ln >> 5);   // k .. k + 3 are consecutive
-            v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (i < total && n < N) {
-                const float* wr = W + (int64_t)n * K;
-                if (wvec && k + 4 <= K) {
-                    v[u] = *reinterpret_cast<const float4*>(wr + k);
-                } else {
-                    v[u].x = k + 0 < K ? wr[k + 0] : 0.0f;
-                    v[u].y = k + 1 < K ? wr[k + 1] : 0.0f;
-                    v[u].z = k + 2 < K ? wr[k + 2] : 0.0f;
-                    v[u].w = k + 3 < K ? wr[k + 3] : 0.0f;
+            for (int u = 0; u < kPer; ++u) {
+                const int i = tid + 64 * kRrWaves * u;
+                const int ln = i & 63, gg = i >> 6;
+                const int ob = (int)(((unsigned)gg * inv) >> 16), g = gg - ob * ng;
+                const int n = ob * 32 + (ln & 31);
+                const int k = rr_k(l, 4 * g, ln >> 5);   // k .. k + 3 are consecutive
+                v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (i < total && n < N) {
+                    const float* wr = W + (int64_t)n * K;
+                    if (wvec && k + 4 <= K) {
+                        v[u] = *reinterpret_cast<const float4*>(wr + k);
+                    } else {
+                        v[u].x = k + 0 < K ? wr[k + 0] : 0.0f;
+                        v[u].y = k + 1 < K ? wr[k + 1] : 0.0f;
+                        v[u].z = k + 2 < K ? wr[k + 2] : 0.0f;
+                        v[u].w = k + 3 < K ? wr[k + 3] : 0.0f;
+                    }
+                }
+            }
+            float4* dst = smem4 + (a.woff[l] >> 2);
+#pragma unroll
+            for (int u = 0; u < kPer; ++u) {
+                const int i = tid + 64 * kRrWaves * u;
+                if (i < total) dst[i] = v[u];
+            }
+            const float* __restrict__ bs = a.bias[l];
+            for (int e = tid; e < rr_blocks(N) * 32; e += 64 * kRrWaves)
+                smem[a.boff[l] + e] = (bs && e < N) ? bs[e] : 0.0f;
+        }
+    };
+
+    // layer l on this wave's tile (rows row - lane % 32 ..): act in, act
+    // out, or the output rows after the last layer
+    auto layer = [&](int l, int64_t row, bool rok) {
+        const int N = a.dims[l + 1];
+        const int nob = rr_blocks(N);
+        const int nj = rr_steps(a.dims, l, a.k0h) / 16;
+        const float4* __restrict__ wl = smem4 + (a.woff[l] >> 2) + lane;
+        f32x16 acc[kRrMaxWidth / 32];
+        switch (nj) {
+            case 1: rr_products_nob<1>(nob, wl, act, acc); break;
+            case 2: rr_products_nob<2>(nob, wl, act, acc); break;
+            case 3: rr_products_nob<3>(nob, wl, act, acc); break;
+            default: rr_products_nob<4>(nob, wl, act, acc); break;
+        }
+        const bool relu = (a.relu_mask >> l) & 1u;
+        const float* __restrict__ bl = smem + a.boff[l];
+        if (l + 1 < a.n_layers) {
+            // bias and activation in place: the accumulators become the
+            // next layer's B operand in its k order (steps past the
+            // layer's blocks are never read)
+#pragma unroll
+            for (int ob = 0; ob < kRrMaxWidth / 32; ++ob) {
+                if (ob < nob) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const float4 b4 = *reinterpret_cast<const float4*>(bl + 32 * ob + 8 * q + 4 * hk);
+                        const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            float v = acc[ob][4 * q + i] + bq[i];
+                            if (relu) v = v > 0.0f ? v : 0.0f;
+                            act[16 * ob + 4 * q + i] = v;
+                        }
+                    }
+                }
+            }
+        } else if (rok) {
+            float* yr = a.y + row * a.ldy;
+#pragma unroll
+            for (int ob = 0; ob < kRrMaxWidth / 32; ++ob) {
+                if (ob < nob) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int c = 32 * ob + 8 * q + 4 * hk;
+                        const float4 b4 = *reinterpret_cast<const float4*>(bl + c);
+                        float v[4] = {acc[ob][4 * q + 0] + b4.x, acc[ob][4 * q + 1] + b4.y,
+                                      acc[ob][4 * q + 2] + b4.z, acc[ob][4 * q + 3] + b4.w};
+                        if (relu) {
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) v[i] = v[i] > 0.0f ? v[i] : 0.0f;
+                        }
+                        if (a.vecy && c + 4 <= N) {
+                            *reinterpret_cast<float4*>(yr + c) = make_float4(v[0], v[1], v[2], v[3]);
+                        } else {
+#pragma unroll
+                            for (int i = 0; i < 4; ++i)
+                                if (c + i < N) yr[c + i] = v[i];
+                        }
+                    }
                 }
             }
         }
-        float4* dst = smem4 + (a.woff[l] >> 2);
-#pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int i = tid + 64 * kRrWaves * u;
-            if (i < total) dst[i] = v[u];
-        }
-        const float* __restrict__ bs = a.bias[l];
-        for (int e = tid; e < rr_blocks(N) * 32; e += 64 * kRrWaves) smem[a.boff[l] + e] = (bs && e < N) ? bs[e] : 0.0f;
-    }
-    __syncthreads();
+    };
 
-    for (int64_t t = t0; t < a.tiles; t += stride) {
-        const int64_t row = t * 32 + (lane & 31);
+    if constexpr (!PHASED) {
+        stage(0, a.n_layers);
+        __syncthreads();
+        for (int64_t t = t0; t < a.tiles; t += stride) {
+            const int64_t row = t * 32 + (lane & 31);
+            const bool rok = row < a.rows;
+            if (t != t0) load_tile(t, act);
+            for (int l = 0; l < a.n_layers; ++l) layer(l, row, rok);
+        }
+    } else {
+        // the weights do not fit at once: the layers run in phases, the
+        // workgroup restaging the LDS between them, and each wave holds at
+        // most one tile (the host guarantees it), whose activations stay in
+        // registers across the phases.  Every wave takes every barrier.
+        const int64_t row = t0 * 32 + (lane & 31);
         const bool rok = row < a.rows;
-        if (t != t0) load_tile(t, act);
-
-        for (int l = 0; l < a.n_layers; ++l) {
-            const int N = a.dims[l + 1];
-            const int nob = rr_blocks(N);
-            const int nj = rr_steps(a.dims, l, a.k0h) / 16;
-            const float4* __restrict__ wl = smem4 + (a.woff[l] >> 2) + lane;
-            f32x16 acc[kRrMaxWidth / 32];
-            switch (nj) {
-                case 1: rr_products_nob<1>(nob, wl, act, acc); break;
-                case 2: rr_products_nob<2>(nob, wl, act, acc); break;
-                case 3: rr_products_nob<3>(nob, wl, act, acc); break;
-                default: rr_products_nob<4>(nob, wl, act, acc); break;
-            }
-            const bool relu = (a.relu_mask >> l) & 1u;
-            const float* __restrict__ bl = smem + a.boff[l];
-            if (l + 1 < a.n_layers) {
-                // bias and activation in place: the accumulators become the
-                // next layer's B operand in its k order (steps past the
-                // layer's blocks are never read)
-#pragma unroll
-                for (int ob = 0; ob < kRrMaxWidth / 32; ++ob) {
-                    if (ob < nob) {
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const float4 b4 = *reinterpret_cast<const float4*>(bl + 32 * ob + 8 * q + 4 * hk);
-                            const float bq[4] = {b4.x, b4.y, b4.z, b4.w};
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) {
-                                float v = acc[ob][4 * q + i] + bq[i];
-                                if (relu) v = v > 0.0f ? v : 0.0f;
-                                act[16 * ob + 4 * q + i] = v;
-                            }
-                        }
-                    }
-                }
-            } else if (rok) {
-                float* yr = a.y + row * a.ldy;
-#pragma unroll
-                for (int ob = 0; ob < kRrMaxWidth / 32; ++ob) {
-                    if (ob < nob) {
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const int c = 32 * ob + 8 * q + 4 * hk;
-                            const float4 b4 = *reinterpret_cast<const float4*>(bl + c);
-                            float v[4] = {acc[ob][4 * q + 0] + b4.x, acc[ob][4 * q + 1] + b4.y,
-                                          acc[ob][4 * q + 2] + b4.z, acc[ob][4 * q + 3] + b4.w};
-                            if (relu) {
-#pragma unroll
-                                for (int i = 0; i < 4; ++i) v[i] = v[i] > 0.0f ? v[i] : 0.0f;
-                            }
-                            if (a.vecy && c + 4 <= N) {
-                                *reinterpret_cast<float4*>(yr + c) = make_float4(v[0], v[1], v[2], v[3]);
-                            } else {
-#pragma unroll
-                                for (int i = 0; i < 4; ++i)
-                                    if (c + i < N) yr[c + i] = v[i];
-                            }
-                        }
-                    }
-                }
-            }
+        for (int p = 0; p < a.nphase; ++p) {
+            if (p > 0) __syncthreads();   // every wave is done with the previous phase's weights
+            stage(a.phase_first[p], a.phase_first[p + 1]);
+            __syncthreads();
+            if (t0 < a.tiles)
+                for (int l = a.phase_first[p]; l < a.phase_first[p + 1]; ++l) layer(l, row, rok);
         }
     }
 }
@@ -350,30 +380,57 @@ struct RrPlan {
     int k0h;
     int lds_floats;
     int woff[MESORASI_MAX_LAYERS], boff[MESORASI_MAX_LAYERS];
+    int nphase;
+    int phase_first[MESORASI_MAX_LAYERS + 1];
 };
 
+// Layers packed greedily into phases whose permuted weights and biases fit
+// the LDS (one phase when they all fit).
 RrPlan rr_plan(int n_layers, const int32_t* dims) {
     RrPlan p{};
     p.k0h = (int)(ceil_div(ceil_div(dims[0], 2), 16) * 16);
-    if (p.k0h > kRrMaxSteps) return p;
-    int off = 0;
+    if (p.k0h > kRrMaxSteps || n_layers < 1) return p;
+    const int cap = kRrMaxLds / (int)sizeof(float);
+    int off = 0, most = 0;
+    p.nphase = 1;
+    p.phase_first[0] = 0;
     for (int l = 0; l < n_layers; ++l) {
         if (dims[l + 1] > kRrMaxWidth || dims[l] > kRrMaxWidth) return p;
         const int nob = rr_blocks(dims[l + 1]);
+        const int size = nob * rr_steps(dims, l, p.k0h) * 64 + nob * 32;
+        if (size > cap) return p;
+        if (off + size > cap) {
+            p.phase_first[p.nphase++] = l;
+            off = 0;
+        }
         p.woff[l] = off;
-        off += nob * rr_steps(dims, l, p.k0h) * 64;
-        p.boff[l] = off;
-        off += nob * 32;
+        p.boff[l] = off + nob * rr_steps(dims, l, p.k0h) * 64;
+        off += size;
+        most = std::max(most, off);
     }
-    if ((size_t)off * sizeof(float) > (size_t)kRrMaxLds) return p;
-    p.lds_floats = off;
+    p.phase_first[p.nphase] = n_layers;
+    p.lds_floats = most;
     p.ok = true;
     return p;
 }
 
+int rr_cus() {
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) cus = v;
+    }
+    return cus;
+}
+
 }  // namespace
 
-bool rr_mlp_supported(int n_layers, const int32_t* dims) { return rr_plan(n_layers, dims).ok; }
+// One phase for any row count; several only while every wave holds at most
+// one 32-row tile (one persistent workgroup of kRrWaves waves per CU).
+bool rr_mlp_supported(int n_layers, const int32_t* dims, int64_t rows) {
+    const RrPlan pl = rr_plan(n_layers, dims);
+    return pl.ok && (pl.nphase == 1 || ceil_div(rows, 32) <= (int64_t)rr_cus() * kRrWaves);
+}
 
 int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, int64_t ld1, int64_t rows,
                int n_layers, const int32_t* dims, const void* const* W, const float* const* bias,
@@ -381,10 +438,17 @@ int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, in
     const RrPlan pl = rr_plan(n_layers, dims);
     MESO_REQUIRE(pl.ok, MESORASI_EUNSUPPORTED, "mesorasi_pointwise_mlp: layers too wide for the register MLP");
     if (rows == 0) return MESORASI_OK;
-    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&mlp_rr_kernel),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, kRrMaxLds);
-    MESO_REQUIRE(attr == hipSuccess, MESORASI_EHIP, "mesorasi_pointwise_mlp: LDS size attribute: %s",
-                 hipGetErrorString(attr));
+    const int cus = rr_cus();
+    MESO_REQUIRE(pl.nphase == 1 || ceil_div(rows, 32) <= (int64_t)cus * kRrWaves, MESORASI_EUNSUPPORTED,
+                 "mesorasi_pointwise_mlp: staged register MLP on more than one tile per wave");
+    static const hipError_t attr[2] = {
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&mlp_rr_kernel<false>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kRrMaxLds),
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&mlp_rr_kernel<true>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kRrMaxLds)};
+    MESO_REQUIRE(attr[0] == hipSuccess && attr[1] == hipSuccess, MESORASI_EHIP,
+                 "mesorasi_pointwise_mlp: LDS size attribute: %s",
+                 hipGetErrorString(attr[0] != hipSuccess ? attr[0] : attr[1]));
     RrArgs a{};
     a.x0 = x0; a.ld0 = ld0; a.x1 = x1; a.ld1 = ld1; a.c0 = c0; a.c1 = x1 ? c1 : 0;
     a.rows = rows;
@@ -398,6 +462,8 @@ int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, in
         a.boff[l] = pl.boff[l];
     }
     a.lds_floats = pl.lds_floats;
+    a.nphase = pl.nphase;
+    for (int q = 0; q <= pl.nphase; ++q) a.phase_first[q] = pl.phase_first[q];
     a.relu_mask = relu_mask;
     a.y = y;
     a.ldy = ld_y;
@@ -410,14 +476,11 @@ int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, in
         a.c1 = 0;
     }
     a.vecy = ld_y % 4 == 0 && aligned(y, 16);
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess) {
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) cus = v;
-    }
     // one persistent workgroup per CU (the weights fill most of the LDS)
     const int64_t grid = std::min<int64_t>(ceil_div(a.tiles, kRrWaves), cus);
-    mlp_rr_kernel<<<dim3((unsigned)grid), dim3(64 * kRrWaves), (size_t)pl.lds_floats * sizeof(float), s>>>(a);
+    const size_t lds = (size_t)pl.lds_floats * sizeof(float);
+    if (pl.nphase > 1) mlp_rr_kernel<true><<<dim3((unsigned)grid), dim3(64 * kRrWaves), lds, s>>>(a);
+    else mlp_rr_kernel<false><<<dim3((unsigned)grid), dim3(64 * kRrWaves), lds, s>>>(a);
     return after_launch("mesorasi_pointwise_mlp (register MLP)");
 }
 

@@ -30,9 +30,11 @@ from ._lib import F32, BF16
 
 class Net:
     def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda", debug: bool = False,
-                 fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True):
+                 fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True,
+                 fuse_head: bool = True):
         self.spec = spec
         self.fuse_aggregation = fuse_aggregation
+        self.fuse_head = fuse_head
         self.fp_coarse_min_rows = fp_coarse_min_rows
         self.fps_prefix = fps_prefix
         self.delayed = delayed
@@ -145,6 +147,11 @@ class PointNet2(Net):
                     a=ops.MLPParams([np.ascontiguousarray(W1[:, :ci])], [None], device=self.device),
                     b=ops.MLPParams([np.ascontiguousarray(W1[:, ci:])], [bs[0]], device=self.device),
                     rest=ops.MLPParams(Ws[1:], bs[1:], device=self.device))
+                if k == len(self.fp) - 1 and "head" in w:
+                    # the level's remaining layers followed by the head, one MLP
+                    hW, hb = w["head"]
+                    self.fp_split[k]["rest_head"] = ops.MLPParams(list(Ws[1:]) + list(hW), list(bs[1:]) + list(hb),
+                                                                  device=self.device)
         if self.delayed == "ltd":
             # limited order (Sec. 7.3): the first layer's product on the input
             # points and on the centroids, its bias, and the remaining layers
@@ -393,7 +400,16 @@ class PointNet2(Net):
                     ws = self._ws(f"ws_fpg{i}", ops.mlp_workspace_bytes(B * coarse_f.shape[1], sp["a"]))
                     ops.pointwise_mlp(coarse_f, sp["a"], relu_mask=0, out=g, ws=ws)
                     h = self._bufs[f"fpp{i}"]
-                    if B * Nf > 32768 and ops.interpolate3_mlp_supported(sp["rest"]):
+                    rh = sp.get("rest_head") if self.fuse_head and self.head is not None else None
+                    if B * Nf > 32768 and rh is not None and ops.interpolate3_mlp_supported(rh, B * Nf):
+                        # the layer formed in the register MLP's row loader,
+                        # then the remaining layers and the head: the logits
+                        logits = self._buf("logits", (B, Nf, self.head.c_out))
+                        ops.interpolate3_mlp(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], g, h, rh,
+                                             relu_mask=(1 << (rh.n - 1)) - 1, out=logits)
+                        res["out"] = logits
+                        return res
+                    if B * Nf > 32768 and ops.interpolate3_mlp_supported(sp["rest"], B * Nf):
                         # the layer formed in the register MLP's row loader
                         ops.interpolate3_mlp(self._bufs[f"nn{i}"], self._bufs[f"nnd{i}"], g, h, sp["rest"], out=y)
                     else:
@@ -478,7 +494,8 @@ class DGCNN(Net):
 
 
 def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", debug: bool = False,
-          fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True) -> Net:
+          fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True,
+          fuse_head: bool = True) -> Net:
     """delayed: True (delayed aggregation), False (conventional) or "ltd"
     (limited delayed aggregation).  debug: every search output is checked
     to lie in range before anything reads through it (index_errors()).
@@ -488,9 +505,13 @@ def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", 
     fine rows take their first product on the coarse points
     (mesorasi_interpolate3_add).  fps_prefix: the sampling of every level
     after the first, which samples the previous level's centroids, is taken
-    as their first M (mesorasi_fps_prefix, the same result)."""
+    as their first M (mesorasi_fps_prefix, the same result).  fuse_head: the
+    last feature-propagation level's remaining layers and the per-point head
+    run in one kernel (mesorasi_interpolate3_mlp), so that level's output
+    (``fp{n-1}``) is not materialised."""
+    args = (spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows, fps_prefix, fuse_head)
     if spec["kind"] in ("pointnet2_cls", "pointnet2_seg"):
-        return PointNet2(spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows, fps_prefix)
+        return PointNet2(*args)
     if spec["kind"] == "dgcnn":
-        return DGCNN(spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows, fps_prefix)
+        return DGCNN(*args)
     raise ValueError(spec["kind"])

@@ -399,18 +399,27 @@ def interpolate3_add(nit: torch.Tensor, dist: torch.Tensor, f_src: torch.Tensor,
     return out
 
 
-def interpolate3_mlp_supported(p: MLPParams) -> bool:
+def interpolate3_mlp_supported(p: MLPParams, rows: int) -> bool:
     """mesorasi_interpolate3_mlp applies: an fp32 MLP whose layers are all at
-    most 128 wide (the register-resident MLP), first layer a multiple of 4."""
+    most 128 wide (the register-resident MLP), first layer a multiple of 4,
+    and, when the layers' permuted weights do not fit 160 KB of LDS
+    together, at most one 32-row tile per wave (8 per compute unit).  This
+    mirrors the library's plan."""
     if p.dtype != F32 or p.dims[0] % 4 != 0 or any(d > 128 for d in p.dims):
         return False
     h0 = ((p.dims[0] + 1) // 2 + 15) // 16 * 16     # first-layer k steps, as the library pads them
-    lds = 0
+    cap, off, phases = 160 * 1024, 0, 1
     for l in range(p.n):
         nob = (p.dims[l + 1] + 31) // 32
         steps = h0 if l == 0 else 16 * ((p.dims[l] + 31) // 32)
-        lds += 4 * (nob * steps * 64 + nob * 32)
-    return lds <= 160 * 1024
+        size = 4 * (nob * steps * 64 + nob * 32)
+        if off + size > cap:
+            phases, off = phases + 1, 0
+        off += size
+    if phases == 1:
+        return True
+    cus = torch.cuda.get_device_properties(torch.cuda.current_device()).multi_processor_count
+    return (rows + 31) // 32 <= 8 * cus
 
 
 def interpolate3_mlp(nit: torch.Tensor, dist: torch.Tensor, f_src: torch.Tensor, add: torch.Tensor, p: MLPParams,

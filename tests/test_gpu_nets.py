@@ -44,6 +44,10 @@ def check_pointnet(spec, got, ref, tol):
         e = normwise(got[f"f{i}"], m["out"])
         assert e <= tol, f"level {i} features {e}"
     for i, f in enumerate(ref.get("fp", [])):
+        if f"fp{i}" not in got:
+            # the last level fused with the head: its output is not kept
+            assert i == len(ref["fp"]) - 1
+            continue
         e = normwise(got[f"fp{i}"], f)
         assert e <= tol, f"fp {i}: {e}"
     e = normwise(got["out"], ref["out"])
@@ -293,3 +297,26 @@ def test_fps_prefix_changes_nothing(gpu, name, B):
     torch.cuda.synchronize()
     for k in ob:
         assert torch.equal(oa[k], ob[k]), k
+
+
+def test_fp_last_level_fused_with_head(gpu):
+    """The last feature-propagation level's remaining layers and the head in
+    one kernel (weights staged in two phases) give the logits of the
+    separate calls within fp32 rounding (the head's first layer sums its
+    k steps in another order), at the benchmark's full batch."""
+    spec = synth.workload("pointnet2_seg")
+    xyz, feat = synth.make_points(spec)
+    w = synth.make_weights(spec)
+    tx = torch.from_numpy(xyz).cuda()
+    tf = torch.from_numpy(feat).cuda()
+    a = nets.build(spec, w, delayed=True, fuse_head=True)
+    b = nets.build(spec, w, delayed=True, fuse_head=False)
+    ga, oa = a.capture(tx, tf)
+    ga.replay()
+    ob = b.forward(tx, tf)
+    torch.cuda.synchronize()
+    assert "fp3" not in oa and "fp3" in ob
+    assert normwise(oa["out"].cpu().numpy(), ob["out"].cpu().numpy()) <= 1e-5
+    for k in ob:
+        if k not in ("out", "fp3", "logits"):
+            assert torch.equal(oa[k], ob[k]), k

@@ -396,6 +396,10 @@ MLP_CASES = [
     ("rr_two_src", 40000, [3, 3], [32, 32, 64], F32),      # element loads of [x0 | x1]
     ("rr_odd_widths", 33001, [5, 2], [33, 17, 9], F32),    # partial 32-channel blocks
     ("rr_depth_max", 32769, [16], [32] * 8, F32),
+    # weights beyond the LDS: staged in phases (at most one 32-row tile per wave)
+    ("rr_staged_head", 65536, [128], [128, 128, 128, 13], F32),
+    ("rr_staged_ragged", 40001, [128], [128, 128, 128, 128, 36], F32),
+    ("staged_too_many_rows", 65600, [128], [128, 128, 128, 13], F32),   # beyond one tile per wave: the GEMMs
     ("rr_unaligned_out", 40000, [128], [98], F32),        # 98-float output rows: element stores
     # the bf16 form (v_mfma_f32_32x32x16_bf16, activations packed in
     # registers), used for first layers of at most 32 inputs
@@ -663,7 +667,10 @@ def test_interpolate3_add(gpu, B, Nd, Ns, C, relu, inplace):
 
 
 @pytest.mark.parametrize("B,Nd,Ns,widths", [(16, 4096, 1024, [128, 128, 128]), (3, 1000, 77, [20, 33, 9]),
-                                             (2, 20000, 500, [64, 128, 13])])
+                                             (2, 20000, 500, [64, 128, 13]),
+                                             # weights beyond the LDS: staged in phases, one tile per wave
+                                             (16, 4096, 1024, [128, 128, 128, 128, 13]),
+                                             (2, 20001, 300, [128, 128, 128, 128, 128, 36])])
 def test_interpolate3_mlp(gpu, B, Nd, Ns, widths):
     """The interpolate-add in the register MLP's loader: the two-call form's
     rows (mesorasi_interpolate3_add) bit for bit, so the same MLP gives the
@@ -678,7 +685,7 @@ def test_interpolate3_mlp(gpu, B, Nd, Ns, widths):
     Ws, bs = _weights(rr, widths)
     relu_mask = (1 << (len(widths) - 2)) - 1       # last layer linear
     p = ops.MLPParams(Ws, bs)
-    assert ops.interpolate3_mlp_supported(p)
+    assert ops.interpolate3_mlp_supported(p, B * Nd)
     nit, dist = ops.three_nn(dev(dst), dev(src))
     y = ops.interpolate3_mlp(nit, dist, dev(f), dev(a), p, relu_mask=relu_mask)
     h = ops.interpolate3_add(nit, dist, dev(f), dev(a))
