@@ -50,6 +50,7 @@ struct FusedArgs {
     int64_t ld1;
     int c0, c1;
     int64_t rows;
+    int64_t ntiles;    // row tiles (gathered inputs: the grid is padded to a multiple of 8)
     int n_layers;
     int dims[MESORASI_MAX_LAYERS + 1];
     const float* W[MESORASI_MAX_LAYERS];
@@ -349,7 +350,18 @@ void mlp_fused_f32_kernel(FusedArgs a) {
     float* H0 = smem;
     float* H1 = smem + a.hsize;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t row_t = (int64_t)blockIdx.x * FBM;
+    int64_t tile = blockIdx.x;
+    if constexpr (IN != kInPlain) {
+        // gathered rows (a cloud's neighbour rows, or the previous module's
+        // feature table): workgroups are dealt to the 8 XCDs round-robin by
+        // id, so renumber them to give each XCD one contiguous range of row
+        // tiles -- whole clouds -- whose gathered rows then stay in that
+        // XCD's L2 instead of every XCD fetching every cloud
+        const int64_t per = gridDim.x >> 3;
+        tile = (int64_t)(blockIdx.x & 7) * per + (blockIdx.x >> 3);
+        if (tile >= a.ntiles) return;   // the whole workgroup, before any barrier
+    }
+    const int64_t row_t = tile * FBM;
     float wb[2][CB][8];
     load_first_slice<CB, H>(a, 0, wave, lane, wb[0]);
 
@@ -517,8 +529,9 @@ int run_fused_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1,
     }
     // one instantiation per input and output form keeps each launch's code
     // (and its instruction-cache footprint) to the path it runs
-    const dim3 grid((unsigned)ceil_div(rows, 32 * H)), block(256);
     const bool gather = g != nullptr;
+    a.ntiles = ceil_div(rows, 32 * H);
+    const dim3 grid((unsigned)(gather ? 8 * ceil_div(a.ntiles, 8) : a.ntiles)), block(256);
     auto go = [&](auto h) {
         constexpr int HH = decltype(h)::value;
         if (pool_group > 0) {
@@ -559,7 +572,8 @@ int run_fused_aggregate_mlp(const float* cxyz, const MlpAggregate& ag, int64_t r
     const int H = fused_halves(rows);
     a.hsize = hmax * (32 * H + 1);
     const size_t lds = sizeof(float) * 2 * (size_t)a.hsize;
-    const dim3 grid((unsigned)ceil_div(rows, 32 * H)), block(256);
+    a.ntiles = ceil_div(rows, 32 * H);
+    const dim3 grid((unsigned)(8 * ceil_div(a.ntiles, 8))), block(256);
     if (H == 1) mlp_fused_f32_kernel<1, kInAgg, kOutF32, 1><<<grid, block, lds, s>>>(a);
     else mlp_fused_f32_kernel<1, kInAgg, kOutF32, 2><<<grid, block, lds, s>>>(a);
     return after_launch("mesorasi_aggregate_mlp");
