@@ -973,7 +973,12 @@ __global__ __launch_bounds__(256) void interp3_apply_kernel(const int32_t* __res
                                                             const float* add = nullptr, int64_t lda = 0,
                                                             int relu = 0) {
     const int cw = VEC4 ? C >> 2 : C;
-    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    // workgroups are dealt to the 8 XCDs round-robin by id (the grid is a
+    // multiple of 8): renumber them so each XCD runs one contiguous range of
+    // destinations -- whole clouds -- and gathers its source rows into its
+    // own L2 only
+    const int64_t lb = (int64_t)(blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+    for (int64_t e = lb * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
         const int64_t r = e / cw;                // global destination b * Nd + i
         const int c = (int)(e - r * cw) * (VEC4 ? 4 : 1);
         const int64_t b = r / Nd;
@@ -1135,7 +1140,7 @@ extern "C" int mesorasi_interpolate3_apply(const int32_t* nit, const float* dist
     MESO_REQUIRE(Ns <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_interpolate3_apply: size");
     const bool vec4 = C % 4 == 0 && ld_src % 4 == 0 && ld_dst % 4 == 0 && aligned(f_src, 16) && aligned(f_dst, 16);
     const int64_t total = B * Nd * (vec4 ? C / 4 : C);
-    const dim3 grid((unsigned)std::min<int64_t>(ceil_div(total, 256), 8192)), block(256);
+    const dim3 grid((unsigned)(8 * ceil_div(std::min<int64_t>(ceil_div(total, 256), 8192), 8))), block(256);
     if (vec4)
         interp3_apply_kernel<true><<<grid, block, 0, as_stream(stream)>>>(nit, dist, f_src, ld_src, Nd, (int)Ns, C,
                                                                          total, f_dst, ld_dst);
@@ -1160,7 +1165,7 @@ extern "C" int mesorasi_interpolate3_add(const int32_t* nit, const float* dist, 
     const bool vec4 = C % 4 == 0 && ld_src % 4 == 0 && ld_dst % 4 == 0 && ld_add % 4 == 0 && aligned(f_src, 16) &&
                       aligned(f_dst, 16) && aligned(add, 16);
     const int64_t total = B * Nd * (vec4 ? C / 4 : C);
-    const dim3 grid((unsigned)std::min<int64_t>(ceil_div(total, 256), 8192)), block(256);
+    const dim3 grid((unsigned)(8 * ceil_div(std::min<int64_t>(ceil_div(total, 256), 8192), 8))), block(256);
     if (vec4)
         interp3_apply_kernel<true, true><<<grid, block, 0, as_stream(stream)>>>(
             nit, dist, f_src, ld_src, Nd, (int)Ns, C, total, f_dst, ld_dst, add, ld_add, relu);

@@ -236,7 +236,14 @@ void mlp_rr_kernel(RrArgs a) {
     // the first tile's rows are requested before the weights are staged,
     // so their HBM round trip overlaps the staging
     const int64_t stride = (int64_t)gridDim.x * kRrWaves;
-    const int64_t t0 = (int64_t)blockIdx.x * kRrWaves + wave;
+    // interpolated rows gather the coarse level's rows of their cloud:
+    // workgroups are dealt to the 8 XCDs round-robin by id, so (the grid
+    // being a multiple of 8 then) renumber them to give each XCD one
+    // contiguous range of tiles -- whole clouds -- and keep those gathers in
+    // its own L2
+    int64_t wg = blockIdx.x;
+    if (a.interp && (gridDim.x & 7) == 0) wg = (int64_t)(blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+    const int64_t t0 = wg * kRrWaves + wave;
     if (t0 < a.tiles) load_tile(t0, act);
 
     // weights: layer l, output block ob, step group g = s / 4, lane, s % 4;
@@ -476,8 +483,11 @@ int run_rr_mlp(const float* x0, int c0, int64_t ld0, const float* x1, int c1, in
         a.c1 = 0;
     }
     a.vecy = ld_y % 4 == 0 && aligned(y, 16);
-    // one persistent workgroup per CU (the weights fill most of the LDS)
-    const int64_t grid = std::min<int64_t>(ceil_div(a.tiles, kRrWaves), cus);
+    // one persistent workgroup per CU (the weights fill most of the LDS);
+    // interpolated rows: a multiple of 8 workgroups where that stays within
+    // the CUs (the kernel then orders tiles by XCD)
+    int64_t grid = std::min<int64_t>(ceil_div(a.tiles, kRrWaves), cus);
+    if (a.interp && 8 * ceil_div(grid, 8) <= cus) grid = 8 * ceil_div(grid, 8);
     const size_t lds = (size_t)pl.lds_floats * sizeof(float);
     if (pl.nphase > 1) mlp_rr_kernel<true><<<dim3((unsigned)grid), dim3(64 * kRrWaves), lds, s>>>(a);
     else mlp_rr_kernel<false><<<dim3((unsigned)grid), dim3(64 * kRrWaves), lds, s>>>(a);
