@@ -130,6 +130,28 @@ int mesorasi_fps_prefix(const int32_t* idx_prev, const float* cxyz_prev, int64_t
                         int32_t* idx, float* cxyz, void* stream);
 
 /*
+ * Several nested levels at once: level v (v < n_levels) is the sampling of
+ * M[v] points from the previous level, level 0's sampling being
+ * (idx0, cxyz0) with M0 points.  By the property above every level is a
+ * prefix of level 0 and its indices follow from idx0 alone:
+ *   idx[v][b][k]  = k, or 0 where k > 0 and idx0[b][k] == 0
+ *   cxyz[v][b][k] = cxyz0[b][k]
+ * (for M[0] >= M[1] >= ..., each level equals mesorasi_fps_prefix on the
+ * previous one).  One launch for all levels.
+ *   idx0 [B, M0] int32, cxyz0 [B, M0, 3] float32 (nullable when no cxyz
+ *        output is requested)
+ *   M    host array [n_levels], 0 <= M[v] <= M0
+ *   idx  host array [n_levels] of device [B, M[v]] int32 outputs
+ *   cxyz host array [n_levels] of device [B, M[v], 3] float32 outputs, or
+ *        NULL; an entry may be NULL
+ * Errors: EINVAL for sizes < 0, n_levels outside [0, MESORASI_MAX_LAYERS],
+ *         M[v] outside [0, M0], NULL M/idx/idx[v]/idx0, cxyz without cxyz0;
+ *         EUNSUPPORTED for M0 > MESORASI_MAX_N_FPS.
+ */
+int mesorasi_fps_prefix_levels(const int32_t* idx0, const float* cxyz0, int64_t B, int64_t M0, int32_t n_levels,
+                               const int64_t* M, int32_t* const* idx, float* const* cxyz, void* stream);
+
+/*
  * Ball query: neighbor search N (Sec. 3.1 "Neighbor Search") producing the
  * NIT (Sec. 4.1 walk-through).  For each query q, the first K point indices
  * in ascending order with squared distance (same rule as FPS) strictly

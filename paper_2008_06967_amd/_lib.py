@@ -28,6 +28,7 @@ SIGNATURES = {
     "mesorasi_fps": (ctypes.c_int, [_p, _i64, _i64, _i64, _p, _p, _p, _size, _p]),
     "mesorasi_fps_workspace": (_size, [_i64, _i64, _i64]),
     "mesorasi_fps_prefix": (ctypes.c_int, [_p, _p, _i64, _i64, _i64, _p, _p, _p]),
+    "mesorasi_fps_prefix_levels": (ctypes.c_int, [_p, _p, _i64, _i64, ctypes.c_int32, _p, _p, _p, _p]),
     "mesorasi_ball_query": (ctypes.c_int, [_p, _p, _i64, _i64, _i64, _f, _i32, _p, _p, _p, _size, _p]),
     "mesorasi_ball_query_workspace": (_size, [_i64, _i64, _i64]),
     "mesorasi_knn": (ctypes.c_int, [_p, _i64, _p, _i64, _i64, _i64, _i64, _i32, _i32, _p, _p, _p]),

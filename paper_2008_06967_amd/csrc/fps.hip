@@ -604,6 +604,39 @@ __global__ __launch_bounds__(256) void fps_prefix_kernel(const int32_t* __restri
     }
 }
 
+// Several nested levels in one launch: level v takes the first M[v] points
+// of level 0's sampling (the prefix of a prefix is a prefix, and the index
+// rule depends only on level 0's indices).  Thread e of the flattened
+// (level, cloud, k) range writes one point.
+struct FpsLevels {
+    int n;
+    int M[MESORASI_MAX_LAYERS];
+    int64_t start[MESORASI_MAX_LAYERS + 1];   // flattened offsets of the levels
+    int32_t* idx[MESORASI_MAX_LAYERS];
+    float* cxyz[MESORASI_MAX_LAYERS];
+};
+
+__global__ __launch_bounds__(256) void fps_prefix_levels_kernel(const int32_t* __restrict__ idx0,
+                                                               const float* __restrict__ cxyz0, int64_t B, int M0,
+                                                               FpsLevels lv) {
+    const int64_t total = lv.start[lv.n];
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int v = 0;
+        while (e >= lv.start[v + 1]) ++v;
+        const int64_t r = e - lv.start[v];
+        const int M = lv.M[v];
+        const int64_t b = r / M;
+        const int k = (int)(r - b * M);
+        const int64_t src = b * M0 + k;
+        lv.idx[v][r] = (k == 0 || idx0[src] != 0) ? k : 0;
+        if (lv.cxyz[v]) {
+            lv.cxyz[v][3 * r + 0] = cxyz0[3 * src + 0];
+            lv.cxyz[v][3 * r + 1] = cxyz0[3 * src + 1];
+            lv.cxyz[v][3 * r + 2] = cxyz0[3 * src + 2];
+        }
+    }
+}
+
 }  // namespace meso
 
 using namespace meso;
@@ -668,4 +701,39 @@ extern "C" int mesorasi_fps_prefix(const int32_t* idx_prev, const float* cxyz_pr
     fps_prefix_kernel<<<dim3(grid), dim3(256), 0, as_stream(stream)>>>(idx_prev, cxyz_prev, B, (int)M_prev, (int)M,
                                                                        idx, cxyz);
     return after_launch("mesorasi_fps_prefix");
+}
+
+extern "C" int mesorasi_fps_prefix_levels(const int32_t* idx0, const float* cxyz0, int64_t B, int64_t M0,
+                                          int32_t n_levels, const int64_t* M, int32_t* const* idx,
+                                          float* const* cxyz, void* stream) {
+    const char* who = "mesorasi_fps_prefix_levels";
+    MESO_REQUIRE(B >= 0 && M0 >= 0, MESORASI_EINVAL, "%s: negative size", who);
+    MESO_REQUIRE(n_levels >= 0 && n_levels <= MESORASI_MAX_LAYERS, MESORASI_EINVAL, "%s: n_levels = %d", who,
+                 n_levels);
+    MESO_REQUIRE(n_levels == 0 || (M && idx), MESORASI_EINVAL, "%s: NULL M or idx", who);
+    MESO_REQUIRE(M0 <= MESORASI_MAX_N_FPS, MESORASI_EUNSUPPORTED, "%s: M0 = %lld > %d", who, (long long)M0,
+                 MESORASI_MAX_N_FPS);
+    MESO_REQUIRE(B <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: B too large", who);
+    FpsLevels lv{};
+    lv.n = n_levels;
+    int64_t total = 0;
+    bool any_xyz = false;
+    for (int v = 0; v < n_levels; ++v) {
+        MESO_REQUIRE(M[v] >= 0 && M[v] <= M0, MESORASI_EINVAL, "%s: M[%d] = %lld outside [0, M0 = %lld]", who, v,
+                     (long long)M[v], (long long)M0);
+        lv.M[v] = (int)M[v];
+        lv.start[v] = total;
+        total += B * M[v];
+        lv.idx[v] = idx[v];
+        lv.cxyz[v] = cxyz ? cxyz[v] : nullptr;
+        MESO_REQUIRE(B * M[v] == 0 || idx[v], MESORASI_EINVAL, "%s: NULL idx[%d]", who, v);
+        any_xyz = any_xyz || (lv.cxyz[v] && B * M[v] > 0);
+    }
+    lv.start[n_levels] = total;
+    if (total == 0) return MESORASI_OK;
+    MESO_REQUIRE(idx0, MESORASI_EINVAL, "%s: NULL idx0", who);
+    MESO_REQUIRE(!any_xyz || cxyz0, MESORASI_EINVAL, "%s: cxyz requested without cxyz0", who);
+    const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(total, 256), 4096);
+    fps_prefix_levels_kernel<<<dim3(grid), dim3(256), 0, as_stream(stream)>>>(idx0, cxyz0, B, (int)M0, lv);
+    return after_launch(who);
 }

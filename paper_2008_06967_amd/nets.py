@@ -196,20 +196,25 @@ class PointNet2(Net):
             for i, m in enumerate(self.spec["sa"]):
                 idx = self._buf(f"idx{i}", (B, m["M"]), torch.int32)
                 cx = self._buf(f"cxyz{i}", (B, m["M"], 3))
-                if i > 0 and self.fps_prefix:
-                    # level i samples level i-1's centroids, themselves a
-                    # sampling in selection order: its first M, exactly
-                    ops.fps_prefix(self._bufs[f"idx{i - 1}"], p, m["M"], out_idx=idx, out_xyz=cx)
-                else:
+                if i == 0 or not self.fps_prefix:
                     ws = self._ws(f"ws_fps{i}", ops.fps_workspace_bytes(B, p.shape[1], m["M"]))
                     ops.fps(p, m["M"], out_idx=idx, out_xyz=cx, ws=ws)
-                self._check_range(f"idx{i}", idx, p.shape[1])
-                if i == 0 or not self.fps_prefix:
+                    self._check_range(f"idx{i}", idx, p.shape[1])
                     e = torch.cuda.Event()
                     e.record(side)
                     ev_fps.append(e)
                 p = cx
                 lv.append(cx)
+            if self.fps_prefix and L > 1:
+                # level i samples level i-1's centroids, themselves a
+                # sampling in selection order: its first M, exactly -- all
+                # levels after the first from the first one, in one launch
+                sa = self.spec["sa"]
+                ops.fps_prefix_levels(self._bufs["idx0"], self._bufs["cxyz0"], [m["M"] for m in sa[1:]],
+                                      out_idx=[self._bufs[f"idx{i}"] for i in range(1, L)],
+                                      out_xyz=[self._bufs[f"cxyz{i}"] for i in range(1, L)])
+                for i in range(1, L):
+                    self._check_range(f"idx{i}", self._bufs[f"idx{i}"], sa[i - 1]["M"])
             if self.fps_prefix and L > 1:
                 for i in range(1, L):
                     self._issue_ball_query(i, lv[i])

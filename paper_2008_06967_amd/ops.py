@@ -89,6 +89,30 @@ def fps_prefix(idx_prev: torch.Tensor, cxyz_prev: torch.Tensor | None, M: int, o
     return idx, cxyz
 
 
+def fps_prefix_levels(idx0: torch.Tensor, cxyz0: torch.Tensor | None, Ms, out_idx=None, out_xyz=None):
+    """Nested levels of M[v] points each, all prefixes of (idx0, cxyz0), in
+    one launch (mesorasi_fps_prefix_levels).  Returns [(idx, cxyz)] per
+    level."""
+    if idx0.dtype != torch.int32 or idx0.dim() != 2 or not idx0.is_contiguous():
+        raise ValueError("idx0 must be a contiguous [B, M0] int32 tensor")
+    B, M0 = idx0.shape
+    if cxyz0 is not None:
+        _check_xyz(cxyz0, "cxyz0")
+    n = len(Ms)
+    idx = list(out_idx) if out_idx is not None else [
+        torch.empty((B, m), dtype=torch.int32, device=idx0.device) for m in Ms]
+    xyz = list(out_xyz) if out_xyz is not None else (
+        [torch.empty((B, m, 3), dtype=torch.float32, device=idx0.device) for m in Ms] if cxyz0 is not None
+        else [None] * n)
+    Mc = (ctypes.c_int64 * max(n, 1))(*Ms)
+    ic = (_vp * max(n, 1))(*[t.data_ptr() for t in idx])
+    xc = (_vp * max(n, 1))(*[None if t is None else t.data_ptr() for t in xyz])
+    check(_lib.lib().mesorasi_fps_prefix_levels(idx0.data_ptr(), _ptr(cxyz0), B, M0, n, ctypes.cast(Mc, _vp),
+                                                ctypes.cast(ic, _vp), ctypes.cast(xc, _vp), _stream()),
+          "fps_prefix_levels")
+    return list(zip(idx, xyz))
+
+
 def ball_query_workspace_bytes(B: int, N: int, M: int) -> int:
     return int(_lib.lib().mesorasi_ball_query_workspace(B, N, M))
 

@@ -68,6 +68,24 @@ def test_fps_prefix_validation():
     assert b"M_prev = 10" in _lib.lib().mesorasi_last_error()
 
 
+def test_fps_prefix_levels_validation():
+    f = "mesorasi_fps_prefix_levels"
+    M = (ctypes.c_int64 * 2)(5, 11)
+    P = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    assert st(f, FAKE, FAKE, 1, 10, 2, M, P, P, NULL) == _lib.EINVAL        # M[1] > M0
+    assert st(f, FAKE, FAKE, -1, 10, 2, M, P, P, NULL) == _lib.EINVAL       # B < 0
+    assert st(f, FAKE, FAKE, 1, 10, 9, M, P, P, NULL) == _lib.EINVAL        # too many levels
+    assert st(f, FAKE, FAKE, 1, 10, 2, NULL, P, P, NULL) == _lib.EINVAL     # NULL M
+    M2 = (ctypes.c_int64 * 2)(5, 3)
+    assert st(f, NULL, FAKE, 1, 10, 2, M2, P, P, NULL) == _lib.EINVAL       # NULL idx0
+    assert st(f, FAKE, NULL, 1, 10, 2, M2, P, P, NULL) == _lib.EINVAL       # cxyz without cxyz0
+    assert st(f, FAKE, FAKE, 1, 70000, 2, M2, P, P, NULL) == _lib.EUNSUPPORTED
+    assert st(f, NULL, NULL, 0, 10, 2, M2, P, P, NULL) == _lib.OK           # empty batch
+    assert st(f, NULL, NULL, 3, 10, 0, NULL, NULL, NULL, NULL) == _lib.OK   # no levels
+    st(f, FAKE, FAKE, 1, 10, 2, M, P, P, NULL)
+    assert b"M[1] = 11" in _lib.lib().mesorasi_last_error()
+
+
 def test_fps_workspace():
     """Small clouds run one workgroup per cloud and need no workspace; large
     ones exchange winners through one, which must be big enough and 8-byte

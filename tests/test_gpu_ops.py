@@ -145,6 +145,14 @@ def test_fps_prefix_bit_exact(gpu, name, B, N, levels, kind):
         prev_i, prev_c = i2, c2
     if kind in ("grid", "dups"):
         assert zero_steps      # the distinct points ran out: steps that take point 0
+    # every level at once from the first: the same as the chain, bit for bit
+    chain = []
+    pi, pc = idx, cxyz
+    for M in levels[1:]:
+        pi, pc = ops.fps_prefix(pi, pc, M)
+        chain.append((pi, pc))
+    for (ci, cc), (li, lc) in zip(chain, ops.fps_prefix_levels(idx, cxyz, levels[1:])):
+        assert torch.equal(ci, li) and torch.equal(cc, lc)
 
 
 # ----------------------------------------------------------------------------
