@@ -84,7 +84,7 @@ class StageTimer:
     """Wraps the ops entry points so every call records a start/end event on
     the stream it is launched on."""
 
-    NAMES = ("fps", "fps_prefix", "ball_query", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3",
+    NAMES = ("fps", "fps_prefix", "fps_prefix_levels", "ball_query", "ball_query_grid_build", "ball_query_grid", "knn", "pointwise_mlp", "aggregate_max", "conventional_module", "interpolate3",
              "three_nn", "interpolate3_apply", "interpolate3_add", "interpolate3_mlp", "aggregate_mlp")
 
     def __init__(self, ops):
@@ -144,8 +144,10 @@ def call_work(name, a, kw, result=None):
 
     fps:            (M-1) * N point updates per cloud, 8 flops each (3 sub,
                     1 mul, 2 fma) -> alu
-    fps_prefix:     the nested sampling as a prefix: compulsory HBM bytes
-                    (indices and coordinates read and written) -> hbm
+    fps_prefix, fps_prefix_levels: the nested sampling as a prefix:
+                    compulsory HBM bytes (indices and coordinates read and
+                    written) -> hbm
+    ball_query_grid_build: the cloud read, its binned copy written -> hbm
     ball_query:     the candidate pairs the search rule scans, 8 flops each
                     -> alu: a query that fills its K slots scans up to its
                     K-th hit (index nit[K-1] + 1), otherwise all N points;
@@ -177,7 +179,13 @@ def call_work(name, a, kw, result=None):
     if name == "fps_prefix":
         ip, M = arg(0, "idx_prev"), arg(2, "M")
         return ("hbm", 32.0 * ip.shape[0] * M / 1e9, None)
-    if name == "ball_query":
+    if name == "fps_prefix_levels":
+        i0, Ms = arg(0, "idx0"), arg(2, "Ms")
+        return ("hbm", 32.0 * i0.shape[0] * sum(Ms) / 1e9, None)
+    if name == "ball_query_grid_build":
+        xyz = arg(0, "xyz")
+        return ("hbm", 28.0 * xyz.shape[0] * xyz.shape[1] / 1e9, None)
+    if name in ("ball_query", "ball_query_grid"):
         xyz, q, K = arg(0, "xyz"), arg(1, "qxyz"), arg(3, "K")
         B, N, M = xyz.shape[0], xyz.shape[1], q.shape[1]
         comp = 12 * B * N + 12 * B * M + 4 * B * M * K
@@ -447,8 +455,12 @@ def measure(tag, args, dev, headline=False):
     per_module, module_ms = {}, {}
     for i, m in enumerate(spec.get("sa", [])):
         per_module[f"sa{i + 1}"] = B * m["M"] / t_step
-        ms = sum(stages.get(f"{n}#{i}", 0.0) for n in ("fps", "ball_query", "pointwise_mlp", "aggregate_max"))
+        ms = sum(stages.get(f"{n}#{i}", 0.0) for n in ("fps", "pointwise_mlp", "aggregate_max"))
         ms += stages.get(f"fps_prefix#{i - 1}", 0.0) if i else 0.0
+        # the first level's ball query may run against a prebuilt grid
+        grid = "ball_query_grid#0" in stages
+        ms += stages.get("ball_query_grid#0", 0.0) if (grid and i == 0) else \
+            stages.get(f"ball_query#{i - 1 if grid else i}", 0.0)
         module_ms[f"sa{i + 1}"] = round(ms, 5)
     if spec["kind"] == "dgcnn":
         for l in range(len(spec["edge"])):

@@ -178,6 +178,29 @@ int mesorasi_ball_query(const float* xyz, const float* qxyz, int64_t B, int64_t 
 size_t mesorasi_ball_query_workspace(int64_t B, int64_t N, int64_t M);
 
 /*
+ * The ball query above in two steps, so the cloud can be binned before its
+ * query centroids exist (the input points of a network are known while its
+ * first sampling still runs):
+ *   mesorasi_ball_query_grid_build bins each cloud of xyz [B, N, 3] into
+ *   cubic cells of edge at least radius (1 + 2^-12) in ws;
+ *   mesorasi_ball_query_grid answers the queries against those cells, with
+ *   exactly the result of mesorasi_ball_query (same rule, same order, same
+ *   padding and counts).
+ * xyz must be the cloud the grid was built from, unchanged since; a query
+ * radius above the build's walks the cloud instead (same result).  The
+ * workspace ws (at least mesorasi_ball_query_grid_workspace(B, N) bytes,
+ * 256-byte aligned) holds the grid between the calls; a query only reads
+ * it, so several queries may share one grid.
+ * Errors: as mesorasi_ball_query; EWORKSPACE when ws is NULL or too small;
+ *         EUNSUPPORTED for N > MESORASI_MAX_N_FPS.
+ */
+size_t mesorasi_ball_query_grid_workspace(int64_t B, int64_t N);
+int mesorasi_ball_query_grid_build(const float* xyz, int64_t B, int64_t N, float radius, void* ws, size_t ws_bytes,
+                                   void* stream);
+int mesorasi_ball_query_grid(const float* xyz, const float* qxyz, int64_t B, int64_t N, int64_t M, float radius,
+                             int32_t K, int32_t* nit, int32_t* cnt, const void* ws, size_t ws_bytes, void* stream);
+
+/*
  * k nearest neighbours in C-dimensional feature space (the DGCNN search in
  * the previous module's output space, Sec. 5.1 "Work Flow").  Squared
  * distance t_c = r_c - q_c, d = fma(t_c, t_c, d) for c ascending from 0;

@@ -31,6 +31,10 @@ SIGNATURES = {
     "mesorasi_fps_prefix_levels": (ctypes.c_int, [_p, _p, _i64, _i64, ctypes.c_int32, _p, _p, _p, _p]),
     "mesorasi_ball_query": (ctypes.c_int, [_p, _p, _i64, _i64, _i64, _f, _i32, _p, _p, _p, _size, _p]),
     "mesorasi_ball_query_workspace": (_size, [_i64, _i64, _i64]),
+    "mesorasi_ball_query_grid_workspace": (_size, [_i64, _i64]),
+    "mesorasi_ball_query_grid_build": (ctypes.c_int, [_p, _i64, _i64, ctypes.c_float, _p, _size, _p]),
+    "mesorasi_ball_query_grid": (ctypes.c_int, [_p, _p, _i64, _i64, _i64, ctypes.c_float, ctypes.c_int32, _p, _p, _p,
+                                                _size, _p]),
     "mesorasi_knn": (ctypes.c_int, [_p, _i64, _p, _i64, _i64, _i64, _i64, _i32, _i32, _p, _p, _p]),
     "mesorasi_pointwise_mlp": (ctypes.c_int, [_p, _i32, _i64, _p, _i32, _i64, _i64, _i32, _p, _p, _p, _u32, _i32,
                                               _i32, _p, _i64, _i64, _p, _size, _p]),

@@ -151,7 +151,7 @@ struct GridInfo {
     double mn[3];
     double inv_h;
     int g[3];
-    int pad;
+    float radius;   // the radius the cells were sized for: they serve queries up to it
 };
 
 struct GridWs {
@@ -238,7 +238,7 @@ __global__ __launch_bounds__(1024) void grid_build_kernel(const float* __restric
             gi.g[d] = (int)(floor(e[d] / h) + 1.0);
         }
         gi.inv_h = 1.0 / h;
-        gi.pad = 0;
+        gi.radius = radius;
         s_gi = gi;
         w.info[b] = gi;
     }
@@ -284,8 +284,9 @@ __global__ __launch_bounds__(1024) void grid_build_kernel(const float* __restric
 // instead (same result).
 __global__ __launch_bounds__(64 * kGridQWaves) void grid_query_kernel(const float* __restrict__ xyz,
                                                                       const float* __restrict__ qxyz, int64_t BM,
-                                                                      int N, int M, float r2, int K, int walk_above,
-                                                                      GridWs w, int32_t* __restrict__ nit,
+                                                                      int N, int M, float radius, float r2, int K,
+                                                                      int walk_above, GridWs w,
+                                                                      int32_t* __restrict__ nit,
                                                                       int32_t* __restrict__ cnt) {
     extern __shared__ uint32_t s_bits[];
     const int words = (N + 31) >> 5;
@@ -317,7 +318,9 @@ __global__ __launch_bounds__(64 * kGridQWaves) void grid_query_kernel(const floa
     }
     for (int o = 8; o > 0; o >>= 1) cand += __shfl_xor(cand, o);
     cand = __shfl(cand, 0);
-    if (cand > walk_above) {
+    // a radius above the one the cells were sized for (a grid built apart,
+    // mesorasi_ball_query_grid) walks as well: same result
+    if (cand > walk_above || !(radius <= gi.radius)) {
         const float* __restrict__ p = xyz + b * (int64_t)N * 3;
         auto pt = [&](int j, float& x, float& y, float& z) {
             x = p[3 * j + 0];
@@ -381,11 +384,13 @@ __global__ __launch_bounds__(64 * kGridQWaves) void grid_query_kernel(const floa
     if (cnt && lane == 0) cnt[gq] = n;
 }
 
-static size_t bq_ws_bytes(int64_t B, int64_t N) {
-    if (B <= 0 || N < kBqGridMinN) return 0;
+static size_t grid_ws_bytes(int64_t B, int64_t N) {
+    if (B <= 0 || N <= 0) return 0;
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     return al(B * sizeof(GridInfo)) + al((size_t)B * (kGridCells + 1) * 4) + al((size_t)B * N * 16);
 }
+
+static size_t bq_ws_bytes(int64_t B, int64_t N) { return N < kBqGridMinN ? 0 : grid_ws_bytes(B, N); }
 
 static GridWs bq_ws_layout(void* ws, int64_t B, int64_t N) {
     (void)N;
@@ -400,6 +405,43 @@ static GridWs bq_ws_layout(void* ws, int64_t B, int64_t N) {
     return w;
 }
 
+static int launch_grid_build(const float* xyz, int64_t B, int64_t N, float radius, const GridWs& w, hipStream_t s,
+                             const char* who) {
+    MESO_REQUIRE(B <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: B too large", who);
+    grid_build_kernel<<<dim3((unsigned)B), dim3(1024), 0, s>>>(xyz, (int)N, radius, w);
+    return after_launch(who);
+}
+
+static int launch_grid_query(const float* xyz, const float* qxyz, int64_t B, int64_t N, int64_t M, float radius,
+                             int32_t K, int32_t* nit, int32_t* cnt, const GridWs& w, hipStream_t s, const char* who) {
+    const int64_t BM = B * M;
+    const int64_t qblocks = ceil_div(BM, kGridQWaves);
+    MESO_REQUIRE(qblocks <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: too many queries", who);
+    const size_t lds = (size_t)kGridQWaves * 64 * ceil_div(ceil_div(N, 32), 64) * 4;
+    // walk or grid: a ball of c candidates holds about 0.155 c points
+    // (sphere over 27 cubes), so a walk scans about K N / (0.155 c);
+    // the two cost the same near c = sqrt(6.45 K N)
+    const int walk_above = (int)std::min(std::sqrt(6.45 * (double)K * (double)N), 2.0e9);
+    grid_query_kernel<<<dim3((unsigned)qblocks), dim3(64 * kGridQWaves), lds, s>>>(
+        xyz, qxyz, BM, (int)N, (int)M, radius, radius * radius, K, walk_above, w, nit, cnt);
+    return after_launch(who);
+}
+
+// Arguments shared by the ball query entry points.
+static int check_bq_args(const char* who, const float* xyz, const float* qxyz, int64_t B, int64_t N, int64_t M,
+                         float radius, int32_t K, const int32_t* nit) {
+    MESO_REQUIRE(B >= 0 && N >= 0 && M >= 0, MESORASI_EINVAL, "%s: negative size", who);
+    MESO_REQUIRE(K >= 1, MESORASI_EINVAL, "%s: K = %d < 1", who, K);
+    MESO_REQUIRE(radius > 0.0f && radius <= 3.0e38f, MESORASI_EINVAL, "%s: radius must be finite and > 0", who);
+    MESO_REQUIRE(K <= MESORASI_MAX_K_BALL, MESORASI_EUNSUPPORTED, "%s: K = %d > %d", who, K, MESORASI_MAX_K_BALL);
+    if (B == 0 || M == 0) return MESORASI_OK;
+    MESO_REQUIRE(N >= 1, MESORASI_EINVAL, "%s: N = 0 with M > 0", who);
+    MESO_REQUIRE(xyz && qxyz && nit, MESORASI_EINVAL, "%s: NULL xyz, qxyz or nit", who);
+    MESO_REQUIRE(N <= 0x7fffffff - 64 * (kBqChunks + 1) && M <= 0x7fffffff, MESORASI_EUNSUPPORTED,
+                 "%s: N or M too large", who);
+    return MESORASI_OK;
+}
+
 }  // namespace meso
 
 using namespace meso;
@@ -412,53 +454,70 @@ extern "C" size_t mesorasi_ball_query_workspace(int64_t B, int64_t N, int64_t M)
 extern "C" int mesorasi_ball_query(const float* xyz, const float* qxyz, int64_t B, int64_t N, int64_t M,
                                    float radius, int32_t K, int32_t* nit, int32_t* cnt, void* ws, size_t ws_bytes,
                                    void* stream) {
-    MESO_REQUIRE(B >= 0 && N >= 0 && M >= 0, MESORASI_EINVAL, "mesorasi_ball_query: negative size");
-    MESO_REQUIRE(K >= 1, MESORASI_EINVAL, "mesorasi_ball_query: K = %d < 1", K);
-    MESO_REQUIRE(radius > 0.0f && radius <= 3.0e38f, MESORASI_EINVAL,
-                 "mesorasi_ball_query: radius must be finite and > 0");
-    MESO_REQUIRE(K <= MESORASI_MAX_K_BALL, MESORASI_EUNSUPPORTED, "mesorasi_ball_query: K = %d > %d", K,
-                 MESORASI_MAX_K_BALL);
-    if (B == 0 || M == 0) return MESORASI_OK;
-    MESO_REQUIRE(N >= 1, MESORASI_EINVAL, "mesorasi_ball_query: N = 0 with M > 0");
-    MESO_REQUIRE(xyz && qxyz && nit, MESORASI_EINVAL, "mesorasi_ball_query: NULL xyz, qxyz or nit");
-    MESO_REQUIRE(N <= 0x7fffffff - 64 * (kBqChunks + 1) && M <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_ball_query: N or M too large");
+    const char* who = "mesorasi_ball_query";
+    int rc = check_bq_args(who, xyz, qxyz, B, N, M, radius, K, nit);
+    if (rc != MESORASI_OK || B == 0 || M == 0) return rc;
     const size_t need = bq_ws_bytes(B, N);
-    MESO_REQUIRE(ws_bytes >= need && (need == 0 || ws), MESORASI_EWORKSPACE,
-                 "mesorasi_ball_query: workspace %zu < %zu bytes", ws_bytes, need);
-    MESO_REQUIRE(need == 0 || aligned(ws, 256), MESORASI_EINVAL, "mesorasi_ball_query: workspace not 256-byte aligned");
-    MESO_REQUIRE(need == 0 || N <= MESORASI_MAX_N_FPS, MESORASI_EUNSUPPORTED, "mesorasi_ball_query: N = %lld > %d",
+    MESO_REQUIRE(ws_bytes >= need && (need == 0 || ws), MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who,
+                 ws_bytes, need);
+    MESO_REQUIRE(need == 0 || aligned(ws, 256), MESORASI_EINVAL, "%s: workspace not 256-byte aligned", who);
+    MESO_REQUIRE(need == 0 || N <= MESORASI_MAX_N_FPS, MESORASI_EUNSUPPORTED, "%s: N = %lld > %d", who,
                  (long long)N, MESORASI_MAX_N_FPS);
     const float r2 = radius * radius;
     const int64_t BM = B * M;
     hipStream_t s = as_stream(stream);
     if (need > 0) {
         const GridWs w = bq_ws_layout(ws, B, N);
-        MESO_REQUIRE(B <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_ball_query: B too large");
-        grid_build_kernel<<<dim3((unsigned)B), dim3(1024), 0, s>>>(xyz, (int)N, radius, w);
-        int rc = after_launch("mesorasi_ball_query");
+        rc = launch_grid_build(xyz, B, N, radius, w, s, who);
         if (rc != MESORASI_OK) return rc;
-        const int64_t qblocks = ceil_div(BM, kGridQWaves);
-        MESO_REQUIRE(qblocks <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_ball_query: too many queries");
-        const size_t lds = (size_t)kGridQWaves * 64 * ceil_div(ceil_div(N, 32), 64) * 4;
-        // walk or grid: a ball of c candidates holds about 0.155 c points
-        // (sphere over 27 cubes), so a walk scans about K N / (0.155 c);
-        // the two cost the same near c = sqrt(6.45 K N)
-        const int walk_above = (int)std::min(std::sqrt(6.45 * (double)K * (double)N), 2.0e9);
-        grid_query_kernel<<<dim3((unsigned)qblocks), dim3(64 * kGridQWaves), lds, s>>>(
-            xyz, qxyz, BM, (int)N, (int)M, r2, K, walk_above, w, nit, cnt);
-        return after_launch("mesorasi_ball_query");
+        return launch_grid_query(xyz, qxyz, B, N, M, radius, K, nit, cnt, w, s, who);
     }
     if (N >= kBqLdsMinN) {
         // below kBqGridMinN points: 3 N floats of LDS, at most 96 KB
         const int64_t qb = ceil_div(M, kBqLdsWaves);
-        MESO_REQUIRE(B * qb <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_ball_query: too many queries");
+        MESO_REQUIRE(B * qb <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: too many queries", who);
         ball_query_lds_kernel<<<dim3((unsigned)(B * qb)), dim3(64 * kBqLdsWaves), (size_t)N * 12, s>>>(
             xyz, qxyz, (int)N, (int)M, (int)qb, r2, K, nit, cnt);
-        return after_launch("mesorasi_ball_query");
+        return after_launch(who);
     }
     const int64_t blocks = ceil_div(BM, kBqWaves);
-    MESO_REQUIRE(blocks <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_ball_query: too many queries");
+    MESO_REQUIRE(blocks <= 0x7fffffff, MESORASI_EUNSUPPORTED, "%s: too many queries", who);
     ball_query_kernel<<<dim3((unsigned)blocks), dim3(64 * kBqWaves), 0, s>>>(xyz, qxyz, BM, (int)N, (int)M, r2, K,
                                                                             nit, cnt);
-    return after_launch("mesorasi_ball_query");
+    return after_launch(who);
+}
+
+extern "C" size_t mesorasi_ball_query_grid_workspace(int64_t B, int64_t N) {
+    if (B < 0 || N < 0 || N > MESORASI_MAX_N_FPS) return 0;
+    return grid_ws_bytes(B, N);
+}
+
+extern "C" int mesorasi_ball_query_grid_build(const float* xyz, int64_t B, int64_t N, float radius, void* ws,
+                                              size_t ws_bytes, void* stream) {
+    const char* who = "mesorasi_ball_query_grid_build";
+    MESO_REQUIRE(B >= 0 && N >= 0, MESORASI_EINVAL, "%s: negative size", who);
+    MESO_REQUIRE(radius > 0.0f && radius <= 3.0e38f, MESORASI_EINVAL, "%s: radius must be finite and > 0", who);
+    MESO_REQUIRE(N <= MESORASI_MAX_N_FPS, MESORASI_EUNSUPPORTED, "%s: N = %lld > %d", who, (long long)N,
+                 MESORASI_MAX_N_FPS);
+    if (B == 0 || N == 0) return MESORASI_OK;
+    MESO_REQUIRE(xyz, MESORASI_EINVAL, "%s: NULL xyz", who);
+    const size_t need = grid_ws_bytes(B, N);
+    MESO_REQUIRE(ws && ws_bytes >= need, MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who, ws_bytes, need);
+    MESO_REQUIRE(aligned(ws, 256), MESORASI_EINVAL, "%s: workspace not 256-byte aligned", who);
+    return launch_grid_build(xyz, B, N, radius, bq_ws_layout(ws, B, N), as_stream(stream), who);
+}
+
+extern "C" int mesorasi_ball_query_grid(const float* xyz, const float* qxyz, int64_t B, int64_t N, int64_t M,
+                                        float radius, int32_t K, int32_t* nit, int32_t* cnt, const void* ws,
+                                        size_t ws_bytes, void* stream) {
+    const char* who = "mesorasi_ball_query_grid";
+    int rc = check_bq_args(who, xyz, qxyz, B, N, M, radius, K, nit);
+    if (rc != MESORASI_OK || B == 0 || M == 0) return rc;
+    MESO_REQUIRE(N <= MESORASI_MAX_N_FPS, MESORASI_EUNSUPPORTED, "%s: N = %lld > %d", who, (long long)N,
+                 MESORASI_MAX_N_FPS);
+    const size_t need = grid_ws_bytes(B, N);
+    MESO_REQUIRE(ws && ws_bytes >= need, MESORASI_EWORKSPACE, "%s: workspace %zu < %zu bytes", who, ws_bytes, need);
+    MESO_REQUIRE(aligned(ws, 256), MESORASI_EINVAL, "%s: workspace not 256-byte aligned", who);
+    return launch_grid_query(xyz, qxyz, B, N, M, radius, K, nit, cnt, bq_ws_layout(const_cast<void*>(ws), B, N),
+                             as_stream(stream), who);
 }

@@ -31,12 +31,14 @@ from ._lib import F32, BF16
 class Net:
     def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda", debug: bool = False,
                  fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True,
-                 fuse_head: bool = True):
+                 fuse_head: bool = True, bq_grid_min_n: int = 4096):
         self.spec = spec
+        self.bq_grid_min_n = bq_grid_min_n
         self.fuse_aggregation = fuse_aggregation
         self.fuse_head = fuse_head
         self.fp_coarse_min_rows = fp_coarse_min_rows
         self.fps_prefix = fps_prefix
+        self._grid0 = None
         self.delayed = delayed
         self.device = torch.device(device)
         self.dt = BF16 if spec.get("dtype") == "bf16" else F32
@@ -234,12 +236,16 @@ class PointNet2(Net):
         return ev_fps
 
     def _issue_ball_query(self, i, p):
-        """Level i's ball query on the current stream."""
+        """Level i's ball query on the current stream (against the input
+        cloud's prebuilt grid for the first level when there is one)."""
         m = self.spec["sa"][i]
         B, N = p.shape[0], p.shape[1]
         nit = self._buf(f"nit{i}", (B, m["M"], m["K"]), torch.int32)
-        ws = self._ws(f"ws_bq{i}", ops.ball_query_workspace_bytes(B, N, m["M"]))
-        ops.ball_query(p, self._bufs[f"cxyz{i}"], m["radius"], m["K"], out=nit, ws=ws)
+        if i == 0 and self._grid0 is not None:
+            ops.ball_query_grid(p, self._bufs["cxyz0"], m["radius"], m["K"], self._grid0, out=nit)
+        else:
+            ws = self._ws(f"ws_bq{i}", ops.ball_query_workspace_bytes(B, N, m["M"]))
+            ops.ball_query(p, self._bufs[f"cxyz{i}"], m["radius"], m["K"], out=nit, ws=ws)
         self._check_range(f"nit{i}", nit, N)
 
     def _ball_query(self, i, p):
@@ -302,6 +308,13 @@ class PointNet2(Net):
         B = xyz.shape[0]
         main = torch.cuda.current_stream(self.device)
         ev_fps = self._search_chain(xyz, B)
+        # the input cloud binned for the first ball query (main stream, while
+        # the first sampling runs on the side stream)
+        self._grid0 = None
+        if self.spec["sa"] and xyz.shape[1] >= self.bq_grid_min_n:
+            N = xyz.shape[1]
+            ws = self._ws("ws_grid0", ops.ball_query_grid_workspace_bytes(B, N))
+            self._grid0 = ops.ball_query_grid_build(xyz, self.spec["sa"][0]["radius"], ws=ws)
         self._fp_pre(-1, feat)
         levels = [(xyz, feat)]
         p, f = xyz, feat
@@ -500,7 +513,7 @@ class DGCNN(Net):
 
 def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", debug: bool = False,
           fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True,
-          fuse_head: bool = True) -> Net:
+          fuse_head: bool = True, bq_grid_min_n: int = 4096) -> Net:
     """delayed: True (delayed aggregation), False (conventional) or "ltd"
     (limited delayed aggregation).  debug: every search output is checked
     to lie in range before anything reads through it (index_errors()).
@@ -513,8 +526,12 @@ def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", 
     as their first M (mesorasi_fps_prefix, the same result).  fuse_head: the
     last feature-propagation level's remaining layers and the per-point head
     run in one kernel (mesorasi_interpolate3_mlp), so that level's output
-    (``fp{n-1}``) is not materialised."""
-    args = (spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows, fps_prefix, fuse_head)
+    (``fp{n-1}``) is not materialised.  bq_grid_min_n: input clouds of at
+    least this many points are binned for the first ball query while the
+    first sampling runs (mesorasi_ball_query_grid_build), so that query
+    only looks up the cells."""
+    args = (spec, weights, delayed, device, debug, fuse_aggregation, fp_coarse_min_rows, fps_prefix, fuse_head,
+            bq_grid_min_n)
     if spec["kind"] in ("pointnet2_cls", "pointnet2_seg"):
         return PointNet2(*args)
     if spec["kind"] == "dgcnn":

@@ -136,6 +136,39 @@ def ball_query(xyz: torch.Tensor, qxyz: torch.Tensor, radius: float, K: int, wan
     return nit, cnt
 
 
+def ball_query_grid_workspace_bytes(B: int, N: int) -> int:
+    return int(_lib.lib().mesorasi_ball_query_grid_workspace(B, N))
+
+
+def ball_query_grid_build(xyz: torch.Tensor, radius: float, ws: torch.Tensor | None = None) -> torch.Tensor:
+    """Bin the clouds of xyz for ball queries of radius up to `radius`
+    (mesorasi_ball_query_grid_build); returns the workspace holding the grid."""
+    _check_xyz(xyz, "xyz")
+    B, N, _ = xyz.shape
+    need = ball_query_grid_workspace_bytes(B, N)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=xyz.device)
+    check(_lib.lib().mesorasi_ball_query_grid_build(xyz.data_ptr(), B, N, float(radius), ws.data_ptr(), ws.numel(),
+                                                    _stream()), "ball_query_grid_build")
+    return ws
+
+
+def ball_query_grid(xyz: torch.Tensor, qxyz: torch.Tensor, radius: float, K: int, grid: torch.Tensor,
+                    want_cnt: bool = False, out: torch.Tensor | None = None):
+    """ball_query() against a grid from ball_query_grid_build() on the same
+    xyz (mesorasi_ball_query_grid): the same result."""
+    _check_xyz(xyz, "xyz")
+    _check_xyz(qxyz, "qxyz")
+    B, N, _ = xyz.shape
+    M = qxyz.shape[1]
+    nit = out if out is not None else torch.empty((B, M, K), dtype=torch.int32, device=xyz.device)
+    cnt = torch.empty((B, M), dtype=torch.int32, device=xyz.device) if want_cnt else None
+    check(_lib.lib().mesorasi_ball_query_grid(xyz.data_ptr(), qxyz.data_ptr(), B, N, M, float(radius), K,
+                                              nit.data_ptr(), _ptr(cnt), grid.data_ptr(), grid.numel(), _stream()),
+          "ball_query_grid")
+    return nit, cnt
+
+
 def knn(ref: torch.Tensor, query: torch.Tensor, K: int, want_dist: bool = False, out: torch.Tensor | None = None):
     """ref [B, N, >=C], query [B, M, >=C] (last dim contiguous, may be
     column slices of wider tensors); C = ref.shape[-1]."""

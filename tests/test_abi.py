@@ -86,6 +86,27 @@ def test_fps_prefix_levels_validation():
     assert b"M[1] = 11" in _lib.lib().mesorasi_last_error()
 
 
+def test_ball_query_grid_validation():
+    f, b = "mesorasi_ball_query_grid", "mesorasi_ball_query_grid_build"
+    L = _lib.lib()
+    need = L.mesorasi_ball_query_grid_workspace(2, 4096)
+    assert need > 2 * 4096 * 16
+    assert L.mesorasi_ball_query_grid_workspace(2, 70000) == 0
+    assert st(b, FAKE, -1, 10, 0.1, FAKE, 1 << 20, NULL) == _lib.EINVAL            # B < 0
+    assert st(b, FAKE, 1, 10, 0.0, FAKE, 1 << 20, NULL) == _lib.EINVAL             # radius 0
+    assert st(b, NULL, 1, 10, 0.1, FAKE, 1 << 20, NULL) == _lib.EINVAL             # NULL xyz
+    assert st(b, FAKE, 1, 10, 0.1, NULL, 1 << 20, NULL) == _lib.EWORKSPACE         # NULL ws
+    assert st(b, FAKE, 1, 10, 0.1, FAKE, 16, NULL) == _lib.EWORKSPACE              # too small
+    assert st(b, FAKE, 1, 70000, 0.1, FAKE, 1 << 30, NULL) == _lib.EUNSUPPORTED
+    assert st(b, NULL, 0, 10, 0.1, NULL, 0, NULL) == _lib.OK                      # empty batch
+    assert st(f, FAKE, FAKE, 1, 10, 5, 0.1, 0, FAKE, NULL, FAKE, 1 << 20, NULL) == _lib.EINVAL      # K = 0
+    assert st(f, FAKE, FAKE, 1, 10, 5, 0.1, 2000, FAKE, NULL, FAKE, 1 << 20, NULL) == _lib.EUNSUPPORTED
+    assert st(f, FAKE, FAKE, 1, 0, 5, 0.1, 8, FAKE, NULL, FAKE, 1 << 20, NULL) == _lib.EINVAL       # N = 0, M > 0
+    assert st(f, FAKE, FAKE, 1, 10, 5, 0.1, 8, FAKE, NULL, NULL, 1 << 20, NULL) == _lib.EWORKSPACE  # no grid
+    assert st(f, FAKE, FAKE, 1, 10, 5, 0.1, 8, FAKE, NULL, FAKE, 16, NULL) == _lib.EWORKSPACE
+    assert st(f, NULL, NULL, 0, 10, 5, 0.1, 8, NULL, NULL, NULL, 0, NULL) == _lib.OK                # empty batch
+
+
 def test_fps_workspace():
     """Small clouds run one workgroup per cloud and need no workspace; large
     ones exchange winners through one, which must be big enough and 8-byte

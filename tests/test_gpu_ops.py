@@ -191,6 +191,29 @@ BQ_CASES = [
 ]
 
 
+@pytest.mark.parametrize("name,B,N,M,r_build,r,K,kind", [
+    ("seg_sa1", 2, 4096, 1024, 0.1, 0.1, 32, "mesh"),
+    ("lidar_sa1", 1, 16384, 4096, 0.1, 0.1, 64, "lidar"),
+    ("ragged_small", 3, 100, 37, 0.5, 0.5, 8, "normal"),
+    ("grid_boundary_ties", 1, 2000, 300, 1.0, 1.0, 40, "grid"),
+    ("query_radius_above_build", 2, 3000, 200, 0.1, 0.3, 32, "mesh"),   # walks: cells too small
+    ("query_radius_below_build", 2, 3000, 200, 0.3, 0.1, 32, "mesh"),
+])
+def test_ball_query_prebuilt_grid(gpu, name, B, N, M, r_build, r, K, kind):
+    """Binning first and querying later gives mesorasi_ball_query's result
+    bit for bit (and the oracle's), two queries sharing one grid."""
+    x = _points(kind, B, N, g(21))
+    q = x[:, g(22).choice(N, M, replace=False)] if M <= N else x
+    ref, rcnt, _ = O.ball_query(x, q, r, K)
+    grid = ops.ball_query_grid_build(dev(x), r_build)
+    for _ in range(2):
+        nit, cnt = ops.ball_query_grid(dev(x), dev(q), r, K, grid, want_cnt=True)
+        assert np.array_equal(host(nit), ref)
+        assert np.array_equal(host(cnt), rcnt)
+    nit2, _ = ops.ball_query(dev(x), dev(q), r, K)
+    assert torch.equal(nit, nit2)
+
+
 @pytest.mark.parametrize("name,B,N,M,r,K,kind", BQ_CASES, ids=[c[0] for c in BQ_CASES])
 def test_ball_query_bit_exact(gpu, name, B, N, M, r, K, kind):
     rr = g(2)
