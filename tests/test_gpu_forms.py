@@ -39,6 +39,30 @@ def test_fps_one_workgroup_equals_several():
     assert np.array_equal(i1.cpu().numpy(), ri)
 
 
+def test_fps_register_form_equals_lds_form():
+    """512 distinct points (registers only) and the same followed by one
+    copy of point 0 (513: the coordinates also in LDS): the copy's running
+    minimum is 0 from the start, so both give the same samples."""
+    x = g(11).standard_normal((3, 512, 3)).astype(np.float32)
+    xx = np.concatenate([x, x[:, :1]], 1)
+    i1, c1 = ops.fps(dev(x), 300)
+    i2, c2 = ops.fps(dev(xx), 300)
+    assert torch.equal(i1, i2) and torch.equal(c1, c2)
+
+
+def test_ball_query_walk_equals_lds_walk():
+    """2047 points (the walk through the caches) and the same plus one point
+    far away (2048: the cloud copied into LDS first): the far point never
+    falls in a ball, and neither form changes the index order."""
+    r = g(12)
+    x = r.uniform(-1, 1, (2, 2047, 3)).astype(np.float32)
+    xx = np.concatenate([x, np.full((2, 1, 3), 50.0, np.float32)], 1)
+    q = np.ascontiguousarray(x[:, :300])
+    n1, c1 = ops.ball_query(dev(x), dev(q), 0.3, 32, want_cnt=True)
+    n2, c2 = ops.ball_query(dev(xx), dev(q), 0.3, 32, want_cnt=True)
+    assert torch.equal(n1, n2) and torch.equal(c1, c2)
+
+
 def test_knn_register_equals_streaming():
     """1000 references (register form) and the same plus 200 references far
     away (1200: streaming form): the far ones never enter the top 20."""
