@@ -30,7 +30,7 @@ from ._lib import F32, BF16
 
 class Net:
     def __init__(self, spec: dict, weights: dict, delayed: bool = True, device="cuda", debug: bool = False,
-                 fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True,
+                 fuse_aggregation: bool = True, fp_coarse_min_rows: int = 4096, fps_prefix: bool = True,
                  fuse_head: bool = True, bq_grid_min_n: int = 4096):
         self.spec = spec
         self.bq_grid_min_n = bq_grid_min_n
@@ -512,7 +512,7 @@ class DGCNN(Net):
 
 
 def build(spec: dict, weights: dict, delayed: bool | str = True, device="cuda", debug: bool = False,
-          fuse_aggregation: bool = True, fp_coarse_min_rows: int = 16384, fps_prefix: bool = True,
+          fuse_aggregation: bool = True, fp_coarse_min_rows: int = 4096, fps_prefix: bool = True,
           fuse_head: bool = True, bq_grid_min_n: int = 4096) -> Net:
     """delayed: True (delayed aggregation), False (conventional) or "ltd"
     (limited delayed aggregation).  debug: every search output is checked
