@@ -307,17 +307,24 @@ __global__ __launch_bounds__(64 * kGridQWaves) void grid_query_kernel(const floa
     const int x0 = max(cx - 1, 0), x1 = min(cx + 1, gi.g[0] - 1);
     const int y0 = max(cy - 1, 0), y1 = min(cy + 1, gi.g[1] - 1);
     const int z0 = max(cz - 1, 0), z1 = min(cz + 1, gi.g[2] - 1);
-    // candidates in the (up to) nine rows of cells, lane t < 9 one row
-    int cand = 0;
+    // candidates in the (up to) nine rows of cells, lane t < 9 one row:
+    // cells x0 .. x1 of a row are consecutive in the sorted copy, so row t
+    // is the range [rs, rs + rn); rp = the rows' inclusive prefix counts
+    int rs = 0, rn = 0;
     if (x0 <= x1 && lane < 9) {
         const int y = y0 + lane % 3, z = z0 + lane / 3;
         if (y <= y1 && z <= z1) {
             const int row = (z * gi.g[1] + y) * gi.g[0];
-            cand = st[row + x1 + 1] - st[row + x0];
+            rs = st[row + x0];
+            rn = st[row + x1 + 1] - rs;
         }
     }
-    for (int o = 8; o > 0; o >>= 1) cand += __shfl_xor(cand, o);
-    cand = __shfl(cand, 0);
+    int rp = rn;
+    for (int o = 1; o < 16; o <<= 1) {
+        const int t = __shfl_up(rp, o);
+        rp += lane >= o ? t : 0;
+    }
+    const int cand = __shfl(rp, 8);
     // a radius above the one the cells were sized for (a grid built apart,
     // mesorasi_ball_query_grid) walks as well: same result
     if (cand > walk_above || !(radius <= gi.radius)) {
@@ -334,23 +341,28 @@ __global__ __launch_bounds__(64 * kGridQWaves) void grid_query_kernel(const floa
 
     for (int i = 0; i < wpl; ++i) bits[lane * wpl + i] = 0u;
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    if (x0 <= x1) {
-        for (int z = z0; z <= z1; ++z)
-            for (int y = y0; y <= y1; ++y) {
-                // cells x0 .. x1 of this row are consecutive in the sorted copy
-                const int row = (z * gi.g[1] + y) * gi.g[0];
-                const int s = st[row + x0], e = st[row + x1 + 1];
-                for (int i = s + lane; i - lane < e; i += 64) {
-                    bool hit = false;
-                    int j = 0;
-                    if (i < e) {
-                        const float4 pt = pts[i];
-                        j = __float_as_int(pt.w);
-                        hit = dist3(pt.x, pt.y, pt.z, qx, qy, qz) < r2;
-                    }
-                    if (hit) atomicOr(bits + (j >> 5), 1u << (j & 31));
-                }
-            }
+    // every candidate of the nine rows at once, 64 per pass: candidate c
+    // lies in the row whose prefix range holds it (all nine rows' loads in
+    // flight together instead of one row after another)
+    int rend[9], rdelta[9];
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+        rend[t] = __builtin_amdgcn_readlane(rp, t);
+        rdelta[t] = __builtin_amdgcn_readlane(rs, t) - (rend[t] - __builtin_amdgcn_readlane(rn, t));
+    }
+    for (int c0 = 0; c0 < cand; c0 += 64) {
+        const int c = c0 + lane;
+        bool hit = false;
+        int j = 0;
+        if (c < cand) {
+            int i = c + rdelta[8];
+#pragma unroll
+            for (int t = 7; t >= 0; --t) i = c < rend[t] ? c + rdelta[t] : i;
+            const float4 pt = pts[i];
+            j = __float_as_int(pt.w);
+            hit = dist3(pt.x, pt.y, pt.z, qx, qy, qz) < r2;
+        }
+        if (hit) atomicOr(bits + (j >> 5), 1u << (j & 31));
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
 
