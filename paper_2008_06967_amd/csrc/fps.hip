@@ -32,10 +32,12 @@
 // (four waves per SIMD at 16 points per thread) and by the reduction chain
 // for small P.
 //
-// From 513 to 16384 points fps_lds_kernel keeps a copy of the coordinates
+// From 513 to 8192 points fps_lds_kernel keeps a copy of the coordinates
 // in LDS as well, so the winners are exchanged as (distance, index) and the
-// new centroid is read from LDS after the block reduction; above 32768
-// points fps_multi_kernel spreads a cloud over several workgroups.
+// new centroid is read from LDS after the block reduction; from 8193 to
+// 16384 points fps_skip_kernel orders the cloud spatially and skips the
+// updates that provably change nothing; above 32768 points fps_multi_kernel
+// spreads a cloud over several workgroups.
 #include <algorithm>
 
 #include "common.h"
@@ -228,26 +230,23 @@ __global__ __launch_bounds__(T) void fps_kernel(const float* __restrict__ xyz, i
     }
 }
 
-// Clouds of 513 to 16384 points: a copy of the cloud's coordinates in LDS.
+// Clouds of 513 to 8192 points: a copy of the cloud's coordinates in LDS.
 // A wave's winner is then published as (distance bits, index) -- by lane
 // 0, both values being wave-uniform -- and after the block reduction every
 // wave reads the new centroid's coordinates from LDS at the winning index
 // (one broadcast read), instead of the winning lane selecting them among
 // its P register slots before the barrier (a chain of selects on the
 // iteration's critical path: 15 % of an iteration at 4096 points, 27 % at
-// 8192).  Above 8192 points the whole cloud does not fit beside the ring:
-// x and y live in LDS and the winning lane publishes z with its slot.
-// Everything else -- the update, the wave reduction, the slot search, the
+// 8192).  Everything else -- the update, the wave reduction, the slot search, the
 // ring of per-wave winners resolved every 64 iterations -- is as in
 // fps_kernel.
-template <int T, int P, bool Z_SLOT>
+template <int T, int P>
 __global__ __launch_bounds__(T) void fps_lds_kernel(const float* __restrict__ xyz, int N, int M,
                                                     int32_t* __restrict__ idx, float* __restrict__ cxyz) {
     constexpr int W = T / 64;
     constexpr int R = 128;                 // ring rows (two result blocks of 64 iterations)
-    constexpr int NC = Z_SLOT ? 2 : 3;     // coordinates per point held in LDS
+    constexpr int NC = 3;                  // coordinates per point held in LDS
     __shared__ int2 s_slot[R][W];          // per-wave winner of iteration m in row m % R: distance bits, index
-    __shared__ float s_z[Z_SLOT ? R : 1][W];
     __shared__ float s_c[T * P * NC];
 
     const int b = blockIdx.x;
@@ -270,11 +269,10 @@ __global__ __launch_bounds__(T) void fps_lds_kernel(const float* __restrict__ xy
         dm[q] = ok ? __builtin_huge_valf() : -1.0f;  // +inf for real points; -1 never wins
         s_c[NC * j + 0] = px[q];
         s_c[NC * j + 1] = py[q];
-        if constexpr (!Z_SLOT) s_c[NC * j + 2] = pz[q];
+        s_c[NC * j + 2] = pz[q];
     }
     __syncthreads();
     float cx = p[0], cy = p[1], cz = p[2];
-    const float z0 = cz;
 
     // lane l of wave 0 resolves iteration (m_last & ~63) + l from the ring
     // and stores it (iteration 0 is point 0)
@@ -295,8 +293,7 @@ __global__ __launch_bounds__(T) void fps_lds_kernel(const float* __restrict__ xy
             if (out_c) {
                 out_c[3 * mi + 0] = s_c[NC * sel + 0];
                 out_c[3 * mi + 1] = s_c[NC * sel + 1];
-                if constexpr (Z_SLOT) out_c[3 * mi + 2] = first ? z0 : s_z[row][bw];
-                else out_c[3 * mi + 2] = s_c[NC * sel + 2];
+                out_c[3 * mi + 2] = s_c[NC * sel + 2];
             }
         }
     };
@@ -320,23 +317,12 @@ __global__ __launch_bounds__(T) void fps_lds_kernel(const float* __restrict__ xy
         const int wl = __builtin_ctzll(ballot(tmax == wmax));
         const int sq = __builtin_amdgcn_readlane(ls, wl);
         const int buf = m & (R - 1);
-        if constexpr (Z_SLOT) {
-            if (lane == wl) {
-                s_slot[buf][wave] = make_int2(wmax, base + sq);
-                s_z[buf][wave] = pz[sq];
-            }
-        } else {
-            if (lane == 0) s_slot[buf][wave] = make_int2(wmax, wave * 64 * P + wl * P + sq);
-        }
+        if (lane == 0) s_slot[buf][wave] = make_int2(wmax, wave * 64 * P + wl * P + sq);
         __syncthreads();
         // 3. block winner: lane w < W inspects wave w's slot; the new
         //    centroid's coordinates from LDS
         int2 sl = make_int2(INT32_MIN, 0);
-        float slz = 0.0f;
-        if (lane < W) {
-            sl = s_slot[buf][lane];
-            if constexpr (Z_SLOT) slz = s_z[buf][lane];
-        }
+        if (lane < W) sl = s_slot[buf][lane];
         int gm;
         if constexpr (W <= 8) gm = __builtin_amdgcn_readlane(oct_max_i32(sl.x), 7);
         else gm = __builtin_amdgcn_readlane(row_max_i32(sl.x), 0);
@@ -344,17 +330,325 @@ __global__ __launch_bounds__(T) void fps_lds_kernel(const float* __restrict__ xy
         const int sel = __builtin_amdgcn_readlane(sl.y, ww);
         cx = s_c[NC * sel + 0];
         cy = s_c[NC * sel + 1];
-        if constexpr (Z_SLOT) cz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(slz), ww));
-        else cz = s_c[NC * sel + 2];
+        cz = s_c[NC * sel + 2];
         if (wave == 0 && (m & 63) == 63) resolve(m);
     }
     if (wave == 0 && ((M - 1) & 63) != 63) resolve(M - 1);
 }
 
-template <int T, int P, bool Z_SLOT>
+template <int T, int P>
 static void launch_fps_lds(const float* xyz, int64_t B, int N, int M, int32_t* idx, float* cxyz, hipStream_t s) {
     static_assert(T >= 256 && T <= 1024 && T % 64 == 0, "4 to 16 waves");
-    fps_lds_kernel<T, P, Z_SLOT><<<dim3((unsigned)B), dim3(T), 0, s>>>(xyz, N, M, idx, cxyz);
+    fps_lds_kernel<T, P><<<dim3((unsigned)B), dim3(T), 0, s>>>(xyz, N, M, idx, cxyz);
+}
+
+
+// ---------------------------------------------------------------------------
+// Clouds of 8193 to 16384 points: spatial order and exact skipping.
+//
+// At 16 points per thread and four waves per SIMD the update of every
+// running minimum is most of an iteration (VALU issue on the cloud's one
+// CU), yet only the points near the newest centroid can change.  This form
+// first puts the cloud in spatial order -- a counting sort of the points by
+// the Morton code of their cell in a 16^3 grid over the cloud's box -- and
+// gives thread t the P consecutive points [t P, t P + P) of that order, so
+// each thread's points are close together.  Each thread keeps the box of its
+// points; a wave skips the update when, for every one of its threads, a
+// lower bound of the distance from the centroid to the thread's box is at
+// least the thread's largest running minimum.  The bound is computed with
+// the distance's own operations in the same order (dist3) on the per-axis
+// gaps between the centroid and the box, max(lo - c, c - hi, 0): every
+// operation is monotone in its operands and each gap is at most the
+// corresponding |point - c| after rounding, so the bound never exceeds the
+// distance the update would compute, and a skipped update is exactly the
+// one that would have changed nothing.  Results are bit-identical to the
+// other forms.
+//
+// Lowest index on ties: within a thread the points are sorted by original
+// index at set-up, so the first slot holding the thread's maximum is its
+// lowest; between lanes and between waves a tie is detected (two lanes or
+// waves holding the maximum) and decided on the original index.  A wave's
+// winner is published as (distance bits, position, original index, z); x
+// and y of every position stay in LDS (the full coordinates of 16384 points
+// would not fit beside the ring).
+// ---------------------------------------------------------------------------
+
+// Float min / max over the wave (all lanes active), uniform result.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+__device__ __forceinline__ float wave_min_f32(float v) {
+    v = fminf(v, dpp_f32<0x121>(v));
+    v = fminf(v, dpp_f32<0x122>(v));
+    v = fminf(v, dpp_f32<0x124>(v));
+    v = fminf(v, dpp_f32<0x128>(v));
+    v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x142, 0xa, 0xf, false)));
+    v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x143, 0xc, 0xf, false)));
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ __forceinline__ float wave_max_f32(float v) {
+    v = fmaxf(v, dpp_f32<0x121>(v));
+    v = fmaxf(v, dpp_f32<0x122>(v));
+    v = fmaxf(v, dpp_f32<0x124>(v));
+    v = fmaxf(v, dpp_f32<0x128>(v));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x142, 0xa, 0xf, false)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x143, 0xc, 0xf, false)));
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+// Int min over the wave (rare tie paths only).
+__device__ __forceinline__ int wave_min_i32_shfl(int v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = min(v, __shfl_xor(v, o));
+    return v;
+}
+
+// 4-bit cell coordinate -> every third bit of a 12-bit Morton code.
+__device__ __forceinline__ uint32_t morton_spread4(uint32_t v) {
+    v &= 0xfu;
+    v = (v | (v << 4)) & 0x0c3u;
+    v = (v | (v << 2)) & 0x249u;
+    return v;
+}
+
+template <int T, int P>
+__global__ __launch_bounds__(T) void fps_skip_kernel(const float* __restrict__ xyz, int N, int M,
+                                                     int32_t* __restrict__ idx, float* __restrict__ cxyz) {
+    constexpr int W = T / 64;
+    constexpr int NP = T * P;
+    constexpr int R = 64;                // ring rows: two result blocks of 32 iterations
+    constexpr int G = 16;                // grid cells per axis
+    constexpr int NCELL = G * G * G;
+    constexpr int CPT = NCELL / T;       // cells per thread in the scan
+    static_assert(NCELL % T == 0 && NCELL <= NP && W <= 16, "shape");
+    __shared__ float2 s_xy[NP];          // x, y of each position (set-up: the permutation, then the histogram)
+    __shared__ int4 s_ring[R][W];        // wave winner of iteration m in row m % R: dist bits, position, index, z
+    __shared__ float s_red[6][W];
+    __shared__ int s_wsum[W];
+    int* s_perm = reinterpret_cast<int*>(s_xy);
+    int* s_hist = s_perm + NP;
+
+    const int b = blockIdx.x;
+    const float* __restrict__ p = xyz + (int64_t)b * N * 3;
+    int32_t* __restrict__ out_idx = idx + (int64_t)b * M;
+    float* __restrict__ out_c = cxyz ? cxyz + (int64_t)b * M * 3 : nullptr;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int base = tid * P;
+
+    float px[P], py[P], pz[P], dm[P];
+    int oi[P];   // original indices (the cell codes during the sort)
+    {
+        // 1. the cloud's box
+        float mnx = __builtin_huge_valf(), mny = mnx, mnz = mnx, mxx = -mnx, mxy = -mnx, mxz = -mnx;
+        for (int j = tid; j < N; j += T) {   // the points are read again for their cells
+            const float x = p[3 * j + 0], y = p[3 * j + 1], z = p[3 * j + 2];
+            mnx = fminf(mnx, x); mxx = fmaxf(mxx, x);
+            mny = fminf(mny, y); mxy = fmaxf(mxy, y);
+            mnz = fminf(mnz, z); mxz = fmaxf(mxz, z);
+        }
+        mnx = wave_min_f32(mnx); mny = wave_min_f32(mny); mnz = wave_min_f32(mnz);
+        mxx = wave_max_f32(mxx); mxy = wave_max_f32(mxy); mxz = wave_max_f32(mxz);
+        if (lane == 0) {
+            s_red[0][wave] = mnx; s_red[1][wave] = mny; s_red[2][wave] = mnz;
+            s_red[3][wave] = mxx; s_red[4][wave] = mxy; s_red[5][wave] = mxz;
+        }
+        for (int c = tid; c < NCELL; c += T) s_hist[c] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            mnx = fminf(mnx, s_red[0][w]); mny = fminf(mny, s_red[1][w]); mnz = fminf(mnz, s_red[2][w]);
+            mxx = fmaxf(mxx, s_red[3][w]); mxy = fmaxf(mxy, s_red[4][w]); mxz = fmaxf(mxz, s_red[5][w]);
+        }
+        const float ix = mxx > mnx ? (float)G / (mxx - mnx) : 0.0f;
+        const float iy = mxy > mny ? (float)G / (mxy - mny) : 0.0f;
+        const float iz = mxz > mnz ? (float)G / (mxz - mnz) : 0.0f;
+        // 2. cell histogram (the cell only orders the points: any cell,
+        //    even of a non-finite coordinate, keeps the result exact)
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            const int j = tid + q * T;
+            const int jj = j < N ? j : 0;
+            const uint32_t gx = (uint32_t)fminf(fmaxf((p[3 * jj + 0] - mnx) * ix, 0.0f), (float)(G - 1));
+            const uint32_t gy = (uint32_t)fminf(fmaxf((p[3 * jj + 1] - mny) * iy, 0.0f), (float)(G - 1));
+            const uint32_t gz = (uint32_t)fminf(fmaxf((p[3 * jj + 2] - mnz) * iz, 0.0f), (float)(G - 1));
+            oi[q] = (int)(morton_spread4(gx) | (morton_spread4(gy) << 1) | (morton_spread4(gz) << 2));
+            if (j < N) atomicAdd(&s_hist[oi[q]], 1);
+        }
+        __syncthreads();
+        // 3. exclusive scan of the counts
+        int cnt[CPT], run = 0;
+#pragma unroll
+        for (int k = 0; k < CPT; ++k) {
+            cnt[k] = s_hist[tid * CPT + k];
+            run += cnt[k];
+        }
+        int incl = run;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int v = __shfl_up(incl, o);
+            if (lane >= o) incl += v;
+        }
+        if (lane == 63) s_wsum[wave] = incl;
+        __syncthreads();
+        int off = incl - run;
+        for (int w = 0; w < wave; ++w) off += s_wsum[w];
+#pragma unroll
+        for (int k = 0; k < CPT; ++k) {
+            s_hist[tid * CPT + k] = off;
+            off += cnt[k];
+        }
+        for (int j = N + tid; j < NP; j += T) s_perm[j] = INT32_MAX;   // padding positions
+        __syncthreads();
+        // 4. scatter the original indices into cell order
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            const int j = tid + q * T;
+            if (j < N) s_perm[atomicAdd(&s_hist[oi[q]], 1)] = j;
+        }
+        __syncthreads();
+        // 5. this thread's positions, ascending in original index
+        //    (odd-even transposition sort)
+#pragma unroll
+        for (int q = 0; q < P; ++q) oi[q] = s_perm[base + q];
+#pragma unroll
+        for (int r = 0; r < P; ++r) {
+#pragma unroll
+            for (int q = r & 1; q + 1 < P; q += 2) {
+                const int lo = min(oi[q], oi[q + 1]), hi = max(oi[q], oi[q + 1]);
+                oi[q] = lo;
+                oi[q + 1] = hi;
+            }
+        }
+        __syncthreads();   // the permutation is read; its space becomes s_xy
+    }
+    float bnx = __builtin_huge_valf(), bny = bnx, bnz = bnx, bxx = -bnx, bxy = -bnx, bxz = -bnx;
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+        const bool ok = oi[q] != INT32_MAX;
+        const int j = ok ? oi[q] : 0;
+        px[q] = ok ? p[3 * j + 0] : 0.0f;
+        py[q] = ok ? p[3 * j + 1] : 0.0f;
+        pz[q] = ok ? p[3 * j + 2] : 0.0f;
+        dm[q] = ok ? __builtin_huge_valf() : -1.0f;   // +inf for real points; -1 never wins
+        s_xy[base + q] = make_float2(px[q], py[q]);
+        if (ok) {
+            bnx = fminf(bnx, px[q]); bxx = fmaxf(bxx, px[q]);
+            bny = fminf(bny, py[q]); bxy = fmaxf(bxy, py[q]);
+            bnz = fminf(bnz, pz[q]); bxz = fmaxf(bxz, pz[q]);
+        }
+    }
+
+    // this thread's largest running minimum; the wave's winner
+    int tmax = 0, wmax = 0, wpos = 0, woi = 0;
+    float wz = 0.0f;
+    auto select = [&]() {
+        tmax = __float_as_int(dm[0]);
+#pragma unroll
+        for (int q = 1; q < P; ++q) tmax = max(tmax, __float_as_int(dm[q]));
+        int ls = P - 1, lo = oi[P - 1];
+        float lz = pz[P - 1];
+#pragma unroll
+        for (int q = P - 2; q >= 0; --q) {
+            const bool e = __float_as_int(dm[q]) == tmax;
+            ls = e ? q : ls;
+            lo = e ? oi[q] : lo;
+            lz = e ? pz[q] : lz;
+        }
+        const int wm = wave_max_i32(tmax);
+        const uint64_t tie = ballot(tmax == wm);
+        int wl = __builtin_ctzll(tie);
+        if (tie & (tie - 1)) {
+            const int key = tmax == wm ? lo : INT32_MAX;
+            wl = __builtin_ctzll(ballot(key == wave_min_i32_shfl(key)));
+        }
+        wmax = wm;
+        wpos = (wave * 64 + wl) * P + __builtin_amdgcn_readlane(ls, wl);
+        woi = __builtin_amdgcn_readlane(lo, wl);
+        wz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lz), wl));
+    };
+    select();
+    __syncthreads();   // s_xy complete
+
+    const float x0 = p[0], y0 = p[1], z0 = p[2];
+    float cx = x0, cy = y0, cz = z0;
+
+    // lane l < 32 of wave 0 resolves iteration (m_last & ~31) + l from the
+    // ring (highest distance, then lowest index) and stores it
+    auto resolve = [&](int m_last) {
+        if (lane < 32) {
+            const int mi = (m_last & ~31) + lane;
+            const int row = mi & (R - 1);
+            int best = INT32_MIN, boi = INT32_MAX, bw = 0;
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+                const int4 e = s_ring[row][w];
+                const bool better = e.x > best || (e.x == best && e.z < boi);
+                best = better ? e.x : best;
+                boi = better ? e.z : boi;
+                bw = better ? w : bw;
+            }
+            if (mi <= m_last) {
+                const bool first = mi == 0;
+                out_idx[mi] = first ? 0 : boi;
+                if (out_c) {
+                    const int4 e = s_ring[row][bw];
+                    const float2 xy = s_xy[e.y];
+                    out_c[3 * mi + 0] = first ? x0 : xy.x;
+                    out_c[3 * mi + 1] = first ? y0 : xy.y;
+                    out_c[3 * mi + 2] = first ? z0 : __int_as_float(e.w);
+                }
+            }
+        }
+    };
+
+    for (int m = 1; m < M; ++m) {
+        // 1. skip test against this thread's box, then the update
+        const float gx = fmaxf(fmaxf(bnx - cx, cx - bxx), 0.0f);
+        const float gy = fmaxf(fmaxf(bny - cy, cy - bxy), 0.0f);
+        const float gz = fmaxf(fmaxf(bnz - cz, cz - bxz), 0.0f);
+        float lb = gx * gx;
+        lb = __builtin_fmaf(gy, gy, lb);
+        lb = __builtin_fmaf(gz, gz, lb);
+        if (ballot(__float_as_int(lb) < tmax)) {
+#pragma unroll
+            for (int q = 0; q < P; ++q)
+                dm[q] = __int_as_float(
+                    min(__float_as_int(dist3(px[q], py[q], pz[q], cx, cy, cz)), __float_as_int(dm[q])));
+            select();
+        }
+        // 2. publish the wave's winner; block winner; the new centroid
+        const int buf = m & (R - 1);
+        if (lane == 0) s_ring[buf][wave] = make_int4(wmax, wpos, woi, __float_as_int(wz));
+        __syncthreads();
+        int4 e = make_int4(INT32_MIN, 0, INT32_MAX, 0);
+        if (lane < W) e = s_ring[buf][lane];
+        int gm;
+        if constexpr (W <= 8) gm = __builtin_amdgcn_readlane(oct_max_i32(e.x), 7);
+        else gm = __builtin_amdgcn_readlane(row_max_i32(e.x), 0);
+        const uint64_t eq = ballot(e.x == gm) & ((1ull << W) - 1);
+        int ww = __builtin_ctzll(eq);
+        if (eq & (eq - 1)) {
+            const int key = (lane < W && e.x == gm) ? e.z : INT32_MAX;
+            ww = __builtin_ctzll(ballot(key == wave_min_i32_shfl(key)));
+        }
+        const int sel = __builtin_amdgcn_readlane(e.y, ww);
+        cz = __int_as_float(__builtin_amdgcn_readlane(e.w, ww));
+        const float2 xy = s_xy[sel];
+        cx = xy.x;
+        cy = xy.y;
+        if (wave == 0 && (m & 31) == 31) resolve(m);
+    }
+    if (wave == 0 && ((M - 1) & 31) != 31) resolve(M - 1);
+}
+
+template <int T, int P>
+static void launch_fps_skip(const float* xyz, int64_t B, int N, int M, int32_t* idx, float* cxyz, hipStream_t s) {
+    fps_skip_kernel<T, P><<<dim3((unsigned)B), dim3(T), 0, s>>>(xyz, N, M, idx, cxyz);
 }
 
 template <int T, int P, bool REG>
@@ -673,11 +967,11 @@ extern "C" int mesorasi_fps(const float* xyz, int64_t B, int64_t N, int64_t M, i
     if (n <= 128) launch_fps<64, 2, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 256) launch_fps<64, 4, true>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 512) launch_fps<256, 2, true>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 1024) launch_fps_lds<256, 4, false>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 2048) launch_fps_lds<512, 4, false>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 4096) launch_fps_lds<512, 8, false>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 8192) launch_fps_lds<1024, 8, false>(xyz, B, n, m, idx, cxyz, s);
-    else if (n <= 16384) launch_fps_lds<1024, 16, true>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 1024) launch_fps_lds<256, 4>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 2048) launch_fps_lds<512, 4>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 4096) launch_fps_lds<512, 8>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 8192) launch_fps_lds<1024, 8>(xyz, B, n, m, idx, cxyz, s);
+    else if (n <= 16384) launch_fps_skip<1024, 16>(xyz, B, n, m, idx, cxyz, s);
     else if (n <= 32768) launch_fps<1024, 32, false>(xyz, B, n, m, idx, cxyz, s);
     else launch_fps<1024, 64, false>(xyz, B, n, m, idx, cxyz, s);
     return after_launch("mesorasi_fps");

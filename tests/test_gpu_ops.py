@@ -68,8 +68,16 @@ FPS_CASES = [
     ("lds_m65", 2, 2048, 65, "mesh"),                  # one result block plus one
     ("lds_grid_ties", 2, 4096, 1500, "grid"),          # 64 distinct points: ties across waves, zero steps
     ("lds_dups", 1, 8192, 2048, "dups"),
-    ("lds_z_slot_grid", 1, 12000, 700, "grid"),        # above 8192 points: z published with the slot
-    ("lds_z_slot_ragged", 3, 8193, 300, "normal"),
+    # 8193 .. 16384 points: spatial order, updates skipped by the box bound
+    ("skip_grid_ties", 1, 12000, 700, "grid"),         # equal distances across lanes and waves
+    ("skip_ragged", 3, 8193, 300, "normal"),           # one real point in the last thread
+    ("skip_m_eq_n", 1, 9000, 9000, "normal"),          # every point, minima down to 0
+    ("skip_dups", 1, 16384, 2048, "dups"),             # duplicates: ties inside one thread's slots
+    ("skip_same", 1, 10000, 100, "same"),              # one point repeated: every minimum 0 after one step
+    ("skip_m33", 2, 16000, 33, "cube"),                # one result block of 32 plus one
+    ("skip_m1", 2, 16384, 1, "normal"),
+    ("skip_mesh", 2, 16384, 3000, "mesh"),
+    ("skip_far_outlier", 1, 12000, 500, "outlier"),    # one point 1e6 away: a coarse grid
     ("lidar_sa1", 1, 16384, 4096, "lidar"),
     ("n20000", 1, 20000, 64, "normal"),
     ("n32768_global_path", 1, 32768, 40, "normal"),   # coordinates re-read from memory per iteration
@@ -97,6 +105,12 @@ def _points(kind, B, N, r):
         return synth.mesh_surfaces(r, B, N)
     if kind == "lidar":
         return synth.lidar_scene(r, B, N)
+    if kind == "same":
+        return np.broadcast_to(r.standard_normal((B, 1, 3)).astype(np.float32), (B, N, 3)).copy()
+    if kind == "outlier":
+        x = r.standard_normal((B, N, 3)).astype(np.float32)
+        x[:, N // 2] = 1e6
+        return x
     return r.standard_normal((B, N, 3)).astype(np.float32)
 
 
