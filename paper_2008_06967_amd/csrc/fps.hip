@@ -414,6 +414,12 @@ __device__ __forceinline__ uint32_t morton_spread4(uint32_t v) {
     return v;
 }
 
+template <int P>
+struct RegVec {
+    typedef float f32 __attribute__((ext_vector_type(P)));
+    typedef int i32 __attribute__((ext_vector_type(P)));
+};
+
 template <int T, int P>
 __global__ __launch_bounds__(T) void fps_skip_kernel(const float* __restrict__ xyz, int N, int M,
                                                      int32_t* __restrict__ idx, float* __restrict__ cxyz) {
@@ -440,8 +446,11 @@ __global__ __launch_bounds__(T) void fps_skip_kernel(const float* __restrict__ x
     const int wave = tid >> 6;
     const int base = tid * P;
 
-    float px[P], py[P], pz[P], dm[P];
-    int oi[P];   // original indices (the cell codes during the sort)
+    // z and the original indices are vectors: the winner's are read out with
+    // a wave-uniform index (one indexed register move, not a select chain)
+    float px[P], py[P], dm[P];
+    typename RegVec<P>::f32 pz;
+    typename RegVec<P>::i32 oi;   // original indices (the cell codes during the sort)
     {
         // 1. the cloud's box
         float mnx = __builtin_huge_valf(), mny = mnx, mnz = mnx, mxx = -mnx, mxy = -mnx, mxz = -mnx;
@@ -550,26 +559,24 @@ __global__ __launch_bounds__(T) void fps_skip_kernel(const float* __restrict__ x
         tmax = __float_as_int(dm[0]);
 #pragma unroll
         for (int q = 1; q < P; ++q) tmax = max(tmax, __float_as_int(dm[q]));
-        int ls = P - 1, lo = oi[P - 1];
-        float lz = pz[P - 1];
+        int ls = P - 1;
 #pragma unroll
-        for (int q = P - 2; q >= 0; --q) {
-            const bool e = __float_as_int(dm[q]) == tmax;
-            ls = e ? q : ls;
-            lo = e ? oi[q] : lo;
-            lz = e ? pz[q] : lz;
-        }
+        for (int q = P - 2; q >= 0; --q) ls = __float_as_int(dm[q]) == tmax ? q : ls;
         const int wm = wave_max_i32(tmax);
         const uint64_t tie = ballot(tmax == wm);
         int wl = __builtin_ctzll(tie);
-        if (tie & (tie - 1)) {
+        if (tie & (tie - 1)) {   // two lanes hold the maximum: the lower original index
+            int lo = oi[P - 1];
+#pragma unroll
+            for (int q = P - 2; q >= 0; --q) lo = ls == q ? oi[q] : lo;
             const int key = tmax == wm ? lo : INT32_MAX;
             wl = __builtin_ctzll(ballot(key == wave_min_i32_shfl(key)));
         }
+        const int sq = __builtin_amdgcn_readlane(ls, wl);
         wmax = wm;
-        wpos = (wave * 64 + wl) * P + __builtin_amdgcn_readlane(ls, wl);
-        woi = __builtin_amdgcn_readlane(lo, wl);
-        wz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lz), wl));
+        wpos = (wave * 64 + wl) * P + sq;
+        woi = __builtin_amdgcn_readlane(oi[sq], wl);
+        wz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pz[sq]), wl));
     };
     select();
     __syncthreads();   // s_xy complete
