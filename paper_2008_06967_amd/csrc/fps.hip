@@ -667,7 +667,8 @@ static void launch_fps(const float* xyz, int64_t B, int N, int M, int32_t* idx, 
 // Large clouds: G one-wave workgroups per cloud.
 //
 // One CU's vector ALUs bound the single-workgroup kernel once every thread
-// holds 16 points (16384-point clouds: about 1.3 us per iteration).  Here
+// holds 16 points (16384-point clouds: about 1.3 us per iteration when every
+// point is updated, 0.8 us with the skipping of fps_skip_kernel).  Here
 // the points are spread over G single-wave workgroups (workgroup g owns the
 // contiguous points [64 P g, 64 P (g + 1)), lane l the P points from
 // 64 P g + P l), so an iteration's update is P points per lane on G CUs,
@@ -855,8 +856,8 @@ static FpsMultiPlan fps_multi_plan(int64_t N) {
 // iteration there, 4.6 us here).  Below, one exchange through global memory
 // (about 0.7 us for one tagged word between CUs, 2-2.5 us for this
 // kernel's four-word slots, measured on MI355X) costs more than a whole
-// single-workgroup iteration (0.63 us at 4096 points, 1.29 us at 16384, 2.66
-// us at 32768 against 2.72 us here).
+// single-workgroup iteration (0.46 us at 4096 points, 0.8 us at 16384 with
+// skipping, 2.66 us at 32768 against 2.72 us here).
 constexpr int64_t kFpsMultiMinN = 32769;
 
 static bool fps_use_multi(int64_t N, int64_t M) {
