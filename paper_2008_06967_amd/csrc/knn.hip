@@ -473,6 +473,7 @@ constexpr int kKnnMfmaLda = 1024 + 8;          // a-table row stride (entries)
 constexpr int kKnnMfmaMaxN = 1024;
 
 typedef float knn_f32x16 __attribute__((ext_vector_type(16)));
+typedef float knn_f32x4 __attribute__((ext_vector_type(4)));
 
 // Four consecutive table entries as float (bf16 or fp32 table).
 __device__ __forceinline__ void load_bounds4(const uint16_t* p, float (&a)[4]) {
@@ -490,36 +491,38 @@ __device__ __forceinline__ void load_bounds4(const float* p, float (&a)[4]) {
     a[3] = v.w;
 }
 
-template <int CH>   // maximum C / 2 (32 or 64)
+template <int CH, int QB = kKnnQpb>   // maximum C / 2 (32 or 64); queries per workgroup (32 or 16)
 __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* __restrict__ ref, int64_t ldr,
                                                                   const float* __restrict__ query, int64_t ldq,
                                                                   int N, int M, int C, int K, int qblocks,
                                                                   int32_t* __restrict__ nit,
                                                                   float* __restrict__ dist) {
     constexpr bool BF = CH <= 32;                        // bf16 table
+    constexpr int QPW = QB / kKnnWaves;                  // queries per wave
+    static_assert(QB == 32 || (QB == 16 && !BF), "32 queries, or 16 with the fp32 table");
     using TabT = std::conditional_t<BF, uint16_t, float>;
     extern __shared__ float smem[];
     TabT* sA = reinterpret_cast<TabT*>(smem);            // [32][kKnnMfmaLda] bounds
     const int CQ = C + 4;                                // query row stride: 16-byte lane reads of
                                                          // 32 rows land on distinct bank groups
-    float* sQ = smem + kKnnQpb * kKnnMfmaLda * sizeof(TabT) / sizeof(float);   // [32][CQ]
-    float* sNy = sQ + kKnnQpb * CQ;                      // [1024]
+    float* sQ = smem + QB * kKnnMfmaLda * sizeof(TabT) / sizeof(float);   // [32][CQ]
+    float* sNy = sQ + QB * CQ;                      // [1024]
     float* sNx = sNy + kKnnMfmaMaxN;                     // [32]
     uint16_t* sCj = reinterpret_cast<uint16_t*>(sNy);    // [kKnnWaves][4][64], after the norms are read
     const int64_t b = blockIdx.x / qblocks;
-    const int q0 = (blockIdx.x % qblocks) * kKnnQpb;
+    const int q0 = (blockIdx.x % qblocks) * QB;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const float inf = __builtin_huge_valf();
     const int HC = C / 2;
 
     // 0. queries into LDS, their squared norms
-    for (int e = tid; e < kKnnQpb * C; e += 64 * kKnnWaves) {
+    for (int e = tid; e < QB * C; e += 64 * kKnnWaves) {
         const int qq = e / C, c = e - qq * C;
         const int qi = q0 + qq;
         sQ[qq * CQ + c] = qi < M ? query[(b * M + qi) * ldq + c] : 0.0f;
     }
     __syncthreads();
-    if (tid < kKnnQpb) {
+    if (tid < QB) {
         float nx = 0.0f;
         for (int c = 0; c < C; ++c) nx = __builtin_fmaf(sQ[tid * CQ + c], sQ[tid * CQ + c], nx);
         sNx[tid] = nx;
@@ -570,7 +573,46 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
             else sA[i * kKnnMfmaLda + j] = av;
         }
     };
-    if constexpr (CH <= 32) {
+    if constexpr (QB == 16) {
+        // 16 x 16 blocks on v_mfma_f32_16x16x4_f32: lane l holds reference
+        // row 16 blk + l % 16 and query row l % 16 for the channel quarter
+        // l / 16 (C % 16 == 0), step s takes channel s of each quarter; the
+        // accumulator holds query 4 (l / 16) + r, reference l % 16
+        const int QC = C / 4;
+        const float* qa4 = sQ + (lane & 15) * CQ + (lane >> 4) * QC;
+        const int nblk16 = (N + 15) / 16;
+        for (int blk = wave; blk < nblk16; blk += kKnnWaves) {
+            const int j = blk * 16 + (lane & 15);
+            const bool valid = j < N;
+            const float* rr = ref + (b * N + (valid ? j : N - 1)) * ldr + (lane >> 4) * QC;
+            float bv[CH / 2];
+#pragma unroll
+            for (int s4 = 0; s4 < CH / 8; ++s4) {
+                const float4 v = s4 * 4 < QC ? *reinterpret_cast<const float4*>(rr + 4 * s4) : make_float4(0.f, 0.f, 0.f, 0.f);
+                bv[4 * s4] = v.x; bv[4 * s4 + 1] = v.y; bv[4 * s4 + 2] = v.z; bv[4 * s4 + 3] = v.w;
+            }
+            float nyq = 0.0f;
+#pragma unroll
+            for (int k = 0; k < CH / 2; ++k) nyq = __builtin_fmaf(bv[k], bv[k], nyq);
+            const float ny2 = nyq + __shfl_xor(nyq, 16);
+            const float ny = ny2 + __shfl_xor(ny2, 32);
+            knn_f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int s4 = 0; s4 < CH / 8; ++s4) {
+                const float4 qv = s4 * 4 < QC ? *reinterpret_cast<const float4*>(qa4 + 4 * s4) : make_float4(0.f, 0.f, 0.f, 0.f);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qv.x, bv[4 * s4], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qv.y, bv[4 * s4 + 1], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qv.z, bv[4 * s4 + 2], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qv.w, bv[4 * s4 + 3], acc, 0, 0, 0);
+            }
+            if (lane < 16 && valid) sNy[j] = ny;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int i = 4 * (lane >> 4) + r;
+                sA[i * kKnnMfmaLda + j] = valid ? __builtin_fmaf(-2.0f, acc[r], sNx[i] + ny) : inf;
+            }
+        }
+    } else if constexpr (CH <= 32) {
         float b0[CH], b1[CH];
         if (wave < nblk) load_b(b0, wave);
         for (int blk = wave; blk < nblk; blk += 2 * kKnnWaves) {
@@ -605,12 +647,12 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
         nyv[4 * t] = v.x; nyv[4 * t + 1] = v.y; nyv[4 * t + 2] = v.z; nyv[4 * t + 3] = v.w;
     }
     __syncthreads();   // every wave holds its norms: sNy becomes the candidate lists
-    uint16_t* cjw = sCj + wave * (kKnnQpw * 64);   // [4][64] candidate indices of this wave
-    int total[kKnnQpw];
-    float tau[kKnnQpw];
+    uint16_t* cjw = sCj + wave * (QPW * 64);   // [4][64] candidate indices of this wave
+    int total[QPW];
+    float tau[QPW];
 #pragma unroll
-    for (int qq = 0; qq < kKnnQpw; ++qq) {
-        const int i = wave * kKnnQpw + qq;
+    for (int qq = 0; qq < QPW; ++qq) {
+        const int i = wave * QPW + qq;
         const float nxq = sNx[i];
         float lo[16];
         float mn = inf;
@@ -648,27 +690,27 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     // exact distances (the oracle's channel order) of this lane's candidate
     // of each query
-    int jc[kKnnQpw];
-    float dx[kKnnQpw];
+    int jc[QPW];
+    float dx[QPW];
 #pragma unroll
-    for (int qq = 0; qq < kKnnQpw; ++qq) {
+    for (int qq = 0; qq < QPW; ++qq) {
         jc[qq] = (total[qq] <= 64 && lane < total[qq]) ? cjw[qq * 64 + lane] : 0;
         dx[qq] = 0.0f;
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     {
-        const float* rr[kKnnQpw];
-        const float* qr[kKnnQpw];
+        const float* rr[QPW];
+        const float* qr[QPW];
 #pragma unroll
-        for (int qq = 0; qq < kKnnQpw; ++qq) {
+        for (int qq = 0; qq < QPW; ++qq) {
             rr[qq] = ref + (b * N + jc[qq]) * ldr;
-            qr[qq] = sQ + (wave * kKnnQpw + qq) * CQ;
+            qr[qq] = sQ + (wave * QPW + qq) * CQ;
         }
 #pragma unroll
         for (int c4 = 0; c4 < CH / 2; ++c4) {
             if (c4 * 4 < C) {
 #pragma unroll
-                for (int qq = 0; qq < kKnnQpw; ++qq) {
+                for (int qq = 0; qq < QPW; ++qq) {
                     const float4 r = *reinterpret_cast<const float4*>(rr[qq] + 4 * c4);
                     const float4 qv = *reinterpret_cast<const float4*>(qr[qq] + 4 * c4);
                     float u = r.x - qv.x;
@@ -683,8 +725,8 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
             }
         }
     }
-    for (int qq = 0; qq < kKnnQpw; ++qq) {
-        const int i = wave * kKnnQpw + qq;
+    for (int qq = 0; qq < QPW; ++qq) {
+        const int i = wave * QPW + qq;
         const int qi = q0 + i;
         const int tot = total[qq];
         if (tot <= 64) {
@@ -1067,6 +1109,18 @@ extern "C" int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query
             MESO_REQUIRE(attr == hipSuccess, MESORASI_EHIP, "mesorasi_knn: LDS size attribute: %s", hipGetErrorString(attr));
             knn_mfma_kernel<32><<<grid, block, lds_m, s>>>(ref, ld_ref, query, ld_query, (int)N, (int)M, C, K, qblocks,
                                                            nit, dist);
+        } else if (C % 16 == 0) {
+            // 16 queries per workgroup (fp32 table of 66 KB): two workgroups
+            // per CU, so one's Gram MFMAs overlap the other's selection
+            constexpr int QB16 = 16;
+            const int qb16 = (int)ceil_div(M, QB16);
+            MESO_REQUIRE(B * qb16 <= 0x7fffffff, MESORASI_EUNSUPPORTED, "mesorasi_knn: too many queries");
+            const size_t lds16 = sizeof(float) * ((size_t)QB16 * kKnnMfmaLda + (size_t)QB16 * (C + 4) + kKnnMfmaMaxN + QB16);
+            static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&knn_mfma_kernel<64, QB16>),
+                                                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            MESO_REQUIRE(attr == hipSuccess, MESORASI_EHIP, "mesorasi_knn: LDS size attribute: %s", hipGetErrorString(attr));
+            knn_mfma_kernel<64, QB16><<<dim3((unsigned)(B * qb16)), block, lds16, s>>>(ref, ld_ref, query, ld_query, (int)N,
+                                                                                    (int)M, C, K, qb16, nit, dist);
         } else {
             static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&knn_mfma_kernel<64>),
                                                                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);

@@ -288,6 +288,11 @@ KNN_CASES = [
     ("mfma_near_duplicates", 1, 1024, 256, 64, 20, "jitter"),   # far more candidates than K in the margin
     ("mfma_large_offset", 1, 1000, 200, 128, 20, "offset"),     # norms >> distances: wide margins
     ("mfma_k64", 1, 1024, 128, 128, 64, "other"),
+    # C > 64 with C % 16 == 0: 16 queries per workgroup on 16 x 16 MFMA blocks
+    ("mfma16_ties_ragged", 2, 333, 77, 80, 20, "grid"),
+    ("mfma16_near_duplicates", 1, 1024, 200, 128, 20, "jitter"),
+    ("mfma16_overflow", 1, 512, 64, 128, 20, "huge"),
+    ("mfma16_m17", 2, 1024, 17, 112, 8, "other"),        # one full block of 16 queries plus one
     # more than 1024 points: the streaming running list
     ("stream_n1500", 1, 1500, 200, 16, 20, "other"),
     ("stream_ties", 1, 1100, 300, 3, 10, "grid"),
