@@ -210,8 +210,9 @@ int mesorasi_ball_query_grid(const float* xyz, const float* qxyz, int64_t B, int
  *   query [B, M, ld_query] float32
  *   nit   [B, M, K] int32 out;  dist [B, M, K] float32 out, nullable
  * Errors: EINVAL for NULL ref/query/nit, sizes < 0, K < 1, K > N, C < 1,
- *         ld < C;  EUNSUPPORTED for K > MESORASI_MAX_K_KNN or
- *         C > MESORASI_MAX_C_KNN.
+ *         ld < C;  EUNSUPPORTED for K > MESORASI_MAX_K_KNN,
+ *         C > MESORASI_MAX_C_KNN, or more query blocks than one launch
+ *         holds (B x ceil(M / 16) above 2^31 - 1).
  */
 int mesorasi_knn(const float* ref, int64_t ld_ref, const float* query, int64_t ld_query, int64_t B, int64_t N,
                  int64_t M, int32_t C, int32_t K, int32_t* nit, float* dist, void* stream);
