@@ -581,16 +581,18 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
         const int QC = C / 4;
         const float* qa4 = sQ + (lane & 15) * CQ + (lane >> 4) * QC;
         const int nblk16 = (N + 15) / 16;
-        for (int blk = wave; blk < nblk16; blk += kKnnWaves) {
+        auto load16 = [&](float (&bv)[CH / 2], int blk) {
             const int j = blk * 16 + (lane & 15);
-            const bool valid = j < N;
-            const float* rr = ref + (b * N + (valid ? j : N - 1)) * ldr + (lane >> 4) * QC;
-            float bv[CH / 2];
+            const float* rr = ref + (b * N + (j < N ? j : N - 1)) * ldr + (lane >> 4) * QC;
 #pragma unroll
             for (int s4 = 0; s4 < CH / 8; ++s4) {
                 const float4 v = s4 * 4 < QC ? *reinterpret_cast<const float4*>(rr + 4 * s4) : make_float4(0.f, 0.f, 0.f, 0.f);
                 bv[4 * s4] = v.x; bv[4 * s4 + 1] = v.y; bv[4 * s4 + 2] = v.z; bv[4 * s4 + 3] = v.w;
             }
+        };
+        auto gram16 = [&](const float (&bv)[CH / 2], int blk) {
+            const int j = blk * 16 + (lane & 15);
+            const bool valid = j < N;
             float nyq = 0.0f;
 #pragma unroll
             for (int k = 0; k < CH / 2; ++k) nyq = __builtin_fmaf(bv[k], bv[k], nyq);
@@ -611,6 +613,18 @@ __global__ __launch_bounds__(64 * kKnnWaves) void knn_mfma_kernel(const float* _
                 const int i = 4 * (lane >> 4) + r;
                 sA[i * kKnnMfmaLda + j] = valid ? __builtin_fmaf(-2.0f, acc[r], sNx[i] + ny) : inf;
             }
+        };
+        // the next block's reference rows load while this block's MFMAs run
+        // (two register sets, pairs of blocks per loop turn)
+        float b0[CH / 2], b1[CH / 2];
+        if (wave < nblk16) load16(b0, wave);
+        for (int blk = wave; blk < nblk16; blk += 2 * kKnnWaves) {
+            const int nb1 = blk + kKnnWaves;
+            if (nb1 < nblk16) load16(b1, nb1);
+            gram16(b0, blk);
+            if (nb1 >= nblk16) break;
+            if (nb1 + kKnnWaves < nblk16) load16(b0, nb1 + kKnnWaves);
+            gram16(b1, nb1);
         }
     } else if constexpr (CH <= 32) {
         float b0[CH], b1[CH];
